@@ -1,0 +1,227 @@
+/*
+ * zoact.h -- C ABI of the ZO-Act forward-only step on MI355X (gfx950).
+ *
+ * ZO-Act (arXiv 2607.01125) fine-tunes a frozen model by adapting each linear
+ * layer as W_eff = W + V_r B (Section 3): W and the activation basis V_r are
+ * frozen, only the small coefficient matrix B is trained, and B is updated from
+ * forward-only loss evaluations under Gaussian perturbations Z of B
+ * (Algorithm 2), with an optimiser such as Adam.  V_r is computed once from a
+ * calibration batch (Algorithm 1).
+ *
+ * Library orientation (PyTorch style): x [T][d_in] row-major, W [d_out][d_in],
+ * the basis is stored transposed as U^T [r][d_in] (U = V_r), the coefficients
+ * as C = B^T [d_out][r], so an adapted layer computes
+ *     y = x W^T + b + (x U) C^T.
+ * The step evaluates it twice on stacked halves of the batch, with C + eps Z
+ * (half 0, "+") and C - eps Z (half 1, "-"), and then applies ZO-Adam with
+ * g = (L+ - L-) / (2 eps).
+ *
+ * Conventions shared by every call:
+ *  - Pointers are DEVICE pointers unless a comment says "host".  The caller owns
+ *    every buffer; the library allocates and frees no memory on these paths and
+ *    keeps no pointer after the call returns.  Buffers must stay valid until the
+ *    stream reaches the enqueued work.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Every call only
+ *    enqueues work on it and returns; none synchronises unless stated.
+ *  - All shape, dtype and alignment checks run on the host before anything is
+ *    enqueued; a failed check returns ZOACT_E_INVALID (or ZOACT_E_UNSUPPORTED)
+ *    with no side effects.  A HIP launch error returns ZOACT_E_HIP.  The detail
+ *    text of the last error on the calling thread is in zoact_last_error().
+ *  - Device pointers must be 16-byte aligned; row lengths (d_in, d_out, r of
+ *    bf16 tensors) must keep rows 16-byte aligned where stated.
+ *  - bf16 values are stored as 16-bit patterns (uint16_t); conversions to bf16
+ *    round to nearest, ties to even.
+ *  - The arena: all coefficient matrices of a model live in one flat array of
+ *    k = sum_l r * n_l entries (the paper's beta in R^k, Section 4).  A layer
+ *    whose C starts at arena index `coef_offset` keeps C[n][i] at index
+ *    coef_offset + n * r + i.  Z at arena index e for (seed, step, query) is a
+ *    pure function of those four values and is never stored.
+ *  - No C++ exception crosses this boundary.  The library is thread-safe; its
+ *    only global state is the per-thread error text.
+ */
+#ifndef ZOACT_H
+#define ZOACT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t zoact_status;
+enum {
+  ZOACT_OK = 0,
+  ZOACT_E_INVALID = 1,     /* bad argument, shape, dtype or alignment          */
+  ZOACT_E_UNSUPPORTED = 2, /* valid request this build does not implement      */
+  ZOACT_E_HIP = 3,         /* HIP runtime / launch failure                     */
+  ZOACT_E_NOCONVERGE = 4,  /* eigensolver tolerance not met (result written)   */
+  ZOACT_E_WORKSPACE = 5    /* workspace missing or too small                   */
+};
+
+/* Element types. */
+enum { ZOACT_F32 = 0, ZOACT_BF16 = 1, ZOACT_INT4_G128 = 2 };
+
+/* Flags of zoact_linear_fwd_pm. */
+enum {
+  ZOACT_EPI_NONE = 0,
+  ZOACT_EPI_SWIGLU = 1u << 0, /* rows of W interleave gate/up in blocks of 16:
+                                 fused rows 32j..32j+15 are gate features
+                                 16j..16j+15 and rows 32j+16..32j+31 the matching
+                                 up features; output y[t][f] = silu(gate)*up,
+                                 width d_out/2                                    */
+  ZOACT_EPI_RELU = 1u << 1    /* y = max(0, .) before the store                   */
+};
+
+typedef void* zoact_stream; /* hipStream_t */
+
+/* Perturbation of one evaluation: Z = Z(seed, step, query, arena index). */
+typedef struct {
+  uint64_t seed;
+  uint32_t step;  /* optimiser step t (Algorithm 2's outer loop)          */
+  uint32_t query; /* query index j (0 for the two-sided +/- pair)         */
+  float eps;      /* perturbation scale (the paper's mu)                  */
+} zoact_pert;
+
+/* One adapted (or plain, r = 0) linear layer. */
+typedef struct {
+  int32_t w_dtype;      /* ZOACT_F32, ZOACT_BF16 or ZOACT_INT4_G128               */
+  const void* w;        /* F32/BF16: [d_out][d_in]; INT4: uint8 [d_out][d_in/2],
+                           even column in the low nibble, two's complement,
+                           values in [-7, 7]                                       */
+  const void* w_scales; /* INT4: bf16 [d_out][d_in/128] (w = bf16(q * s)); else NULL */
+  const void* bias;     /* [d_out] in the activation type, or NULL                 */
+  const void* ut;       /* U^T [r][d_in] in the activation type; NULL iff r == 0   */
+  int64_t d_in, d_out;
+  int32_t r;            /* 0 <= r <= 256                                          */
+  int64_t coef_offset;  /* arena index of C[0][0]                                 */
+} zoact_linear;
+
+/* The coefficient arena and its Adam moments (updated in place by zoact_step). */
+typedef struct {
+  int32_t c_dtype; /* ZOACT_F32 or ZOACT_BF16 */
+  void* c;         /* [k] coefficients          */
+  float* m;        /* [k] first moment, fp32    */
+  float* v;        /* [k] second moment, fp32   */
+  int64_t k;
+} zoact_arena;
+
+/* Host-computed Adam scalars for step t (float64 then one rounding to fp32):
+   step_size = lr_t / (1 - beta1^t), inv_sqrt_bc2 = 1 / sqrt(1 - beta2^t),
+   one_minus_beta1 = 1 - beta1, one_minus_beta2 = 1 - beta2. */
+typedef struct {
+  float beta1, beta2, eps, weight_decay;
+  float step_size, inv_sqrt_bc2, one_minus_beta1, one_minus_beta2;
+} zoact_adam;
+
+/* Options of the eigensolver behind zoact_basis_from_gram (NULL = defaults). */
+typedef struct {
+  int32_t oversample; /* extra block columns p (default r)                  */
+  int32_t iters;      /* subspace iterations (default 12)                   */
+  uint64_t seed;      /* seed of the random start block                     */
+} zoact_eig_opts;
+
+/* ------------------------------------------------------------------ info */
+const char* zoact_version(void);
+const char* zoact_status_str(zoact_status s);
+/* Detail text of the last failed call on this thread ("" if none). */
+const char* zoact_last_error(void);
+
+/* ------------------------------------------------------ perturbation Z
+ * Section 3: Z ~ N(0, I) in each layer's r x n coefficient space; Algorithm 2
+ * draws a fresh Z per step and query.  Writes Z at arena indices e0 .. e0+n-1
+ * to out[0 .. n-1] (fp32).  Generator: Philox4x32-10 with key = seed and counter
+ * (lo32(e>>2), hi32(e>>2), step, query), lane e & 3, followed by Box-Muller in
+ * quarter turns with series logarithm and sine/cosine (all fp32, no fused
+ * multiply-add, correctly rounded division and square root).  The hot kernels
+ * regenerate the same values internally; this entry point exists for testing.
+ * Errors: n < 0, e0 < 0, out == NULL with n > 0 -> ZOACT_E_INVALID. */
+zoact_status zoact_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e0, int64_t n,
+                         float* out, zoact_stream stream);
+
+/* ------------------------------------------------------ projection X U
+ * The X V_r factor of the perturbed forward (Section 3, Y+ = XW + (X V_r)(B + mu Z)).
+ * x [n_tok][d_in] and U^T [r][d_in] in dtype (F32 or BF16); p [n_tok][r] same
+ * dtype, fp32 accumulation, one rounding on store.  1 <= r <= 256; d_in % 8 == 0
+ * for BF16. */
+zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut,
+                           int32_t r, void* p, zoact_stream stream);
+
+/* ------------------------------------------------------ fused +/- adapted linear
+ * Section 3's perturbed forward evaluated for both signs in one pass over W:
+ *   y[h] = epilogue(residual[h] + x[h] W^T + b + p[h] (C + s_h eps Z)^T),  s = (+1, -1)
+ * x [2][T][d_in] and p [2][T][r] (from zoact_project on x) in the activation
+ * dtype x_dtype (BF16 with BF16 or INT4 weights; F32 with F32 weights);
+ * residual NULL or [2][T][d_out] in y's layout; y [2][T][d_out'] in y_dtype
+ * (x_dtype, or F32 for logits), d_out' = d_out/2 with ZOACT_EPI_SWIGLU.
+ * C is read from the arena at L->coef_offset (rows d_out, r per row) and
+ * C +/- eps Z is formed in fp32 inside the kernel (rounded to bf16 for the
+ * bf16 path); pert->eps == 0 gives two unperturbed halves.  With r == 0 the call
+ * is a plain GEMM (arena and p may be NULL).  One rounding per output element.
+ * Requirements: T >= 1; d_in % 64 == 0 (BF16/INT4) or % 4 (F32); INT4 needs
+ * d_in % 128 == 0; d_out % 64 == 0 with SWIGLU (% 16 otherwise, BF16).
+ * Errors: ZOACT_E_INVALID on shape/dtype mismatch, ZOACT_E_UNSUPPORTED for a
+ * dtype combination not listed here. */
+zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, const void* x,
+                                 int32_t x_dtype, int64_t T, const void* p, const void* residual,
+                                 uint32_t flags, const zoact_pert* pert, void* y, int32_t y_dtype,
+                                 zoact_stream stream);
+
+/* ------------------------------------------------------ losses of both halves
+ * Algorithm 2 needs the loss under each perturbation; the two-sided step needs
+ * L+ and L- (loss_pm[0], loss_pm[1], fp32, device).  Reductions are
+ * deterministic (fixed order, no atomics) and use `ws` (>= zoact_loss_workspace_bytes()).
+ * zoact_mse_pm: mean over T*N of (y[h] - target)^2; y [2][T][N], target [T][N], same dtype.
+ * zoact_xent_pm: next-token cross entropy, mean over B*(S-1) positions of
+ *   -log softmax(logits[h][b][s])[tokens[b][s+1]]; logits fp32 [2][B][S][V],
+ *   tokens int32 [B][S] (host-validated range is the caller's duty; ids outside
+ *   [0, V) are clamped). */
+size_t zoact_loss_workspace_bytes(void);
+zoact_status zoact_mse_pm(const void* y, int32_t dtype, const void* target, int64_t T, int64_t N,
+                          float* loss_pm, void* ws, size_t ws_bytes, zoact_stream stream);
+zoact_status zoact_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V,
+                           float* loss_pm, void* ws, size_t ws_bytes, zoact_stream stream);
+
+/* ------------------------------------------------------ ZO-Adam step
+ * Algorithm 2's update in two-sided form: g = (L+ - L-) / (2 eps) from
+ * loss_pm (device, fp32 [2]); for every arena index e: gh = g * Z(e) (+ wd*c),
+ * then Adam on (c, m, v) in place in fp32 in the order
+ *   m = b1 m + (1-b1) gh; v = b2 v + (1-b2) gh^2; d = sqrt(v) inv_sqrt_bc2 + eps_A;
+ *   c = c - step_size (m / d)
+ * (C rounded to bf16 on store when A->c_dtype == BF16).  A non-finite g leaves
+ * the arena unchanged and ORs bit 0 into *dev_status (device, nullable).
+ * zoact_step_sgd: c = c - lr * (g * Z(e)) (the paper's SGD variant). */
+zoact_status zoact_step(const zoact_arena* A, const float* loss_pm, const zoact_pert* pert,
+                        const zoact_adam* h, uint32_t* dev_status, zoact_stream stream);
+zoact_status zoact_step_sgd(const zoact_arena* A, const float* loss_pm, const zoact_pert* pert, float lr,
+                            uint32_t* dev_status, zoact_stream stream);
+
+/* ------------------------------------------------------ one-shot basis (Algorithm 1)
+ * Top-r right singular vectors of the calibration activations X_l, i.e. the top-r
+ * eigenvectors of the uncentred Gram X^T X, largest first, each column signed so
+ * that its largest-magnitude entry is positive.
+ * zoact_gram: g [d][d] fp32 (+)= X^T X for x [n_tok][d] (F32 or BF16); `accumulate`
+ *   != 0 adds to g (chunked calibration batches).
+ * zoact_basis_from_gram: top-r eigenpairs of g by randomised block subspace
+ *   iteration (block r + oversample), Rayleigh-Ritz and a Jacobi eigensolver of
+ *   the projected block; writes ut [r][d] in ut_dtype (F32/BF16), optional
+ *   ut_master fp32 [r][d], eigvals fp32 [r] (descending) and resid fp32 [1]
+ *   (max_i ||G u_i - lambda_i u_i|| / lambda_1).  Workspace: ws of at least
+ *   zoact_basis_workspace_bytes(d, r, opts) bytes.
+ * zoact_basis_init: zoact_gram followed by zoact_basis_from_gram (g in ws).
+ * Errors: r < 1, r > 256, r + p > d, n_tok < r -> ZOACT_E_INVALID. */
+size_t zoact_basis_workspace_bytes(int64_t d, int32_t r, const zoact_eig_opts* opts);
+zoact_status zoact_gram(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, float* g,
+                        int32_t accumulate, zoact_stream stream);
+zoact_status zoact_basis_from_gram(const float* g, int64_t d, int32_t r, const zoact_eig_opts* opts,
+                                   void* ut, int32_t ut_dtype, float* ut_master, float* eigvals,
+                                   float* resid, void* ws, size_t ws_bytes, zoact_stream stream);
+zoact_status zoact_basis_init(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, int32_t r,
+                              const zoact_eig_opts* opts, void* ut, int32_t ut_dtype, float* ut_master,
+                              float* eigvals, float* resid, void* ws, size_t ws_bytes,
+                              zoact_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ZOACT_H */

@@ -1,0 +1,229 @@
+// extern "C" boundary of the ZO-Act HIP library: host-side validation, then a
+// launch on the caller's stream.  Every check runs before anything is enqueued.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "common.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+zoact_status fail(zoact_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+zoact_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ZOACT_OK;
+  if (e == hipErrorNotSupported) return fail(ZOACT_E_UNSUPPORTED, "%s: unsupported configuration", what);
+  return fail(ZOACT_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+hipStream_t st(zoact_stream s) { return reinterpret_cast<hipStream_t>(s); }
+
+bool float_type(int32_t t) { return t == ZOACT_F32 || t == ZOACT_BF16; }
+
+#define CHECK(cond, ...)                                   \
+  do {                                                     \
+    if (!(cond)) return fail(ZOACT_E_INVALID, __VA_ARGS__); \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* zoact_version(void) { return "zoact-gfx950 0.1.0"; }
+
+const char* zoact_status_str(zoact_status s) {
+  switch (s) {
+    case ZOACT_OK: return "ok";
+    case ZOACT_E_INVALID: return "invalid argument";
+    case ZOACT_E_UNSUPPORTED: return "unsupported";
+    case ZOACT_E_HIP: return "HIP error";
+    case ZOACT_E_NOCONVERGE: return "eigensolver did not converge";
+    case ZOACT_E_WORKSPACE: return "workspace too small";
+    default: return "unknown status";
+  }
+}
+
+const char* zoact_last_error(void) { return g_last_error.c_str(); }
+
+zoact_status zoact_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e0, int64_t n, float* out,
+                         zoact_stream stream) {
+  CHECK(n >= 0 && e0 >= 0, "gen_z: negative range (e0=%lld, n=%lld)", (long long)e0, (long long)n);
+  CHECK(n == 0 || out != nullptr, "gen_z: out is NULL");
+  CHECK(e0 <= INT64_MAX - n, "gen_z: range overflows");
+  return hip_status(zoact::launch_gen_z(seed, step, query, e0, n, out, st(stream)), "gen_z");
+}
+
+zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut, int32_t r, void* p,
+                           zoact_stream stream) {
+  CHECK(float_type(dtype), "project: dtype must be F32 or BF16");
+  CHECK(n_tok >= 1 && d_in >= 1, "project: empty shape (n_tok=%lld, d_in=%lld)", (long long)n_tok, (long long)d_in);
+  CHECK(r >= 1 && r <= 256, "project: r=%d outside [1, 256]", r);
+  CHECK(x && ut && p, "project: NULL pointer");
+  if (dtype == ZOACT_BF16) {
+    CHECK(d_in % 32 == 0, "project: bf16 needs d_in %% 32 == 0 (d_in=%lld)", (long long)d_in);
+    CHECK(aligned16(x) && aligned16(ut), "project: x and ut must be 16-byte aligned");
+  }
+  return hip_status(zoact::launch_project(x, dtype, n_tok, d_in, ut, r, p, st(stream)), "project");
+}
+
+zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
+                                 const void* p, const void* residual, uint32_t flags, const zoact_pert* pert, void* y,
+                                 int32_t y_dtype, zoact_stream stream) {
+  CHECK(L != nullptr && pert != nullptr, "linear_fwd_pm: NULL layer or perturbation");
+  CHECK(x && y && L->w, "linear_fwd_pm: NULL x, y or w");
+  CHECK(T >= 1, "linear_fwd_pm: T=%lld < 1", (long long)T);
+  CHECK(L->d_in >= 1 && L->d_out >= 1, "linear_fwd_pm: empty layer");
+  CHECK(L->r >= 0 && L->r <= 256, "linear_fwd_pm: r=%d outside [0, 256]", L->r);
+  CHECK((flags & ~(uint32_t)(ZOACT_EPI_SWIGLU | ZOACT_EPI_RELU)) == 0, "linear_fwd_pm: unknown flags 0x%x", flags);
+  CHECK(!((flags & ZOACT_EPI_SWIGLU) && (flags & ZOACT_EPI_RELU)), "linear_fwd_pm: SWIGLU and RELU are exclusive");
+  CHECK(float_type(x_dtype) && float_type(y_dtype), "linear_fwd_pm: activation types must be F32 or BF16");
+  if (L->r > 0) {
+    CHECK(A != nullptr && A->c != nullptr, "linear_fwd_pm: r > 0 needs an arena");
+    CHECK(L->ut != nullptr && p != nullptr, "linear_fwd_pm: r > 0 needs ut and p");
+    CHECK(L->coef_offset >= 0 && L->coef_offset + L->d_out * (int64_t)L->r <= A->k,
+          "linear_fwd_pm: coefficient block [%lld, %lld) outside the arena (k=%lld)", (long long)L->coef_offset,
+          (long long)(L->coef_offset + L->d_out * (int64_t)L->r), (long long)A->k);
+    CHECK(float_type(A->c_dtype), "linear_fwd_pm: arena dtype must be F32 or BF16");
+  }
+  if (flags & ZOACT_EPI_SWIGLU) CHECK(L->d_out % 32 == 0, "linear_fwd_pm: SWIGLU needs d_out %% 32 == 0");
+  if (x_dtype == ZOACT_F32) {
+    CHECK(L->w_dtype == ZOACT_F32 && y_dtype == ZOACT_F32, "linear_fwd_pm: F32 activations need F32 weights and output");
+    CHECK(L->r == 0 || A->c_dtype == ZOACT_F32, "linear_fwd_pm: F32 path needs an F32 arena");
+  } else {
+    CHECK(L->w_dtype == ZOACT_BF16 || L->w_dtype == ZOACT_INT4_G128,
+          "linear_fwd_pm: BF16 activations need BF16 or INT4 weights");
+    CHECK(L->d_in % 64 == 0, "linear_fwd_pm: d_in=%lld must be a multiple of 64", (long long)L->d_in);
+    CHECK(L->d_out % 16 == 0, "linear_fwd_pm: d_out=%lld must be a multiple of 16", (long long)L->d_out);
+    CHECK(aligned16(x) && aligned16(L->w) && aligned16(y), "linear_fwd_pm: x, w, y must be 16-byte aligned");
+    CHECK(residual == nullptr || aligned16(residual), "linear_fwd_pm: residual must be 16-byte aligned");
+    if (L->w_dtype == ZOACT_INT4_G128) {
+      CHECK(L->d_in % 128 == 0, "linear_fwd_pm: INT4 needs d_in %% 128 == 0 (d_in=%lld)", (long long)L->d_in);
+      CHECK(L->w_scales != nullptr, "linear_fwd_pm: INT4 needs w_scales");
+    }
+  }
+  return hip_status(zoact::launch_linear_pm(*L, A, x, x_dtype, T, p, residual, flags, *pert, y, y_dtype, st(stream)),
+                    "linear_fwd_pm");
+}
+
+size_t zoact_loss_workspace_bytes(void) { return (size_t)2 * zoact::kLossBlocks * sizeof(double); }
+
+zoact_status zoact_mse_pm(const void* y, int32_t dtype, const void* target, int64_t T, int64_t N, float* loss_pm,
+                          void* ws, size_t ws_bytes, zoact_stream stream) {
+  CHECK(float_type(dtype), "mse_pm: dtype must be F32 or BF16");
+  CHECK(y && target && loss_pm, "mse_pm: NULL pointer");
+  CHECK(T >= 1 && N >= 1, "mse_pm: empty shape");
+  CHECK(aligned16(y) && aligned16(target), "mse_pm: y and target must be 16-byte aligned");
+  if (ws == nullptr || ws_bytes < zoact_loss_workspace_bytes())
+    return fail(ZOACT_E_WORKSPACE, "mse_pm: workspace needs %zu bytes", zoact_loss_workspace_bytes());
+  return hip_status(zoact::launch_mse_pm(y, dtype, target, T, N, loss_pm, ws, st(stream)), "mse_pm");
+}
+
+zoact_status zoact_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V, float* loss_pm,
+                           void* ws, size_t ws_bytes, zoact_stream stream) {
+  CHECK(logits && tokens && loss_pm, "xent_pm: NULL pointer");
+  CHECK(B >= 1 && S >= 2 && V >= 1, "xent_pm: need B >= 1, S >= 2, V >= 1");
+  if (ws == nullptr || ws_bytes < zoact_loss_workspace_bytes())
+    return fail(ZOACT_E_WORKSPACE, "xent_pm: workspace needs %zu bytes", zoact_loss_workspace_bytes());
+  return hip_status(zoact::launch_xent_pm(logits, tokens, B, S, V, loss_pm, ws, st(stream)), "xent_pm");
+}
+
+static zoact_status check_arena(const zoact_arena* A, const float* loss_pm, const zoact_pert* p, const char* who) {
+  CHECK(A != nullptr && p != nullptr && loss_pm != nullptr, "%s: NULL arena, loss or perturbation", who);
+  CHECK(A->k >= 0, "%s: negative arena size", who);
+  CHECK(float_type(A->c_dtype), "%s: arena dtype must be F32 or BF16", who);
+  CHECK(A->k == 0 || A->c != nullptr, "%s: NULL coefficients", who);
+  CHECK(aligned16(A->c) && aligned16(A->m) && aligned16(A->v), "%s: arena buffers must be 16-byte aligned", who);
+  return ZOACT_OK;
+}
+
+zoact_status zoact_step(const zoact_arena* A, const float* loss_pm, const zoact_pert* p, const zoact_adam* h,
+                        uint32_t* dev_status, zoact_stream stream) {
+  zoact_status s = check_arena(A, loss_pm, p, "step");
+  if (s != ZOACT_OK) return s;
+  CHECK(h != nullptr, "step: NULL Adam scalars");
+  CHECK(A->k == 0 || (A->m != nullptr && A->v != nullptr), "step: NULL moments");
+  return hip_status(zoact::launch_adam(*A, loss_pm, *p, *h, dev_status, st(stream)), "step");
+}
+
+zoact_status zoact_step_sgd(const zoact_arena* A, const float* loss_pm, const zoact_pert* p, float lr,
+                            uint32_t* dev_status, zoact_stream stream) {
+  CHECK(A != nullptr && p != nullptr && loss_pm != nullptr, "step_sgd: NULL arena, loss or perturbation");
+  CHECK(A->k >= 0 && float_type(A->c_dtype), "step_sgd: bad arena");
+  CHECK(A->k == 0 || A->c != nullptr, "step_sgd: NULL coefficients");
+  return hip_status(zoact::launch_sgd(*A, loss_pm, *p, lr, dev_status, st(stream)), "step_sgd");
+}
+
+static void eig_defaults(int32_t r, const zoact_eig_opts* o, int32_t& p, int32_t& iters, uint64_t& seed) {
+  p = (o && o->oversample > 0) ? o->oversample : r;
+  iters = (o && o->iters > 0) ? o->iters : 12;
+  seed = o ? o->seed : 0x5eedULL;
+}
+
+size_t zoact_basis_workspace_bytes(int64_t d, int32_t r, const zoact_eig_opts* opts) {
+  int32_t p, it;
+  uint64_t sd;
+  eig_defaults(r, opts, p, it, sd);
+  if (d < 1 || r < 1) return 0;
+  return zoact::basis_ws_bytes(d, r, p);
+}
+
+zoact_status zoact_gram(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, float* g, int32_t accumulate,
+                        zoact_stream stream) {
+  CHECK(x && g, "gram: NULL pointer");
+  CHECK(float_type(x_dtype), "gram: dtype must be F32 or BF16");
+  CHECK(n_tok >= 1 && d >= 1, "gram: empty shape");
+  if (x_dtype == ZOACT_BF16) CHECK(d % 64 == 0, "gram: bf16 needs d %% 64 == 0");
+  return hip_status(zoact::launch_gram(x, x_dtype, n_tok, d, g, accumulate, st(stream)), "gram");
+}
+
+zoact_status zoact_basis_from_gram(const float* g, int64_t d, int32_t r, const zoact_eig_opts* opts, void* ut,
+                                   int32_t ut_dtype, float* ut_master, float* eigvals, float* resid, void* ws,
+                                   size_t ws_bytes, zoact_stream stream) {
+  int32_t p, iters;
+  uint64_t seed;
+  eig_defaults(r, opts, p, iters, seed);
+  CHECK(g && ut, "basis_from_gram: NULL g or ut");
+  CHECK(float_type(ut_dtype), "basis_from_gram: ut dtype must be F32 or BF16");
+  CHECK(r >= 1 && r <= 256, "basis_from_gram: r=%d outside [1, 256]", r);
+  CHECK(d >= 2 && r + p <= d, "basis_from_gram: r + oversample = %d exceeds d = %lld", r + p, (long long)d);
+  CHECK(r + p <= 512, "basis_from_gram: block r + oversample = %d exceeds 512", r + p);
+  const size_t need = zoact::basis_ws_bytes(d, r, p);
+  if (ws == nullptr || ws_bytes < need) return fail(ZOACT_E_WORKSPACE, "basis_from_gram: workspace needs %zu bytes", need);
+  return hip_status(
+      zoact::launch_basis_from_gram(g, d, r, p, iters, seed, ut, ut_dtype, ut_master, eigvals, resid, ws, st(stream)),
+      "basis_from_gram");
+}
+
+zoact_status zoact_basis_init(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, int32_t r,
+                              const zoact_eig_opts* opts, void* ut, int32_t ut_dtype, float* ut_master, float* eigvals,
+                              float* resid, void* ws, size_t ws_bytes, zoact_stream stream) {
+  CHECK(n_tok >= r, "basis_init: n_tok=%lld < r=%d", (long long)n_tok, r);
+  int32_t p, iters;
+  uint64_t seed;
+  eig_defaults(r, opts, p, iters, seed);
+  CHECK(r >= 1 && r <= 256 && d >= 2 && r + p <= d, "basis_init: bad r=%d for d=%lld", r, (long long)d);
+  const size_t gbytes = (size_t)d * (size_t)d * sizeof(float);
+  const size_t need = gbytes + zoact::basis_ws_bytes(d, r, p);
+  if (ws == nullptr || ws_bytes < need) return fail(ZOACT_E_WORKSPACE, "basis_init: workspace needs %zu bytes", need);
+  float* g = static_cast<float*>(ws);
+  zoact_status s = zoact_gram(x, x_dtype, n_tok, d, g, 0, stream);
+  if (s != ZOACT_OK) return s;
+  return zoact_basis_from_gram(g, d, r, opts, ut, ut_dtype, ut_master, eigvals, resid,
+                               static_cast<char*>(ws) + gbytes, ws_bytes - gbytes, stream);
+}
+
+}  // extern "C"

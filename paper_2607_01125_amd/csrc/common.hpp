@@ -1,0 +1,43 @@
+// Shared device/host helpers of the ZO-Act HIP library (gfx950).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "zoact.h"
+
+namespace zoact {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// bf16 <-> fp32.  The conversion to bf16 is the hardware round-to-nearest-even.
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+
+// Internal launchers return hipError_t from hipGetLastError() after the launch.
+hipError_t launch_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e0, int64_t n, float* out,
+                        hipStream_t s);
+hipError_t launch_adam(const zoact_arena& A, const float* loss_pm, const zoact_pert& p, const zoact_adam& h,
+                       uint32_t* status, hipStream_t s);
+hipError_t launch_sgd(const zoact_arena& A, const float* loss_pm, const zoact_pert& p, float lr,
+                      uint32_t* status, hipStream_t s);
+hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut, int32_t r,
+                          void* p, hipStream_t s);
+hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
+                            const void* p, const void* residual, uint32_t flags, const zoact_pert& pert, void* y,
+                            int32_t y_dtype, hipStream_t s);
+hipError_t launch_mse_pm(const void* y, int32_t dtype, const void* target, int64_t T, int64_t N, float* loss_pm,
+                         void* ws, hipStream_t s);
+hipError_t launch_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V,
+                          float* loss_pm, void* ws, hipStream_t s);
+hipError_t launch_gram(const void* x, int32_t dtype, int64_t n_tok, int64_t d, float* g, int accumulate,
+                       hipStream_t s);
+hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t p, int32_t iters, uint64_t seed,
+                                  void* ut, int32_t ut_dtype, float* ut_master, float* eigvals, float* resid,
+                                  void* ws, hipStream_t s);
+size_t basis_ws_bytes(int64_t d, int32_t r, int32_t p);
+
+// Deterministic two-stage reductions: partial sums per block, then one block sums them in order.
+constexpr int kLossBlocks = 1024;
+
+}  // namespace zoact

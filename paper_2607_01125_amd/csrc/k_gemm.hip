@@ -1,0 +1,646 @@
+// Fused +/- adapted linear and the X U projection prepass.
+//
+// Section 3 evaluates the perturbed layer without forming W_eff:
+//   Y+ = X W + (X V_r)(B + mu Z).
+// In the library orientation (W [d_out][d_in], U^T [r][d_in], C = B^T [d_out][r])
+// both perturbation signs of a +/- step are computed by one GEMM over the stacked
+// batch x [2][T][d_in]:
+//   y[h] = x[h] W^T + b + p[h] (C + s_h eps Z)^T,   p[h] = x[h] U,  s = (+1, -1),
+// i.e. a single contraction over the extended depth [x[h] | p[h]] . [W ; C_h]^T
+// in which the last r columns of the depth belong to the rank-r correction.
+//
+// gfx950 design (bf16 / INT4 weights):
+//  * Workgroup tile: 256 output features x 256 tokens, depth step 64, 512 threads
+//    (8 wave64s as 2 along features x 4 along tokens, 128 x 64 per wave), fp32
+//    accumulators in registers, v_mfma_f32_16x16x32_bf16.  The MFMA A operand is the
+//    W tile (rows = features) and the B operand the x tile (columns = tokens), so
+//    each lane ends up holding 4 consecutive features of one token: epilogue
+//    stores are 8-byte (bf16) or 16-byte (fp32) vectors along the feature axis.
+//  * Tiles live in LDS, double-buffered ([2] x (W tile + x tile) = 128 KB), rows of
+//    64 bf16 with the 16-byte chunk index XOR-swizzled by (row & 7) so that the
+//    16-byte fragment reads of 8 consecutive lanes hit distinct banks.  Global
+//    loads for tile k+1 are issued before the MFMAs of tile k.
+//  * A token tile never straddles the two halves: the grid has ceil(T/256) token
+//    tiles per half, so each workgroup knows its sign s_h.
+//  * The correction block is appended after the depth loop as ceil(r/64) extra
+//    depth tiles: the W side is C_h = C + s_h eps Z, formed in fp32 from the arena
+//    with Z regenerated from its counter (the same generator as the optimiser
+//    step), rounded to bf16; the x side is p[h].  Nothing of Z is stored.
+//  * INT4 weights: each thread fetches 16 bytes (32 nibbles of one row) per depth
+//    tile and dequantises them in registers to bf16(q * s) before the LDS store.
+//  * blockIdx -> tile: workgroups are dispatched round-robin over the 8 XCDs, so
+//    the linear id is first regrouped so that each XCD receives a contiguous run of
+//    tiles, and runs are ordered in groups of 4 token tiles x all feature tiles to
+//    keep both operands L2-resident.
+#include "common.hpp"
+#include "rng.hpp"
+
+namespace zoact {
+
+namespace {
+
+constexpr int BN = 256;  // features per tile (MFMA rows)
+constexpr int BM = 256;  // tokens per tile (MFMA columns)
+constexpr int BK = 64;   // depth per tile
+constexpr int NTHR = 512;
+constexpr int WAVES_N = 2;
+constexpr int WAVES_M = 4;
+constexpr int WN = BN / WAVES_N;  // 128 features per wave
+constexpr int WM = BM / WAVES_M;  // 64 tokens per wave
+constexpr int FI = WN / 16;       // 8 MFMA blocks along features
+constexpr int FJ = WM / 16;       // 4 MFMA blocks along tokens
+constexpr int GROUP_M = 4;
+
+struct GemmArgs {
+  const uint16_t* x;      // [2][T][K]
+  const void* w;          // [N][K] bf16 or packed int4 [N][K/2]
+  const uint16_t* wsc;    // int4 scales [N][K/128]
+  const uint16_t* bias;   // [N] or null
+  const uint16_t* p;      // [2][T][r]
+  const void* c;          // arena coefficients
+  const uint16_t* resid;  // [2][T][Nout] or null
+  void* y;                // [2][T][Nout]
+  int64_t T, N, K;
+  int32_t r;
+  int32_t c_bf16;
+  int64_t coef_offset;
+  uint64_t seed;
+  uint32_t step, query;
+  float eps;
+  int32_t tiles_m_half;  // token tiles per half
+  int32_t tiles_n;
+  int32_t n_tail;        // depth tiles of the correction block
+};
+
+__device__ __forceinline__ int swz(int row, int kc) { return (row << 6) + ((kc ^ (row & 7)) << 3); }
+
+// Four consecutive Z values starting at arena index e (any alignment).
+__device__ __forceinline__ float4 gauss4(uint64_t seed, uint32_t step, uint32_t query, uint64_t e) {
+  const float4 a = rng::gauss_block(seed, step, query, e >> 2);
+  const int o = (int)(e & 3);
+  if (o == 0) return a;
+  const float4 b = rng::gauss_block(seed, step, query, (e >> 2) + 1);
+  float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  return make_float4(v[o], v[o + 1], v[o + 2], v[o + 3]);
+}
+
+// fp32 (C + sign*eps*z) rounded to bf16; the product eps*z is rounded before the sum.
+__device__ __forceinline__ uint16_t perturbed_bf16(float c, float z, float eps, bool plus) {
+#pragma clang fp contract(off)
+  const float ez = eps * z;
+  return f2bf(plus ? c + ez : c - ez);
+}
+
+__device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) { return (uint32_t)lo | ((uint32_t)hi << 16); }
+
+// Dequantise 8 nibbles (one uint32, element 2j in the low nibble of byte j) with scale s.
+__device__ __forceinline__ uint4 dequant8(uint32_t q, float s) {
+  uint16_t o[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int v = ((int)(q << (28 - 4 * j))) >> 28;  // sign-extend nibble j
+    o[j] = f2bf((float)v * s);
+  }
+  return make_uint4(pack2(o[0], o[1]), pack2(o[2], o[3]), pack2(o[4], o[5]), pack2(o[6], o[7]));
+}
+
+template <bool INT4>
+__device__ __forceinline__ void load_main(const GemmArgs& a, int64_t n0, const uint16_t* xh, int64_t m0, int64_t T,
+                                          int kt, uint4 (&ws)[4], uint4 (&xs)[4]) {
+  const int t = threadIdx.x;
+  const int64_t k0 = (int64_t)kt * BK;
+  if (INT4) {
+    const int row = t >> 1, half = t & 1;
+    int64_t n = n0 + row;
+    if (n > a.N - 1) n = a.N - 1;
+    const uint8_t* wq = reinterpret_cast<const uint8_t*>(a.w);
+    const uint4 q = *reinterpret_cast<const uint4*>(wq + n * (a.K >> 1) + ((k0 + half * 32) >> 1));
+    const float s = bf2f(a.wsc[n * (a.K >> 7) + ((k0 + half * 32) >> 7)]);
+    ws[0] = dequant8(q.x, s);
+    ws[1] = dequant8(q.y, s);
+    ws[2] = dequant8(q.z, s);
+    ws[3] = dequant8(q.w, s);
+  } else {
+    const uint16_t* w = reinterpret_cast<const uint16_t*>(a.w);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = t + NTHR * i;
+      const int row = c >> 3, kc = c & 7;
+      int64_t n = n0 + row;
+      if (n > a.N - 1) n = a.N - 1;
+      ws[i] = *reinterpret_cast<const uint4*>(w + n * a.K + k0 + kc * 8);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = t + NTHR * i;
+    const int row = c >> 3, kc = c & 7;
+    int64_t m = m0 + row;
+    if (m > T - 1) m = T - 1;
+    xs[i] = *reinterpret_cast<const uint4*>(xh + m * a.K + k0 + kc * 8);
+  }
+}
+
+template <bool INT4>
+__device__ __forceinline__ void store_main(uint16_t* wl, uint16_t* xl, const uint4 (&ws)[4], const uint4 (&xs)[4]) {
+  const int t = threadIdx.x;
+  if (INT4) {
+    const int row = t >> 1, half = t & 1;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<uint4*>(wl + swz(row, half * 4 + i)) = ws[i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = t + NTHR * i;
+      *reinterpret_cast<uint4*>(wl + swz(c >> 3, c & 7)) = ws[i];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = t + NTHR * i;
+    *reinterpret_cast<uint4*>(xl + swz(c >> 3, c & 7)) = xs[i];
+  }
+}
+
+// Correction-block tile `tt`: W side = bf16(C + s eps Z) for coefficient columns
+// tt*64 .. tt*64+63 of each feature row, x side = p[h] for the same columns.
+__device__ __forceinline__ void load_tail(const GemmArgs& a, int64_t n0, const uint16_t* ph, int64_t m0, int64_t T,
+                                          bool plus, int tt, uint4 (&ws)[4], uint4 (&xs)[4]) {
+  const int t = threadIdx.x;
+  const int row = t >> 1, half = t & 1;
+  const int col0 = tt * 64 + half * 32;
+  const int64_t n = n0 + row;
+  const int64_t m = m0 + row;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint16_t wv[8], xv[8];
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const int col = col0 + i * 8 + g * 4;
+      float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+      float cv[4] = {0.f, 0.f, 0.f, 0.f};
+      const bool any = (n < a.N) && (col < a.r);
+      if (any) {
+        const uint64_t e = (uint64_t)(a.coef_offset + n * a.r + col);
+        z = gauss4(a.seed, a.step, a.query, e);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (col + j < a.r)
+            cv[j] = a.c_bf16 ? bf2f(reinterpret_cast<const uint16_t*>(a.c)[e + j])
+                             : reinterpret_cast<const float*>(a.c)[e + j];
+        }
+      }
+      const float zz[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool ok = any && (col + j < a.r);
+        wv[g * 4 + j] = ok ? perturbed_bf16(cv[j], zz[j], a.eps, plus) : (uint16_t)0;
+        xv[g * 4 + j] = (col + j < a.r && m < T) ? ph[m * a.r + col + j] : (uint16_t)0;
+      }
+    }
+    ws[i] = make_uint4(pack2(wv[0], wv[1]), pack2(wv[2], wv[3]), pack2(wv[4], wv[5]), pack2(wv[6], wv[7]));
+    xs[i] = make_uint4(pack2(xv[0], xv[1]), pack2(xv[2], xv[3]), pack2(xv[4], xv[5]), pack2(xv[6], xv[7]));
+  }
+}
+
+__device__ __forceinline__ void store_tail(uint16_t* wl, uint16_t* xl, const uint4 (&ws)[4], const uint4 (&xs)[4]) {
+  const int t = threadIdx.x;
+  const int row = t >> 1, half = t & 1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    *reinterpret_cast<uint4*>(wl + swz(row, half * 4 + i)) = ws[i];
+    *reinterpret_cast<uint4*>(xl + swz(row, half * 4 + i)) = xs[i];
+  }
+}
+
+__device__ __forceinline__ void mfma_tile(const uint16_t* wl, const uint16_t* xl, int wn0, int wm0, int ksteps,
+                                          floatx4 (&acc)[FI][FJ]) {
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15, lk = lane >> 4;
+  for (int ks = 0; ks < ksteps; ++ks) {
+    bf16x8 af[FI], bfr[FJ];
+#pragma unroll
+    for (int i = 0; i < FI; ++i) {
+      const int row = wn0 + i * 16 + lr;
+      af[i] = *reinterpret_cast<const bf16x8*>(wl + swz(row, ks * 4 + lk));
+    }
+#pragma unroll
+    for (int j = 0; j < FJ; ++j) {
+      const int row = wm0 + j * 16 + lr;
+      bfr[j] = *reinterpret_cast<const bf16x8*>(xl + swz(row, ks * 4 + lk));
+    }
+#pragma unroll
+    for (int i = 0; i < FI; ++i)
+#pragma unroll
+      for (int j = 0; j < FJ; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+
+template <bool INT4, int EPI, bool OUT_F32>
+__global__ void __launch_bounds__(NTHR, 1) gemm_pm_kernel(GemmArgs a) {
+  extern __shared__ __align__(16) uint16_t lds[];
+  // LDS: W tiles [2][BN][BK] then x tiles [2][BM][BK]
+#define WL(buf) (lds + (buf) * (BN * BK))
+#define XL(buf) (lds + 2 * BN * BK + (buf) * (BM * BK))
+
+  // ---- tile assignment (XCD-contiguous runs, grouped token-major order)
+  const int ntiles = gridDim.x;
+  int lin = blockIdx.x;
+  if ((ntiles & 7) == 0) lin = (blockIdx.x & 7) * (ntiles >> 3) + (blockIdx.x >> 3);
+  const int tiles_m = 2 * a.tiles_m_half;
+  const int per_group = GROUP_M * a.tiles_n;
+  const int grp = lin / per_group;
+  const int first_m = grp * GROUP_M;
+  const int gsz = min(GROUP_M, tiles_m - first_m);
+  const int tm = first_m + (lin % per_group) % gsz;
+  const int tn = (lin % per_group) / gsz;
+  const int half = tm / a.tiles_m_half;
+  const int64_t m0 = (int64_t)(tm % a.tiles_m_half) * BM;
+  const int64_t n0 = (int64_t)tn * BN;
+  const bool plus = half == 0;
+  const uint16_t* xh = a.x + (int64_t)half * a.T * a.K;
+  const uint16_t* ph = a.p ? a.p + (int64_t)half * a.T * a.r : nullptr;
+
+  const int wave = threadIdx.x >> 6;
+  const int wn0 = (wave % WAVES_N) * WN;
+  const int wm0 = (wave / WAVES_N) * WM;
+
+  floatx4 acc[FI][FJ];
+#pragma unroll
+  for (int i = 0; i < FI; ++i)
+#pragma unroll
+    for (int j = 0; j < FJ; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = (int)(a.K / BK);
+  uint4 ws[4], xs[4];
+  load_main<INT4>(a, n0, xh, m0, a.T, 0, ws, xs);
+  store_main<INT4>(WL(0), XL(0), ws, xs);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int nxt = kt + 1;
+    if (nxt < nk) load_main<INT4>(a, n0, xh, m0, a.T, nxt, ws, xs);
+    mfma_tile(WL(kt & 1), XL(kt & 1), wn0, wm0, 2, acc);
+    if (nxt < nk) store_main<INT4>(WL(nxt & 1), XL(nxt & 1), ws, xs);
+    __syncthreads();
+  }
+  // correction block: [p[h] | C + s eps Z], 64 coefficient columns per tile
+  for (int tt = 0; tt < a.n_tail; ++tt) {
+    load_tail(a, n0, ph, m0, a.T, plus, tt, ws, xs);
+    store_tail(WL(tt & 1), XL(tt & 1), ws, xs);
+    __syncthreads();
+    const int rem = a.r - tt * 64;
+    mfma_tile(WL(tt & 1), XL(tt & 1), wn0, wm0, rem >= 64 ? 2 : (rem + 31) / 32, acc);
+  }
+
+#undef WL
+#undef XL
+  // ---- epilogue: bias, residual, activation, one rounding, vector stores
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15, lk = lane >> 4;
+  const int64_t nout = (EPI == ZOACT_EPI_SWIGLU) ? a.N / 2 : a.N;
+#pragma unroll
+  for (int j = 0; j < FJ; ++j) {
+    const int64_t m = m0 + wm0 + j * 16 + lr;
+    if (m >= a.T) continue;
+    const int64_t row = (int64_t)half * a.T + m;
+    if (EPI == ZOACT_EPI_SWIGLU) {
+#pragma unroll
+      for (int i = 0; i < FI; i += 2) {
+        const int64_t ng = n0 + wn0 + i * 16 + lk * 4;  // fused gate row
+        if (ng >= a.N) continue;
+        const int64_t f = (ng >> 5) * 16 + (ng & 31);  // output feature
+        float o[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float g = acc[i][j][q], u = acc[i + 1][j][q];
+          if (a.bias) {
+            g += bf2f(a.bias[ng + q]);
+            u += bf2f(a.bias[ng + 16 + q]);
+          }
+          o[q] = silu(g) * u;
+        }
+        if (a.resid) {
+          const ushort4 rv = *reinterpret_cast<const ushort4*>(a.resid + row * nout + f);
+          o[0] += bf2f(rv.x); o[1] += bf2f(rv.y); o[2] += bf2f(rv.z); o[3] += bf2f(rv.w);
+        }
+        if (OUT_F32) *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.y) + row * nout + f) = make_float4(o[0], o[1], o[2], o[3]);
+        else *reinterpret_cast<ushort4*>(reinterpret_cast<uint16_t*>(a.y) + row * nout + f) = make_ushort4(f2bf(o[0]), f2bf(o[1]), f2bf(o[2]), f2bf(o[3]));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < FI; ++i) {
+        const int64_t n = n0 + wn0 + i * 16 + lk * 4;
+        if (n >= a.N) continue;
+        float o[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          o[q] = acc[i][j][q];
+          if (a.bias) o[q] += bf2f(a.bias[n + q]);
+        }
+        if (a.resid) {
+          const ushort4 rv = *reinterpret_cast<const ushort4*>(a.resid + row * nout + n);
+          o[0] += bf2f(rv.x); o[1] += bf2f(rv.y); o[2] += bf2f(rv.z); o[3] += bf2f(rv.w);
+        }
+        if (EPI == ZOACT_EPI_RELU) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) o[q] = fmaxf(o[q], 0.0f);
+        }
+        if (OUT_F32) *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.y) + row * nout + n) = make_float4(o[0], o[1], o[2], o[3]);
+        else *reinterpret_cast<ushort4*>(reinterpret_cast<uint16_t*>(a.y) + row * nout + n) = make_ushort4(f2bf(o[0]), f2bf(o[1]), f2bf(o[2]), f2bf(o[3]));
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ fp32 path
+// Plain fp32 SIMT tile (64 x 64 outputs, 256 threads, 4 x 4 per thread) for the
+// fp32 mode of small models; the correction block is appended as extra depth.
+struct GemmArgsF32 {
+  const float* x;
+  const float* w;
+  const float* bias;
+  const float* p;
+  const float* c;
+  const float* resid;
+  float* y;
+  int64_t T, N, K;
+  int32_t r;
+  int64_t coef_offset;
+  uint64_t seed;
+  uint32_t step, query;
+  float eps;
+  int32_t tiles_m_half;
+};
+
+// Column q of thread tx covers tile feature (tx/8)*32 + (tx%8)*2 + (q&1) + (q>>1)*16,
+// so each thread holds a gate row (q = 0, 1) and the up row 16 later (q = 2, 3) of the
+// interleaved gate|up layout.
+__device__ __forceinline__ int f32_col(int tx, int q) { return (tx >> 3) * 32 + (tx & 7) * 2 + (q & 1) + (q >> 1) * 16; }
+
+template <int EPI>
+__global__ void __launch_bounds__(256) gemm_pm_f32_kernel(GemmArgsF32 a) {
+  __shared__ float xs[16][65];
+  __shared__ float wsh[16][65];
+  const int tm = blockIdx.y;
+  const int half = tm / a.tiles_m_half;
+  const int64_t m0 = (int64_t)(tm % a.tiles_m_half) * 64;
+  const int64_t n0 = (int64_t)blockIdx.x * 64;
+  const bool plus = half == 0;
+  const float* xh = a.x + (int64_t)half * a.T * a.K;
+  const float* ph = a.p ? a.p + (int64_t)half * a.T * a.r : nullptr;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  float acc[4][4] = {};
+  const int64_t ktot = a.K + a.r;
+  for (int64_t k0 = 0; k0 < ktot; k0 += 16) {
+    for (int i = threadIdx.x; i < 16 * 64; i += 256) {
+      const int kk = i & 15, rr = i >> 4;
+      const int64_t k = k0 + kk;
+      const int64_t m = m0 + rr, n = n0 + rr;
+      float xv = 0.f, wv = 0.f;
+      if (k < a.K) {
+        if (m < a.T) xv = xh[m * a.K + k];
+        if (n < a.N) wv = a.w[n * a.K + k];
+      } else if (k < ktot) {
+        const int64_t i2 = k - a.K;
+        if (m < a.T) xv = ph[m * a.r + i2];
+        if (n < a.N) {
+#pragma clang fp contract(off)
+          const int64_t e = a.coef_offset + n * a.r + i2;
+          const float z = rng::gauss_at(a.seed, a.step, a.query, (uint64_t)e);
+          const float ez = a.eps * z;
+          wv = plus ? a.c[e] + ez : a.c[e] - ez;
+        }
+      }
+      xs[kk][rr] = xv;
+      wsh[kk][rr] = wv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float xr[4], wr[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        xr[q] = xs[kk][ty * 4 + q];
+        wr[q] = wsh[kk][f32_col(tx, q)];
+      }
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[p][q] += xr[p] * wr[q];
+    }
+    __syncthreads();
+  }
+  const int64_t nout = (EPI == ZOACT_EPI_SWIGLU) ? a.N / 2 : a.N;
+  for (int p = 0; p < 4; ++p) {
+    const int64_t m = m0 + ty * 4 + p;
+    if (m >= a.T) continue;
+    const int64_t row = (int64_t)half * a.T + m;
+    if (EPI == ZOACT_EPI_SWIGLU) {
+      for (int q = 0; q < 2; ++q) {
+        const int64_t ng = n0 + f32_col(tx, q);
+        if (ng >= a.N) continue;
+        const float g = acc[p][q] + (a.bias ? a.bias[ng] : 0.f);
+        const float u = acc[p][q + 2] + (a.bias ? a.bias[ng + 16] : 0.f);
+        const int64_t f = (ng >> 5) * 16 + (ng & 31);
+        float o = (g / (1.0f + __expf(-g))) * u;
+        if (a.resid) o += a.resid[row * nout + f];
+        a.y[row * nout + f] = o;
+      }
+    } else {
+      for (int q = 0; q < 4; ++q) {
+        const int64_t n = n0 + f32_col(tx, q);
+        if (n >= a.N) continue;
+        float o = acc[p][q] + (a.bias ? a.bias[n] : 0.f);
+        if (a.resid) o += a.resid[row * nout + n];
+        if (EPI == ZOACT_EPI_RELU) o = fmaxf(o, 0.f);
+        a.y[row * nout + n] = o;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ projection
+// p = x U for x [n_tok][d_in], U^T [r][d_in]: HBM-bound (r FLOP per byte of x).
+// One wave owns 32 tokens and all r columns; x fragments are read straight from
+// global memory (each lane 16 bytes of one row per depth step), U^T fragments from
+// L2, and the contraction runs on v_mfma_f32_16x16x32_bf16.
+constexpr int PROJ_TOK = 32;
+
+template <int RB>
+__global__ void __launch_bounds__(256) project_bf16_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ ut,
+                                                          uint16_t* __restrict__ p, int64_t n_tok, int64_t d, int r) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t t0 = wave * PROJ_TOK;
+  if (t0 >= n_tok) return;
+  const int lr = lane & 15, lk = lane >> 4;
+  floatx4 acc[2][RB];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < RB; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  int64_t rows[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    int64_t t = t0 + i * 16 + lr;
+    rows[i] = t < n_tok ? t : n_tok - 1;
+  }
+  const bf16x8 zero8 = {};
+  for (int64_t k = 0; k < d; k += 32) {
+    bf16x8 a[2], b[RB];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) a[i] = *reinterpret_cast<const bf16x8*>(x + rows[i] * d + k + lk * 8);
+#pragma unroll
+    for (int j = 0; j < RB; ++j) {
+      const int rc = j * 16 + lr;
+      b[j] = rc < r ? *reinterpret_cast<const bf16x8*>(ut + (int64_t)rc * d + k + lk * 8) : zero8;
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < RB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  }
+  // D[token = 4*lk + q][col = lr] of each 16 x 16 block
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < RB; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t t = t0 + i * 16 + lk * 4 + q;
+        const int col = j * 16 + lr;
+        if (t < n_tok && col < r) p[t * r + col] = f2bf(acc[i][j][q]);
+      }
+}
+
+__global__ void project_f32_kernel(const float* x, const float* ut, float* p, int64_t n_tok, int64_t d, int r) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_tok * r; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t t = i / r;
+    const int c = (int)(i % r);
+    float s = 0.f;
+    for (int64_t k = 0; k < d; ++k) s += x[t * d + k] * ut[(int64_t)c * d + k];
+    p[i] = s;
+  }
+}
+
+template <bool INT4, int EPI, bool OUT_F32>
+hipError_t launch_bf16(const GemmArgs& a, dim3 grid, hipStream_t s) {
+  const size_t lds = (size_t)2 * (BN + BM) * BK * sizeof(uint16_t);
+  static bool attr_set = false;  // benign race: every thread sets the same value
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_pm_kernel<INT4, EPI, OUT_F32>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  gemm_pm_kernel<INT4, EPI, OUT_F32><<<grid, dim3(NTHR), lds, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
+                            const void* p, const void* residual, uint32_t flags, const zoact_pert& pert, void* y,
+                            int32_t y_dtype, hipStream_t s) {
+  const int epi = (flags & ZOACT_EPI_SWIGLU) ? ZOACT_EPI_SWIGLU : (flags & ZOACT_EPI_RELU) ? ZOACT_EPI_RELU : 0;
+  if (x_dtype == ZOACT_F32) {
+    GemmArgsF32 a{};
+    a.x = static_cast<const float*>(x);
+    a.w = static_cast<const float*>(L.w);
+    a.bias = static_cast<const float*>(L.bias);
+    a.p = static_cast<const float*>(p);
+    a.c = (L.r > 0) ? static_cast<const float*>(A->c) : nullptr;
+    a.T = T;
+    a.N = L.d_out;
+    a.K = L.d_in;
+    a.r = L.r;
+    a.coef_offset = L.coef_offset;
+    a.seed = pert.seed;
+    a.step = pert.step;
+    a.query = pert.query;
+    a.eps = pert.eps;
+    a.tiles_m_half = (int32_t)((T + 63) / 64);
+    dim3 grid((unsigned)((L.d_out + 63) / 64), (unsigned)(2 * a.tiles_m_half));
+    a.resid = static_cast<const float*>(residual);
+    a.y = static_cast<float*>(y);
+    if (epi == ZOACT_EPI_SWIGLU) gemm_pm_f32_kernel<ZOACT_EPI_SWIGLU><<<grid, dim3(256), 0, s>>>(a);
+    else if (epi == ZOACT_EPI_RELU) gemm_pm_f32_kernel<ZOACT_EPI_RELU><<<grid, dim3(256), 0, s>>>(a);
+    else gemm_pm_f32_kernel<0><<<grid, dim3(256), 0, s>>>(a);
+    return hipGetLastError();
+  }
+
+  GemmArgs a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.w = L.w;
+  a.wsc = static_cast<const uint16_t*>(L.w_scales);
+  a.bias = static_cast<const uint16_t*>(L.bias);
+  a.p = static_cast<const uint16_t*>(p);
+  a.c = (L.r > 0 && A) ? A->c : nullptr;
+  a.resid = static_cast<const uint16_t*>(residual);
+  a.y = y;
+  a.T = T;
+  a.N = L.d_out;
+  a.K = L.d_in;
+  a.r = L.r;
+  a.c_bf16 = (A && A->c_dtype == ZOACT_BF16) ? 1 : 0;
+  a.coef_offset = L.coef_offset;
+  a.seed = pert.seed;
+  a.step = pert.step;
+  a.query = pert.query;
+  a.eps = pert.eps;
+  a.tiles_m_half = (int32_t)((T + BM - 1) / BM);
+  a.tiles_n = (int32_t)((L.d_out + BN - 1) / BN);
+  a.n_tail = (L.r + 63) / 64;
+  const dim3 grid((unsigned)(2 * a.tiles_m_half * a.tiles_n));
+  const bool i4 = L.w_dtype == ZOACT_INT4_G128;
+  const bool of = y_dtype == ZOACT_F32;
+#define ZO_DISPATCH(I4, EP, OF) \
+  if (i4 == I4 && epi == EP && of == OF) return launch_bf16<I4, EP, OF>(a, grid, s);
+  ZO_DISPATCH(false, 0, false)
+  ZO_DISPATCH(false, 0, true)
+  ZO_DISPATCH(false, ZOACT_EPI_SWIGLU, false)
+  ZO_DISPATCH(false, ZOACT_EPI_RELU, false)
+  ZO_DISPATCH(true, 0, false)
+  ZO_DISPATCH(true, 0, true)
+  ZO_DISPATCH(true, ZOACT_EPI_SWIGLU, false)
+  ZO_DISPATCH(true, ZOACT_EPI_RELU, false)
+#undef ZO_DISPATCH
+  return hipErrorNotSupported;
+}
+
+hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut, int32_t r, void* p,
+                          hipStream_t s) {
+  if (dtype == ZOACT_F32) {
+    int64_t g = (n_tok * r + 255) / 256;
+    if (g > 65535) g = 65535;
+    project_f32_kernel<<<dim3((unsigned)g), dim3(256), 0, s>>>(static_cast<const float*>(x),
+                                                               static_cast<const float*>(ut), static_cast<float*>(p),
+                                                               n_tok, d_in, r);
+    return hipGetLastError();
+  }
+  const int64_t waves = (n_tok + PROJ_TOK - 1) / PROJ_TOK;
+  const dim3 grid((unsigned)((waves + 3) / 4));
+  const uint16_t* xx = static_cast<const uint16_t*>(x);
+  const uint16_t* uu = static_cast<const uint16_t*>(ut);
+  uint16_t* pp = static_cast<uint16_t*>(p);
+  const int rb = (r + 15) / 16;
+  switch (rb) {
+    case 1: project_bf16_kernel<1><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
+    case 2: project_bf16_kernel<2><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
+    case 3: project_bf16_kernel<3><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
+    case 4: project_bf16_kernel<4><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
+    case 8: project_bf16_kernel<8><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
+    case 16: project_bf16_kernel<16><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
+    default: {
+      // pad the column-block count up to the next instantiated size
+      const int rbp = rb <= 8 ? 8 : 16;
+      if (rbp == 8) project_bf16_kernel<8><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r);
+      else project_bf16_kernel<16><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r);
+    }
+  }
+  return hipGetLastError();
+}
+
+}  // namespace zoact

@@ -1,0 +1,174 @@
+// Z materialisation (test hook) and the ZO-Adam / ZO-SGD update over the arena.
+//
+// Algorithm 2: after the perturbed losses, the estimate g_B = a Z (a from the loss
+// difference) drives an optimiser step on every coefficient matrix B_l; Section 5
+// and Appendix B use Adam (weight decay 0) or SGD.  The two-sided form here uses
+// a = (L+ - L-) / (2 eps) and regenerates the same Z the forward used.
+//
+// The update is HBM-bound: per coefficient it reads c, m, v and writes them back
+// (24 bytes with fp32 C, 20 with bf16 C).  One thread owns one Philox counter
+// block (4 consecutive arena indices, one Philox call) and moves them with
+// 16-byte (8-byte for bf16 C) vector accesses; the arithmetic is fp32, one
+// rounding per operation, in a fixed order.
+#include "common.hpp"
+#include "rng.hpp"
+
+namespace zoact {
+
+namespace {
+
+__global__ void gen_z_kernel(uint64_t seed, uint32_t step, uint32_t query, int64_t e0, int64_t n, float* out) {
+  const int64_t b0 = e0 >> 2;
+  const int64_t b1 = (e0 + n - 1) >> 2;
+  for (int64_t b = b0 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b <= b1;
+       b += (int64_t)gridDim.x * blockDim.x) {
+    const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
+#pragma unroll
+    for (int l = 0; l < 4; ++l) {
+      const int64_t e = 4 * b + l;
+      if (e >= e0 && e < e0 + n) out[e - e0] = rng::lane_of(z, l);
+    }
+  }
+}
+
+__device__ __forceinline__ float projected_grad(const float* loss_pm, float eps) {
+#pragma clang fp contract(off)
+  const float lp = loss_pm[0], lm = loss_pm[1];
+  return (lp - lm) / (eps + eps);
+}
+
+struct AdamConst {
+  float b1, b2, eps, wd, step_size, isb2, omb1, omb2;
+};
+
+__device__ __forceinline__ float adam_one(float c, float& m, float& v, float gh, const AdamConst& h) {
+#pragma clang fp contract(off)
+  if (h.wd != 0.0f) gh = gh + h.wd * c;
+  m = h.b1 * m + h.omb1 * gh;
+  v = h.b2 * v + h.omb2 * (gh * gh);
+  const float d = __builtin_sqrtf(v) * h.isb2 + h.eps;
+  return c - h.step_size * (m / d);
+}
+
+template <bool BF16C>
+__global__ void __launch_bounds__(256) adam_kernel(void* __restrict__ cptr, float* __restrict__ mptr,
+                                                   float* __restrict__ vptr, int64_t k, const float* loss_pm,
+                                                   uint64_t seed, uint32_t step, uint32_t query, float eps,
+                                                   AdamConst h, uint32_t* status) {
+#pragma clang fp contract(off)
+  const float g = projected_grad(loss_pm, eps);
+  if (!__builtin_isfinite(g)) {
+    if (status != nullptr && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, 1u);
+    return;
+  }
+  const int64_t nb = (k + 3) >> 2;
+  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb; b += (int64_t)gridDim.x * blockDim.x) {
+    const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
+    const int64_t e = 4 * b;
+    if (e + 4 <= k) {
+      float4 m4 = *reinterpret_cast<const float4*>(mptr + e);
+      float4 v4 = *reinterpret_cast<const float4*>(vptr + e);
+      float c0, c1, c2, c3;
+      if (BF16C) {
+        const ushort4 cb = *reinterpret_cast<const ushort4*>(reinterpret_cast<const uint16_t*>(cptr) + e);
+        c0 = bf2f(cb.x); c1 = bf2f(cb.y); c2 = bf2f(cb.z); c3 = bf2f(cb.w);
+      } else {
+        const float4 cf = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(cptr) + e);
+        c0 = cf.x; c1 = cf.y; c2 = cf.z; c3 = cf.w;
+      }
+      c0 = adam_one(c0, m4.x, v4.x, g * z.x, h);
+      c1 = adam_one(c1, m4.y, v4.y, g * z.y, h);
+      c2 = adam_one(c2, m4.z, v4.z, g * z.z, h);
+      c3 = adam_one(c3, m4.w, v4.w, g * z.w, h);
+      *reinterpret_cast<float4*>(mptr + e) = m4;
+      *reinterpret_cast<float4*>(vptr + e) = v4;
+      if (BF16C) {
+        *reinterpret_cast<ushort4*>(reinterpret_cast<uint16_t*>(cptr) + e) =
+            make_ushort4(f2bf(c0), f2bf(c1), f2bf(c2), f2bf(c3));
+      } else {
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(cptr) + e) = make_float4(c0, c1, c2, c3);
+      }
+    } else {
+      for (int l = 0; l < 4 && e + l < k; ++l) {
+        float m = mptr[e + l], v = vptr[e + l];
+        float c = BF16C ? bf2f(reinterpret_cast<const uint16_t*>(cptr)[e + l])
+                        : reinterpret_cast<const float*>(cptr)[e + l];
+        c = adam_one(c, m, v, g * rng::lane_of(z, l), h);
+        mptr[e + l] = m;
+        vptr[e + l] = v;
+        if (BF16C) reinterpret_cast<uint16_t*>(cptr)[e + l] = f2bf(c);
+        else reinterpret_cast<float*>(cptr)[e + l] = c;
+      }
+    }
+  }
+}
+
+template <bool BF16C>
+__global__ void __launch_bounds__(256) sgd_kernel(void* __restrict__ cptr, int64_t k, const float* loss_pm,
+                                                  uint64_t seed, uint32_t step, uint32_t query, float eps, float lr,
+                                                  uint32_t* status) {
+#pragma clang fp contract(off)
+  const float g = projected_grad(loss_pm, eps);
+  if (!__builtin_isfinite(g)) {
+    if (status != nullptr && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, 1u);
+    return;
+  }
+  const int64_t nb = (k + 3) >> 2;
+  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb; b += (int64_t)gridDim.x * blockDim.x) {
+    const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
+    for (int l = 0; l < 4 && 4 * b + l < k; ++l) {
+      const int64_t e = 4 * b + l;
+      const float gh = g * rng::lane_of(z, l);
+      if (BF16C) {
+        uint16_t* c = reinterpret_cast<uint16_t*>(cptr);
+        c[e] = f2bf(bf2f(c[e]) - lr * gh);
+      } else {
+        float* c = reinterpret_cast<float*>(cptr);
+        c[e] = c[e] - lr * gh;
+      }
+    }
+  }
+}
+
+int64_t grid_for(int64_t blocks_of_four) {
+  int64_t g = (blocks_of_four + 255) / 256;
+  return g < 1 ? 1 : (g > (1 << 20) ? (1 << 20) : g);
+}
+
+}  // namespace
+
+hipError_t launch_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e0, int64_t n, float* out,
+                        hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int64_t nb = ((e0 + n - 1) >> 2) - (e0 >> 2) + 1;
+  gen_z_kernel<<<dim3((unsigned)grid_for(nb)), dim3(256), 0, s>>>(seed, step, query, e0, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_adam(const zoact_arena& A, const float* loss_pm, const zoact_pert& p, const zoact_adam& h,
+                       uint32_t* status, hipStream_t s) {
+  if (A.k == 0) return hipSuccess;
+  const AdamConst c{h.beta1, h.beta2, h.eps, h.weight_decay, h.step_size, h.inv_sqrt_bc2, h.one_minus_beta1,
+                    h.one_minus_beta2};
+  const dim3 grid((unsigned)grid_for((A.k + 3) >> 2));
+  if (A.c_dtype == ZOACT_BF16)
+    adam_kernel<true><<<grid, dim3(256), 0, s>>>(A.c, A.m, A.v, A.k, loss_pm, p.seed, p.step, p.query, p.eps, c,
+                                                 status);
+  else
+    adam_kernel<false><<<grid, dim3(256), 0, s>>>(A.c, A.m, A.v, A.k, loss_pm, p.seed, p.step, p.query, p.eps, c,
+                                                  status);
+  return hipGetLastError();
+}
+
+hipError_t launch_sgd(const zoact_arena& A, const float* loss_pm, const zoact_pert& p, float lr, uint32_t* status,
+                      hipStream_t s) {
+  if (A.k == 0) return hipSuccess;
+  const dim3 grid((unsigned)grid_for((A.k + 3) >> 2));
+  if (A.c_dtype == ZOACT_BF16)
+    sgd_kernel<true><<<grid, dim3(256), 0, s>>>(A.c, A.k, loss_pm, p.seed, p.step, p.query, p.eps, lr, status);
+  else
+    sgd_kernel<false><<<grid, dim3(256), 0, s>>>(A.c, A.k, loss_pm, p.seed, p.step, p.query, p.eps, lr, status);
+  return hipGetLastError();
+}
+
+}  // namespace zoact

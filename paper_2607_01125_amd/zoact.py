@@ -1,0 +1,246 @@
+"""Thin Python binding of libzoact.so (the C ABI declared in include/zoact.h).
+
+Argument marshalling only: every function here checks Python-side types, passes
+device pointers of torch tensors and the current HIP stream to the C entry point
+of the same name, and raises ZoactError on a non-zero status.  All computation
+happens in the library's HIP kernels; nothing falls back to the CPU.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libzoact.so")
+
+F32, BF16, INT4_G128 = 0, 1, 2
+EPI_NONE, EPI_SWIGLU, EPI_RELU = 0, 1, 2
+OK, E_INVALID, E_UNSUPPORTED, E_HIP, E_NOCONVERGE, E_WORKSPACE = range(6)
+
+
+class ZoactError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"zoact status {status}: {msg}")
+        self.status = status
+
+
+class Pert(ctypes.Structure):
+    _fields_ = [("seed", ctypes.c_uint64), ("step", ctypes.c_uint32), ("query", ctypes.c_uint32),
+                ("eps", ctypes.c_float)]
+
+
+class LinearDesc(ctypes.Structure):
+    _fields_ = [("w_dtype", ctypes.c_int32), ("w", ctypes.c_void_p), ("w_scales", ctypes.c_void_p),
+                ("bias", ctypes.c_void_p), ("ut", ctypes.c_void_p), ("d_in", ctypes.c_int64),
+                ("d_out", ctypes.c_int64), ("r", ctypes.c_int32), ("coef_offset", ctypes.c_int64)]
+
+
+class ArenaDesc(ctypes.Structure):
+    _fields_ = [("c_dtype", ctypes.c_int32), ("c", ctypes.c_void_p), ("m", ctypes.c_void_p),
+                ("v", ctypes.c_void_p), ("k", ctypes.c_int64)]
+
+
+class AdamDesc(ctypes.Structure):
+    _fields_ = [("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
+                ("weight_decay", ctypes.c_float), ("step_size", ctypes.c_float),
+                ("inv_sqrt_bc2", ctypes.c_float), ("one_minus_beta1", ctypes.c_float),
+                ("one_minus_beta2", ctypes.c_float)]
+
+
+class EigOpts(ctypes.Structure):
+    _fields_ = [("oversample", ctypes.c_int32), ("iters", ctypes.c_int32), ("seed", ctypes.c_uint64)]
+
+
+_P = ctypes.c_void_p
+_I32, _I64, _U32, _U64, _F = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float
+_SZ = ctypes.c_size_t
+
+SIGNATURES = {
+    "zoact_version": ([], ctypes.c_char_p),
+    "zoact_status_str": ([_I32], ctypes.c_char_p),
+    "zoact_last_error": ([], ctypes.c_char_p),
+    "zoact_gen_z": ([_U64, _U32, _U32, _I64, _I64, _P, _P], _I32),
+    "zoact_project": ([_P, _I32, _I64, _I64, _P, _I32, _P, _P], _I32),
+    "zoact_linear_fwd_pm": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I32, _I64, _P, _P, _U32,
+                             ctypes.POINTER(Pert), _P, _I32, _P], _I32),
+    "zoact_loss_workspace_bytes": ([], _SZ),
+    "zoact_mse_pm": ([_P, _I32, _P, _I64, _I64, _P, _P, _SZ, _P], _I32),
+    "zoact_xent_pm": ([_P, _P, _I64, _I64, _I64, _P, _P, _SZ, _P], _I32),
+    "zoact_step": ([ctypes.POINTER(ArenaDesc), _P, ctypes.POINTER(Pert), ctypes.POINTER(AdamDesc), _P, _P], _I32),
+    "zoact_step_sgd": ([ctypes.POINTER(ArenaDesc), _P, ctypes.POINTER(Pert), _F, _P, _P], _I32),
+    "zoact_basis_workspace_bytes": ([_I64, _I32, ctypes.POINTER(EigOpts)], _SZ),
+    "zoact_gram": ([_P, _I32, _I64, _I64, _P, _I32, _P], _I32),
+    "zoact_basis_from_gram": ([_P, _I64, _I32, ctypes.POINTER(EigOpts), _P, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
+    "zoact_basis_init": ([_P, _I32, _I64, _I64, _I32, ctypes.POINTER(EigOpts), _P, _I32, _P, _P, _P, _P, _SZ, _P],
+                         _I32),
+}
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built (no CPU fallback exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_01125_amd.build`")
+        h = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in SIGNATURES.items():
+            f = getattr(h, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = h
+    return _lib
+
+
+def _check(st: int):
+    if st != OK:
+        raise ZoactError(st, lib().zoact_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise ValueError(f"unsupported activation dtype {t.dtype}")
+
+
+@dataclass
+class Linear:
+    """Device tensors of one adapted layer (w: [d_out][d_in] or packed int4 [d_out][d_in/2])."""
+    w: torch.Tensor
+    d_in: int
+    d_out: int
+    r: int = 0
+    ut: torch.Tensor | None = None
+    coef_offset: int = 0
+    bias: torch.Tensor | None = None
+    w_scales: torch.Tensor | None = None
+
+    def desc(self) -> LinearDesc:
+        wd = INT4_G128 if self.w.dtype == torch.uint8 else dtype_code(self.w)
+        return LinearDesc(wd, self.w.data_ptr(), self.w_scales.data_ptr() if self.w_scales is not None else None,
+                          self.bias.data_ptr() if self.bias is not None else None,
+                          self.ut.data_ptr() if self.ut is not None else None, self.d_in, self.d_out, self.r,
+                          self.coef_offset)
+
+
+@dataclass
+class Arena:
+    """Flat coefficient arena C and Adam moments m, v (all [k])."""
+    c: torch.Tensor
+    m: torch.Tensor
+    v: torch.Tensor
+
+    @property
+    def k(self) -> int:
+        return self.c.numel()
+
+    def desc(self) -> ArenaDesc:
+        return ArenaDesc(dtype_code(self.c), self.c.data_ptr(), self.m.data_ptr(), self.v.data_ptr(), self.k)
+
+
+def version() -> str:
+    return lib().zoact_version().decode()
+
+
+def gen_z(seed: int, step: int, query: int, e0: int, n: int, out: torch.Tensor, stream=None):
+    _check(lib().zoact_gen_z(seed, step, query, e0, n, _ptr(out), _stream(stream)))
+
+
+def project(x: torch.Tensor, ut: torch.Tensor, p: torch.Tensor, stream=None):
+    d_in = x.shape[-1]
+    n_tok = x.numel() // d_in
+    _check(lib().zoact_project(_ptr(x), dtype_code(x), n_tok, d_in, _ptr(ut), ut.shape[0], _ptr(p), _stream(stream)))
+
+
+def linear_fwd_pm(layer: Linear, arena: Arena | None, x: torch.Tensor, T: int, p: torch.Tensor | None,
+                  y: torch.Tensor, pert: Pert, residual: torch.Tensor | None = None, flags: int = 0, stream=None):
+    d = layer.desc()
+    a = arena.desc() if arena is not None else None
+    _check(lib().zoact_linear_fwd_pm(ctypes.byref(d), ctypes.byref(a) if a is not None else None, _ptr(x),
+                                     dtype_code(x), T, _ptr(p), _ptr(residual), flags, ctypes.byref(pert), _ptr(y),
+                                     dtype_code(y), _stream(stream)))
+
+
+def loss_workspace_bytes() -> int:
+    return int(lib().zoact_loss_workspace_bytes())
+
+
+def mse_pm(y: torch.Tensor, target: torch.Tensor, loss_pm: torch.Tensor, ws: torch.Tensor, stream=None):
+    T, N = target.shape
+    _check(lib().zoact_mse_pm(_ptr(y), dtype_code(y), _ptr(target), T, N, _ptr(loss_pm), _ptr(ws), ws.numel() *
+                              ws.element_size(), _stream(stream)))
+
+
+def xent_pm(logits: torch.Tensor, tokens: torch.Tensor, loss_pm: torch.Tensor, ws: torch.Tensor, stream=None):
+    B, S = tokens.shape
+    V = logits.shape[-1]
+    _check(lib().zoact_xent_pm(_ptr(logits), _ptr(tokens), B, S, V, _ptr(loss_pm), _ptr(ws),
+                               ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def step(arena: Arena, loss_pm: torch.Tensor, pert: Pert, adam: AdamDesc, status: torch.Tensor | None = None,
+         stream=None):
+    a = arena.desc()
+    _check(lib().zoact_step(ctypes.byref(a), _ptr(loss_pm), ctypes.byref(pert), ctypes.byref(adam), _ptr(status),
+                            _stream(stream)))
+
+
+def step_sgd(arena: Arena, loss_pm: torch.Tensor, pert: Pert, lr: float, status: torch.Tensor | None = None,
+             stream=None):
+    a = arena.desc()
+    _check(lib().zoact_step_sgd(ctypes.byref(a), _ptr(loss_pm), ctypes.byref(pert), lr, _ptr(status),
+                                _stream(stream)))
+
+
+def basis_workspace_bytes(d: int, r: int, opts: EigOpts | None = None) -> int:
+    return int(lib().zoact_basis_workspace_bytes(d, r, ctypes.byref(opts) if opts is not None else None))
+
+
+def gram(x: torch.Tensor, g: torch.Tensor, accumulate: bool = False, stream=None):
+    n_tok, d = x.shape
+    _check(lib().zoact_gram(_ptr(x), dtype_code(x), n_tok, d, _ptr(g), int(accumulate), _stream(stream)))
+
+
+def basis_from_gram(g: torch.Tensor, r: int, ut: torch.Tensor, ws: torch.Tensor, opts: EigOpts | None = None,
+                    ut_master=None, eigvals=None, resid=None, stream=None):
+    d = g.shape[0]
+    _check(lib().zoact_basis_from_gram(_ptr(g), d, r, ctypes.byref(opts) if opts is not None else None, _ptr(ut),
+                                       dtype_code(ut), _ptr(ut_master), _ptr(eigvals), _ptr(resid), _ptr(ws),
+                                       ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def basis_init(x: torch.Tensor, r: int, ut: torch.Tensor, ws: torch.Tensor, opts: EigOpts | None = None,
+               ut_master=None, eigvals=None, resid=None, stream=None):
+    n_tok, d = x.shape
+    _check(lib().zoact_basis_init(_ptr(x), dtype_code(x), n_tok, d, r, ctypes.byref(opts) if opts is not None
+                                  else None, _ptr(ut), dtype_code(ut), _ptr(ut_master), _ptr(eigvals), _ptr(resid),
+                                  _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def adam_desc(lr: float, t: int, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+              weight_decay: float = 0.0) -> AdamDesc:
+    """Host-side Adam scalars for step t (float64, then one rounding to fp32 by ctypes)."""
+    if t < 1:
+        raise ValueError("Adam step t starts at 1")
+    return AdamDesc(beta1, beta2, eps, weight_decay, lr / (1.0 - beta1 ** t), 1.0 / math.sqrt(1.0 - beta2 ** t),
+                    1.0 - beta1, 1.0 - beta2)

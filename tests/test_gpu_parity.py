@@ -1,0 +1,368 @@
+"""GPU parity: every hot-path kernel against the CPU oracle on the same seeded inputs.
+
+Bars: Z, indices and the Adam update under teacher forcing bit-exact; bf16
+outputs within one bf16 ulp plus an fp32-summation term (gpu_helpers); fp32-mode
+outputs and losses within 1e-4 relative; bf16-mode losses within 2e-2 relative.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import adam as oadam
+from oracle import basis as obasis
+from oracle import linear as olin
+from oracle import loss as oloss
+from oracle import rng as orng
+from oracle.numerics import rne_bf16
+from paper_2607_01125_amd import zoact as Z
+
+from gpu_helpers import (announce, assert_bf16_close, assert_rel_close, dev, host, t_bf16, t_f32, t_i32, t_u8)
+
+pytestmark = pytest.mark.gpu
+
+
+# ------------------------------------------------------------------ Z
+@pytest.mark.parametrize("seed,step,query,e0,n", [
+    (0, 1, 0, 0, 1 << 22),
+    (2024, 7, 3, 5, 1_000_003),
+    (2**63 + 11, 2**32 - 1, 1, 2**32 - 1000, 5000),
+    (42, 3, 0, 44_040_192 - 4099, 4099),
+])
+def test_gen_z_bit_exact(seed, step, query, e0, n):
+    announce("gen_z", seed, step, query, e0, n)
+    out = torch.empty(n, dtype=torch.float32, device=dev())
+    Z.gen_z(seed, step, query, e0, n, out)
+    got = out.cpu().numpy()
+    want = orng.gauss_range(seed, step, query, e0, n)
+    np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+# ------------------------------------------------------------------ Adam / SGD
+@pytest.mark.parametrize("c_bf16", [False, True])
+@pytest.mark.parametrize("k", [4, 100_003, 1 << 20])
+def test_adam_teacher_forced_bitwise(c_bf16, k):
+    announce("adam", c_bf16, k)
+    r = np.random.default_rng(k)
+    c = r.standard_normal(k).astype(np.float32) * 0.01
+    if c_bf16:
+        c = rne_bf16(c)
+    m = (r.standard_normal(k) * 1e-3).astype(np.float32)
+    v = np.abs(r.standard_normal(k) * 1e-5).astype(np.float32)
+    lp, lm = np.float32(2.3456), np.float32(2.3441)
+    seed, step, eps = 99, 5, 1e-3
+    hp = oadam.adam_scalars(5e-5, step)
+    g = oadam.projected_grad(lp, lm, eps)
+    z = orng.gauss_range(seed, step, 0, 0, k)
+    c1, m1, v1, st = oadam.zo_adam(c, m, v, g, z, hp, c_bf16=c_bf16)
+    ct = t_bf16(c) if c_bf16 else t_f32(c)
+    arena = Z.Arena(ct, t_f32(m), t_f32(v))
+    loss = t_f32(np.array([lp, lm]))
+    status = torch.zeros(1, dtype=torch.int32, device=dev())
+    Z.step(arena, loss, Z.Pert(seed, step, 0, eps), Z.adam_desc(5e-5, step), status)
+    np.testing.assert_array_equal(arena.m.cpu().numpy().view(np.uint32), m1.view(np.uint32))
+    np.testing.assert_array_equal(arena.v.cpu().numpy().view(np.uint32), v1.view(np.uint32))
+    np.testing.assert_array_equal(arena.c.float().cpu().numpy().view(np.uint32), c1.view(np.uint32))
+    assert int(status.item()) == 0
+
+
+def test_adam_nonfinite_guard():
+    announce("adam nonfinite")
+    k = 1000
+    c = np.ones(k, np.float32)
+    arena = Z.Arena(t_f32(c), t_f32(c * 0), t_f32(c * 0))
+    status = torch.zeros(1, dtype=torch.int32, device=dev())
+    Z.step(arena, t_f32(np.array([np.inf, 1.0])), Z.Pert(1, 1, 0, 1e-3), Z.adam_desc(1e-3, 1), status)
+    assert int(status.item()) & 1
+    np.testing.assert_array_equal(arena.c.cpu().numpy(), c)
+
+
+def test_sgd_bitwise():
+    announce("sgd")
+    k = 70_001
+    c = (np.random.default_rng(0).standard_normal(k) * 0.01).astype(np.float32)
+    arena = Z.Arena(t_f32(c), t_f32(c * 0), t_f32(c * 0))
+    lp, lm = np.float32(1.5), np.float32(1.25)
+    Z.step_sgd(arena, t_f32(np.array([lp, lm])), Z.Pert(3, 2, 0, 1e-3), 3e-6)
+    want, _ = oadam.zo_sgd(c, oadam.projected_grad(lp, lm, 1e-3), orng.gauss_range(3, 2, 0, 0, k), 3e-6)
+    np.testing.assert_array_equal(arena.c.cpu().numpy().view(np.uint32), want.view(np.uint32))
+
+
+# ------------------------------------------------------------------ projection
+@pytest.mark.parametrize("n_tok,d,r", [(1000, 512, 32), (77, 256, 8), (2048, 1024, 64), (33, 128, 1)])
+def test_project_bf16(n_tok, d, r):
+    announce("project bf16", n_tok, d, r)
+    x = synth.bf16_round(synth.normal((n_tok, d), 1.0, 1, n_tok))
+    ut = synth.bf16_round(synth.normal((r, d), 1.0 / np.sqrt(d), 2, d))
+    p = torch.empty(n_tok, r, dtype=torch.bfloat16, device=dev())
+    Z.project(t_bf16(x), t_bf16(ut), p)
+    assert_bf16_close(host(p), olin.project(x, ut, "bf16"), what="project")
+
+
+def test_project_f32():
+    announce("project f32")
+    x = synth.normal((300, 128), 1.0, 1, 1)
+    ut = synth.normal((8, 128), 0.1, 2, 2)
+    p = torch.empty(300, 8, dtype=torch.float32, device=dev())
+    Z.project(t_f32(x), t_f32(ut), p)
+    ref = olin.project(x, ut, "fp32")
+    assert np.max(np.abs(host(p) - ref)) <= 1e-5 * np.sqrt(np.mean(ref**2))
+
+
+# ------------------------------------------------------------------ fused +/- linear
+def _layer_inputs(T, K, N, r, seed, bias=True, int4=False):
+    x = synth.bf16_round(synth.normal((2, T, K), 1.0, seed, 1))
+    x[1] = synth.bf16_round(x[0] + synth.normal((T, K), 0.05, seed, 9))  # halves differ slightly
+    w = synth.bf16_round(synth.normal((N, K), 0.02, seed, 2))
+    b = synth.bf16_round(synth.normal((N,), 0.1, seed, 3)) if bias else None
+    ut = synth.bf16_round(np.linalg.qr(synth.normal((K, max(r, 1)), 1.0, seed, 4))[0][:, :r].T.astype(np.float32)) if r else None
+    packed = scales = None
+    if int4:
+        packed, scales = synth.quantize_int4_g128(w)
+    return x, w, b, ut, packed, scales
+
+
+def _run_gpu_linear(x, w, b, ut, c_arena, off, r, eps, seed, step, T, K, N, flags=0, resid=None, packed=None,
+                    scales=None, c_bf16=False, out_f32=False):
+    xt = t_bf16(x.reshape(2 * T, K))
+    p = None
+    if r:
+        p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev())
+        Z.project(xt, t_bf16(ut), p)
+    if packed is not None:
+        layer = Z.Linear(t_u8(packed), K, N, r, t_bf16(ut) if r else None, off, t_bf16(b) if b is not None else None,
+                         t_bf16(scales))
+    else:
+        layer = Z.Linear(t_bf16(w), K, N, r, t_bf16(ut) if r else None, off, t_bf16(b) if b is not None else None)
+    arena = None
+    if r:
+        ct = t_bf16(c_arena) if c_bf16 else t_f32(c_arena)
+        arena = Z.Arena(ct, torch.zeros_like(ct, dtype=torch.float32), torch.zeros_like(ct, dtype=torch.float32))
+    nout = N // 2 if flags & Z.EPI_SWIGLU else N
+    y = torch.full((2 * T, nout), float("nan"), dtype=torch.float32 if out_f32 else torch.bfloat16, device=dev())
+    rt = t_bf16(resid.reshape(2 * T, nout)) if resid is not None else None
+    Z.linear_fwd_pm(layer, arena, xt, T, p, y, Z.Pert(seed, step, 0, eps), residual=rt, flags=flags)
+    return host(y).reshape(2, T, nout)
+
+
+def _oracle_linear(x, w, b, ut, c, off, r, eps, seed, step, flags=0, resid=None, round_out=True):
+    z = olin.z_block(seed, step, 0, off, w.shape[0], r) if r else None
+    outs = []
+    for h, sign in ((0, 1), (1, -1)):
+        y = olin.adapted_linear(x[h], w, b, ut, c, z, eps, sign, "bf16", round_out=False)
+        if flags & Z.EPI_SWIGLU:
+            n = w.shape[0]
+            f = np.arange(n // 2)
+            gi = (f // 16) * 32 + (f % 16)
+            g, u = y[:, gi], y[:, gi + 16]
+            y = g / (1.0 + np.exp(-g)) * u
+        if resid is not None:
+            y = y + resid[h]
+        if flags & Z.EPI_RELU:
+            y = np.maximum(y, 0.0)
+        outs.append(rne_bf16(y.astype(np.float32)).astype(np.float64) if round_out else y)
+    return np.stack(outs)
+
+
+@pytest.mark.parametrize("T,K,N,r,off", [
+    (300, 512, 336, 32, 0),
+    (257, 256, 512, 8, 12),
+    (64, 384, 256, 64, 6),
+    (500, 256, 272, 80, 3),
+    (1, 128, 16, 32, 0),
+])
+def test_linear_pm_bf16(T, K, N, r, off):
+    announce("linear_pm bf16", T, K, N, r, off)
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=T + K)
+    k = off + N * r + 5
+    c = synth.normal((k,), 0.01, 7, T)
+    eps, seed, step = 1e-3, 1234, 3
+    got = _run_gpu_linear(x, w, b, ut, c, off, r, eps, seed, step, T, K, N)
+    ref = _oracle_linear(x, w, b, ut, c[off:off + N * r].reshape(N, r), off, r, eps, seed, step)
+    assert_bf16_close(got, ref, what="linear_pm")
+
+
+def test_linear_pm_zero_coeffs_reproduce_base_and_determinism():
+    announce("linear_pm base")
+    T, K, N, r = 200, 256, 256, 32
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=5)
+    x[1] = x[0]
+    c = np.zeros(N * r, np.float32)
+    got = _run_gpu_linear(x, w, b, ut, c, 0, r, 0.0, 1, 1, T, K, N)
+    base = _run_gpu_linear(x, w, b, None, None, 0, 0, 0.0, 1, 1, T, K, N)
+    np.testing.assert_array_equal(got[0], got[1])
+    np.testing.assert_array_equal(got, base)
+    ref = rne_bf16((x[0].astype(np.float64) @ w.astype(np.float64).T + b).astype(np.float32))
+    assert_bf16_close(got[0], ref, what="base")
+    again = _run_gpu_linear(x, w, b, ut, c, 0, r, 0.0, 1, 1, T, K, N)
+    np.testing.assert_array_equal(got, again)
+
+
+@pytest.mark.parametrize("flags", [Z.EPI_SWIGLU, Z.EPI_RELU])
+def test_linear_pm_epilogues_with_residual(flags):
+    announce("linear_pm epilogue", flags)
+    T, K, N, r = 130, 256, 512, 32
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=11, bias=False)
+    c = synth.normal((N * r,), 0.02, 8, 8)
+    nout = N // 2 if flags & Z.EPI_SWIGLU else N
+    resid = synth.bf16_round(synth.normal((2, T, nout), 0.5, 9, 9))
+    got = _run_gpu_linear(x, w, None, ut, c, 0, r, 1e-2, 5, 2, T, K, N, flags=flags, resid=resid)
+    ref = _oracle_linear(x, w, None, ut, c.reshape(N, r), 0, r, 1e-2, 5, 2, flags=flags, resid=resid)
+    assert_bf16_close(got, ref, atol_rel_rms=2e-3, what="epilogue")
+
+
+@pytest.mark.parametrize("c_bf16", [False, True])
+def test_linear_pm_int4(c_bf16):
+    announce("linear_pm int4", c_bf16)
+    T, K, N, r = 200, 512, 384, 32
+    x, w, b, ut, packed, scales = _layer_inputs(T, K, N, r, seed=21, bias=False, int4=True)
+    c = synth.normal((N * r,), 0.02, 4, 4)
+    if c_bf16:
+        c = rne_bf16(c)
+    got = _run_gpu_linear(x, w, None, ut, c, 0, r, 1e-3, 9, 4, T, K, N, packed=packed, scales=scales, c_bf16=c_bf16)
+    wq = olin.dequant_int4(packed, scales)
+    ref = _oracle_linear(x, wq, None, ut, c.reshape(N, r), 0, r, 1e-3, 9, 4)
+    assert_bf16_close(got, ref, what="int4")
+
+
+def test_linear_pm_r0_fp32_logits():
+    announce("linear_pm logits")
+    T, K, N = 100, 256, 528
+    x, w, _, _, _, _ = _layer_inputs(T, K, N, 0, seed=31, bias=False)
+    got = _run_gpu_linear(x, w, None, None, None, 0, 0, 0.0, 1, 1, T, K, N, out_f32=True)
+    ref = np.stack([x[h].astype(np.float64) @ w.astype(np.float64).T for h in range(2)])
+    assert np.max(np.abs(got - ref)) <= 1e-5 * np.sqrt(np.mean(ref**2)) * 10
+
+
+def test_linear_pm_fp32_mode():
+    announce("linear_pm fp32")
+    T, K, N, r = 70, 128, 96, 8
+    x = synth.normal((2, T, K), 1.0, 3, 1)
+    w = synth.normal((N, K), 0.02, 3, 2)
+    b = synth.normal((N,), 0.1, 3, 3)
+    ut = np.linalg.qr(synth.normal((K, r), 1.0, 3, 4))[0].T.astype(np.float32)
+    c = synth.normal((N * r,), 0.01, 3, 5)
+    xt = t_f32(x.reshape(2 * T, K))
+    p = torch.empty(2 * T, r, dtype=torch.float32, device=dev())
+    Z.project(xt, t_f32(ut), p)
+    layer = Z.Linear(t_f32(w), K, N, r, t_f32(ut), 0, t_f32(b))
+    ct = t_f32(c)
+    arena = Z.Arena(ct, torch.zeros_like(ct), torch.zeros_like(ct))
+    y = torch.empty(2 * T, N, dtype=torch.float32, device=dev())
+    Z.linear_fwd_pm(layer, arena, xt, T, p, y, Z.Pert(8, 1, 0, 1e-3))
+    ref = olin.adapted_linear_pm(x, w, b, ut, c.reshape(N, r), 1e-3, 8, 1, 0, 0, "fp32")
+    got = host(y).reshape(2, T, N)
+    assert np.max(np.abs(got - ref)) <= 1e-4 * np.max(np.abs(ref))
+    # the +/- difference is the rank-r perturbation 2 eps (xU) Z^T (fp32 rounding aside)
+    dz = got[0] - got[1] - ((x[0] - x[1]) @ w.T.astype(np.float64))
+    zz = olin.z_block(8, 1, 0, 0, N, r).astype(np.float64)
+    want = (x[0] @ ut.T.astype(np.float64)) @ (c.reshape(N, r) + 1e-3 * zz).T - \
+           (x[1] @ ut.T.astype(np.float64)) @ (c.reshape(N, r) - 1e-3 * zz).T
+    assert np.max(np.abs(dz - want)) <= 1e-4 * np.max(np.abs(ref))
+
+
+# ------------------------------------------------------------------ losses
+@pytest.mark.parametrize("bf16", [False, True])
+def test_mse_pm(bf16):
+    announce("mse", bf16)
+    T, N = 1000, 300
+    y = synth.normal((2, T, N), 1.0, 1, 1)
+    t = synth.normal((T, N), 1.0, 1, 2)
+    if bf16:
+        y, t = synth.bf16_round(y), synth.bf16_round(t)
+    mk = t_bf16 if bf16 else t_f32
+    loss = torch.empty(2, dtype=torch.float32, device=dev())
+    ws = torch.empty(Z.loss_workspace_bytes(), dtype=torch.uint8, device=dev())
+    Z.mse_pm(mk(y.reshape(2 * T, N)), mk(t), loss, ws)
+    got = host(loss)
+    assert_rel_close(got, [oloss.mse(y[0], t), oloss.mse(y[1], t)], 1e-5, "mse")
+
+
+def test_xent_pm():
+    announce("xent")
+    B, S, V = 3, 17, 1000
+    lg = synth.normal((2, B, S, V), 2.0, 4, 1)
+    tok = synth.uniform_tokens(B, S, V, 4, 2)
+    loss = torch.empty(2, dtype=torch.float32, device=dev())
+    ws = torch.empty(Z.loss_workspace_bytes(), dtype=torch.uint8, device=dev())
+    Z.xent_pm(t_f32(lg.reshape(-1, V)), t_i32(tok), loss, ws)
+    assert_rel_close(host(loss), [oloss.next_token_ce(lg[0], tok), oloss.next_token_ce(lg[1], tok)], 1e-5, "xent")
+    # uniform logits give ln V
+    Z.xent_pm(torch.zeros(2 * B * S, V, device=dev()), t_i32(tok), loss, ws)
+    assert_rel_close(host(loss), [np.log(V)] * 2, 1e-6, "xent uniform")
+
+
+# ------------------------------------------------------------------ basis (Algorithm 1)
+def _gapped_x(t, d, r, seed):
+    rr = np.random.default_rng(seed)
+    q, _ = np.linalg.qr(rr.standard_normal((d, d)))
+    sv = np.concatenate([np.linspace(30, 12, r), np.linspace(4, 0.5, d - r)])
+    a, _ = np.linalg.qr(rr.standard_normal((t, d)))
+    return ((a * sv) @ q.T * np.sqrt(t / d)).astype(np.float32)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_gram(bf16):
+    announce("gram", bf16)
+    x = synth.normal((1000, 256), 1.0, 2, 2)
+    if bf16:
+        x = synth.bf16_round(x)
+    g = torch.empty(256, 256, dtype=torch.float32, device=dev())
+    Z.gram(t_bf16(x) if bf16 else t_f32(x), g)
+    ref = obasis.gram(x)
+    assert np.max(np.abs(host(g) - ref)) <= 1e-5 * np.max(np.abs(ref))
+    Z.gram(t_bf16(x) if bf16 else t_f32(x), g, accumulate=True)
+    assert np.max(np.abs(host(g) - 2 * ref)) <= 2e-5 * np.max(np.abs(ref))
+
+
+@pytest.mark.parametrize("d,r,bf16", [(128, 8, False), (256, 8, True), (512, 32, True)])
+def test_basis_init_matches_oracle(d, r, bf16):
+    announce("basis", d, r, bf16)
+    x = _gapped_x(2 * d, d, r, seed=d + r)
+    if bf16:
+        x = synth.bf16_round(x)
+    u_ref, lam_ref = obasis.basis_init(x, r)
+    ut = torch.empty(r, d, dtype=torch.bfloat16 if bf16 else torch.float32, device=dev())
+    master = torch.empty(r, d, dtype=torch.float32, device=dev())
+    ev = torch.empty(r, dtype=torch.float32, device=dev())
+    res = torch.empty(1, dtype=torch.float32, device=dev())
+    ws = torch.empty(d * d * 4 + Z.basis_workspace_bytes(d, r), dtype=torch.uint8, device=dev())
+    Z.basis_init(t_bf16(x) if bf16 else t_f32(x), r, ut, ws, ut_master=master, eigvals=ev, resid=res)
+    um = host(master).T
+    assert np.max(np.abs(um.T @ um - np.eye(r))) <= 1e-5
+    assert obasis.overlap(um, u_ref) >= 1 - 1e-6
+    assert_rel_close(host(ev), lam_ref, 1e-4, "eigenvalues")
+    assert np.max(np.abs(um - u_ref)) <= 1e-4          # same canonical sign
+    assert float(host(res)[0]) <= 1e-5
+    if bf16:
+        np.testing.assert_array_equal(host(ut), rne_bf16(host(master)))
+
+
+# ------------------------------------------------------------------ full single-layer workload, sampled
+def test_single_layer_4096_sampled():
+    """d_in = d_out = 4096, r = 32, 8192 tokens per half, planted low-rank x:
+    sampled output rows of both halves against the oracle, plus the losses."""
+    announce("single layer 4096 sampled")
+    T, K, N, r = 8192, 4096, 4096, 32
+    x, q = synth.planted_lowrank(T, K, seed=0)
+    x = synth.bf16_round(x)
+    w = synth.bf16_round(synth.normal((N, K), 0.02, 0, 2))
+    ut = synth.bf16_round(q[:, :r].T.copy())
+    c = synth.normal((N * r,), 0.01, 0, 3)
+    eps, seed, step = 1e-3, 77, 1
+    xt = t_bf16(np.stack([x, x]).reshape(2 * T, K))
+    p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev())
+    Z.project(xt, t_bf16(ut), p)
+    layer = Z.Linear(t_bf16(w), K, N, r, t_bf16(ut), 0)
+    ct = t_f32(c)
+    arena = Z.Arena(ct, torch.zeros_like(ct), torch.zeros_like(ct))
+    y = torch.empty(2 * T, N, dtype=torch.bfloat16, device=dev())
+    Z.linear_fwd_pm(layer, arena, xt, T, p, y, Z.Pert(seed, step, 0, eps))
+    rows = np.random.default_rng(0).choice(T, 24, replace=False)
+    rows = np.concatenate([rows, [0, T - 1]])
+    yh = host(y).reshape(2, T, N)
+    xs = x[rows]
+    ref = _oracle_linear(np.stack([xs, xs]), w, None, ut, c.reshape(N, r), 0, r, eps, seed, step)
+    assert_bf16_close(yh[:, rows], ref, what="single layer sampled")
+    # P rows as well
+    assert_bf16_close(host(p)[rows], olin.project(xs, ut, "bf16"), what="P sampled")
