@@ -1,0 +1,66 @@
+// Argument block and small device helpers shared by the fused +/- GEMM kernels.
+#pragma once
+#include "common.hpp"
+#include "rng.hpp"
+
+namespace zoact {
+namespace gemm {
+
+struct GemmArgs {
+  const uint16_t* x;      // [2][T][K]
+  const void* w;          // [N][K] bf16 or packed int4 [N][K/2]
+  const uint16_t* wsc;    // int4 scales [N][K/128]
+  const uint16_t* bias;   // [N] or null
+  const uint16_t* p;      // [2][T][r]
+  const void* c;          // arena coefficients
+  const uint16_t* resid;  // [2][T][Nout] or null
+  void* y;                // [2][T][Nout]
+  int64_t T, N, K;
+  int32_t r;
+  int32_t c_bf16;
+  int64_t coef_offset;
+  uint64_t seed;
+  uint32_t step, query;
+  float eps;
+  int32_t tiles_m_half;  // token tiles per half
+  int32_t tiles_n;
+  int32_t n_tail;        // depth tiles of the correction block
+};
+
+__device__ __forceinline__ int swz(int row, int kc) { return (row << 6) + ((kc ^ (row & 7)) << 3); }
+
+// Four consecutive Z values starting at arena index e (any alignment).
+__device__ __forceinline__ float4 gauss4(uint64_t seed, uint32_t step, uint32_t query, uint64_t e) {
+  const float4 a = rng::gauss_block(seed, step, query, e >> 2);
+  const int o = (int)(e & 3);
+  if (o == 0) return a;
+  const float4 b = rng::gauss_block(seed, step, query, (e >> 2) + 1);
+  float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  return make_float4(v[o], v[o + 1], v[o + 2], v[o + 3]);
+}
+
+// fp32 (C + sign*eps*z) rounded to bf16; the product eps*z is rounded before the sum.
+__device__ __forceinline__ uint16_t perturbed_bf16(float c, float z, float eps, bool plus) {
+#pragma clang fp contract(off)
+  const float ez = eps * z;
+  return f2bf(plus ? c + ez : c - ez);
+}
+
+__device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) { return (uint32_t)lo | ((uint32_t)hi << 16); }
+
+// Dequantise 8 nibbles (one uint32, element 2j in the low nibble of byte j) with scale s.
+__device__ __forceinline__ uint4 dequant8(uint32_t q, float s) {
+  uint16_t o[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int v = ((int)(q << (28 - 4 * j))) >> 28;  // sign-extend nibble j
+    o[j] = f2bf((float)v * s);
+  }
+  return make_uint4(pack2(o[0], o[1]), pack2(o[2], o[3]), pack2(o[4], o[5]), pack2(o[6], o[7]));
+}
+
+
+__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+
+}  // namespace gemm
+}  // namespace zoact

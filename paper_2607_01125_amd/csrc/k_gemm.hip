@@ -32,12 +32,15 @@
 //    the linear id is first regrouped so that each XCD receives a contiguous run of
 //    tiles, and runs are ordered in groups of 4 token tiles x all feature tiles to
 //    keep both operands L2-resident.
-#include "common.hpp"
-#include "rng.hpp"
+#include <stdlib.h>
+
+#include "gemm_common.hpp"
 
 namespace zoact {
 
 namespace {
+
+using namespace gemm;
 
 constexpr int BN = 256;  // features per tile (MFMA rows)
 constexpr int BM = 256;  // tokens per tile (MFMA columns)
@@ -50,59 +53,6 @@ constexpr int WM = BM / WAVES_M;  // 64 tokens per wave
 constexpr int FI = WN / 16;       // 8 MFMA blocks along features
 constexpr int FJ = WM / 16;       // 4 MFMA blocks along tokens
 constexpr int GROUP_M = 4;
-
-struct GemmArgs {
-  const uint16_t* x;      // [2][T][K]
-  const void* w;          // [N][K] bf16 or packed int4 [N][K/2]
-  const uint16_t* wsc;    // int4 scales [N][K/128]
-  const uint16_t* bias;   // [N] or null
-  const uint16_t* p;      // [2][T][r]
-  const void* c;          // arena coefficients
-  const uint16_t* resid;  // [2][T][Nout] or null
-  void* y;                // [2][T][Nout]
-  int64_t T, N, K;
-  int32_t r;
-  int32_t c_bf16;
-  int64_t coef_offset;
-  uint64_t seed;
-  uint32_t step, query;
-  float eps;
-  int32_t tiles_m_half;  // token tiles per half
-  int32_t tiles_n;
-  int32_t n_tail;        // depth tiles of the correction block
-};
-
-__device__ __forceinline__ int swz(int row, int kc) { return (row << 6) + ((kc ^ (row & 7)) << 3); }
-
-// Four consecutive Z values starting at arena index e (any alignment).
-__device__ __forceinline__ float4 gauss4(uint64_t seed, uint32_t step, uint32_t query, uint64_t e) {
-  const float4 a = rng::gauss_block(seed, step, query, e >> 2);
-  const int o = (int)(e & 3);
-  if (o == 0) return a;
-  const float4 b = rng::gauss_block(seed, step, query, (e >> 2) + 1);
-  float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-  return make_float4(v[o], v[o + 1], v[o + 2], v[o + 3]);
-}
-
-// fp32 (C + sign*eps*z) rounded to bf16; the product eps*z is rounded before the sum.
-__device__ __forceinline__ uint16_t perturbed_bf16(float c, float z, float eps, bool plus) {
-#pragma clang fp contract(off)
-  const float ez = eps * z;
-  return f2bf(plus ? c + ez : c - ez);
-}
-
-__device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) { return (uint32_t)lo | ((uint32_t)hi << 16); }
-
-// Dequantise 8 nibbles (one uint32, element 2j in the low nibble of byte j) with scale s.
-__device__ __forceinline__ uint4 dequant8(uint32_t q, float s) {
-  uint16_t o[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int v = ((int)(q << (28 - 4 * j))) >> 28;  // sign-extend nibble j
-    o[j] = f2bf((float)v * s);
-  }
-  return make_uint4(pack2(o[0], o[1]), pack2(o[2], o[3]), pack2(o[4], o[5]), pack2(o[6], o[7]));
-}
 
 template <bool INT4>
 __device__ __forceinline__ void load_main(const GemmArgs& a, int64_t n0, const uint16_t* xh, int64_t m0, int64_t T,
@@ -236,7 +186,6 @@ __device__ __forceinline__ void mfma_tile(const uint16_t* wl, const uint16_t* xl
   }
 }
 
-__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
 template <bool INT4, int EPI, bool OUT_F32>
 __global__ void __launch_bounds__(NTHR, 1) gemm_pm_kernel(GemmArgs a) {
@@ -539,7 +488,24 @@ hipError_t launch_bf16(const GemmArgs& a, dim3 grid, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Schedule of the bf16 fused GEMM: 0 = four-wave pipelined (default, fastest measured),
+// 1 = eight-wave ping-pong, 2 = generic.  ZOACT_GEMM_SCHEDULE selects one for A/B
+// measurements; the generic kernel is the fallback for shapes outside the others' coverage.
+int schedule_choice() {
+  static const int v = [] {
+    const char* e = getenv("ZOACT_GEMM_SCHEDULE");
+    if (e == nullptr) return 0;
+    if (e[0] == '1') return 1;
+    if (e[0] == '2') return 2;
+    return 0;
+  }();
+  return v;
+}
+
 }  // namespace
+
+hipError_t launch_linear_pm_pp(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
+hipError_t launch_linear_pm_4w(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
 
 hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
                             const void* p, const void* residual, uint32_t flags, const zoact_pert& pert, void* y,
@@ -596,6 +562,15 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
   const dim3 grid((unsigned)(2 * a.tiles_m_half * a.tiles_n));
   const bool i4 = L.w_dtype == ZOACT_INT4_G128;
   const bool of = y_dtype == ZOACT_F32;
+  const int sched = schedule_choice();
+  if (sched == 0) {
+    const hipError_t e = launch_linear_pm_4w(a, L.w_dtype, epi, of, s);
+    if (e != hipErrorNotSupported) return e;
+  }
+  if (sched <= 1) {
+    const hipError_t e = launch_linear_pm_pp(a, L.w_dtype, epi, of, s);
+    if (e != hipErrorNotSupported) return e;
+  }
 #define ZO_DISPATCH(I4, EP, OF) \
   if (i4 == I4 && epi == EP && of == OF) return launch_bf16<I4, EP, OF>(a, grid, s);
   ZO_DISPATCH(false, 0, false)

@@ -1,0 +1,404 @@
+// Fused +/- adapted GEMM, four-wave software-pipelined schedule for gfx950
+// (bf16 weights, 0 <= r <= 64, r % 8 == 0).
+//
+// Same contraction as the other kernels: y[h] = x[h] W^T + b + p[h] (C + s_h eps Z)^T
+// (Section 3, factored perturbed forward), over a 256-feature x 256-token tile.
+//
+//  * One wave per SIMD, each owning a 128 x 128 sub-tile: 64 fp32 accumulator blocks of
+//    v_mfma_f32_16x16x32_bf16 (256 accumulator registers).  A wave reads 16 fragments per
+//    32-deep step for 64 MFMAs, a quarter of a fragment per MFMA, which keeps the CU's LDS
+//    traffic (about 128 bytes per clock) well below what the matrix cores consume.
+//  * The fragments of step s + 1 are read from LDS while the 64 MFMAs of step s issue
+//    (double-buffered fragment registers), so the matrix core never waits on LDS latency.
+//  * Global -> LDS by the direct path (buffer_load_dwordx4 ... lds, 1 KB per instruction),
+//    four 32 KB stages (W + x, 32-deep) in flight; stage s + 4 is issued at the start of
+//    step s into the stage step s has just vacated, so each load has about three steps to
+//    land.  The XOR swizzle (16-byte chunk c of row r at chunk c ^ ((r >> 1) & 3)) is
+//    applied on the global side.  Buffer descriptors bound both matrices: rows past the
+//    end read as 0.  One workgroup barrier per step.
+//  * C_h = bf16(C + s_h eps Z) for the tile's 256 features is generated in the prologue,
+//    while the first stages are in flight, into a dedicated 32 KB LDS region; the rank-r
+//    correction runs as one or two extra 32-deep steps against p[h] read from global memory.
+#include "gemm_common.hpp"
+
+namespace zoact {
+
+namespace {
+
+using namespace gemm;
+
+constexpr int NT = 256;
+constexpr int OP_ELEMS = 256 * 32;               // one operand tile (bf16 elements, 16 KB)
+constexpr int STAGE_ELEMS = 2 * OP_ELEMS;        // W + x
+constexpr int NSTAGE = 4;
+constexpr int CH_ELEMS = 256 * 64;               // C_h region, 64 coefficient columns per feature
+constexpr int LDS_BYTES = (NSTAGE * STAGE_ELEMS + CH_ELEMS) * 2;  // 160 KB
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// s_waitcnt immediates (gfx9 encoding: vmcnt[3:0,15:14], expcnt[6:4], lgkmcnt[11:8])
+constexpr int WAIT_VM0 = 0x0F70;
+constexpr int WAIT_VM8 = 0x0F78;
+constexpr int WAIT_VM16 = 0x4F70;
+constexpr int WAIT_LGKM0 = 0xC07F;
+constexpr int WAIT_ALL0 = 0x0070;
+
+__device__ __forceinline__ void barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Element offset of (row, 16-byte chunk c) in a 32-deep operand tile (rows of 64 bytes).
+__device__ __forceinline__ int swz32(int row, int c) { return (row << 5) + ((c ^ ((row >> 1) & 3)) << 3); }
+
+// One 1 KB DMA run: rows row0 .. row0+15, depth k0 .. k0+31 -> LDS at dst.
+__device__ __forceinline__ void dma_run(__amdgpu_buffer_rsrc_t src, int64_t ld, int64_t row0, int64_t k0,
+                                        uint16_t* dst) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = row0 + (lane >> 2);
+  const int c = (lane & 3) ^ ((lane >> 3) & 3);
+  const int off = (int)((row * ld + k0 + c * 8) * 2);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void_t*)dst, 16, off, 0, 0, 0);
+}
+
+template <int EPI, bool OUT_F32, bool HAS_R>
+__global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
+  extern __shared__ __align__(16) uint16_t lds[];
+
+  // ---- tile assignment (XCD-contiguous runs, grouped token-major order)
+  const int ntiles = gridDim.x;
+  int lin = blockIdx.x;
+  if ((ntiles & 7) == 0) lin = (blockIdx.x & 7) * (ntiles >> 3) + (blockIdx.x >> 3);
+  const int tiles_m = 2 * a.tiles_m_half;
+  const int per_group = 4 * a.tiles_n;
+  const int grp_t = lin / per_group;
+  const int first_m = grp_t * 4;
+  const int gsz = min(4, tiles_m - first_m);
+  const int tm = first_m + (lin % per_group) % gsz;
+  const int tn = (lin % per_group) / gsz;
+  const int half = tm / a.tiles_m_half;
+  const int64_t m0 = (int64_t)(tm % a.tiles_m_half) * 256;
+  const int64_t n0 = (int64_t)tn * 256;
+  const bool plus = half == 0;
+  const uint16_t* xh = a.x + (int64_t)half * a.T * a.K;
+  const uint16_t* w = reinterpret_cast<const uint16_t*>(a.w);
+
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15, lk = lane >> 4;
+  const int wn0 = (wave & 1) * 128;   // features of this wave
+  const int wm0 = (wave >> 1) * 128;  // tokens of this wave
+  const int S = (int)(a.K >> 5);      // 32-deep steps
+
+  // ---- C_h chunks (4 coefficients each), coefficient bits loaded before any DMA
+  const int gmax = a.r <= 32 ? 8 : 16;
+  const int qn = HAS_R ? (256 * gmax) / NT : 0;  // 8 or 16 chunks per thread
+  uint32_t cbits[16][4];
+  {
+    const int esize = a.c_bf16 ? 2 : 4;
+    const __amdgpu_buffer_rsrc_t crs =
+        buffer_rsrc(static_cast<const char*>(a.c) + a.coef_offset * esize, (uint32_t)(a.N * a.r * esize));
+    int base[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int c = q * NT + threadIdx.x;
+      const int f = c / gmax, g = c % gmax;
+      const int64_t n = n0 + f;
+      const bool valid = HAS_R && q < qn && 4 * g < a.r && n < a.N;
+      base[q] = valid ? (int)((n * a.r + 4 * g) * esize) : 0x7FFFFF00;
+    }
+    if (HAS_R) {
+      if (a.c_bf16) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) cbits[q][j] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(crs, base[q] + 2 * j, 0, 0);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) cbits[q][j] = __builtin_amdgcn_raw_buffer_load_b32(crs, base[q] + 4 * j, 0, 0);
+      }
+    }
+  }
+  uint16_t* chreg = lds + NSTAGE * STAGE_ELEMS;
+  auto gen_chunk = [&](int q) {
+    const int c = q * NT + threadIdx.x;
+    const int f = c / gmax, g = c % gmax;
+    const int64_t n = n0 + f;
+    uint2 packed = make_uint2(0u, 0u);
+    if (4 * g < a.r && n < a.N) {
+      const uint64_t e = (uint64_t)(a.coef_offset + n * a.r + 4 * g);
+      const float4 z = gauss4(a.seed, a.step, a.query, e);
+      float cv[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cv[j] = a.c_bf16 ? bf2f((uint16_t)cbits[q][j]) : __uint_as_float(cbits[q][j]);
+      packed.x = pack2(perturbed_bf16(cv[0], z.x, a.eps, plus), perturbed_bf16(cv[1], z.y, a.eps, plus));
+      packed.y = pack2(perturbed_bf16(cv[2], z.z, a.eps, plus), perturbed_bf16(cv[3], z.w, a.eps, plus));
+    }
+    *reinterpret_cast<uint2*>(chreg + swz(f, g >> 1) + (g & 1) * 4) = packed;
+  };
+
+  // ---- stage DMA: each wave moves 4 W runs and 4 x runs (16 rows each) per step
+  const __amdgpu_buffer_rsrc_t wrs = buffer_rsrc(w, (uint32_t)(a.N * a.K * 2));
+  const __amdgpu_buffer_rsrc_t xrs = buffer_rsrc(xh, (uint32_t)(a.T * a.K * 2));
+  auto dma_step = [&](int st) {
+    uint16_t* dst = lds + (st & (NSTAGE - 1)) * STAGE_ELEMS + wave * 4 * 512;
+    const int64_t k0 = (int64_t)st * 32;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dma_run(wrs, a.K, n0 + wave * 64 + j * 16, k0, dst + j * 512);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dma_run(xrs, a.K, m0 + wave * 64 + j * 16, k0, dst + OP_ELEMS + j * 512);
+  };
+
+  floatx4 acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 fa0[8], fb0[8], fa1[8], fb1[8];
+
+  auto read_frags = [&](int st, bf16x8 (&fa)[8], bf16x8 (&fb)[8]) {
+    const uint16_t* sp = lds + (st & (NSTAGE - 1)) * STAGE_ELEMS;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      fa[i] = *reinterpret_cast<const bf16x8*>(sp + swz32(wn0 + i * 16 + lr, lk));
+      fb[i] = *reinterpret_cast<const bf16x8*>(sp + OP_ELEMS + swz32(wm0 + i * 16 + lr, lk));
+    }
+  };
+  // 64 MFMAs on (fa, fb) while the fragments of the next step are read into (na, nb) and
+  // the 8 DMA runs of step dma_st are issued, one after each row of 8 MFMAs, so that the
+  // CU's vector-memory path never holds the matrix core up.
+  auto step_body = [&](bf16x8 (&fa)[8], bf16x8 (&fb)[8], bf16x8 (&na)[8], bf16x8 (&nb)[8], int next_st,
+                       bool has_next, int dma_st, bool dma) {
+    const uint16_t* sp = lds + (next_st & (NSTAGE - 1)) * STAGE_ELEMS;
+    uint16_t* dst = lds + (dma_st & (NSTAGE - 1)) * STAGE_ELEMS + wave * 4 * 512;
+    const int64_t k0 = (int64_t)dma_st * 32;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      if (dma) {
+        if (i < 4) dma_run(wrs, a.K, n0 + wave * 64 + i * 16, k0, dst + i * 512);
+        else dma_run(xrs, a.K, m0 + wave * 64 + (i - 4) * 16, k0, dst + OP_ELEMS + (i - 4) * 512);
+      }
+      if (has_next) {
+        na[i] = *reinterpret_cast<const bf16x8*>(sp + swz32(wn0 + i * 16 + lr, lk));
+        nb[i] = *reinterpret_cast<const bf16x8*>(sp + OP_ELEMS + swz32(wm0 + i * 16 + lr, lk));
+      }
+    }
+  };
+
+  // ---- prologue: coefficients, stages 0..3 in flight, C_h while they land, stages 0 and
+  // 1 landed, fragments of step 0, then a barrier so that stage 0 may be refilled
+  const int npro = S < NSTAGE ? S : NSTAGE;
+  for (int st = 0; st < npro; ++st) dma_step(st);
+  if (HAS_R) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+      if (q < qn) gen_chunk(q);
+  }
+  if (npro >= 4) __builtin_amdgcn_s_waitcnt(WAIT_VM16);
+  else if (npro == 3) __builtin_amdgcn_s_waitcnt(WAIT_VM8);
+  else __builtin_amdgcn_s_waitcnt(WAIT_VM0);
+  __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
+  barrier();
+  read_frags(0, fa0, fb0);
+  __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
+  barrier();
+
+  // ---- main loop, two steps per iteration (static fragment buffers).  At the end of step
+  // s every wave has waited for the stage of step s + 2 (its own DMA two steps old), so
+  // the barrier makes stage s + 2 visible before step s + 1 reads it.
+  auto one_step = [&](int s, bf16x8 (&fa)[8], bf16x8 (&fb)[8], bf16x8 (&na)[8], bf16x8 (&nb)[8]) {
+    const bool dma = s + 4 < S;
+    step_body(fa, fb, na, nb, s + 1, s + 1 < S, s + 4, dma);
+    const bool d1 = s + 3 < S;   // DMA issued in step s - 1 still allowed in flight
+    if (dma && d1) __builtin_amdgcn_s_waitcnt(WAIT_VM16);
+    else if (dma || d1) __builtin_amdgcn_s_waitcnt(WAIT_VM8);
+    else __builtin_amdgcn_s_waitcnt(WAIT_VM0);
+    __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
+    barrier();
+  };
+  for (int s = 0; s < S; s += 2) {
+    one_step(s, fa0, fb0, fa1, fb1);
+    if (s + 1 < S) one_step(s + 1, fa1, fb1, fa0, fb0);
+  }
+
+  // ---- rank-r correction: [p[h] | C_h] as ceil(r/32) extra 32-deep steps
+  if (HAS_R) {
+    const int kts = (a.r + 31) >> 5;
+    const uint16_t* ph = a.p + (int64_t)half * a.T * a.r;
+    const bf16x8 zero8 = {};
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      if (t < kts) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          int64_t m = m0 + wm0 + j * 16 + lr;
+          m = m > a.T - 1 ? a.T - 1 : m;
+          const int col = t * 32 + lk * 8;
+          fb0[j] = col < a.r ? *reinterpret_cast<const bf16x8*>(ph + m * a.r + col) : zero8;
+          fa0[j] = *reinterpret_cast<const bf16x8*>(chreg + swz(wn0 + j * 16 + lr, t * 4 + lk));
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa0[i], fb0[j], acc[i][j], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- epilogue through LDS: each wave stages its 128 x 128 tile as fp32 in its own 32 KB
+  // slice of the (now idle) stage area, 64 tokens at a time, then applies bias, residual and
+  // activation on rows and stores 16 bytes per lane along the feature axis (one rounding).
+  __builtin_amdgcn_s_waitcnt(WAIT_ALL0);
+  barrier();
+  float* ep = reinterpret_cast<float*>(lds) + wave * (64 * 132);
+  constexpr int LDR = 132;  // padded fp32 row
+  const int64_t nout = (EPI == ZOACT_EPI_SWIGLU) ? a.N / 2 : a.N;
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int j = pass * 4 + jj;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        *reinterpret_cast<floatx4*>(ep + (jj * 16 + lr) * LDR + i * 16 + lk * 4) = acc[i][j];
+    }
+    __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
+    if (EPI == ZOACT_EPI_SWIGLU) {
+      // 64 output features per wave: lane -> chunk c = lane & 7 (8 outputs), rows lane >> 3 + 8 it
+      const int c = lane & 7;
+      const int g0 = (c >> 1) * 32 + (c & 1) * 8;           // fused gate index inside the wave
+      const int64_t ng = n0 + wn0 + g0;
+      const int64_t fo = (n0 + wn0) / 2 + c * 8;           // output feature
+      float bg[8], bu[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        bg[e] = (a.bias && ng < a.N) ? bf2f(a.bias[ng + e]) : 0.f;
+        bu[e] = (a.bias && ng < a.N) ? bf2f(a.bias[ng + 16 + e]) : 0.f;
+      }
+#pragma unroll
+      for (int it = 0; it < 8; ++it) {
+        const int tl = (lane >> 3) + 8 * it;
+        const int64_t m = m0 + wm0 + pass * 64 + tl;
+        if (m >= a.T || ng >= a.N) continue;
+        const int64_t row = (int64_t)half * a.T + m;
+        const floatx4 g_lo = *reinterpret_cast<const floatx4*>(ep + tl * LDR + g0);
+        const floatx4 g_hi = *reinterpret_cast<const floatx4*>(ep + tl * LDR + g0 + 4);
+        const floatx4 u_lo = *reinterpret_cast<const floatx4*>(ep + tl * LDR + g0 + 16);
+        const floatx4 u_hi = *reinterpret_cast<const floatx4*>(ep + tl * LDR + g0 + 20);
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          o[e] = silu(g_lo[e] + bg[e]) * (u_lo[e] + bu[e]);
+          o[e + 4] = silu(g_hi[e] + bg[e + 4]) * (u_hi[e] + bu[e + 4]);
+        }
+        if (a.resid) {
+          const uint4 rv = *reinterpret_cast<const uint4*>(a.resid + row * nout + fo);
+          const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            o[2 * e] += bf2f((uint16_t)(rw[e] & 0xFFFF));
+            o[2 * e + 1] += bf2f((uint16_t)(rw[e] >> 16));
+          }
+        }
+        if (OUT_F32) {
+          float* yp = reinterpret_cast<float*>(a.y) + row * nout + fo;
+          *reinterpret_cast<float4*>(yp) = make_float4(o[0], o[1], o[2], o[3]);
+          *reinterpret_cast<float4*>(yp + 4) = make_float4(o[4], o[5], o[6], o[7]);
+        } else {
+          *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.y) + row * nout + fo) =
+              make_uint4(pack2(f2bf(o[0]), f2bf(o[1])), pack2(f2bf(o[2]), f2bf(o[3])), pack2(f2bf(o[4]), f2bf(o[5])),
+                         pack2(f2bf(o[6]), f2bf(o[7])));
+        }
+      }
+    } else {
+      // 128 features per wave: lane -> chunk c = lane & 15 (8 features), rows lane >> 4 + 4 it
+      const int c = lane & 15;
+      const int64_t n = n0 + wn0 + c * 8;
+      float bb[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) bb[e] = (a.bias && n < a.N) ? bf2f(a.bias[n + e]) : 0.f;
+#pragma unroll
+      for (int it = 0; it < 16; ++it) {
+        const int tl = (lane >> 4) + 4 * it;
+        const int64_t m = m0 + wm0 + pass * 64 + tl;
+        if (m >= a.T || n >= a.N) continue;
+        const int64_t row = (int64_t)half * a.T + m;
+        const floatx4 v_lo = *reinterpret_cast<const floatx4*>(ep + tl * LDR + c * 8);
+        const floatx4 v_hi = *reinterpret_cast<const floatx4*>(ep + tl * LDR + c * 8 + 4);
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          o[e] = v_lo[e] + bb[e];
+          o[e + 4] = v_hi[e] + bb[e + 4];
+        }
+        if (a.resid) {
+          const uint4 rv = *reinterpret_cast<const uint4*>(a.resid + row * nout + n);
+          const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            o[2 * e] += bf2f((uint16_t)(rw[e] & 0xFFFF));
+            o[2 * e + 1] += bf2f((uint16_t)(rw[e] >> 16));
+          }
+        }
+        if (EPI == ZOACT_EPI_RELU) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = fmaxf(o[e], 0.0f);
+        }
+        if (OUT_F32) {
+          float* yp = reinterpret_cast<float*>(a.y) + row * nout + n;
+          *reinterpret_cast<float4*>(yp) = make_float4(o[0], o[1], o[2], o[3]);
+          *reinterpret_cast<float4*>(yp + 4) = make_float4(o[4], o[5], o[6], o[7]);
+        } else {
+          *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.y) + row * nout + n) =
+              make_uint4(pack2(f2bf(o[0]), f2bf(o[1])), pack2(f2bf(o[2]), f2bf(o[3])), pack2(f2bf(o[4]), f2bf(o[5])),
+                         pack2(f2bf(o[6]), f2bf(o[7])));
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
+  }
+}
+
+template <int EPI, bool OUT_F32, bool HAS_R>
+hipError_t launch_4w(const GemmArgs& a, hipStream_t s) {
+  static bool attr_set = false;  // benign race: every thread sets the same value
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_4w_kernel<EPI, OUT_F32, HAS_R>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const dim3 grid((unsigned)(2 * a.tiles_m_half * a.tiles_n));
+  gemm_4w_kernel<EPI, OUT_F32, HAS_R><<<grid, dim3(NT), LDS_BYTES, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// Returns hipErrorNotSupported outside this kernel's coverage (non-bf16 weights, r > 64,
+// r % 8 != 0, depth not a multiple of 32, a half of x or W of 2 GiB or more).
+hipError_t launch_linear_pm_4w(const GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s) {
+  if (w_dtype != ZOACT_BF16 || a.r > 64 || (a.r % 8) != 0 || (a.K % 32) != 0) return hipErrorNotSupported;
+  if (a.T * a.K * 2 >= (int64_t(1) << 31) || a.N * a.K * 2 >= (int64_t(1) << 31)) return hipErrorNotSupported;
+  // The correction-enabled instantiation also serves r = 0 (no chunks, no correction
+  // steps): it is the one whose register assignment keeps the accumulators in AGPRs.
+#define ZO_4W(EP, OF) \
+  if (epi == EP && out_f32 == OF) return launch_4w<EP, OF, true>(a, s);
+  ZO_4W(0, false)
+  ZO_4W(0, true)
+  ZO_4W(ZOACT_EPI_SWIGLU, false)
+  ZO_4W(ZOACT_EPI_RELU, false)
+#undef ZO_4W
+  return hipErrorNotSupported;
+}
+
+}  // namespace zoact

@@ -170,6 +170,9 @@ def _oracle_linear(x, w, b, ut, c, off, r, eps, seed, step, flags=0, resid=None,
     (64, 384, 256, 64, 6),
     (500, 256, 272, 80, 3),
     (1, 128, 16, 32, 0),
+    (50, 64, 64, 16, 0),
+    (300, 1024, 512, 32, 4),
+    (513, 2048, 768, 64, 0),
 ])
 def test_linear_pm_bf16(T, K, N, r, off):
     announce("linear_pm bf16", T, K, N, r, off)
