@@ -411,57 +411,74 @@ __global__ void __launch_bounds__(256) gemm_pm_f32_kernel(GemmArgsF32 a) {
 }
 
 // ------------------------------------------------------------------ projection
-// p = x U for x [n_tok][d_in], U^T [r][d_in]: HBM-bound (r FLOP per byte of x).
-// One wave owns 32 tokens and all r columns; x fragments are read straight from
-// global memory (each lane 16 bytes of one row per depth step), U^T fragments from
-// L2, and the contraction runs on v_mfma_f32_16x16x32_bf16.
+// p = x U for x [n_tok][d_in], U^T [r][d_in]: HBM-bound (r FLOP per byte of x), so the
+// design goal is to keep enough of x in flight.  A workgroup owns 32 tokens and splits the
+// depth over its 4 waves; each wave reads its x fragments straight from global memory
+// (16 bytes per lane per 32-deep step, 4 steps in flight) and U^T fragments from L2, runs
+// v_mfma_f32_16x16x32_bf16 into fp32 partials, and the 4 partials are summed in a fixed
+// order through LDS before the single rounding to bf16.
 constexpr int PROJ_TOK = 32;
 
 template <int RB>
 __global__ void __launch_bounds__(256) project_bf16_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ ut,
-                                                          uint16_t* __restrict__ p, int64_t n_tok, int64_t d, int r) {
-  const int lane = threadIdx.x & 63;
-  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int64_t t0 = wave * PROJ_TOK;
-  if (t0 >= n_tok) return;
+                                                          uint16_t* __restrict__ p, int64_t n_tok, int64_t d, int r,
+                                                          int64_t dq) {
+  __shared__ float part[4][PROJ_TOK][RB * 16 + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t t0 = (int64_t)blockIdx.x * PROJ_TOK;
   const int lr = lane & 15, lk = lane >> 4;
   floatx4 acc[2][RB];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < RB; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  int64_t rows[2];
+  const uint16_t* xr[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     int64_t t = t0 + i * 16 + lr;
-    rows[i] = t < n_tok ? t : n_tok - 1;
+    t = t < n_tok ? t : n_tok - 1;
+    xr[i] = x + t * d + lk * 8;
   }
   const bf16x8 zero8 = {};
-  for (int64_t k = 0; k < d; k += 32) {
-    bf16x8 a[2], b[RB];
+  const int64_t k_begin = (int64_t)wave * dq, k_end = k_begin + dq < d ? k_begin + dq : d;
+  for (int64_t k = k_begin; k < k_end; k += 128) {
+    bf16x8 a[4][2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) a[i] = *reinterpret_cast<const bf16x8*>(x + rows[i] * d + k + lk * 8);
+    for (int u = 0; u < 4; ++u)
 #pragma unroll
-    for (int j = 0; j < RB; ++j) {
-      const int rc = j * 16 + lr;
-      b[j] = rc < r ? *reinterpret_cast<const bf16x8*>(ut + (int64_t)rc * d + k + lk * 8) : zero8;
+      for (int i = 0; i < 2; ++i) a[u][i] = (k + u * 32 < k_end) ? *reinterpret_cast<const bf16x8*>(xr[i] + k + u * 32) : zero8;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (k + u * 32 < k_end) {
+        bf16x8 b[RB];
+#pragma unroll
+        for (int j = 0; j < RB; ++j) {
+          const int rc = j * 16 + lr;
+          b[j] = rc < r ? *reinterpret_cast<const bf16x8*>(ut + (int64_t)rc * d + k + u * 32 + lk * 8) : zero8;
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < RB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][i], b[j], acc[i][j], 0, 0, 0);
+      }
     }
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < RB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
   }
-  // D[token = 4*lk + q][col = lr] of each 16 x 16 block
+  // D[token = 4*lk + q][col = lr] of each 16 x 16 block -> LDS partials
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < RB; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t t = t0 + i * 16 + lk * 4 + q;
-        const int col = j * 16 + lr;
-        if (t < n_tok && col < r) p[t * r + col] = f2bf(acc[i][j][q]);
-      }
+      for (int q = 0; q < 4; ++q) part[wave][i * 16 + lk * 4 + q][j * 16 + lr] = acc[i][j][q];
+  __syncthreads();
+  for (int e = threadIdx.x; e < PROJ_TOK * RB * 16; e += 256) {
+    const int tl = e / (RB * 16), col = e % (RB * 16);
+    const int64_t t = t0 + tl;
+    if (t < n_tok && col < r) {
+      const float v = ((part[0][tl][col] + part[1][tl][col]) + part[2][tl][col]) + part[3][tl][col];
+      p[t * r + col] = f2bf(v);
+    }
+  }
 }
 
 __global__ void project_f32_kernel(const float* x, const float* ut, float* p, int64_t n_tok, int64_t d, int r) {
@@ -595,26 +612,19 @@ hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d
                                                                n_tok, d_in, r);
     return hipGetLastError();
   }
-  const int64_t waves = (n_tok + PROJ_TOK - 1) / PROJ_TOK;
-  const dim3 grid((unsigned)((waves + 3) / 4));
+  const dim3 grid((unsigned)((n_tok + PROJ_TOK - 1) / PROJ_TOK));
+  // depth quarter per wave, a multiple of 32 (the last wave may get less or nothing)
+  int64_t dq = (d_in + 3) / 4;
+  dq = (dq + 31) / 32 * 32;
   const uint16_t* xx = static_cast<const uint16_t*>(x);
   const uint16_t* uu = static_cast<const uint16_t*>(ut);
   uint16_t* pp = static_cast<uint16_t*>(p);
   const int rb = (r + 15) / 16;
-  switch (rb) {
-    case 1: project_bf16_kernel<1><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
-    case 2: project_bf16_kernel<2><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
-    case 3: project_bf16_kernel<3><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
-    case 4: project_bf16_kernel<4><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
-    case 8: project_bf16_kernel<8><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
-    case 16: project_bf16_kernel<16><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r); break;
-    default: {
-      // pad the column-block count up to the next instantiated size
-      const int rbp = rb <= 8 ? 8 : 16;
-      if (rbp == 8) project_bf16_kernel<8><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r);
-      else project_bf16_kernel<16><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r);
-    }
-  }
+  if (rb <= 1) project_bf16_kernel<1><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq);
+  else if (rb <= 2) project_bf16_kernel<2><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq);
+  else if (rb <= 4) project_bf16_kernel<4><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq);
+  else if (rb <= 8) project_bf16_kernel<8><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq);
+  else project_bf16_kernel<16><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq);
   return hipGetLastError();
 }
 
