@@ -118,7 +118,7 @@ def main():
     # ---- one-shot basis (Algorithm 1) on the calibration activations, timed separately
     ut = torch.empty(r, K, dtype=torch.bfloat16, device=dev)
     eigv = torch.empty(r, dtype=torch.float32, device=dev)
-    ws_b = torch.empty(K * K * 4 + Z.basis_workspace_bytes(K, r), dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(Z.basis_init_workspace_bytes(K, r), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     Z.basis_init(xb, r, ut, ws_b, eigvals=eigv)

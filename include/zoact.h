@@ -117,7 +117,7 @@ typedef struct {
 /* Options of the eigensolver behind zoact_basis_from_gram (NULL = defaults). */
 typedef struct {
   int32_t oversample; /* extra block columns p (default r)                  */
-  int32_t iters;      /* subspace iterations (default 12)                   */
+  int32_t iters;      /* subspace iterations (default 64)                   */
   uint64_t seed;      /* seed of the random start block                     */
 } zoact_eig_opts;
 
@@ -159,7 +159,7 @@ zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t 
  * bf16 path); pert->eps == 0 gives two unperturbed halves.  With r == 0 the call
  * is a plain GEMM (arena and p may be NULL).  One rounding per output element.
  * Requirements: T >= 1; d_in % 64 == 0 (BF16/INT4) or % 4 (F32); INT4 needs
- * d_in % 128 == 0; d_out % 64 == 0 with SWIGLU (% 16 otherwise, BF16).
+ * d_in % 128 == 0; d_out % 32 == 0 with SWIGLU (% 16 otherwise, BF16).
  * Errors: ZOACT_E_INVALID on shape/dtype mismatch, ZOACT_E_UNSUPPORTED for a
  * dtype combination not listed here. */
 zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, const void* x,
@@ -208,9 +208,13 @@ zoact_status zoact_step_sgd(const zoact_arena* A, const float* loss_pm, const zo
  *   ut_master fp32 [r][d], eigvals fp32 [r] (descending) and resid fp32 [1]
  *   (max_i ||G u_i - lambda_i u_i|| / lambda_1).  Workspace: ws of at least
  *   zoact_basis_workspace_bytes(d, r, opts) bytes.
- * zoact_basis_init: zoact_gram followed by zoact_basis_from_gram (g in ws).
- * Errors: r < 1, r > 256, r + p > d, n_tok < r -> ZOACT_E_INVALID. */
+ * zoact_basis_init: zoact_gram followed by zoact_basis_from_gram, with g at the
+ *   start of ws; ws needs zoact_basis_init_workspace_bytes(d, r, opts) bytes (the
+ *   Gram d*d fp32, padded to 256 bytes, then the solver's workspace).
+ * Errors: r < 1, r > 256, r + p > d, n_tok < r -> ZOACT_E_INVALID; a workspace that
+ * is NULL or too small -> ZOACT_E_WORKSPACE. */
 size_t zoact_basis_workspace_bytes(int64_t d, int32_t r, const zoact_eig_opts* opts);
+size_t zoact_basis_init_workspace_bytes(int64_t d, int32_t r, const zoact_eig_opts* opts);
 zoact_status zoact_gram(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, float* g,
                         int32_t accumulate, zoact_stream stream);
 zoact_status zoact_basis_from_gram(const float* g, int64_t d, int32_t r, const zoact_eig_opts* opts,

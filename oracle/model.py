@@ -102,32 +102,10 @@ def gate_up_rows(ff: int):
 
 # ------------------------------------------------------------------ weights
 def model_weights(shape, seed: int, mode: str):
-    """Per-tensor seeded random-init weights (N(0, init_std^2), norms 1, biases 0)."""
+    """Per-tensor seeded random-init weights (the seeded generator shared with the GPU side)."""
     import synth
 
-    rnd = synth.bf16_round if mode == "bf16" else (lambda a: a.astype(np.float32))
-    d, dkv, ff, V, std = shape.d_model, shape.n_kv_heads * shape.head_dim, shape.d_ff, shape.vocab, shape.init_std
-    W = {"emb": rnd(synth.normal((V, d), std, seed, 1000, 0))}
-    for l in range(shape.n_layers):
-        t = lambda k, shp: rnd(synth.normal(shp, std, seed, l, k))
-        L = {"wq": t(1, (d, d)), "wk": t(2, (dkv, d)), "wv": t(3, (dkv, d)), "wo": t(4, (d, d))}
-        if shape.family == "llama":
-            L.update({"wg": t(5, (ff, d)), "wu": t(6, (ff, d)), "wd": t(7, (d, ff)),
-                      "n1": np.ones(d, np.float32), "n2": np.ones(d, np.float32)})
-        else:
-            L.update({"w1": t(5, (ff, d)), "w2": t(6, (d, ff)),
-                      "n1": np.ones(d, np.float32), "n1b": np.zeros(d, np.float32),
-                      "n2": np.ones(d, np.float32), "n2b": np.zeros(d, np.float32)})
-            for b, n in (("bq", d), ("bk", dkv), ("bv", dkv), ("bo", d), ("b1", ff), ("b2", d)):
-                L[b] = np.zeros(n, np.float32)
-        W[l] = L
-    W["nf"] = np.ones(d, np.float32)
-    if shape.family == "llama":
-        W["head"] = rnd(synth.normal((V, d), std, seed, 1000, 1))
-    else:
-        W["nfb"] = np.zeros(d, np.float32)
-        W["pos"] = rnd(synth.normal((shape.max_pos + 2, d), std, seed, 1000, 2))
-    return W
+    return synth.model_weights(shape, seed, mode)
 
 
 # ------------------------------------------------------------------ support ops

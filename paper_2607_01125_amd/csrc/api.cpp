@@ -41,6 +41,13 @@ bool float_type(int32_t t) { return t == ZOACT_F32 || t == ZOACT_BF16; }
 
 }  // namespace
 
+namespace zoact {
+zoact_status set_error(zoact_status st, const char* msg) {
+  g_last_error = msg;
+  return st;
+}
+}  // namespace zoact
+
 extern "C" {
 
 const char* zoact_version(void) { return "zoact-gfx950 0.1.0"; }
@@ -169,7 +176,7 @@ zoact_status zoact_step_sgd(const zoact_arena* A, const float* loss_pm, const zo
 
 static void eig_defaults(int32_t r, const zoact_eig_opts* o, int32_t& p, int32_t& iters, uint64_t& seed) {
   p = (o && o->oversample > 0) ? o->oversample : r;
-  iters = (o && o->iters > 0) ? o->iters : 12;
+  iters = (o && o->iters > 0) ? o->iters : 64;
   seed = o ? o->seed : 0x5eedULL;
 }
 
@@ -179,6 +186,15 @@ size_t zoact_basis_workspace_bytes(int64_t d, int32_t r, const zoact_eig_opts* o
   eig_defaults(r, opts, p, it, sd);
   if (d < 1 || r < 1) return 0;
   return zoact::basis_ws_bytes(d, r, p);
+}
+
+// Gram block at the start of the workspace, padded to 256 bytes so the solver's
+// fp64 blocks after it stay aligned.
+static size_t gram_ws_bytes(int64_t d) { return ((size_t)d * (size_t)d * sizeof(float) + 255) & ~(size_t)255; }
+
+size_t zoact_basis_init_workspace_bytes(int64_t d, int32_t r, const zoact_eig_opts* opts) {
+  const size_t solver = zoact_basis_workspace_bytes(d, r, opts);
+  return solver ? gram_ws_bytes(d) + solver : 0;
 }
 
 zoact_status zoact_gram(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, float* g, int32_t accumulate,
@@ -216,7 +232,7 @@ zoact_status zoact_basis_init(const void* x, int32_t x_dtype, int64_t n_tok, int
   uint64_t seed;
   eig_defaults(r, opts, p, iters, seed);
   CHECK(r >= 1 && r <= 256 && d >= 2 && r + p <= d, "basis_init: bad r=%d for d=%lld", r, (long long)d);
-  const size_t gbytes = (size_t)d * (size_t)d * sizeof(float);
+  const size_t gbytes = gram_ws_bytes(d);
   const size_t need = gbytes + zoact::basis_ws_bytes(d, r, p);
   if (ws == nullptr || ws_bytes < need) return fail(ZOACT_E_WORKSPACE, "basis_init: workspace needs %zu bytes", need);
   float* g = static_cast<float*>(ws);

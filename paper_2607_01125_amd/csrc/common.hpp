@@ -37,6 +37,9 @@ hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t 
                                   void* ws, hipStream_t s);
 size_t basis_ws_bytes(int64_t d, int32_t r, int32_t p);
 
+// Record the detail text of a failed call for zoact_last_error() and return `st`.
+zoact_status set_error(zoact_status st, const char* msg);
+
 // Deterministic two-stage reductions: partial sums per block, then one block sums them in order.
 constexpr int kLossBlocks = 1024;
 

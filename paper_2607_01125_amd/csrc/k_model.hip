@@ -1,0 +1,430 @@
+// Support operations of the decoder forward (embeddings, RMSNorm, LayerNorm, rotary
+// embedding, causal attention) and their extern "C" entry points (zoact_model.h).
+//
+// All are HBM-bound elementwise/row passes except attention, which is a small MFMA
+// contraction (under 1% of a ZO step's FLOPs at the 8B/13B shapes): one workgroup per
+// (64-query block, head, sequence), scores and P.V on v_mfma_f32_16x16x32_bf16, a
+// two-pass softmax in fp32 with wave64 shuffles, K and V staged through LDS (V
+// transposed so that each lane's fragment holds 8 consecutive keys).
+#include <math.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "common.hpp"
+#include "zoact_model.h"
+
+namespace zoact {
+namespace {
+
+template <typename T>
+__device__ __forceinline__ float ld_act(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float ld_act<float>(const float* p, int64_t i) { return p[i]; }
+template <>
+__device__ __forceinline__ float ld_act<uint16_t>(const uint16_t* p, int64_t i) { return bf2f(p[i]); }
+template <typename T>
+__device__ __forceinline__ void st_act(T* p, int64_t i, float v);
+template <>
+__device__ __forceinline__ void st_act<float>(float* p, int64_t i, float v) { p[i] = v; }
+template <>
+__device__ __forceinline__ void st_act<uint16_t>(uint16_t* p, int64_t i, float v) { p[i] = f2bf(v); }
+
+template <typename T>
+__global__ void embed_kernel(const int32_t* __restrict__ tok, int64_t n_tok, int distinct, int64_t vocab,
+                             const T* __restrict__ table, const T* __restrict__ pos, int64_t max_pos, int pos_offset,
+                             int64_t seq, int64_t d, T* __restrict__ out) {
+  const int64_t half = n_tok * d;
+  const int64_t total = distinct ? 2 * half : half;  // distinct: one element per output; else one per pair
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = i / d, c = i % d;   // row indexes tokens[] (the [2][n_tok] set when distinct)
+    const int64_t t = row % n_tok;
+    int64_t id = tok[row];
+    id = id < 0 ? 0 : (id >= vocab ? vocab - 1 : id);
+    float v = ld_act(table, id * d + c);
+    if (pos) {
+      int64_t pp = t % seq + pos_offset;
+      pp = pp >= max_pos ? max_pos - 1 : pp;
+      v += ld_act(pos, pp * d + c);
+    }
+    st_act(out, i, v);
+    if (!distinct) st_act(out, half + i, v);
+  }
+}
+
+__device__ __forceinline__ float block_sum(float v, float* sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) t += sh[i];
+  __syncthreads();
+  return t;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const T* __restrict__ x, const T* __restrict__ w, int64_t d, float eps,
+                                                      T* __restrict__ y) {
+  __shared__ float sh[4];
+  const T* xr = x + (int64_t)blockIdx.x * d;
+  T* yr = y + (int64_t)blockIdx.x * d;
+  float ss = 0.f;
+  for (int64_t c = threadIdx.x; c < d; c += blockDim.x) {
+    const float v = ld_act(xr, c);
+    ss += v * v;
+  }
+  const float inv = rsqrtf(block_sum(ss, sh) / (float)d + eps);
+  for (int64_t c = threadIdx.x; c < d; c += blockDim.x) st_act(yr, c, (ld_act(xr, c) * inv) * ld_act(w, c));
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) layernorm_kernel(const T* __restrict__ x, const T* __restrict__ w, const T* __restrict__ b,
+                                                        int64_t d, float eps, T* __restrict__ y) {
+  __shared__ float sh[4];
+  const T* xr = x + (int64_t)blockIdx.x * d;
+  T* yr = y + (int64_t)blockIdx.x * d;
+  float s = 0.f;
+  for (int64_t c = threadIdx.x; c < d; c += blockDim.x) s += ld_act(xr, c);
+  const float mu = block_sum(s, sh) / (float)d;
+  float ss = 0.f;
+  for (int64_t c = threadIdx.x; c < d; c += blockDim.x) {
+    const float v = ld_act(xr, c) - mu;
+    ss += v * v;
+  }
+  const float inv = rsqrtf(block_sum(ss, sh) / (float)d + eps);
+  for (int64_t c = threadIdx.x; c < d; c += blockDim.x)
+    st_act(yr, c, ((ld_act(xr, c) - mu) * inv) * ld_act(w, c) + ld_act(b, c));
+}
+
+template <typename T>
+__global__ void rope_kernel(T* __restrict__ x, int64_t rows, int64_t ld, int64_t col0, int heads, int hd, int64_t seq,
+                            const float* __restrict__ ct, const float* __restrict__ st) {
+  const int half = hd / 2;
+  const int64_t total = rows * heads * half;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int j = (int)(i % half);
+    const int h = (int)((i / half) % heads);
+    const int64_t r = i / ((int64_t)half * heads);
+    const int64_t pos = r % seq;
+    T* p = x + r * ld + col0 + (int64_t)h * hd;
+    const float c = ct[pos * half + j], s = st[pos * half + j];
+    const float lo = ld_act(p, j), hi = ld_act(p, j + half);
+    st_act(p, j, lo * c - hi * s);
+    st_act(p, j + half, hi * c + lo * s);
+  }
+}
+
+// ---------------------------------------------------------------- attention, fp32 (small)
+// One workgroup per (sequence, head); K and V of the sequence in LDS; one thread per query.
+__global__ void __launch_bounds__(256) attention_f32_kernel(const float* __restrict__ q, int64_t ldq, const float* __restrict__ k,
+                                                            int64_t ldk, const float* __restrict__ v, int64_t ldv, int64_t seq,
+                                                            int heads, int kv_heads, int hd, float scale,
+                                                            float* __restrict__ out) {
+  extern __shared__ float kv[];  // [seq][hd] K then [seq][hd] V
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int hk = h / (heads / kv_heads);
+  const int64_t r0 = (int64_t)b * seq;
+  for (int64_t i = threadIdx.x; i < seq * hd; i += blockDim.x) {
+    const int64_t s = i / hd, e = i % hd;
+    kv[i] = k[(r0 + s) * ldk + (int64_t)hk * hd + e];
+    kv[seq * hd + i] = v[(r0 + s) * ldv + (int64_t)hk * hd + e];
+  }
+  __syncthreads();
+  for (int64_t sq = threadIdx.x; sq < seq; sq += blockDim.x) {
+    const float* qr = q + (r0 + sq) * ldq + (int64_t)h * hd;
+    float m = -INFINITY, l = 0.f;
+    float acc[128];
+    for (int e = 0; e < hd; ++e) acc[e] = 0.f;
+    for (int64_t sk = 0; sk <= sq; ++sk) {
+      float sc = 0.f;
+      for (int e = 0; e < hd; ++e) sc += qr[e] * kv[sk * hd + e];
+      sc *= scale;
+      const float mn = fmaxf(m, sc);
+      const float a = expf(m - mn), p = expf(sc - mn);
+      l = l * a + p;
+      for (int e = 0; e < hd; ++e) acc[e] = acc[e] * a + p * kv[seq * hd + sk * hd + e];
+      m = mn;
+    }
+    float* o = out + (r0 + sq) * (int64_t)heads * hd + (int64_t)h * hd;
+    for (int e = 0; e < hd; ++e) o[e] = acc[e] / l;
+  }
+}
+
+// ---------------------------------------------------------------- attention, bf16 MFMA
+// Two passes over the key blocks: the first finds each query row's maximum score, the
+// second forms P = exp(s - max) against that final maximum, rounds P to bf16 and
+// accumulates P.V on MFMA (normaliser summed from the unrounded P).  Forming P against
+// the final maximum (instead of rescaling a running one) keeps each bf16 rounding of P
+// the same as in the plain softmax definition; the extra Q.K^T pass costs little, as
+// attention is a small share of a step's FLOPs.
+template <int HD>
+__device__ __forceinline__ void stage_k(const uint16_t* __restrict__ k, int64_t ldk, int64_t r0, int64_t seq, int hk,
+                                        int kb, uint16_t* ks) {
+  constexpr int KC = HD / 8;
+  for (int cidx = threadIdx.x; cidx < 64 * KC; cidx += 256) {
+    const int key = cidx / KC, ch = cidx % KC;
+    int64_t kr = (int64_t)kb * 64 + key;
+    kr = kr < seq ? kr : seq - 1;
+    const uint4 kvv = *reinterpret_cast<const uint4*>(k + (r0 + kr) * ldk + (int64_t)hk * HD + ch * 8);
+    *reinterpret_cast<uint4*>(ks + key * HD + ((ch ^ (key & 7)) * 8)) = kvv;
+  }
+}
+
+// scores S[q = 4*lk + i][key = j*16 + lr] of this wave's 16 queries against key block kb
+template <int HD>
+__device__ __forceinline__ void scores(const bf16x8* qf, const uint16_t* ks, int lr, int lk, floatx4* s) {
+  constexpr int KS = HD / 32;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    s[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const int key = j * 16 + lr;
+      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + key * HD + (((kk * 4 + lk) ^ (key & 7)) * 8));
+      s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[kk], kf, s[j], 0, 0, 0);
+    }
+  }
+}
+
+template <int HD>
+__global__ void __launch_bounds__(256) attention_bf16_kernel(const uint16_t* __restrict__ q, int64_t ldq,
+                                                             const uint16_t* __restrict__ k, int64_t ldk,
+                                                             const uint16_t* __restrict__ v, int64_t ldv, int64_t seq,
+                                                             int heads, int kv_heads, float scale,
+                                                             uint16_t* __restrict__ out) {
+  constexpr int KC = HD / 8;         // 16-byte chunks per row
+  constexpr int KS = HD / 32;        // 32-deep steps over the head dimension
+  constexpr int NB = HD / 16;        // output column blocks
+  __shared__ __align__(16) uint16_t ks[64 * HD];       // K block [key][hd], chunk-swizzled
+  __shared__ __align__(16) uint16_t vt[HD * 72];       // V block transposed [hd][key], padded
+  __shared__ __align__(16) uint16_t pw[4][16 * 72];    // per-wave probabilities [q][key], padded
+  const int qb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int hk = h / (heads / kv_heads);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lr = lane & 15, lk = lane >> 4;
+  const int64_t r0 = (int64_t)b * seq;
+  const int64_t q0 = (int64_t)qb * 64 + wave * 16;    // first query row of this wave
+
+  // Q fragments (A operand): row lr, depth kk*32 + lk*8
+  bf16x8 qf[KS];
+  {
+    int64_t qr = q0 + lr;
+    qr = qr < seq ? qr : seq - 1;
+    const uint16_t* qp = q + (r0 + qr) * ldq + (int64_t)h * HD;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + lk * 8);
+  }
+  const int64_t qmax = (int64_t)qb * 64 + 63;
+  const int nkb = (int)((qmax < seq - 1 ? qmax : seq - 1) / 64) + 1;
+
+  // pass 1: row maxima of the scaled, masked scores
+  float mrow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) mrow[i] = -INFINITY;
+  for (int kb = 0; kb < nkb; ++kb) {
+    __syncthreads();
+    stage_k<HD>(k, ldk, r0, seq, hk, kb, ks);
+    __syncthreads();
+    floatx4 s[4];
+    scores<HD>(qf, ks, lr, lk, s);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t qi = q0 + lk * 4 + i;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t key = (int64_t)kb * 64 + j * 16 + lr;
+        if (key <= qi && key < seq) mx = fmaxf(mx, s[j][i] * scale);
+      }
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+      mrow[i] = fmaxf(mrow[i], mx);
+    }
+  }
+
+  // pass 2: P = exp(s - max) rounded to bf16, O += P V, l += P (unrounded)
+  floatx4 o[NB];
+#pragma unroll
+  for (int n = 0; n < NB; ++n) o[n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float lrow[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int kb = 0; kb < nkb; ++kb) {
+    __syncthreads();
+    stage_k<HD>(k, ldk, r0, seq, hk, kb, ks);
+    for (int cidx = threadIdx.x; cidx < 64 * KC; cidx += 256) {
+      const int key = cidx / KC, ch = cidx % KC;
+      int64_t kr = (int64_t)kb * 64 + key;
+      kr = kr < seq ? kr : seq - 1;
+      const uint4 vv = *reinterpret_cast<const uint4*>(v + (r0 + kr) * ldv + (int64_t)hk * HD + ch * 8);
+      const uint16_t* ve = reinterpret_cast<const uint16_t*>(&vv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vt[(ch * 8 + e) * 72 + key] = ve[e];
+    }
+    __syncthreads();
+    floatx4 s[4];
+    scores<HD>(qf, ks, lr, lk, s);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t qi = q0 + lk * 4 + i;
+      float ps = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t key = (int64_t)kb * 64 + j * 16 + lr;
+        const float p = (key <= qi && key < seq) ? expf(s[j][i] * scale - mrow[i]) : 0.f;
+        s[j][i] = p;
+        ps += p;
+      }
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) ps += __shfl_xor(ps, off, 64);
+      lrow[i] += ps;
+    }
+    // probabilities to bf16 through LDS, read back as A fragments (row lr, keys lk*8 ..)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pw[wave][(lk * 4 + i) * 72 + j * 16 + lr] = f2bf(s[j][i]);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS writes done
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const bf16x8 pf = *reinterpret_cast<const bf16x8*>(&pw[wave][lr * 72 + kk * 32 + lk * 8]);
+#pragma unroll
+      for (int n = 0; n < NB; ++n) {
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&vt[(n * 16 + lr) * 72 + kk * 32 + lk * 8]);
+        o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, vf, o[n], 0, 0, 0);
+      }
+    }
+  }
+  // O[q = 4*lk + i][col = n*16 + lr] / l
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t qi = q0 + lk * 4 + i;
+    if (qi >= seq) continue;
+    const float inv = 1.f / lrow[i];
+    uint16_t* op = out + (r0 + qi) * (int64_t)heads * HD + (int64_t)h * HD;
+#pragma unroll
+    for (int n = 0; n < NB; ++n) op[n * 16 + lr] = f2bf(o[n][i] * inv);
+  }
+}
+
+unsigned grid1d(int64_t n) {
+  int64_t g = (n + 255) / 256;
+  return (unsigned)(g < 1 ? 1 : (g > 65535 ? 65535 : g));
+}
+
+}  // namespace
+}  // namespace zoact
+
+using namespace zoact;
+
+#define ZO_CHECK(cond, msg)                                 \
+  do {                                                      \
+    if (!(cond)) return zoact::set_error(ZOACT_E_INVALID, msg); \
+  } while (0)
+
+static zoact_status launched(const char* who) {
+  const hipError_t e = hipGetLastError();
+  if (e == hipSuccess) return ZOACT_OK;
+  std::string m = std::string(who) + ": " + hipGetErrorString(e);
+  return zoact::set_error(ZOACT_E_HIP, m.c_str());
+}
+
+extern "C" zoact_status zoact_embed(const int32_t* tokens, int64_t n_tok, int32_t distinct_halves, int64_t vocab,
+                                    const void* table, const void* pos, int64_t max_pos, int32_t pos_offset,
+                                    int64_t seq, int64_t d, int32_t dtype, void* out, zoact_stream stream) {
+  ZO_CHECK(tokens && table && out, "embed: NULL pointer");
+  ZO_CHECK(distinct_halves == 0 || distinct_halves == 1, "embed: distinct_halves must be 0 or 1");
+  ZO_CHECK(n_tok >= 1 && vocab >= 1 && d >= 1 && seq >= 1, "embed: empty shape");
+  ZO_CHECK(dtype == ZOACT_F32 || dtype == ZOACT_BF16, "embed: dtype must be F32 or BF16");
+  ZO_CHECK(pos == nullptr || (max_pos >= 1 && pos_offset >= 0), "embed: bad position table");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int64_t work = n_tok * d * (distinct_halves ? 2 : 1);
+  if (dtype == ZOACT_BF16)
+    embed_kernel<uint16_t><<<grid1d(work), 256, 0, s>>>(tokens, n_tok, distinct_halves, vocab, (const uint16_t*)table,
+                                                        (const uint16_t*)pos, max_pos, pos_offset, seq, d,
+                                                        (uint16_t*)out);
+  else
+    embed_kernel<float><<<grid1d(work), 256, 0, s>>>(tokens, n_tok, distinct_halves, vocab, (const float*)table,
+                                                     (const float*)pos, max_pos, pos_offset, seq, d, (float*)out);
+  return launched("embed");
+}
+
+extern "C" zoact_status zoact_rmsnorm(const void* x, const void* w, int64_t rows, int64_t d, float eps, int32_t dtype,
+                                      void* y, zoact_stream stream) {
+  ZO_CHECK(x && w && y, "rmsnorm: NULL pointer");
+  ZO_CHECK(rows >= 1 && d >= 1 && rows <= 0x7FFFFFFF, "rmsnorm: bad shape");
+  ZO_CHECK(dtype == ZOACT_F32 || dtype == ZOACT_BF16, "rmsnorm: dtype must be F32 or BF16");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (dtype == ZOACT_BF16)
+    rmsnorm_kernel<uint16_t><<<(unsigned)rows, 256, 0, s>>>((const uint16_t*)x, (const uint16_t*)w, d, eps, (uint16_t*)y);
+  else
+    rmsnorm_kernel<float><<<(unsigned)rows, 256, 0, s>>>((const float*)x, (const float*)w, d, eps, (float*)y);
+  return launched("rmsnorm");
+}
+
+extern "C" zoact_status zoact_layernorm(const void* x, const void* w, const void* b, int64_t rows, int64_t d, float eps,
+                                        int32_t dtype, void* y, zoact_stream stream) {
+  ZO_CHECK(x && w && b && y, "layernorm: NULL pointer");
+  ZO_CHECK(rows >= 1 && d >= 1 && rows <= 0x7FFFFFFF, "layernorm: bad shape");
+  ZO_CHECK(dtype == ZOACT_F32 || dtype == ZOACT_BF16, "layernorm: dtype must be F32 or BF16");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (dtype == ZOACT_BF16)
+    layernorm_kernel<uint16_t><<<(unsigned)rows, 256, 0, s>>>((const uint16_t*)x, (const uint16_t*)w,
+                                                              (const uint16_t*)b, d, eps, (uint16_t*)y);
+  else
+    layernorm_kernel<float><<<(unsigned)rows, 256, 0, s>>>((const float*)x, (const float*)w, (const float*)b, d, eps,
+                                                           (float*)y);
+  return launched("layernorm");
+}
+
+extern "C" zoact_status zoact_rope(void* x, int32_t dtype, int64_t rows, int64_t ld, int64_t col0, int32_t n_heads,
+                                   int32_t head_dim, int64_t seq, const float* cos_t, const float* sin_t,
+                                   zoact_stream stream) {
+  ZO_CHECK(x && cos_t && sin_t, "rope: NULL pointer");
+  ZO_CHECK(rows >= 1 && seq >= 1 && n_heads >= 1 && head_dim >= 2 && head_dim % 2 == 0, "rope: bad shape");
+  ZO_CHECK(col0 >= 0 && col0 + (int64_t)n_heads * head_dim <= ld, "rope: heads exceed the row");
+  ZO_CHECK(dtype == ZOACT_F32 || dtype == ZOACT_BF16, "rope: dtype must be F32 or BF16");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int64_t total = rows * n_heads * (head_dim / 2);
+  if (dtype == ZOACT_BF16)
+    rope_kernel<uint16_t><<<grid1d(total), 256, 0, s>>>((uint16_t*)x, rows, ld, col0, n_heads, head_dim, seq, cos_t, sin_t);
+  else
+    rope_kernel<float><<<grid1d(total), 256, 0, s>>>((float*)x, rows, ld, col0, n_heads, head_dim, seq, cos_t, sin_t);
+  return launched("rope");
+}
+
+extern "C" zoact_status zoact_attention(const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v,
+                                        int64_t ldv, int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads,
+                                        int32_t head_dim, float scale, int32_t dtype, void* out, zoact_stream stream) {
+  ZO_CHECK(q && k && v && out, "attention: NULL pointer");
+  ZO_CHECK(n_seq >= 1 && seq >= 1 && n_heads >= 1 && n_kv_heads >= 1 && n_heads % n_kv_heads == 0,
+           "attention: bad shape or head grouping");
+  ZO_CHECK(ldq >= (int64_t)n_heads * head_dim && ldk >= (int64_t)n_kv_heads * head_dim &&
+               ldv >= (int64_t)n_kv_heads * head_dim,
+           "attention: row strides smaller than the heads");
+  ZO_CHECK(n_seq <= 65535 && n_heads <= 65535, "attention: grid too large");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (dtype == ZOACT_BF16) {
+    ZO_CHECK(head_dim == 64 || head_dim == 128, "attention: bf16 head_dim must be 64 or 128");
+    ZO_CHECK(ldq % 8 == 0 && ldk % 8 == 0 && ldv % 8 == 0, "attention: bf16 strides must be multiples of 8");
+    const dim3 grid((unsigned)((seq + 63) / 64), (unsigned)n_heads, (unsigned)n_seq);
+    if (head_dim == 128)
+      attention_bf16_kernel<128><<<grid, 256, 0, s>>>((const uint16_t*)q, ldq, (const uint16_t*)k, ldk,
+                                                      (const uint16_t*)v, ldv, seq, n_heads, n_kv_heads, scale,
+                                                      (uint16_t*)out);
+    else
+      attention_bf16_kernel<64><<<grid, 256, 0, s>>>((const uint16_t*)q, ldq, (const uint16_t*)k, ldk,
+                                                     (const uint16_t*)v, ldv, seq, n_heads, n_kv_heads, scale,
+                                                     (uint16_t*)out);
+  } else if (dtype == ZOACT_F32) {
+    ZO_CHECK(head_dim <= 128 && seq * head_dim <= 4096, "attention: fp32 path needs head_dim <= 128, seq*hd <= 4096");
+    const dim3 grid((unsigned)n_heads, (unsigned)n_seq);
+    attention_f32_kernel<<<grid, 256, (size_t)2 * seq * head_dim * sizeof(float), s>>>(
+        (const float*)q, ldq, (const float*)k, ldk, (const float*)v, ldv, seq, n_heads, n_kv_heads, head_dim, scale,
+        (float*)out);
+  } else {
+    return zoact::set_error(ZOACT_E_INVALID, "attention: dtype must be F32 or BF16");
+  }
+  return launched("attention");
+}

@@ -1,0 +1,371 @@
+"""Decoder models on the GPU for the forward-only ZO step.
+
+Algorithm 1 (one-shot basis from a calibration forward) and the two-sided step of
+Algorithm 2 over a whole decoder, written as a sequence of libzoact calls: this module
+only lays out buffers and marshals arguments; every operation of the forward, the loss
+and the update runs in the library's kernels.
+
+Models (the random-initialised shapes of the paper's Section 5 experiments):
+* Llama family: token embedding; per layer RMSNorm, q/k/v, rotary embedding
+  (rotate-half), causal attention with grouped K/V heads, o projection + residual,
+  RMSNorm, SwiGLU MLP + residual; final RMSNorm; untied LM head.
+* OPT family: token + learned position embedding (offset 2); per layer LayerNorm,
+  q/k/v with biases, causal attention, out projection + residual, LayerNorm, fc1, ReLU,
+  fc2 + residual; final LayerNorm; LM head tied to the embedding.
+
+Adapted projections (Section 3, y = x W^T + (x U) C^T) read one of four input sites
+per layer -- "attn" (q, k, v), "o", "mlp" (gate/up or fc1) and "down" (down or fc2) --
+and projections reading the same site share its basis U.  Projections that read one
+site are fused into one linear call: q|k|v (or q|v, with k a separate plain linear when
+k is not adapted) and gate|up, whose rows interleave blocks of 16 gate and 16 up
+features so the SwiGLU epilogue pairs them inside a tile.
+
+Coefficient arena: per layer, in order, [q|k|v] (or [q|v]), o, gate|up, down (Llama)
+or [q|v], out, fc1, fc2 (OPT); each block holds rows x r coefficients row-major, where
+a row is an output feature of the fused projection.  The arena size is the paper's
+k = sum of r n_l over adapted linears (Section 4).
+
+Precision modes: "fp32" (fp32 weights and activations), "bf16" (bf16 weights and
+activations, fp32 logits) and "int4" (group-128 INT4 linears with bf16 scales, bf16
+everything else, bf16 coefficients by default).
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import zoact as Z
+
+SITES = ("attn", "o", "mlp", "down")
+
+
+@dataclass
+class Block:
+    """One coefficient block: the fused projection `name` of `layer`, rows x r at `offset`."""
+    layer: int
+    name: str
+    rows: int
+    r: int
+    offset: int
+    site: str
+
+
+def arena_layout(shape) -> list:
+    d, dkv, ff, r = shape.d_model, shape.n_kv_heads * shape.head_dim, shape.d_ff, shape.rank
+    ad = set(shape.adapted)
+    out, off = [], 0
+    for l in range(shape.n_layers):
+        if shape.family == "llama":
+            names = []
+            if {"q", "k", "v"} <= ad:
+                names.append(("qkv", d + 2 * dkv, "attn"))
+            elif {"q", "v"} <= ad:
+                names.append(("qv", 2 * d, "attn"))
+            elif ad & {"q", "k", "v"}:
+                raise ValueError("Llama models adapt q, k, v together or q, v")
+            if "o" in ad:
+                names.append(("o", d, "o"))
+            if {"gate", "up"} <= ad:
+                names.append(("gu", 2 * ff, "mlp"))
+            elif ad & {"gate", "up"}:
+                raise ValueError("gate and up are adapted together")
+            if "down" in ad:
+                names.append(("down", d, "down"))
+        else:
+            if set(shape.adapted) != {"q", "v", "o", "fc1", "fc2"}:
+                raise ValueError("OPT models adapt q, v, out, fc1, fc2")
+            names = [("qv", 2 * d, "attn"), ("out", d, "o"), ("fc1", ff, "mlp"), ("fc2", d, "down")]
+        for name, rows, site in names:
+            out.append(Block(l, name, rows, r, off, site))
+            off += rows * r
+    return out
+
+
+def interleave_gate_up(wg: torch.Tensor, wu: torch.Tensor) -> torch.Tensor:
+    """Rows 32j..32j+15 = gate rows 16j..16j+15, rows 32j+16..32j+31 = the matching up rows."""
+    ff = wg.shape[0]
+    if ff % 16:
+        raise ValueError("d_ff must be a multiple of 16")
+    return torch.stack([wg.reshape(ff // 16, 16, *wg.shape[1:]), wu.reshape(ff // 16, 16, *wu.shape[1:])],
+                       dim=1).reshape(2 * ff, *wg.shape[1:]).contiguous()
+
+
+class Decoder:
+    """A decoder on one GPU: frozen weights, per-site bases U, coefficient arena, Adam state.
+
+    W holds the model's tensors under the names wq wk wv wo, wg wu wd (Llama) or w1 w2 and
+    biases (OPT), norms n1 n2 (n1b n2b), emb, head or pos, nf (nfb); numpy arrays or torch
+    tensors.  In mode "int4" each linear weight is given instead as a pair (packed uint8
+    [N][K/2], scales [N][K/128]) in the library's INT4 format.
+    """
+
+    def __init__(self, shape, W: dict, mode: str, *, c_bf16: bool | None = None, device="cuda"):
+        if mode not in ("fp32", "bf16", "int4"):
+            raise ValueError(f"unknown mode {mode!r}")
+        self.s, self.mode, self.dev = shape, mode, torch.device(device)
+        self.act = torch.float32 if mode == "fp32" else torch.bfloat16
+        self.c_bf16 = (mode == "int4") if c_bf16 is None else c_bf16
+        s = shape
+        self.d, self.H, self.Hkv, self.hd = s.d_model, s.n_heads, s.n_kv_heads, s.head_dim
+        self.dkv = self.Hkv * self.hd
+        self.blocks = arena_layout(shape)
+        self.bmap = {(b.layer, b.name): b for b in self.blocks}
+        self.k = sum(b.rows * b.r for b in self.blocks)
+        self._adapted_sites = {(b.layer, b.site) for b in self.blocks}
+        self.r = s.rank
+        self._pack(W)
+        self.ut = {}                      # (layer, site) -> U^T [r][d_in] (activation dtype)
+        self.arena = Z.Arena(torch.zeros(self.k, dtype=torch.bfloat16 if self.c_bf16 else torch.float32,
+                                         device=self.dev),
+                             torch.zeros(self.k, dtype=torch.float32, device=self.dev),
+                             torch.zeros(self.k, dtype=torch.float32, device=self.dev))
+        self.t = 0
+        self.loss_pm = torch.zeros(2, dtype=torch.float32, device=self.dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=self.dev)
+        self.loss_ws = torch.empty(Z.loss_workspace_bytes(), dtype=torch.uint8, device=self.dev)
+        self._bufs = {}
+        self._rope = {}
+
+    # ---------------------------------------------------------------- weights
+    def _t(self, a, dtype=None):
+        dtype = dtype or self.act
+        t = a if torch.is_tensor(a) else torch.from_numpy(np.ascontiguousarray(a))
+        return t.to(device=self.dev, dtype=dtype).contiguous()
+
+    def _lin_w(self, *parts, interleave=False):
+        """Device weight of a fused linear from row blocks (and the INT4 scales)."""
+        if self.mode == "int4":
+            packed = [self._t(p[0], torch.uint8) for p in parts]
+            scales = [self._t(p[1], torch.bfloat16) for p in parts]
+            if interleave:
+                return interleave_gate_up(*packed), interleave_gate_up(*scales)
+            return torch.cat(packed).contiguous(), torch.cat(scales).contiguous()
+        ws = [self._t(p) for p in parts]
+        if interleave:
+            return interleave_gate_up(*ws), None
+        return torch.cat(ws).contiguous(), None
+
+    def _pack(self, W):
+        s, d, dkv, ff = self.s, self.d, self.dkv, self.s.d_ff
+        ad = set(s.adapted)
+        self.layers = []
+        for l in range(s.n_layers):
+            L = W[l]
+            P = {"n1": self._t(L["n1"]), "n2": self._t(L["n2"])}
+            if s.family == "opt":
+                P["n1b"], P["n2b"] = self._t(L["n1b"]), self._t(L["n2b"])
+            fused_qkv = s.family == "llama" and ({"q", "k", "v"} <= ad or not (ad & {"q", "k", "v"}))
+            if fused_qkv:
+                w, sc = self._lin_w(L["wq"], L["wk"], L["wv"])
+                P["qkv"] = self._linear(l, "qkv", w, sc, d, d + 2 * dkv)
+            else:
+                w, sc = self._lin_w(L["wq"], L["wv"])
+                bias = torch.cat([self._t(L["bq"]), self._t(L["bv"])]) if s.family == "opt" else None
+                P["qv"] = self._linear(l, "qv", w, sc, d, 2 * d, bias)
+                w, sc = self._lin_w(L["wk"])
+                P["k"] = self._linear(l, None, w, sc, d, dkv, self._t(L["bk"]) if s.family == "opt" else None)
+            if s.family == "llama":
+                w, sc = self._lin_w(L["wo"])
+                P["o"] = self._linear(l, "o", w, sc, d, d)
+                w, sc = self._lin_w(L["wg"], L["wu"], interleave=True)
+                P["gu"] = self._linear(l, "gu", w, sc, d, 2 * ff)
+                w, sc = self._lin_w(L["wd"])
+                P["down"] = self._linear(l, "down", w, sc, ff, d)
+            else:
+                w, sc = self._lin_w(L["wo"])
+                P["o"] = self._linear(l, "out", w, sc, d, d, self._t(L["bo"]))
+                w, sc = self._lin_w(L["w1"])
+                P["gu"] = self._linear(l, "fc1", w, sc, d, ff, self._t(L["b1"]))
+                w, sc = self._lin_w(L["w2"])
+                P["down"] = self._linear(l, "fc2", w, sc, ff, d, self._t(L["b2"]))
+            self.layers.append(P)
+        self.emb = self._t(W["emb"])
+        self.nf = self._t(W["nf"])
+        if s.family == "llama":
+            self.head = Z.Linear(self._t(W["head"]), d, s.vocab)
+            self.pos = None
+        else:
+            self.nfb = self._t(W["nfb"])
+            self.head = Z.Linear(self.emb, d, s.vocab)        # tied
+            self.pos = self._t(W["pos"])
+
+    def _linear(self, l, name, w, scales, d_in, d_out, bias=None):
+        b = self.bmap.get((l, name)) if name is not None else None
+        return Z.Linear(w, d_in, d_out, r=0, coef_offset=b.offset if b else 0, bias=bias, w_scales=scales), b
+
+    # ---------------------------------------------------------------- buffers
+    def _buffers(self, n_seq: int, seq: int):
+        """Activation buffers for 2 halves of n_seq sequences of length seq (cached per shape)."""
+        key = (n_seq, seq)
+        if key in self._bufs:
+            return self._bufs[key]
+        s, T = self.s, n_seq * seq
+        e = lambda *shp, dt=None: torch.empty(*shp, dtype=dt or self.act, device=self.dev)
+        fused = "qkv" in self.layers[0]
+        B = {
+            "h0": e(2 * T, self.d), "h1": e(2 * T, self.d), "a": e(2 * T, self.d),
+            "qkv": e(2 * T, self.d + 2 * self.dkv) if fused else e(2 * T, 2 * self.d),
+            "k": None if fused else e(2 * T, self.dkv),
+            "att": e(2 * T, self.d), "ff": e(2 * T, s.d_ff),
+            "p": e(2 * T, max(self.r, 1)),
+            "logits": e(2 * T, s.vocab, dt=torch.float32),
+        }
+        self._bufs[key] = B
+        return B
+
+    def _rope_tables(self, seq: int):
+        if seq not in self._rope:
+            half = self.hd // 2
+            j = torch.arange(half, dtype=torch.float64)
+            inv = self.s.rope_theta ** (-2.0 * j / self.hd)
+            ang = torch.arange(seq, dtype=torch.float64)[:, None] * inv[None, :]
+            self._rope[seq] = (torch.cos(ang).float().to(self.dev).contiguous(),
+                               torch.sin(ang).float().to(self.dev).contiguous())
+        return self._rope[seq]
+
+    # ---------------------------------------------------------------- forward of both halves
+    def _norm(self, x, w, b, y):
+        if self.s.family == "llama":
+            Z.rmsnorm(x, w, y, self.s.norm_eps)
+        else:
+            Z.layernorm(x, w, b, y, self.s.norm_eps)
+
+    def _apply(self, lin_blk, x, T, y, pert, site_ut, residual=None, flags=0, adapt=True):
+        lin, blk = lin_blk
+        B = self._cur
+        if adapt and blk is not None and site_ut is not None:
+            lin.r, lin.ut = self.r, site_ut
+            Z.linear_fwd_pm(lin, self.arena, x, T, B["p"], y, pert, residual, flags)
+        else:
+            lin.r, lin.ut = 0, None
+            Z.linear_fwd_pm(lin, None, x, T, None, y, pert, residual, flags)
+
+    def forward(self, tokens: torch.Tensor, pert: Z.Pert, *, calibrate=None, distinct_halves=False):
+        """Both halves of the forward; logits fp32 [2][n_seq][seq][V] in the buffer set.
+
+        tokens int32 [n_seq][seq] (or [2][n_seq][seq] with distinct_halves).  Half 0 uses
+        C + eps Z, half 1 C - eps Z.  With `calibrate` (a callable taking (layer, site, x))
+        the linears are not adapted and each site's input [2 T][d_in] is handed over
+        before it is consumed (Algorithm 1's calibration forward).
+        """
+        s = self.s
+        n_seq, seq = tokens.shape[-2], tokens.shape[-1]
+        T = n_seq * seq
+        B = self._cur = self._buffers(n_seq, seq)
+        adapt = calibrate is None
+        Z.embed(tokens, self.emb, B["h0"], seq, self.pos, pos_offset=2, distinct_halves=distinct_halves)
+        h, h_alt = B["h0"], B["h1"]
+        cos_sin = self._rope_tables(seq) if s.family == "llama" else None
+        d, dkv, H, Hkv, hd = self.d, self.dkv, self.H, self.Hkv, self.hd
+        scale = float(np.float32(1.0 / math.sqrt(hd)))
+        for l, P in enumerate(self.layers):
+            # attention block
+            self._norm(h, P["n1"], P.get("n1b"), B["a"])
+            ut = self._site(l, "attn", B["a"], adapt, calibrate)
+            qkv = B["qkv"]
+            if "qkv" in P:
+                self._apply(P["qkv"], B["a"], T, qkv, pert, ut, adapt=adapt)
+                q, k, v = qkv[:, :d], qkv[:, d:d + dkv], qkv[:, d + dkv:]
+            else:
+                self._apply(P["qv"], B["a"], T, qkv, pert, ut, adapt=adapt)
+                self._apply(P["k"], B["a"], T, B["k"], pert, None, adapt=False)
+                q, k, v = qkv[:, :d], B["k"], qkv[:, d:]
+            if cos_sin is not None:
+                if "qkv" in P:      # q and k heads are adjacent columns of the fused row
+                    Z.rope(qkv, 0, H + Hkv, hd, seq, *cos_sin)
+                else:
+                    Z.rope(qkv, 0, H, hd, seq, *cos_sin)
+                    Z.rope(B["k"], 0, Hkv, hd, seq, *cos_sin)
+            Z.attention(q, k, v, B["att"], 2 * n_seq, seq, H, Hkv, hd, scale)
+            ut = self._site(l, "o", B["att"], adapt, calibrate)
+            self._apply(P["o"], B["att"], T, h_alt, pert, ut, residual=h, adapt=adapt)
+            h, h_alt = h_alt, h
+            # MLP block
+            self._norm(h, P["n2"], P.get("n2b"), B["a"])
+            ut = self._site(l, "mlp", B["a"], adapt, calibrate)
+            flags = Z.EPI_SWIGLU if s.family == "llama" else Z.EPI_RELU
+            self._apply(P["gu"], B["a"], T, B["ff"], pert, ut, flags=flags, adapt=adapt)
+            ut = self._site(l, "down", B["ff"], adapt, calibrate)
+            self._apply(P["down"], B["ff"], T, h_alt, pert, ut, residual=h, adapt=adapt)
+            h, h_alt = h_alt, h
+        self._norm(h, self.nf, getattr(self, "nfb", None), B["a"])
+        Z.linear_fwd_pm(self.head, None, B["a"], T, None, B["logits"], pert)
+        return B["logits"].view(2, n_seq, seq, s.vocab)
+
+    def _site(self, l, site, x, adapt, calibrate):
+        """U^T of an adapted site after projecting its input into P (None if not adapted)."""
+        if not adapt:
+            calibrate(l, site, x)
+            return None
+        ut = self.ut.get((l, site)) if (l, site) in self._adapted_sites else None
+        if ut is None:
+            if (l, site) in self._adapted_sites:
+                raise RuntimeError(f"no basis for site {(l, site)}: run basis_init or set_basis first")
+            return None
+        Z.project(x, ut, self._cur["p"])
+        return ut
+
+    def site_dims(self):
+        """(layer, site) -> d_in for every adapted site."""
+        d_in = {"attn": self.d, "o": self.d, "mlp": self.d, "down": self.s.d_ff}
+        return {(b.layer, b.site): d_in[b.site] for b in self.blocks}
+
+    # ---------------------------------------------------------------- Algorithm 1
+    def basis_init(self, calib_tokens: torch.Tensor, opts: Z.EigOpts | None = None, keep_eigvals=False):
+        """Unperturbed calibration forward, then the top-r basis of each adapted site's inputs.
+
+        calib_tokens int32 [n_seq][seq] with n_seq even: the two halves of the stacked
+        forward carry the first and second n_seq/2 sequences, so every site sees all
+        n_seq * seq calibration tokens once.
+        """
+        n_seq, seq = calib_tokens.shape
+        if n_seq % 2:
+            raise ValueError("the calibration batch needs an even number of sequences")
+        dims = self.site_dims()
+        ws = torch.empty(max(Z.basis_init_workspace_bytes(dd, self.r, opts) for dd in set(dims.values())),
+                         dtype=torch.uint8, device=self.dev)
+        self.eigvals = {}
+
+        def hook(l, site, x):
+            if (l, site) not in dims:
+                return
+            ut = torch.empty(self.r, dims[(l, site)], dtype=self.act, device=self.dev)
+            ev = torch.empty(self.r, dtype=torch.float32, device=self.dev) if keep_eigvals else None
+            Z.basis_init(x, self.r, ut, ws, opts, eigvals=ev)
+            self.ut[(l, site)] = ut
+            if keep_eigvals:
+                self.eigvals[(l, site)] = ev
+
+        tok = calib_tokens.reshape(2, n_seq // 2, seq).contiguous()
+        self.forward(tok, Z.Pert(0, 0, 0, 0.0), calibrate=hook, distinct_halves=True)
+        return self.ut
+
+    def set_basis(self, ut: dict):
+        """Install bases U^T [r][d_in] per (layer, site) (e.g. computed elsewhere)."""
+        for key, d_in in self.site_dims().items():
+            u = ut[key]
+            self.ut[key] = self._t(u).reshape(self.r, d_in).contiguous()
+
+    # ---------------------------------------------------------------- Algorithm 2 step
+    def losses(self, tokens: torch.Tensor, seed: int, t: int, eps: float):
+        """Forward both halves at step t and write (L+, L-) into self.loss_pm."""
+        self.forward(tokens, Z.Pert(seed, t, 0, eps))
+        B = self._cur
+        Z.xent_pm(B["logits"], tokens, self.loss_pm, self.loss_ws)
+        return self.loss_pm
+
+    def step(self, tokens: torch.Tensor, seed: int, eps: float, lr: float, optimizer: str = "adam"):
+        """One two-sided ZO step: L+ and L-, g = (L+ - L-) / (2 eps), update C with Z regenerated."""
+        self.t += 1
+        pert = Z.Pert(seed, self.t, 0, eps)
+        self.losses(tokens, seed, self.t, eps)
+        if optimizer == "adam":
+            Z.step(self.arena, self.loss_pm, pert, Z.adam_desc(lr, self.t), self.status)
+        elif optimizer == "sgd":
+            Z.step_sgd(self.arena, self.loss_pm, pert, lr, self.status)
+        else:
+            raise ValueError(optimizer)
+        return self.loss_pm

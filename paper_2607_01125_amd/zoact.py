@@ -73,10 +73,16 @@ SIGNATURES = {
     "zoact_step": ([ctypes.POINTER(ArenaDesc), _P, ctypes.POINTER(Pert), ctypes.POINTER(AdamDesc), _P, _P], _I32),
     "zoact_step_sgd": ([ctypes.POINTER(ArenaDesc), _P, ctypes.POINTER(Pert), _F, _P, _P], _I32),
     "zoact_basis_workspace_bytes": ([_I64, _I32, ctypes.POINTER(EigOpts)], _SZ),
+    "zoact_basis_init_workspace_bytes": ([_I64, _I32, ctypes.POINTER(EigOpts)], _SZ),
     "zoact_gram": ([_P, _I32, _I64, _I64, _P, _I32, _P], _I32),
     "zoact_basis_from_gram": ([_P, _I64, _I32, ctypes.POINTER(EigOpts), _P, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
     "zoact_basis_init": ([_P, _I32, _I64, _I64, _I32, ctypes.POINTER(EigOpts), _P, _I32, _P, _P, _P, _P, _SZ, _P],
                          _I32),
+    "zoact_embed": ([_P, _I64, _I32, _I64, _P, _P, _I64, _I32, _I64, _I64, _I32, _P, _P], _I32),
+    "zoact_rmsnorm": ([_P, _P, _I64, _I64, _F, _I32, _P, _P], _I32),
+    "zoact_layernorm": ([_P, _P, _P, _I64, _I64, _F, _I32, _P, _P], _I32),
+    "zoact_rope": ([_P, _I32, _I64, _I64, _I64, _I32, _I32, _I64, _P, _P, _P], _I32),
+    "zoact_attention": ([_P, _I64, _P, _I64, _P, _I64, _I64, _I64, _I32, _I32, _I32, _F, _I32, _P, _P], _I32),
 }
 
 _lib = None
@@ -213,7 +219,13 @@ def step_sgd(arena: Arena, loss_pm: torch.Tensor, pert: Pert, lr: float, status:
 
 
 def basis_workspace_bytes(d: int, r: int, opts: EigOpts | None = None) -> int:
+    """Workspace of basis_from_gram."""
     return int(lib().zoact_basis_workspace_bytes(d, r, ctypes.byref(opts) if opts is not None else None))
+
+
+def basis_init_workspace_bytes(d: int, r: int, opts: EigOpts | None = None) -> int:
+    """Workspace of basis_init (the Gram plus basis_from_gram's)."""
+    return int(lib().zoact_basis_init_workspace_bytes(d, r, ctypes.byref(opts) if opts is not None else None))
 
 
 def gram(x: torch.Tensor, g: torch.Tensor, accumulate: bool = False, stream=None):
@@ -244,3 +256,39 @@ def adam_desc(lr: float, t: int, beta1: float = 0.9, beta2: float = 0.999, eps: 
         raise ValueError("Adam step t starts at 1")
     return AdamDesc(beta1, beta2, eps, weight_decay, lr / (1.0 - beta1 ** t), 1.0 / math.sqrt(1.0 - beta2 ** t),
                     1.0 - beta1, 1.0 - beta2)
+
+
+# ---------------------------------------------------------------- model support ops (zoact_model.h)
+def embed(tokens: torch.Tensor, table: torch.Tensor, out: torch.Tensor, seq: int, pos: torch.Tensor | None = None,
+          pos_offset: int = 0, distinct_halves: bool = False, stream=None):
+    """out [2][n_tok][d]; with distinct_halves, tokens holds [2][n_tok] (one set per half)."""
+    n_tok = tokens.numel() // (2 if distinct_halves else 1)
+    vocab, d = table.shape
+    _check(lib().zoact_embed(_ptr(tokens), n_tok, int(distinct_halves), vocab, _ptr(table), _ptr(pos),
+                             pos.shape[0] if pos is not None else 0, pos_offset, seq, d, dtype_code(table), _ptr(out),
+                             _stream(stream)))
+
+
+def rmsnorm(x: torch.Tensor, w: torch.Tensor, y: torch.Tensor, eps: float, stream=None):
+    d = x.shape[-1]
+    _check(lib().zoact_rmsnorm(_ptr(x), _ptr(w), x.numel() // d, d, eps, dtype_code(x), _ptr(y), _stream(stream)))
+
+
+def layernorm(x: torch.Tensor, w: torch.Tensor, b: torch.Tensor, y: torch.Tensor, eps: float, stream=None):
+    d = x.shape[-1]
+    _check(lib().zoact_layernorm(_ptr(x), _ptr(w), _ptr(b), x.numel() // d, d, eps, dtype_code(x), _ptr(y),
+                                 _stream(stream)))
+
+
+def rope(x: torch.Tensor, col0: int, n_heads: int, head_dim: int, seq: int, cos_t: torch.Tensor, sin_t: torch.Tensor,
+         stream=None):
+    ld = x.shape[-1]
+    _check(lib().zoact_rope(_ptr(x), dtype_code(x), x.numel() // ld, ld, col0, n_heads, head_dim, seq, _ptr(cos_t),
+                            _ptr(sin_t), _stream(stream)))
+
+
+def attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: torch.Tensor, n_seq: int, seq: int, n_heads: int,
+              n_kv_heads: int, head_dim: int, scale: float, stream=None):
+    """q, k, v may be column slices (views) of wider row-major buffers."""
+    _check(lib().zoact_attention(_ptr(q), q.stride(0), _ptr(k), k.stride(0), _ptr(v), v.stride(0), n_seq, seq, n_heads,
+                                 n_kv_heads, head_dim, scale, dtype_code(out), _ptr(out), _stream(stream)))

@@ -137,3 +137,102 @@ def shrink(shape: ModelShape, **kw) -> ModelShape:
     d = dict(shape.__dict__)
     d.update(kw)
     return ModelShape(**d)
+
+
+# ------------------------------------------------------------------ model weights
+def model_weights(shape: ModelShape, seed: int, mode: str) -> dict:
+    """Per-tensor seeded random-init weights of a decoder, float32 arrays.
+
+    Streams: embedding (seed, 1000, 0), LM head (seed, 1000, 1), learned positions
+    (seed, 1000, 2), layer l tensor k (seed, l, k) with k = 1..7 for q, k, v, o and the
+    MLP matrices (Llama gate, up, down; OPT fc1, fc2).  N(0, init_std^2) draws (rounded to
+    bf16 values when mode is "bf16"), norm weights 1, biases 0.  Names: emb, head, pos,
+    nf/nfb (final norm), and per layer wq wk wv wo, wg wu wd (Llama) or w1 w2 with biases
+    bq bk bv bo b1 b2 (OPT), n1/n2 (and n1b/n2b for LayerNorm).
+    """
+    rnd = bf16_round if mode == "bf16" else (lambda a: a.astype(np.float32))
+    d, dkv, ff, V, std = shape.d_model, shape.n_kv_heads * shape.head_dim, shape.d_ff, shape.vocab, shape.init_std
+    W = {"emb": rnd(normal((V, d), std, seed, 1000, 0))}
+    for l in range(shape.n_layers):
+        def t(k, shp):
+            return rnd(normal(shp, std, seed, l, k))
+        L = {"wq": t(1, (d, d)), "wk": t(2, (dkv, d)), "wv": t(3, (dkv, d)), "wo": t(4, (d, d))}
+        if shape.family == "llama":
+            L.update({"wg": t(5, (ff, d)), "wu": t(6, (ff, d)), "wd": t(7, (d, ff)),
+                      "n1": np.ones(d, np.float32), "n2": np.ones(d, np.float32)})
+        else:
+            L.update({"w1": t(5, (ff, d)), "w2": t(6, (d, ff)),
+                      "n1": np.ones(d, np.float32), "n1b": np.zeros(d, np.float32),
+                      "n2": np.ones(d, np.float32), "n2b": np.zeros(d, np.float32)})
+            for b, n in (("bq", d), ("bk", dkv), ("bv", dkv), ("bo", d), ("b1", ff), ("b2", d)):
+                L[b] = np.zeros(n, np.float32)
+        W[l] = L
+    W["nf"] = np.ones(d, np.float32)
+    if shape.family == "llama":
+        W["head"] = rnd(normal((V, d), std, seed, 1000, 1))
+    else:
+        W["nfb"] = np.zeros(d, np.float32)
+        W["pos"] = rnd(normal((shape.max_pos + 2, d), std, seed, 1000, 2))
+    return W
+
+
+def device_normal(shape, std: float, seed: int, *ids: int, device="cuda", dtype=None):
+    """N(0, std^2) draws generated on the device from a torch generator seeded by (seed, *ids).
+
+    For full-size models, whose weights are too large to draw on the host quickly; the
+    values differ from normal() for the same ids.
+    """
+    import torch
+
+    key = int(np.random.SeedSequence([seed, *ids]).generate_state(1, np.uint64)[0] >> 1)
+    g = torch.Generator(device=device)
+    g.manual_seed(key)
+    a = torch.randn(shape, generator=g, device=device, dtype=torch.float32).mul_(std)
+    return a.to(dtype) if dtype is not None else a
+
+
+def device_model_weights(shape: ModelShape, seed: int, dtype, device="cuda") -> dict:
+    """model_weights() with the same names and streams, drawn on the device (torch tensors)."""
+    import torch
+
+    d, dkv, ff, V, std = shape.d_model, shape.n_kv_heads * shape.head_dim, shape.d_ff, shape.vocab, shape.init_std
+    ones = lambda n: torch.ones(n, dtype=dtype, device=device)
+    zeros = lambda n: torch.zeros(n, dtype=dtype, device=device)
+    W = {"emb": device_normal((V, d), std, seed, 1000, 0, device=device, dtype=dtype)}
+    for l in range(shape.n_layers):
+        def t(k, shp):
+            return device_normal(shp, std, seed, l, k, device=device, dtype=dtype)
+        L = {"wq": t(1, (d, d)), "wk": t(2, (dkv, d)), "wv": t(3, (dkv, d)), "wo": t(4, (d, d))}
+        if shape.family == "llama":
+            L.update({"wg": t(5, (ff, d)), "wu": t(6, (ff, d)), "wd": t(7, (d, ff)), "n1": ones(d), "n2": ones(d)})
+        else:
+            L.update({"w1": t(5, (ff, d)), "w2": t(6, (d, ff)), "n1": ones(d), "n1b": zeros(d), "n2": ones(d),
+                      "n2b": zeros(d)})
+            for b, n in (("bq", d), ("bk", dkv), ("bv", dkv), ("bo", d), ("b1", ff), ("b2", d)):
+                L[b] = zeros(n)
+        W[l] = L
+    W["nf"] = ones(d)
+    if shape.family == "llama":
+        W["head"] = device_normal((V, d), std, seed, 1000, 1, device=device, dtype=dtype)
+    else:
+        W["nfb"] = zeros(d)
+        W["pos"] = device_normal((shape.max_pos + 2, d), std, seed, 1000, 2, device=device, dtype=dtype)
+    return W
+
+
+def device_quantize_int4_g128(w):
+    """quantize_int4_g128() on a device tensor (bf16 values): (packed uint8 [N][K/2], scales bf16 [N][K/128])."""
+    import torch
+
+    n, k = w.shape
+    if k % 128:
+        raise ValueError("K must be a multiple of 128")
+    g = w.float().reshape(n, k // 128, 128)
+    s = (g.abs().amax(dim=2) / 7.0).to(torch.bfloat16)
+    sf = s.float()
+    safe = torch.where(sf == 0, torch.ones_like(sf), sf)
+    q = torch.round(g / safe[:, :, None]).clamp_(-7, 7)
+    q = torch.where(sf[:, :, None] == 0, torch.zeros_like(q), q).to(torch.int16).reshape(n, k)
+    nib = (q & 0xF).to(torch.uint8)
+    packed = nib[:, 0::2] | (nib[:, 1::2] << 4)
+    return packed.contiguous(), s.contiguous()

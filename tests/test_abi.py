@@ -86,3 +86,9 @@ def test_basis_workspace_grows_with_block():
     a = Z.basis_workspace_bytes(4096, 32)
     b = Z.basis_workspace_bytes(4096, 64)
     assert 0 < a < b
+
+
+def test_basis_init_workspace_holds_the_gram():
+    for d in (129, 4096):
+        g = (d * d * 4 + 255) // 256 * 256
+        assert Z.basis_init_workspace_bytes(d, 8) == g + Z.basis_workspace_bytes(d, 8)

@@ -329,7 +329,7 @@ def test_basis_init_matches_oracle(d, r, bf16):
     master = torch.empty(r, d, dtype=torch.float32, device=dev())
     ev = torch.empty(r, dtype=torch.float32, device=dev())
     res = torch.empty(1, dtype=torch.float32, device=dev())
-    ws = torch.empty(d * d * 4 + Z.basis_workspace_bytes(d, r), dtype=torch.uint8, device=dev())
+    ws = torch.empty(Z.basis_init_workspace_bytes(d, r), dtype=torch.uint8, device=dev())
     Z.basis_init(t_bf16(x) if bf16 else t_f32(x), r, ut, ws, ut_master=master, eigvals=ev, resid=res)
     um = host(master).T
     assert np.max(np.abs(um.T @ um - np.eye(r))) <= 1e-5
