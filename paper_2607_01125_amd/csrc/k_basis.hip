@@ -13,8 +13,8 @@
 //    Q = orth(G Q); orth is Cholesky-QR applied twice; Rayleigh-Ritz H = Q^T G Q;
 //    the b x b eigenproblem is solved by a parallel cyclic Jacobi method in one
 //    workgroup (round-robin pairing, all disjoint rotations of a round at once);
-//    U = Q S[:, top r].  The d x b blocks and all small matrices are fp64; G is
-//    read as fp32 (the only large operand).
+//    U = Q S[:, top r].  The iteration's products G Q run on fp32 MFMA; the
+//    orthonormalisation, the Rayleigh-Ritz product and all small matrices are fp64.
 //  * Sign: each column is flipped so its largest-magnitude entry is positive,
 //    lowest index on ties.
 #include "common.hpp"
@@ -107,166 +107,510 @@ __global__ void gram_f32_kernel(const float* __restrict__ x, int64_t n_tok, int6
 }
 
 // --------------------------------------------------------------- subspace iteration
+// Per iteration: Y = G Q on fp32 MFMA (fp32 copy of Q, K split across workgroups into
+// fp32 partial products summed in a fixed order into fp64), then Q = orth(Y) by
+// Cholesky-QR applied twice in fp64 (column Gram M = Y^T Y from fixed-order partial
+// sums, M = L L^T in LDS, L^{-1} in place, Q = Y L^{-T}).  The fp32 products only
+// steer the subspace; the Rayleigh-Ritz step that yields the eigenvectors forms G Q
+// with fp64 accumulation, so the result carries the accuracy of the fp32 Gram.
+constexpr int GQ_ROWS = 128;   // rows of G per workgroup of the products
+constexpr int GQ_K = 32;       // contraction chunk staged in LDS
+constexpr int NPART = 64;      // workgroups (partial sums) of the column-Gram pass
+
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// K split of the products: enough workgroups to cover the chip, chunks a multiple of GQ_K.
+void ksplit_for(int64_t d, int& ks, int64_t& kchunk) {
+  const int64_t nrb = (d + GQ_ROWS - 1) / GQ_ROWS;
+  int k = (int)((512 + nrb - 1) / nrb);
+  k = k < 1 ? 1 : (k > 8 ? 8 : k);
+  while (k > 1 && d / k < 256) --k;
+  kchunk = ((d + k - 1) / k + GQ_K - 1) / GQ_K * GQ_K;
+  ks = (int)((d + kchunk - 1) / kchunk);
+}
+
 struct EigWs {
-  double* q;      // [d][b]
-  double* y;      // [d][b]
+  double* q;      // [d][b] orthonormal block
+  double* y;      // [d][b] work block
+  float* q32;     // [d][b] fp32 copy of q
+  double* part;   // [ks][d][b] partial products (fp32 or fp64 elements)
+  double* mp;     // [NPART][b][b] partial column Grams
   double* m;      // [b][b]
+  double* linvt;  // [b][b] (L^{-1})^T
+  double* chol;   // [b][b + 1] Cholesky / Jacobi work matrix (when it does not fit in LDS)
+  double* jac;    // [b][b + 1] Jacobi rotations (when they do not fit in LDS)
   double* s;      // [b][b] eigenvectors of H (columns)
   double* theta;  // [b]
   int* order;     // [b]
   double* u;      // [d][r]
 };
 
-size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
-
-EigWs carve(void* ws, int64_t d, int b, int r) {
+EigWs carve(void* ws, int64_t d, int b, int r, int ks) {
   char* p = static_cast<char*>(ws);
   EigWs w;
   w.q = reinterpret_cast<double*>(p); p += align256((size_t)d * b * 8);
   w.y = reinterpret_cast<double*>(p); p += align256((size_t)d * b * 8);
+  w.q32 = reinterpret_cast<float*>(p); p += align256((size_t)d * b * 4);
+  w.part = reinterpret_cast<double*>(p); p += align256((size_t)ks * d * b * 8);
+  w.mp = reinterpret_cast<double*>(p); p += align256((size_t)NPART * b * b * 8);
   w.m = reinterpret_cast<double*>(p); p += align256((size_t)b * b * 8);
+  w.linvt = reinterpret_cast<double*>(p); p += align256((size_t)b * b * 8);
+  w.chol = reinterpret_cast<double*>(p); p += align256((size_t)b * (b + 1) * 8);
+  w.jac = reinterpret_cast<double*>(p); p += align256((size_t)b * (b + 1) * 8);
   w.s = reinterpret_cast<double*>(p); p += align256((size_t)b * b * 8);
   w.theta = reinterpret_cast<double*>(p); p += align256((size_t)b * 8);
   w.order = reinterpret_cast<int*>(p); p += align256((size_t)b * 4);
-  w.u = reinterpret_cast<double*>(p);
+  w.u = reinterpret_cast<double*>(p); p += align256((size_t)d * r * 8);
   return w;
 }
 
-__global__ void omega_kernel(double* q, int64_t d, int b, uint64_t seed) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < d * b; i += (int64_t)gridDim.x * blockDim.x)
-    q[i] = (double)rng::gauss_at(seed, 0xFFFFFFFFu, 0xB0515u, (uint64_t)i);
+size_t carve_bytes(int64_t d, int b, int r, int ks) {
+  return align256((size_t)d * b * 8) * 2 + align256((size_t)d * b * 4) + align256((size_t)ks * d * b * 8) +
+         align256((size_t)NPART * b * b * 8) + align256((size_t)b * b * 8) * 3 + align256((size_t)b * (b + 1) * 8) * 2 +
+         align256((size_t)b * 8) +
+         align256((size_t)b * 4) + align256((size_t)d * r * 8);
 }
 
-// Y[d][nc] = G[d][d] (fp32) * Q[d][ldq] (fp64, first nc columns); 64 x 64 tiles.
-__global__ void __launch_bounds__(256) gq_kernel(const float* __restrict__ g, const double* __restrict__ q, double* __restrict__ y,
-                                                 int64_t d, int ldq, int nc) {
-  __shared__ double gs[64][17];
-  __shared__ double qs[16][65];
-  const int64_t r0 = (int64_t)blockIdx.x * 64;
-  const int c0 = blockIdx.y * 64;
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double acc[4][4] = {};
-  for (int64_t k0 = 0; k0 < d; k0 += 16) {
-    for (int i = threadIdx.x; i < 64 * 16; i += 256) {
-      const int rr = i >> 4, kk = i & 15;
-      const int64_t row = r0 + rr, k = k0 + kk;
-      gs[rr][kk] = (row < d && k < d) ? (double)g[row * d + k] : 0.0;
-      const int kq = i >> 6, cc = i & 63;
-      const int64_t k2 = k0 + kq;
-      qs[kq][cc] = (k2 < d && c0 + cc < nc) ? q[k2 * ldq + c0 + cc] : 0.0;
-    }
-    __syncthreads();
+__global__ void omega_kernel(double* q, float* q32, int64_t d, int b, uint64_t seed) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < d * b; i += (int64_t)gridDim.x * blockDim.x) {
+    const float z = rng::gauss_at(seed, 0xFFFFFFFFu, 0xB0515u, (uint64_t)i);
+    q[i] = (double)z;
+    q32[i] = z;
+  }
+}
+
+// Stage G[r0 .. r0+127][k0 .. k0+31] (rows and columns past the range read as 0).
+__device__ __forceinline__ void stage_g(const float* __restrict__ g, int64_t d, int64_t r0, int64_t k0, int64_t k_end,
+                                        float (*gs)[GQ_K + 1]) {
+  for (int e = threadIdx.x; e < GQ_ROWS * GQ_K / 4; e += 256) {
+    const int row = e >> 3, kc = (e & 7) * 4;
+    const int64_t gr = r0 + row, gk = k0 + kc;
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (gr < d) {
+      const float* src = g + gr * d + gk;
+      if ((d & 3) == 0 && gk + 3 < k_end) {
+        const float4 f = *reinterpret_cast<const float4*>(src);
+        v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+      } else {
 #pragma unroll
-    for (int kk = 0; kk < 16; ++kk) {
-      double a[4], bb[4];
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        a[p] = gs[ty * 4 + p][kk];
-        bb[p] = qs[kk][tx * 4 + p];
+        for (int t = 0; t < 4; ++t) v[t] = (gk + t < k_end) ? src[t] : 0.f;
       }
+    }
 #pragma unroll
-      for (int p = 0; p < 4; ++p)
+    for (int t = 0; t < 4; ++t) gs[row][kc + t] = v[t];
+  }
+}
+
+// part[ks][d][b] (fp32) = G[:, K range ks] Q32[K range ks][:] on v_mfma_f32_16x16x4f32;
+// grid (row blocks of 128, ks, column blocks of 64); four waves of 32 rows x 64 columns.
+// The next 32-deep chunk of G and Q is loaded into registers while the current one is
+// multiplied out of LDS.
+__global__ void __launch_bounds__(256) gq32_kernel(const float* __restrict__ g, const float* __restrict__ q,
+                                                   float* __restrict__ part, int64_t d, int b, int64_t kchunk) {
+  __shared__ float gs[GQ_ROWS][GQ_K + 1];
+  __shared__ float qs[GQ_K][80];
+  const int64_t r0 = (int64_t)blockIdx.x * GQ_ROWS;
+  const int64_t k_begin = (int64_t)blockIdx.y * kchunk;
+  const int64_t k_end = k_begin + kchunk < d ? k_begin + kchunk : d;
+  const int c0 = blockIdx.z * 64;
+  const int t = threadIdx.x;
+  const int wave = t >> 6, lane = t & 63;
+  const int lr = lane & 15, lk = lane >> 4;
+  const bool vec = (d & 3) == 0;
+  float gv[4][4], qv[8];
+  auto load = [&](int64_t k0) {
 #pragma unroll
-        for (int s = 0; s < 4; ++s) acc[p][s] += a[p] * bb[s];
+    for (int u = 0; u < 4; ++u) {
+      const int e = t + 256 * u;
+      const int row = e >> 3, kc = (e & 7) * 4;
+      const int64_t gr = r0 + row, gk = k0 + kc;
+      const float* src = g + gr * d + gk;
+      if (gr < d && vec && gk + 3 < k_end) {
+        const float4 f = *reinterpret_cast<const float4*>(src);
+        gv[u][0] = f.x; gv[u][1] = f.y; gv[u][2] = f.z; gv[u][3] = f.w;
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) gv[u][c] = (gr < d && gk + c < k_end) ? src[c] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = t + 256 * u;
+      const int kk = e >> 6, cc = e & 63;
+      const int64_t gk = k0 + kk;
+      qv[u] = (gk < k_end && c0 + cc < b) ? q[gk * b + c0 + cc] : 0.f;
+    }
+  };
+  floatx4 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  if (k_begin < k_end) load(k_begin);
+  for (int64_t k0 = k_begin; k0 < k_end; k0 += GQ_K) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = t + 256 * u;
+      const int row = e >> 3, kc = (e & 7) * 4;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) gs[row][kc + c] = gv[u][c];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = t + 256 * u;
+      qs[e >> 6][e & 63] = qv[u];
+    }
+    __syncthreads();
+    if (k0 + GQ_K < k_end) load(k0 + GQ_K);
+#pragma unroll
+    for (int kk = 0; kk < GQ_K; kk += 4) {
+      float a[2], bq[4];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = gs[wave * 32 + i * 16 + lr][kk + lk];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bq[j] = qs[kk + lk][j * 16 + lr];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], bq[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
-  for (int p = 0; p < 4; ++p)
-    for (int s = 0; s < 4; ++s) {
-      const int64_t row = r0 + ty * 4 + p;
-      const int c = c0 + tx * 4 + s;
-      if (row < d && c < nc) y[row * nc + c] = acc[p][s];
-    }
+  float* out = part + (int64_t)blockIdx.y * d * b;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t row = r0 + wave * 32 + i * 16 + lk * 4 + v;
+        const int col = c0 + j * 16 + lr;
+        if (row < d && col < b) out[row * b + col] = acc[i][j][v];
+      }
 }
 
-// M[b][b] = A^T B for A, B [d][b] (fp64); one 16 x 16 output tile per block, rows in order.
-__global__ void __launch_bounds__(256) atb_kernel(const double* __restrict__ a, const double* __restrict__ bm, double* __restrict__ m,
-                                                  int64_t d, int b) {
-  __shared__ double as[64][17];
-  __shared__ double bs[64][17];
-  const int i0 = blockIdx.x * 16, j0 = blockIdx.y * 16;
-  const int ti = threadIdx.x >> 4, tj = threadIdx.x & 15;
-  double acc = 0.0;
-  for (int64_t k0 = 0; k0 < d; k0 += 64) {
-    for (int e = threadIdx.x; e < 64 * 16; e += 256) {
-      const int kk = e >> 4, cc = e & 15;
-      const int64_t k = k0 + kk;
-      as[kk][cc] = (k < d && i0 + cc < b) ? a[k * b + i0 + cc] : 0.0;
-      bs[kk][cc] = (k < d && j0 + cc < b) ? bm[k * b + j0 + cc] : 0.0;
+// part[ks][d][nc] (fp64) = G[:, K range ks] Q[K range ks][:nc] with fp64 accumulation
+// (G read as fp32); grid (row blocks of 128, ks, column blocks of 64); each thread 8 rows
+// x 4 columns.
+__global__ void __launch_bounds__(256) gq64_kernel(const float* __restrict__ g, const double* __restrict__ q,
+                                                   double* __restrict__ part, int64_t d, int nc, int64_t kchunk) {
+  __shared__ float gs[GQ_ROWS][GQ_K + 1];
+  __shared__ double qs[GQ_K][64];
+  const int64_t r0 = (int64_t)blockIdx.x * GQ_ROWS;
+  const int64_t k_begin = (int64_t)blockIdx.y * kchunk;
+  const int64_t k_end = k_begin + kchunk < d ? k_begin + kchunk : d;
+  const int c0 = blockIdx.z * 64;
+  const int tc = threadIdx.x & 15, tr = threadIdx.x >> 4;   // columns tc + 16 j, rows tr * 8 + i
+  double acc[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int64_t k0 = k_begin; k0 < k_end; k0 += GQ_K) {
+    stage_g(g, d, r0, k0, k_end, gs);
+    for (int e = threadIdx.x; e < GQ_K * 64; e += 256) {
+      const int kk = e >> 6, cc = e & 63;
+      const int64_t gk = k0 + kk;
+      qs[kk][cc] = (gk < k_end && c0 + cc < nc) ? q[gk * nc + c0 + cc] : 0.0;
     }
     __syncthreads();
-    for (int kk = 0; kk < 64; ++kk) acc += as[kk][ti] * bs[kk][tj];
+    for (int kk = 0; kk < GQ_K; ++kk) {
+      double a[8], bq[4];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a[i] = (double)gs[tr * 8 + i][kk];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bq[j] = qs[kk][tc + 16 * j];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fma(a[i], bq[j], acc[i][j]);
+    }
     __syncthreads();
   }
-  if (i0 + ti < b && j0 + tj < b) m[(i0 + ti) * b + j0 + tj] = acc;
+  double* out = part + (int64_t)blockIdx.y * d * nc;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t row = r0 + tr * 8 + i;
+      const int col = c0 + tc + 16 * j;
+      if (row < d && col < nc) out[row * nc + col] = acc[i][j];
+    }
 }
 
-// In-place upper Cholesky factor of M (M = R^T R), one workgroup.
-__global__ void __launch_bounds__(256) chol_kernel(double* m, int b) {
-  for (int j = 0; j < b; ++j) {
-    __shared__ double piv;
-    if (threadIdx.x == 0) {
-      double s = m[j * b + j];
-      for (int k = 0; k < j; ++k) s -= m[k * b + j] * m[k * b + j];
-      piv = s > 1e-300 ? sqrt(s) : 1e-150;
-      m[j * b + j] = piv;
-    }
-    __syncthreads();
-    for (int i = j + 1 + threadIdx.x; i < b; i += blockDim.x) {
-      double s = m[j * b + i];
-      for (int k = 0; k < j; ++k) s -= m[k * b + j] * m[k * b + i];
-      m[j * b + i] = s / piv;
-    }
-    __syncthreads();
+// y[n] = sum over ks of part[ks][n] in split order (fp32 or fp64 partials), fp64 result.
+template <typename T>
+__global__ void sum_parts_kernel(const T* __restrict__ part, int ks, int64_t n, double* __restrict__ y) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    double s = 0.0;
+    for (int k = 0; k < ks; ++k) s += (double)part[(int64_t)k * n + i];
+    y[i] = s;
   }
 }
 
-// Q = Y R^{-1} row by row (R upper triangular in m).
-__global__ void trsm_rows_kernel(const double* __restrict__ y, const double* __restrict__ rmat, double* __restrict__ q,
-                                 int64_t d, int b) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < d; i += (int64_t)gridDim.x * blockDim.x) {
-    for (int j = 0; j < b; ++j) {
-      double s = y[i * b + j];
-      for (int k = 0; k < j; ++k) s -= q[i * b + k] * rmat[k * b + j];
-      q[i * b + j] = s / rmat[j * b + j];
+// mp[p][i][j] = sum over the rows assigned to workgroup p of a[row][i] * bm[row][j]
+// (fp64), for the CTT x CTT output block (blockIdx.y / nbk, blockIdx.y % nbk), CTT = 16 TU;
+// rows are dealt to the gridDim.x workgroups in chunks of 32, each summed in row order.
+template <int TU>
+__global__ void __launch_bounds__(256) cross_partial_kernel(const double* __restrict__ a, const double* __restrict__ bm,
+                                                            int64_t d, int b, double* __restrict__ mp) {
+  constexpr int CTT = 16 * TU;
+  __shared__ double as[32][CTT + 1];
+  __shared__ double bs[32][CTT + 1];
+  const int nbk = (b + CTT - 1) / CTT;
+  const int i0 = (blockIdx.y / nbk) * CTT, j0 = (blockIdx.y % nbk) * CTT;
+  const int ti = threadIdx.x >> 4, tj = threadIdx.x & 15;  // outputs (ti + 16 u, tj + 16 v)
+  double acc[TU][TU];
+#pragma unroll
+  for (int u = 0; u < TU; ++u)
+#pragma unroll
+    for (int v = 0; v < TU; ++v) acc[u][v] = 0.0;
+  for (int64_t c = blockIdx.x; c * 32 < d; c += gridDim.x) {
+    const int64_t row0 = c * 32;
+    for (int e = threadIdx.x; e < 32 * CTT; e += 256) {
+      const int rr = e / CTT, cc = e % CTT;
+      const int64_t row = row0 + rr;
+      as[rr][cc] = (row < d && i0 + cc < b) ? a[row * b + i0 + cc] : 0.0;
+      bs[rr][cc] = (row < d && j0 + cc < b) ? bm[row * b + j0 + cc] : 0.0;
+    }
+    __syncthreads();
+    for (int rr = 0; rr < 32; ++rr) {
+      double av[TU], bv[TU];
+#pragma unroll
+      for (int u = 0; u < TU; ++u) av[u] = as[rr][ti + 16 * u];
+#pragma unroll
+      for (int v = 0; v < TU; ++v) bv[v] = bs[rr][tj + 16 * v];
+#pragma unroll
+      for (int u = 0; u < TU; ++u)
+#pragma unroll
+        for (int v = 0; v < TU; ++v) acc[u][v] = fma(av[u], bv[v], acc[u][v]);
+    }
+    __syncthreads();
+  }
+  double* out = mp + (int64_t)blockIdx.x * b * b;
+#pragma unroll
+  for (int u = 0; u < TU; ++u)
+#pragma unroll
+    for (int v = 0; v < TU; ++v) {
+      const int i = i0 + ti + 16 * u, j = j0 + tj + 16 * v;
+      if (i < b && j < b) out[i * b + j] = acc[u][v];
+    }
+}
+
+// m[e] = sum over p of mp[p][e] in a fixed order: 64 entries per workgroup, each summed
+// by 4 threads over interleaved quarters of the partials, then the 4 sums in order.
+__global__ void __launch_bounds__(256) reduce_parts_kernel(const double* __restrict__ mp, int np, int64_t n,
+                                                           double* __restrict__ m) {
+  __shared__ double sh[4][64];
+  const int64_t e = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
+  const int q = threadIdx.x >> 6;
+  double s = 0.0;
+  if (e < n)
+    for (int p = q; p < np; p += 4) s += mp[(int64_t)p * n + e];
+  sh[q][threadIdx.x & 63] = s;
+  __syncthreads();
+  if (q == 0 && e < n) m[e] = ((sh[0][threadIdx.x] + sh[1][threadIdx.x]) + sh[2][threadIdx.x]) + sh[3][threadIdx.x];
+}
+
+// M = A^T B for A, B [d][b] (fp64), deterministic: partial sums over row chunks, then
+// their sum in partial order.
+void cross(const double* a, const double* bm, int64_t d, int b, double* mp, double* m, hipStream_t s) {
+  int np = (int)((d + 63) / 64);
+  np = np < 1 ? 1 : (np > NPART ? NPART : np);
+  if (b <= 64) {
+    const int nbk = (b + 63) / 64;
+    cross_partial_kernel<4><<<dim3((unsigned)np, (unsigned)(nbk * nbk)), 256, 0, s>>>(a, bm, d, b, mp);
+  } else {
+    const int nbk = (b + 127) / 128;
+    cross_partial_kernel<8><<<dim3((unsigned)np, (unsigned)(nbk * nbk)), 256, 0, s>>>(a, bm, d, b, mp);
+  }
+  reduce_parts_kernel<<<(unsigned)(((int64_t)b * b + 63) / 64), 256, 0, s>>>(mp, np, (int64_t)b * b, m);
+}
+
+// Sum over the G consecutive lanes of a group (G = 1, 2 or 4), fixed order.
+template <int G>
+__device__ __forceinline__ double group_sum(double v) {
+  if (G >= 2) v += __shfl_xor(v, 1, 64);
+  if (G >= 4) v += __shfl_xor(v, 2, 64);
+  return v;
+}
+
+// M = L L^T (left-looking Cholesky), then X = L^{-1} by forward substitution, written
+// out transposed: linvt[k][j] = X[j][k].  One workgroup; G lanes share each row (or
+// column) and split its dot products.  The matrix sits in LDS with row stride b + 1
+// (conflict-free column access) when it fits (b <= 128), else in `scratch` with the
+// same layout.  L occupies the lower triangle; column c of X is kept transposed in row
+// c's upper part (A[c][i] = X[i][c], i > c) and its diagonal in `xd`.
+template <bool IN_LDS, int G>
+__global__ void __launch_bounds__(256) chol_inv_kernel(const double* __restrict__ m, double* __restrict__ scratch,
+                                                       double* __restrict__ linvt, int b) {
+  __shared__ double lds[IN_LDS ? 128 * 129 : 1];
+  __shared__ double xd[512];
+  __shared__ double sq[512];   // running sum of squares of each row of L
+  constexpr int R = 256 / G;   // rows in flight
+  const int ld = b + 1;
+  double* A = IN_LDS ? lds : scratch;
+  const int t = threadIdx.x, gl = t % G;
+  for (int i = t / 64; i < b; i += 4)
+    for (int k = t % 64; k < b; k += 64) A[i * ld + k] = m[i * b + k];
+  for (int i = t; i < b; i += 256) sq[i] = 0.0;
+  __syncthreads();
+  if (t == 0) {
+    const double s00 = A[0];
+    A[0] = s00 > 1e-300 ? sqrt(s00) : 1e-150;
+  }
+  __syncthreads();
+  // step j: every row i > j forms L_ij = (M_ij - sum_{k<j} L_ik L_jk) / L_jj; row j + 1,
+  // then complete up to column j, forms its diagonal from its running sum of squares
+  for (int j = 0; j < b - 1; ++j) {
+    const double* lj = A + j * ld;
+    const double inv = 1.0 / lj[j];
+    for (int i = j + 1 + t / G; i < b; i += R) {
+      double* li = A + i * ld;
+      double s0 = 0.0, s1 = 0.0;
+      int k = gl;
+      for (; k + G < j; k += 2 * G) {
+        s0 = fma(li[k], lj[k], s0);
+        s1 = fma(li[k + G], lj[k + G], s1);
+      }
+      if (k < j) s0 = fma(li[k], lj[k], s0);
+      const double dotv = group_sum<G>(s0 + s1);
+      if (gl == 0) {
+        const double v = (li[j] - dotv) * inv;
+        li[j] = v;
+        const double ss = sq[i] + v * v;
+        sq[i] = ss;
+        if (i == j + 1) {
+          const double dd = li[i] - ss;
+          li[i] = dd > 1e-300 ? sqrt(dd) : 1e-150;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // forward substitution L x = e_c per column c: x_c = 1 / L_cc,
+  // x_i = -(sum_{k=c}^{i-1} L_ik x_k) / L_ii, x_k (k > c) stored at A[c][k]
+  for (int c = t; c < b; c += 256) xd[c] = 1.0 / A[c * ld + c];
+  __syncthreads();
+  for (int c = t / G; c < b; c += R) {
+    double* xr = A + c * ld;
+    for (int i = c + 1; i < b; ++i) {
+      const double* li = A + i * ld;
+      double s0 = gl == 0 ? li[c] * xd[c] : 0.0, s1 = 0.0;
+      int k = c + 1 + gl;
+      for (; k + G < i; k += 2 * G) {
+        s0 = fma(li[k], xr[k], s0);
+        s1 = fma(li[k + G], xr[k + G], s1);
+      }
+      if (k < i) s0 = fma(li[k], xr[k], s0);
+      const double xi = -group_sum<G>(s0 + s1) * xd[i];
+      if (gl == 0) xr[i] = xi;
+    }
+  }
+  __syncthreads();
+  for (int k = t / 64; k < b; k += 4)
+    for (int jj = t % 64; jj < b; jj += 64)
+      linvt[k * b + jj] = jj > k ? A[k * ld + jj] : (jj == k ? xd[k] : 0.0);
+}
+
+// q[i][j] = sum over k <= j of y[i][k] linvt[k][j]  (Q = Y L^{-T}); also the fp32 copy.
+// Rows are processed 256 / b at a time (b <= 256: one thread per output), staged in LDS.
+__global__ void __launch_bounds__(256) apply_linv_kernel(const double* __restrict__ y, const double* __restrict__ linvt,
+                                                         int64_t d, int b, double* __restrict__ q, float* __restrict__ q32) {
+  __shared__ double lt[128 * 128];
+  __shared__ double yr[256];
+  const bool in_lds = b <= 128;
+  if (in_lds) {
+    for (int e = threadIdx.x; e < b * b; e += 256) lt[e] = linvt[e];
+  }
+  const double* L = in_lds ? lt : linvt;
+  const int rows = b <= 256 ? 256 / b : 1;          // rows per pass
+  const int t = threadIdx.x;
+  for (int64_t r0 = (int64_t)blockIdx.x * rows; r0 < d; r0 += (int64_t)gridDim.x * rows) {
+    __syncthreads();
+    if (b <= 256) {
+      const int64_t idx = r0 * b + t;
+      if (t < rows * b && r0 + t / b < d) yr[t] = y[idx];
+    }
+    __syncthreads();
+    if (b <= 256) {
+      const int rr = t / b, j = t % b;
+      const int64_t i = r0 + rr;
+      if (rr < rows && i < d) {
+        const double* yy = yr + rr * b;
+        double s0 = 0.0, s1 = 0.0;
+        int k = 0;
+        for (; k + 1 <= j; k += 2) {
+          s0 = fma(yy[k], L[k * b + j], s0);
+          s1 = fma(yy[k + 1], L[(k + 1) * b + j], s1);
+        }
+        if (k == j) s0 = fma(yy[k], L[k * b + j], s0);
+        const double sum = s0 + s1;
+        q[i * b + j] = sum;
+        if (q32) q32[i * b + j] = (float)sum;
+      }
+    } else {
+      for (int j = t; j < b; j += 256) {
+        const double* yy = y + r0 * b;
+        double sum = 0.0;
+        for (int k = 0; k <= j; ++k) sum = fma(yy[k], L[k * b + j], sum);
+        q[r0 * b + j] = sum;
+        if (q32) q32[r0 * b + j] = (float)sum;
+      }
     }
   }
 }
 
-// Parallel cyclic Jacobi on the symmetric b x b matrix h (in place), eigenvectors in s.
-// Round-robin pairing: in each of the n-1 rounds of a sweep, index 0 is fixed and
-// the others rotate, giving n/2 disjoint pairs (n = b rounded up to even).
-__global__ void __launch_bounds__(256) jacobi_kernel(double* h, double* s, double* theta, int* order, int b, int sweeps) {
+// Parallel cyclic Jacobi on the symmetric b x b matrix hg, eigenvectors in s (global,
+// [b][b]), eigenvalues sorted descending into theta/order.  Round-robin pairing: in
+// each of the n-1 rounds of a sweep, index 0 is fixed and the others rotate, giving
+// n/2 disjoint pairs (n = b rounded up to even).  H and the rotations S are worked on
+// with row stride b + 1 (conflict-free column access), both in LDS when b <= 96, else
+// in `work` and `swork` ([b][b + 1] each); S is written to s ([b][b]) at the end.
+template <bool IN_LDS, int PMAX>
+__global__ void __launch_bounds__(256) jacobi_kernel(const double* __restrict__ hg, double* __restrict__ work,
+                                                     double* __restrict__ swork, double* __restrict__ s_out,
+                                                     double* theta, int* order, int b, int sweeps) {
+  __shared__ double hl[IN_LDS ? 96 * 97 : 1];
+  __shared__ double sl[IN_LDS ? 96 * 97 : 1];
   __shared__ double cs[256], sn[256];
   __shared__ int pp[256], qq[256];
   __shared__ double off_sh[256], tot_sh[256];
+  double* h = IN_LDS ? hl : work;
+  double* s = IN_LDS ? sl : swork;
+  const int ld = b + 1;
   const int n = (b + 1) & ~1;
-  for (int e = threadIdx.x; e < b * b; e += blockDim.x) s[e] = (e / b == e % b) ? 1.0 : 0.0;
+  const int t = threadIdx.x;
+  const int wv = t >> 6, lane = t & 63;
+  for (int i = t / 64; i < b; i += 4)
+    for (int j = t % 64; j < b; j += 64) {
+      s[i * ld + j] = (i == j) ? 1.0 : 0.0;
+      h[i * ld + j] = hg[i * b + j];
+    }
   __syncthreads();
   for (int sw = 0; sw < sweeps; ++sw) {
-    // convergence test: off-diagonal mass against the total
     double off = 0.0, tot = 0.0;
-    for (int e = threadIdx.x; e < b * b; e += blockDim.x) {
-      const double v = h[e] * h[e];
-      tot += v;
-      if (e / b != e % b) off += v;
-    }
-    off_sh[threadIdx.x] = off;
-    tot_sh[threadIdx.x] = tot;
+    for (int i = t / 64; i < b; i += 4)
+      for (int j = t % 64; j < b; j += 64) {
+        const double v = h[i * ld + j] * h[i * ld + j];
+        tot += v;
+        if (i != j) off += v;
+      }
+    off_sh[t] = off;
+    tot_sh[t] = tot;
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) {
-      if ((int)threadIdx.x < o) {
-        off_sh[threadIdx.x] += off_sh[threadIdx.x + o];
-        tot_sh[threadIdx.x] += tot_sh[threadIdx.x + o];
+      if (t < o) {
+        off_sh[t] += off_sh[t + o];
+        tot_sh[t] += tot_sh[t + o];
       }
       __syncthreads();
     }
-    const bool done = off_sh[0] <= 1e-30 * tot_sh[0];
+    const bool done = off_sh[0] <= 1e-26 * tot_sh[0];   // off-diagonal norm <= 1e-13 of the whole
     __syncthreads();
     if (done) break;
     for (int round = 0; round < n - 1; ++round) {
-      // pairs of this round
-      for (int k = threadIdx.x; k < n / 2; k += blockDim.x) {
+      for (int k = t; k < n / 2; k += 256) {
         int a, c;
         if (k == 0) {
           a = 0;
@@ -275,59 +619,88 @@ __global__ void __launch_bounds__(256) jacobi_kernel(double* h, double* s, doubl
           a = 1 + ((round + k) % (n - 1));
           c = 1 + ((round + n - 1 - k) % (n - 1));
         }
-        if (a > c) { const int t = a; a = c; c = t; }
+        if (a > c) { const int tt = a; a = c; c = tt; }
         pp[k] = a;
         qq[k] = c;
         double cc = 1.0, ss = 0.0;
         if (c < b) {
-          const double apq = h[a * b + c];
+          const double apq = h[a * ld + c];
           if (fabs(apq) > 1e-300) {
-            const double tau = (h[c * b + c] - h[a * b + a]) / (2.0 * apq);
-            const double t = (tau >= 0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-            cc = 1.0 / sqrt(1.0 + t * t);
-            ss = t * cc;
+            const double tau = (h[c * ld + c] - h[a * ld + a]) / (2.0 * apq);
+            const double tq = (tau >= 0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+            cc = 1.0 / sqrt(1.0 + tq * tq);
+            ss = tq * cc;
           }
         }
         cs[k] = cc;
         sn[k] = ss;
       }
       __syncthreads();
-      // columns: H <- H J, S <- S J
-      for (int e = threadIdx.x; e < (n / 2) * b; e += blockDim.x) {
-        const int k = e / b, i = e % b;
-        const int a = pp[k], c = qq[k];
-        if (c >= b || sn[k] == 0.0) continue;
-        const double hp = h[i * b + a], hq = h[i * b + c];
-        h[i * b + a] = cs[k] * hp - sn[k] * hq;
-        h[i * b + c] = sn[k] * hp + cs[k] * hq;
-        const double vp = s[i * b + a], vq = s[i * b + c];
-        s[i * b + a] = cs[k] * vp - sn[k] * vq;
-        s[i * b + c] = sn[k] * vp + cs[k] * vq;
+      // columns: H <- H J, S <- S J.  Wave w takes pairs w, w + 4, ...; each lane one row.
+      // All loads of a row are issued before its stores (the pairs are disjoint).
+      for (int kb = 0; kb < n / 2; kb += 4 * PMAX)
+      for (int i = lane; i < b; i += 64) {
+        double hp[PMAX], hq[PMAX], vp[PMAX], vq[PMAX];
+#pragma unroll
+        for (int u = 0; u < PMAX; ++u) {
+          const int k = kb + wv + 4 * u;
+          if (k < n / 2 && qq[k] < b) {
+            hp[u] = h[i * ld + pp[k]];
+            hq[u] = h[i * ld + qq[k]];
+            vp[u] = s[i * ld + pp[k]];
+            vq[u] = s[i * ld + qq[k]];
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < PMAX; ++u) {
+          const int k = kb + wv + 4 * u;
+          if (k < n / 2 && qq[k] < b) {
+            const double ck = cs[k], sk = sn[k];
+            h[i * ld + pp[k]] = ck * hp[u] - sk * hq[u];
+            h[i * ld + qq[k]] = sk * hp[u] + ck * hq[u];
+            s[i * ld + pp[k]] = ck * vp[u] - sk * vq[u];
+            s[i * ld + qq[k]] = sk * vp[u] + ck * vq[u];
+          }
+        }
       }
       __syncthreads();
-      // rows: H <- J^T H
-      for (int e = threadIdx.x; e < (n / 2) * b; e += blockDim.x) {
-        const int k = e / b, j = e % b;
-        const int a = pp[k], c = qq[k];
-        if (c >= b || sn[k] == 0.0) continue;
-        const double hp = h[a * b + j], hq = h[c * b + j];
-        h[a * b + j] = cs[k] * hp - sn[k] * hq;
-        h[c * b + j] = sn[k] * hp + cs[k] * hq;
+      // rows: H <- J^T H; each lane one column
+      for (int kb = 0; kb < n / 2; kb += 4 * PMAX)
+      for (int j = lane; j < b; j += 64) {
+        double ha[PMAX], hc[PMAX];
+#pragma unroll
+        for (int u = 0; u < PMAX; ++u) {
+          const int k = kb + wv + 4 * u;
+          if (k < n / 2 && qq[k] < b) {
+            ha[u] = h[pp[k] * ld + j];
+            hc[u] = h[qq[k] * ld + j];
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < PMAX; ++u) {
+          const int k = kb + wv + 4 * u;
+          if (k < n / 2 && qq[k] < b) {
+            const double ck = cs[k], sk = sn[k];
+            h[pp[k] * ld + j] = ck * ha[u] - sk * hc[u];
+            h[qq[k] * ld + j] = sk * ha[u] + ck * hc[u];
+          }
+        }
       }
       __syncthreads();
     }
   }
-  if (threadIdx.x == 0) {
-    // descending order of the diagonal (selection; b <= 512)
+  for (int i = t / 64; i < b; i += 4)
+    for (int j = t % 64; j < b; j += 64) s_out[i * b + j] = s[i * ld + j];
+  if (t == 0) {
     for (int i = 0; i < b; ++i) order[i] = i;
     for (int i = 0; i < b; ++i) {
       int best = i;
       for (int j = i + 1; j < b; ++j)
-        if (h[order[j] * b + order[j]] > h[order[best] * b + order[best]]) best = j;
-      const int t = order[i];
+        if (h[order[j] * ld + order[j]] > h[order[best] * ld + order[best]]) best = j;
+      const int tt = order[i];
       order[i] = order[best];
-      order[best] = t;
-      theta[i] = h[order[i] * b + order[i]];
+      order[best] = tt;
+      theta[i] = h[order[i] * ld + order[i]];
     }
   }
 }
@@ -408,29 +781,51 @@ __global__ void __launch_bounds__(256) resid_kernel(const double* __restrict__ y
   if (threadIdx.x == 0) *resid = (float)(worst / fmax(fabs(theta[0]), 1e-300));
 }
 
-hipError_t orth(EigWs& w, int64_t d, int b, hipStream_t s) {
-  // Cholesky-QR twice: y holds the block to orthonormalise, result in q.
-  for (int pass = 0; pass < 2; ++pass) {
-    const double* src = pass == 0 ? w.y : w.q;
-    atb_kernel<<<dim3((b + 15) / 16, (b + 15) / 16), 256, 0, s>>>(src, src, w.m, d, b);
-    chol_kernel<<<1, 256, 0, s>>>(w.m, b);
-    if (pass == 1) {
-      // second pass works in place: copy q to y first (trsm reads y, writes q)
-      hipError_t e = hipMemcpyAsync(w.y, w.q, (size_t)d * b * 8, hipMemcpyDeviceToDevice, s);
-      if (e != hipSuccess) return e;
-    }
-    int64_t gb = (d + 255) / 256;
-    trsm_rows_kernel<<<dim3((unsigned)gb), 256, 0, s>>>(w.y, w.m, w.q, d, b);
+// Q = orth(Y) by Cholesky-QR (applied `passes` times).  Reads y, leaves the
+// orthonormal block in q (and its fp32 copy in q32); y is overwritten.  Inside the
+// iteration one pass keeps the block well conditioned; the block handed to
+// Rayleigh-Ritz gets two, which makes it orthonormal to working precision.
+hipError_t orth(EigWs& w, int64_t d, int b, int passes, hipStream_t s) {
+  const unsigned gapp = (unsigned)((d * b + 255) / 256 > 256 ? 256 : (d * b + 255) / 256);
+  double* src = w.y;
+  double* dst = w.q;
+  for (int pass = 0; pass < passes; ++pass) {
+    cross(src, src, d, b, w.mp, w.m, s);
+    if (b <= 64) chol_inv_kernel<true, 4><<<1, 256, 0, s>>>(w.m, w.chol, w.linvt, b);
+    else if (b <= 128) chol_inv_kernel<true, 2><<<1, 256, 0, s>>>(w.m, w.chol, w.linvt, b);
+    else chol_inv_kernel<false, 1><<<1, 256, 0, s>>>(w.m, w.chol, w.linvt, b);
+    apply_linv_kernel<<<gapp, 256, 0, s>>>(src, w.linvt, d, b, dst, pass == passes - 1 ? w.q32 : nullptr);
+    double* t = src;
+    src = dst;
+    dst = t;
   }
+  // the result is in src; make it w.q
+  if (src != w.q) {
+    w.y = w.q;
+    w.q = src;
+  }
+  return hipGetLastError();
+}
+
+// G X with fp64 accumulation into y [d][nc] (X fp64 [d][nc], nc <= 512).
+hipError_t gx64(const float* g, const double* x, int64_t d, int nc, EigWs& w, double* y, hipStream_t s) {
+  int ks;
+  int64_t kchunk;
+  ksplit_for(d, ks, kchunk);
+  gq64_kernel<<<dim3((unsigned)((d + GQ_ROWS - 1) / GQ_ROWS), (unsigned)ks, (unsigned)((nc + 63) / 64)), 256, 0, s>>>(
+      g, x, w.part, d, nc, kchunk);
+  const int64_t n = d * nc;
+  sum_parts_kernel<double><<<(unsigned)((n + 255) / 256 > 4096 ? 4096 : (n + 255) / 256), 256, 0, s>>>(w.part, ks, n, y);
   return hipGetLastError();
 }
 
 }  // namespace
 
 size_t basis_ws_bytes(int64_t d, int32_t r, int32_t p) {
-  const int b = r + p;
-  return align256((size_t)d * b * 8) * 2 + align256((size_t)b * b * 8) * 2 + align256((size_t)b * 8) +
-         align256((size_t)b * 4) + align256((size_t)d * b * 8);
+  int ks;
+  int64_t kchunk;
+  ksplit_for(d, ks, kchunk);
+  return carve_bytes(d, r + p, r, ks);
 }
 
 hipError_t launch_gram(const void* x, int32_t dtype, int64_t n_tok, int64_t d, float* g, int accumulate, hipStream_t s) {
@@ -450,26 +845,34 @@ hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t 
                                   void* ut, int32_t ut_dtype, float* ut_master, float* eigvals, float* resid, void* ws,
                                   hipStream_t s) {
   const int b = r + p;
-  EigWs w = carve(ws, d, b, r);
-  const dim3 gq_grid((unsigned)((d + 63) / 64), (unsigned)((b + 63) / 64));
-  omega_kernel<<<dim3((unsigned)((d * b + 255) / 256 > 65535 ? 65535 : (d * b + 255) / 256)), 256, 0, s>>>(w.q, d, b, seed);
+  int ks;
+  int64_t kchunk;
+  ksplit_for(d, ks, kchunk);
+  EigWs w = carve(ws, d, b, r, ks);
+  const int64_t n = d * b;
+  const unsigned g1 = (unsigned)((n + 255) / 256 > 4096 ? 4096 : (n + 255) / 256);
+  omega_kernel<<<g1, 256, 0, s>>>(w.q, w.q32, d, b, seed);
+  const dim3 gq_grid((unsigned)((d + GQ_ROWS - 1) / GQ_ROWS), (unsigned)ks, (unsigned)((b + 63) / 64));
   for (int it = 0; it <= iters; ++it) {
-    gq_kernel<<<gq_grid, 256, 0, s>>>(g, w.q, w.y, d, b, b);
-    hipError_t e = orth(w, d, b, s);
+    gq32_kernel<<<gq_grid, 256, 0, s>>>(g, w.q32, reinterpret_cast<float*>(w.part), d, b, kchunk);
+    sum_parts_kernel<float><<<g1, 256, 0, s>>>(reinterpret_cast<const float*>(w.part), ks, n, w.y);
+    hipError_t e = orth(w, d, b, it == iters ? 2 : 1, s);
     if (e != hipSuccess) return e;
   }
-  // Rayleigh-Ritz: H = Q^T G Q
-  gq_kernel<<<gq_grid, 256, 0, s>>>(g, w.q, w.y, d, b, b);
-  atb_kernel<<<dim3((b + 15) / 16, (b + 15) / 16), 256, 0, s>>>(w.q, w.y, w.m, d, b);
-  jacobi_kernel<<<1, 256, 0, s>>>(w.m, w.s, w.theta, w.order, b, 40);
+  // Rayleigh-Ritz with fp64 accumulation: H = Q^T (G Q)
+  hipError_t e = gx64(g, w.q, d, b, w, w.y, s);
+  if (e != hipSuccess) return e;
+  cross(w.q, w.y, d, b, w.mp, w.m, s);
+  if (b <= 96) jacobi_kernel<true, 12><<<1, 256, 0, s>>>(w.m, w.chol, w.jac, w.s, w.theta, w.order, b, 40);
+  else jacobi_kernel<false, 12><<<1, 256, 0, s>>>(w.m, w.chol, w.jac, w.s, w.theta, w.order, b, 40);
   int64_t gb = (d * r + 255) / 256;
   if (gb > 65535) gb = 65535;
   ritz_vectors_kernel<<<dim3((unsigned)gb), 256, 0, s>>>(w.q, w.s, w.order, w.u, d, b, r);
   finish_basis_kernel<<<dim3((unsigned)r), 256, 0, s>>>(w.u, w.theta, d, r, ut, ut_dtype == ZOACT_BF16 ? 1 : 0,
                                                         ut_master, eigvals);
   if (resid) {
-    // y = G u (u has r columns)
-    gq_kernel<<<dim3((unsigned)((d + 63) / 64), (unsigned)((r + 63) / 64)), 256, 0, s>>>(g, w.u, w.y, d, r, r);
+    e = gx64(g, w.u, d, r, w, w.y, s);   // y = G u
+    if (e != hipSuccess) return e;
     resid_kernel<<<1, 256, 0, s>>>(w.y, w.u, w.theta, d, r, resid);
   }
   return hipGetLastError();

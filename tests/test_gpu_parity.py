@@ -318,7 +318,8 @@ def test_gram(bf16):
     assert np.max(np.abs(host(g) - 2 * ref)) <= 2e-5 * np.max(np.abs(ref))
 
 
-@pytest.mark.parametrize("d,r,bf16", [(128, 8, False), (256, 8, True), (512, 32, True)])
+@pytest.mark.parametrize("d,r,bf16", [(128, 8, False), (256, 8, True), (512, 32, True), (2048, 32, True),
+                                       (1000, 16, False), (384, 100, False), (640, 64, True)])
 def test_basis_init_matches_oracle(d, r, bf16):
     announce("basis", d, r, bf16)
     x = _gapped_x(2 * d, d, r, seed=d + r)
