@@ -1,6 +1,6 @@
 """Benchmark of the forward-only ZO step on one MI355X.
 
-Workload (default, `single_linear_4096`): one adapted linear layer in bf16,
+Headline workload (`single_linear_4096`): one adapted linear layer in bf16,
 d_in = d_out = 4096, rank r = 32, 8192 tokens per perturbation half, activations
 with a planted low-rank structure (64 directions carrying 90% of the variance),
 W ~ N(0, 0.02^2).  One step is the whole hot path of a +/- ZO step:
@@ -9,16 +9,26 @@ W ~ N(0, 0.02^2).  One step is the whole hot path of a +/- ZO step:
 The activation basis U comes from the one-shot basis initialisation (timed
 separately, outside the step).  Inputs are resident in HBM before timing starts.
 
-Prints one JSON line: steps/s, ms/step, the roofline entry of the dominant kernel
-(the fused GEMM: algorithmic FLOPs per launch / its mean duration measured with
-HIP events on its stream, against the 2.5 PFLOP/s dense bf16 MFMA peak) and the
-oracle's throughput on the host cores for the same workload.
+Besides the headline line the run measures (unless --quick):
+  * the fused +/- adapted linear (projection + fused GEMM) at the Llama-3-8B layer
+    shapes, M = 8192 stacked rows, bf16 and INT4 weights: TFLOP/s per shape and
+    the FLOP-weighted mean;
+  * full ZO steps of random-initialised decoders: Llama-3-8B shape in bf16 and with
+    INT4 weights (16 x 256 tokens, r = 32 on all seven projections) and OPT-13B
+    shape in bf16 (8 x 512 tokens, r = 64 on q, v, out, fc1, fc2, basis
+    initialisation from 32 x 512 calibration tokens timed): steps/s, model TFLOP/s;
+  * ZO-Adam over the Llama-3-8B arena (44,040,192 coefficients): GB/s against HBM.
+
+Prints one JSON line.  `roofline` is the fused GEMM of the headline workload:
+algorithmic FLOPs per launch over its mean duration (HIP events on its stream),
+against the 2.5 PFLOP/s dense bf16 MFMA peak.
 """
 from __future__ import annotations
 
 import argparse
 import hashlib
 import json
+import math
 import os
 import sys
 import time
@@ -28,14 +38,21 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
+METRIC = "ZO steps/sec (±ε forwards + Adam) and adapted-linear TFLOP/s at 8B shapes"
+DOMINANT_KERNEL = "gemm_4w_kernel"
+DOMINANT_SOURCE = os.path.join("paper_2607_01125_amd", "csrc", "k_gemm_4w.hip")
 
 
-def gemm_source_hash() -> str:
-    with open(os.path.join(ROOT, "paper_2607_01125_amd", "csrc", "k_gemm.hip"), "rb") as f:
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def source_hash(rel: str) -> str:
+    with open(os.path.join(ROOT, rel), "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def traffic_record(kernel: str, workload: str):
+def traffic_record(kernel: str, workload: str, source: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or None when
     the summary is missing or was taken on a different kernel source."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -43,13 +60,15 @@ def traffic_record(kernel: str, workload: str):
         return None
     with open(path) as f:
         rec = json.load(f).get(f"{kernel}@{workload}")
-    if not rec or rec.get("source_sha256_16") != gemm_source_hash():
+    if not rec or rec.get("source_sha256_16") != source_hash(source):
         return None
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(T, K, N, r, steps=2):
-    """The oracle (NumPy, float64 products, bf16 rounding emulated) on the same workload."""
+# ------------------------------------------------------------------ CPU baseline (the oracle)
+def cpu_baseline(T, K, N, r, budget_s=12.0):
+    """The oracle (NumPy, float64 products, bf16 rounding emulated) on the same workload:
+    whole steps until about `budget_s` seconds of host time have been spent."""
     import numpy as np
 
     import synth
@@ -68,44 +87,32 @@ def cpu_baseline(T, K, N, r, steps=2):
     v = np.zeros_like(c)
     xs = np.stack([x, x])
     t0 = time.perf_counter()
-    for t in range(1, steps + 1):
+    steps = 0
+    while steps < 2 or time.perf_counter() - t0 < budget_s:
+        t = steps + 1
         y = olin.adapted_linear_pm(xs, w, None, ut, c.reshape(N, r), 1e-3, 1, t, 0, 0, "bf16")
         g = oadam.projected_grad(oloss.mse(y[0], tgt), oloss.mse(y[1], tgt), 1e-3)
         c, m, v, _ = oadam.zo_adam(c, m, v, g, orng.gauss_range(1, t, 0, 0, N * r), oadam.adam_scalars(1e-4, t))
+        steps += 1
     dt = time.perf_counter() - t0
     try:
         cores = len(os.sched_getaffinity(0))
     except AttributeError:
         cores = os.cpu_count()
-    return {"value": steps / dt, "unit": "ZO steps/s", "cores": cores, "kind": "oracle",
-            "sample": f"{steps} full steps of the same workload ({T} tokens per half, d={K}, r={r}), "
+    return {"value": round(steps / dt, 4), "unit": "ZO steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"{steps} full steps of the headline workload ({T} tokens per half, d={K}, r={r}), "
                       f"NumPy float64 products with bf16 rounding emulated, {dt:.1f} s"}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="single_linear_4096")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the multi-GPU path is a "
-              f"design, not a build)", file=sys.stderr)
-        sys.exit(2)
-
-    import numpy as np
+# ------------------------------------------------------------------ headline: single adapted linear
+def bench_single_linear(args, dev):
     import torch
 
     import synth
     from paper_2607_01125_amd import zoact as Z
 
-    dev = torch.device("cuda:0")
     T, K, N, r = 8192, 4096, 4096, 32
     eps, lr, seed = 1e-3, 1e-4, 1
-
-    # ---- synthetic inputs, resident in HBM
     x, q = synth.planted_lowrank(T, K, seed=0)
     xb = torch.from_numpy(synth.bf16_round(x)).to(dev).to(torch.bfloat16)
     x_pm = torch.cat([xb, xb], dim=0).contiguous()                 # [2][T][K], halves share x here
@@ -115,10 +122,11 @@ def main():
     qr = torch.from_numpy(q[:, :r].copy()).to(dev)
     tgt = (xb.float() @ (w.float() + cstar @ qr.T).T).to(torch.bfloat16).contiguous()
 
-    # ---- one-shot basis (Algorithm 1) on the calibration activations, timed separately
+    # one-shot basis (Algorithm 1) on the calibration activations, timed separately
     ut = torch.empty(r, K, dtype=torch.bfloat16, device=dev)
     eigv = torch.empty(r, dtype=torch.float32, device=dev)
     ws_b = torch.empty(Z.basis_init_workspace_bytes(K, r), dtype=torch.uint8, device=dev)
+    Z.basis_init(xb, r, ut, ws_b, eigvals=eigv)       # first call loads the code objects
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     Z.basis_init(xb, r, ut, ws_b, eigvals=eigv)
@@ -165,35 +173,240 @@ def main():
     gemm_flops = 2 * (2 * T) * N * K + 2 * (2 * T) * r * N
     achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
     assert int(status.item()) == 0, "non-finite projected gradient"
+    return {
+        "ms_per_step": ms_per_step, "init_ms": init_ms, "flops": flops,
+        "roofline": {"kernel": f"{DOMINANT_KERNEL} (fused ± adapted GEMM, M=16384, N=K=4096, r=32)",
+                     "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": traffic_record(DOMINANT_KERNEL, "single_linear_4096", DOMINANT_SOURCE),
+                     "flops_per_launch": gemm_flops, "mean_launch_us": round(gemm_ms * 1e3, 1)},
+        "losses": [float(v) for v in loss.cpu().numpy()],
+        "config": {"tokens_per_half": T, "d_in": K, "d_out": N, "rank": r, "eps": eps},
+    }
 
+
+# ------------------------------------------------------------------ adapted linear at the 8B layer shapes
+def bench_linear_shapes(dev, reps=10):
+    """projection + fused +/- GEMM per Llama-3-8B layer shape, M = 8192 stacked rows, r = 32."""
+    import torch
+
+    import synth
+    from paper_2607_01125_amd import zoact as Z
+
+    T, r = 4096, 32
+    shapes = [("qkv", 4096, 6144, 0), ("o", 4096, 4096, 0), ("gate|up", 4096, 28672, Z.EPI_SWIGLU),
+              ("down", 14336, 4096, 0)]
+    out = {}
+    for mode in ("bf16", "int4"):
+        res, tot_flop, tot_s = {}, 0.0, 0.0
+        for name, K, N, flags in shapes:
+            x = synth.device_normal((2 * T, K), 1.0, 9, K, device=dev, dtype=torch.bfloat16)
+            w = synth.device_normal((N, K), 0.02, 9, N, K, device=dev, dtype=torch.bfloat16)
+            ut = synth.device_normal((r, K), 1.0 / math.sqrt(K), 9, r, K, device=dev, dtype=torch.bfloat16)
+            if mode == "int4":
+                packed, scales = synth.device_quantize_int4_g128(w)
+                layer = Z.Linear(packed, K, N, r, ut, 0, w_scales=scales)
+                del w
+            else:
+                layer = Z.Linear(w, K, N, r, ut, 0)
+            c = torch.zeros(N * r, dtype=torch.bfloat16 if mode == "int4" else torch.float32, device=dev)
+            arena = Z.Arena(c, torch.zeros(N * r, device=dev), torch.zeros(N * r, device=dev))
+            p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev)
+            y = torch.empty(2 * T, N // 2 if flags else N, dtype=torch.bfloat16, device=dev)
+            pert = Z.Pert(3, 1, 0, 1e-3)
+
+            def call():
+                Z.project(x, ut, p)
+                Z.linear_fwd_pm(layer, arena, x, T, p, y, pert, flags=flags)
+
+            call()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                call()
+            e1.record()
+            torch.cuda.synchronize()
+            sec = e0.elapsed_time(e1) / reps * 1e-3
+            M = 2 * T
+            flop = 2 * M * N * K + 2 * M * K * r + 2 * M * r * N
+            res[name] = {"M": M, "N": N, "K": K, "us": round(sec * 1e6, 1), "tflops": round(flop / sec / 1e12, 1)}
+            tot_flop += flop
+            tot_s += sec
+            del x, layer, arena, p, y
+            torch.cuda.empty_cache()
+        mean = tot_flop / tot_s / 1e12
+        out[mode] = {"shapes": res, "flop_weighted_tflops": round(mean, 1),
+                     "frac_of_bf16_peak": round(mean / PEAK_BF16_TFLOPS, 4)}
+        log(f"8B shapes {mode}: {mean:.1f} TFLOP/s")
+    return out
+
+
+# ------------------------------------------------------------------ full models
+def model_step_flops(shape, B, S):
+    """Algorithmic FLOPs of one +/- step: both halves' linears, LM head, causal attention,
+    projection (once per adapted site) and correction."""
+    M = 2 * B * S
+    d, dkv, ff, V, r, L = shape.d_model, shape.n_kv_heads * shape.head_dim, shape.d_ff, shape.vocab, shape.rank, \
+        shape.n_layers
+    if shape.family == "llama":
+        nk = [(d, d), (dkv, d), (dkv, d), (d, d), (ff, d), (ff, d), (d, ff)]
+        width = {"q": d, "k": dkv, "v": dkv, "o": d, "gate": ff, "up": ff, "down": d}
+        site_in = {"attn": d, "o": d, "mlp": d, "down": ff}
+        sites = {"attn": {"q", "k", "v"}, "o": {"o"}, "mlp": {"gate", "up"}, "down": {"down"}}
+    else:
+        nk = [(d, d), (d, d), (d, d), (d, d), (ff, d), (d, ff)]
+        width = {"q": d, "v": d, "o": d, "fc1": ff, "fc2": d}
+        site_in = {"attn": d, "o": d, "mlp": d, "down": ff}
+        sites = {"attn": {"q", "v"}, "o": {"o"}, "mlp": {"fc1"}, "down": {"fc2"}}
+    ad = set(shape.adapted)
+    lin = 2 * M * sum(n * k for n, k in nk) * L
+    head = 2 * M * d * V
+    attn = 4 * B * shape.n_heads * S * S * shape.head_dim * L          # both halves, QK^T and PV, causal half
+    proj = 2 * M * r * sum(site_in[s] for s, ps in sites.items() if ps & ad) * L
+    corr = 2 * M * r * sum(width[p] for p in ad) * L
+    return lin + head + attn + proj + corr
+
+
+def bench_model(dev, which, warmup=2, steps=5):
+    import torch
+
+    import synth
+    from paper_2607_01125_amd import model as gm
+    from paper_2607_01125_amd import zoact as Z
+
+    if which in ("llama_bf16", "llama_int4"):
+        shape, B, S, CB, CS, lr = synth.LLAMA3_8B, 16, 256, 16, 256, 5e-5
+    else:
+        shape, B, S, CB, CS, lr = synth.OPT_13B, 8, 512, 32, 512, 2.5e-5
+    t0 = time.perf_counter()
+    W = synth.device_model_weights(shape, 0, torch.bfloat16, device=dev)
+    mode = "bf16"
+    if which == "llama_int4":
+        mode = "int4"
+        for l in range(shape.n_layers):
+            for n in ("wq", "wk", "wv", "wo", "wg", "wu", "wd"):
+                W[l][n] = synth.device_quantize_int4_g128(W[l][n])
+    g = gm.Decoder(shape, W, mode, device=dev)
+    del W
+    torch.cuda.empty_cache()
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t0
+    calib = torch.from_numpy(synth.uniform_tokens(CB, CS, shape.vocab, 0, 1)).to(dev)
+    tok = torch.from_numpy(synth.uniform_tokens(B, S, shape.vocab, 0, 2)).to(dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    g.basis_init(calib)
+    torch.cuda.synchronize()
+    init_s = time.perf_counter() - t0
+    for _ in range(warmup):
+        g.step(tok, 1, 1e-3, lr)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        g.step(tok, 1, 1e-3, lr)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    flops = model_step_flops(shape, B, S)
+    rec = {"steps_per_s": round(1e3 / ms, 3), "ms_per_step": round(ms, 2),
+           "model_tflops": round(flops / (ms * 1e-3) / 1e12, 1), "step_tflop": round(flops / 1e12, 2),
+           "basis_init_s": round(init_s, 3), "calibration_tokens": CB * CS, "tokens_per_half": B * S,
+           "rank": shape.rank, "k": g.k, "losses": [float(v) for v in g.loss_pm.cpu().numpy()],
+           "status": int(g.status.item()), "setup_s": round(setup_s, 1)}
+    if which in ("llama_bf16", "llama_int4"):
+        # ZO-Adam over the model's arena (HBM-bound): 24 B per coefficient (fp32 C), 20 (bf16 C)
+        pert = Z.Pert(1, 99, 0, 1e-3)
+        adam = Z.adam_desc(lr, 99)
+        Z.step(g.arena, g.loss_pm, pert, adam, g.status)
+        torch.cuda.synchronize()
+        reps = 20
+        e0.record()
+        for _ in range(reps):
+            Z.step(g.arena, g.loss_pm, pert, adam, g.status)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        per = 20 if g.c_bf16 else 24
+        gbs = g.k * per / (us * 1e-6) / 1e9
+        rec["adam"] = {"coefficients": g.k, "bytes_per_coefficient": per, "us": round(us, 1),
+                       "achieved_GBps": round(gbs, 1), "peak_GBps": PEAK_HBM_GBS,
+                       "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    del g
+    torch.cuda.empty_cache()
+    log(f"{which}: {rec['steps_per_s']} steps/s, {rec['model_tflops']} TFLOP/s, init {rec['basis_init_s']} s")
+    return rec
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="single_linear_4096", choices=["single_linear_4096"])
+    ap.add_argument("--quick", action="store_true", help="headline workload only")
+    ap.add_argument("--models", default="llama_bf16,llama_int4,opt_bf16",
+                    help="comma-separated model runs (llama_bf16, llama_int4, opt_bf16; empty for none)")
+    ap.add_argument("--no-shapes", action="store_true", help="skip the 8B layer-shape sweep")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (reference for HBM counters)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the multi-GPU path is a "
+              f"design, not a build)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    dev = torch.device("cuda:0")
+    log("headline: single adapted linear 4096, r=32, 8192 tokens per half")
+    head = bench_single_linear(args, dev)
+    ms = head["ms_per_step"]
     out = {
-        "metric": "ZO steps/sec (±ε forwards + Adam) and adapted-linear TFLOP/s at 8B shapes",
-        "value": round(1e3 / ms_per_step, 3),
+        "metric": METRIC,
+        "value": round(1e3 / ms, 3),
         "unit": "ZO steps/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": round(ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (planted low-rank activations, random-init W, seeded)",
         "config": {"workload": "single adapted linear, bf16, d_in=d_out=4096, r=32, 8192 tokens per ± half "
-                               "(fused ± forward + projection + MSE + ZO-Adam)",
-                   "tokens_per_half": T, "d_in": K, "d_out": N, "rank": r, "eps": eps,
-                   "parallelism": "single GPU"},
-        "adapted_linear_tflops": round(flops / (ms_per_step * 1e-3) / 1e12, 1),
-        "basis_init_ms": round(init_ms, 1),
-        "roofline": {"kernel": "gemm_pm_kernel (fused ± adapted GEMM)", "bound": "mfma",
-                     "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic_record("gemm_pm_kernel", args.workload),
-                     "flops_per_launch": gemm_flops, "mean_launch_us": round(gemm_ms * 1e3, 1)},
-        "losses": [float(v) for v in loss.cpu().numpy()],
+                               "(projection + fused ± forward + MSE + ZO-Adam)",
+                   **head["config"], "parallelism": "single GPU"},
+        "adapted_linear_tflops": round(head["flops"] / (ms * 1e-3) / 1e12, 1),
+        "basis_init_ms": round(head["init_ms"], 1),
+        "roofline": head["roofline"],
+        "losses": head["losses"],
     }
+    log(f"headline: {out['value']} steps/s, fused GEMM {head['roofline']['achieved']} TFLOP/s")
+    if not args.quick:
+        if not args.no_shapes:
+            out["adapted_linear_8b_shapes"] = bench_linear_shapes(dev)
+        runs = [w for w in args.models.split(",") if w]
+        for w in runs:
+            if w not in ("llama_bf16", "llama_int4", "opt_bf16"):
+                raise SystemExit(f"unknown model run {w!r}")
+        if runs:
+            out["models"] = {w: bench_model(dev, w) for w in runs}
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = n
+        del src, dst
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(T, K, N, r)
+        log("cpu baseline (oracle)")
+        out["cpu_baseline"] = cpu_baseline(8192, 4096, 4096, 32)
     print(json.dumps(out), flush=True)
 
 
