@@ -40,19 +40,22 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 METRIC = "ZO steps/sec (±ε forwards + Adam) and adapted-linear TFLOP/s at 8B shapes"
 DOMINANT_KERNEL = "gemm_4w_kernel"
-DOMINANT_SOURCE = os.path.join("paper_2607_01125_amd", "csrc", "k_gemm_4w.hip")
+DOMINANT_SOURCES = [os.path.join("paper_2607_01125_amd", "csrc", f) for f in ("k_gemm_4w.hip", "gemm_common.hpp")]
 
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def source_hash(rel: str) -> str:
-    with open(os.path.join(ROOT, rel), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def source_hash(rels) -> str:
+    h = hashlib.sha256()
+    for rel in rels:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
-def traffic_record(kernel: str, workload: str, source: str):
+def traffic_record(kernel: str, workload: str, sources):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or None when
     the summary is missing or was taken on a different kernel source."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -60,7 +63,7 @@ def traffic_record(kernel: str, workload: str, source: str):
         return None
     with open(path) as f:
         rec = json.load(f).get(f"{kernel}@{workload}")
-    if not rec or rec.get("source_sha256_16") != source_hash(source):
+    if not rec or rec.get("source_sha256_16") != source_hash(sources):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -178,7 +181,7 @@ def bench_single_linear(args, dev):
         "roofline": {"kernel": f"{DOMINANT_KERNEL} (fused ± adapted GEMM, M=16384, N=K=4096, r=32)",
                      "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic_record(DOMINANT_KERNEL, "single_linear_4096", DOMINANT_SOURCE),
+                     "traffic": traffic_record(DOMINANT_KERNEL, "single_linear_4096", DOMINANT_SOURCES),
                      "flops_per_launch": gemm_flops, "mean_launch_us": round(gemm_ms * 1e3, 1)},
         "losses": [float(v) for v in loss.cpu().numpy()],
         "config": {"tokens_per_half": T, "d_in": K, "d_out": N, "rank": r, "eps": eps},
