@@ -50,6 +50,14 @@ __device__ __forceinline__ float adam_one(float c, float& m, float& v, float gh,
   return c - h.step_size * (m / d);
 }
 
+typedef float vf4 __attribute__((ext_vector_type(4)));
+typedef uint32_t vu2 __attribute__((ext_vector_type(2)));
+
+// Streaming (nontemporal) 16- and 8-byte accesses: every arena byte is touched once per
+// step, so keeping it out of the caches leaves them to the data that is reused.
+__device__ __forceinline__ vf4 ld_nt(const float* p) { return __builtin_nontemporal_load(reinterpret_cast<const vf4*>(p)); }
+__device__ __forceinline__ void st_nt(float* p, vf4 v) { __builtin_nontemporal_store(v, reinterpret_cast<vf4*>(p)); }
+
 template <bool BF16C>
 __global__ void __launch_bounds__(256) adam_kernel(void* __restrict__ cptr, float* __restrict__ mptr,
                                                    float* __restrict__ vptr, int64_t k, const float* loss_pm,
@@ -63,32 +71,35 @@ __global__ void __launch_bounds__(256) adam_kernel(void* __restrict__ cptr, floa
   }
   const int64_t nb = (k + 3) >> 2;
   for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb; b += (int64_t)gridDim.x * blockDim.x) {
-    const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
     const int64_t e = 4 * b;
     if (e + 4 <= k) {
-      float4 m4 = *reinterpret_cast<const float4*>(mptr + e);
-      float4 v4 = *reinterpret_cast<const float4*>(vptr + e);
+      vf4 m4 = ld_nt(mptr + e);
+      vf4 v4 = ld_nt(vptr + e);
       float c0, c1, c2, c3;
       if (BF16C) {
-        const ushort4 cb = *reinterpret_cast<const ushort4*>(reinterpret_cast<const uint16_t*>(cptr) + e);
-        c0 = bf2f(cb.x); c1 = bf2f(cb.y); c2 = bf2f(cb.z); c3 = bf2f(cb.w);
+        const vu2 cb = __builtin_nontemporal_load(reinterpret_cast<const vu2*>(reinterpret_cast<const uint16_t*>(cptr) + e));
+        c0 = bf2f((uint16_t)(cb.x & 0xFFFFu)); c1 = bf2f((uint16_t)(cb.x >> 16));
+        c2 = bf2f((uint16_t)(cb.y & 0xFFFFu)); c3 = bf2f((uint16_t)(cb.y >> 16));
       } else {
-        const float4 cf = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(cptr) + e);
+        const vf4 cf = ld_nt(reinterpret_cast<const float*>(cptr) + e);
         c0 = cf.x; c1 = cf.y; c2 = cf.z; c3 = cf.w;
       }
-      c0 = adam_one(c0, m4.x, v4.x, g * z.x, h);
-      c1 = adam_one(c1, m4.y, v4.y, g * z.y, h);
-      c2 = adam_one(c2, m4.z, v4.z, g * z.z, h);
-      c3 = adam_one(c3, m4.w, v4.w, g * z.w, h);
-      *reinterpret_cast<float4*>(mptr + e) = m4;
-      *reinterpret_cast<float4*>(vptr + e) = v4;
+      const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
+      float mx = m4.x, my = m4.y, mz = m4.z, mw = m4.w, vx = v4.x, vy = v4.y, vz = v4.z, vw = v4.w;
+      c0 = adam_one(c0, mx, vx, g * z.x, h);
+      c1 = adam_one(c1, my, vy, g * z.y, h);
+      c2 = adam_one(c2, mz, vz, g * z.z, h);
+      c3 = adam_one(c3, mw, vw, g * z.w, h);
+      st_nt(mptr + e, vf4{mx, my, mz, mw});
+      st_nt(vptr + e, vf4{vx, vy, vz, vw});
       if (BF16C) {
-        *reinterpret_cast<ushort4*>(reinterpret_cast<uint16_t*>(cptr) + e) =
-            make_ushort4(f2bf(c0), f2bf(c1), f2bf(c2), f2bf(c3));
+        const vu2 cb = {(uint32_t)f2bf(c0) | ((uint32_t)f2bf(c1) << 16), (uint32_t)f2bf(c2) | ((uint32_t)f2bf(c3) << 16)};
+        __builtin_nontemporal_store(cb, reinterpret_cast<vu2*>(reinterpret_cast<uint16_t*>(cptr) + e));
       } else {
-        *reinterpret_cast<float4*>(reinterpret_cast<float*>(cptr) + e) = make_float4(c0, c1, c2, c3);
+        st_nt(reinterpret_cast<float*>(cptr) + e, vf4{c0, c1, c2, c3});
       }
     } else {
+      const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
       for (int l = 0; l < 4 && e + l < k; ++l) {
         float m = mptr[e + l], v = vptr[e + l];
         float c = BF16C ? bf2f(reinterpret_cast<const uint16_t*>(cptr)[e + l])
