@@ -95,6 +95,11 @@ typedef struct {
   int64_t d_in, d_out;
   int32_t r;            /* 0 <= r <= 256                                          */
   int64_t coef_offset;  /* arena index of C[0][0]                                 */
+  const void* ch;       /* optional (BF16 activations): the perturbed coefficients
+                           bf16(C +/- eps Z) of this layer from zoact_perturb_coeffs,
+                           half 0 [d_out][r] at ch, half 1 at ch + ch_half_stride
+                           elements; NULL = formed inside the kernel (same values)  */
+  int64_t ch_half_stride;
 } zoact_linear;
 
 /* The coefficient arena and its Adam moments (updated in place by zoact_step). */
@@ -166,6 +171,16 @@ zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, co
                                  int32_t x_dtype, int64_t T, const void* p, const void* residual,
                                  uint32_t flags, const zoact_pert* pert, void* y, int32_t y_dtype,
                                  zoact_stream stream);
+
+/* ------------------------------------------------------ perturbed coefficients
+ * out[h][e - e0] = bf16(fp32(C[e]) + s_h fp32(eps Z(e))), s = (+1, -1), for arena
+ * indices e0 <= e < e0 + n: the C +/- eps Z of Section 3's perturbed forward, exactly
+ * as the fused GEMM forms it.  Computing it once per step for a whole model (one
+ * streaming pass over the arena) lets every GEMM workgroup read it instead of
+ * regenerating Z; pass a layer's slice as zoact_linear.ch with ch_half_stride = n.
+ * out bf16 [2][n], 16-byte aligned.  Errors: range outside the arena, n < 1. */
+zoact_status zoact_perturb_coeffs(const zoact_arena* A, int64_t e0, int64_t n, const zoact_pert* pert, void* out,
+                                  zoact_stream stream);
 
 /* ------------------------------------------------------ losses of both halves
  * Algorithm 2 needs the loss under each perturbation; the two-sided step needs

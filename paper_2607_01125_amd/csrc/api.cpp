@@ -107,6 +107,12 @@ zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, co
     CHECK(float_type(A->c_dtype), "linear_fwd_pm: arena dtype must be F32 or BF16");
   }
   if (flags & ZOACT_EPI_SWIGLU) CHECK(L->d_out % 32 == 0, "linear_fwd_pm: SWIGLU needs d_out %% 32 == 0");
+  if (L->ch != nullptr) {
+    CHECK(x_dtype == ZOACT_BF16 && L->r > 0 && L->r % 8 == 0,
+          "linear_fwd_pm: precomputed coefficients need BF16 activations and r %% 8 == 0");
+    CHECK(aligned16(L->ch) && L->ch_half_stride % 8 == 0 && L->ch_half_stride >= L->d_out * (int64_t)L->r,
+          "linear_fwd_pm: ch must be 16-byte aligned with a half stride >= d_out * r, multiple of 8");
+  }
   if (x_dtype == ZOACT_F32) {
     CHECK(L->w_dtype == ZOACT_F32 && y_dtype == ZOACT_F32, "linear_fwd_pm: F32 activations need F32 weights and output");
     CHECK(L->r == 0 || A->c_dtype == ZOACT_F32, "linear_fwd_pm: F32 path needs an F32 arena");
@@ -124,6 +130,16 @@ zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, co
   }
   return hip_status(zoact::launch_linear_pm(*L, A, x, x_dtype, T, p, residual, flags, *pert, y, y_dtype, st(stream)),
                     "linear_fwd_pm");
+}
+
+zoact_status zoact_perturb_coeffs(const zoact_arena* A, int64_t e0, int64_t n, const zoact_pert* pert, void* out,
+                                  zoact_stream stream) {
+  CHECK(A != nullptr && pert != nullptr && out != nullptr && A->c != nullptr, "perturb_coeffs: NULL argument");
+  CHECK(float_type(A->c_dtype), "perturb_coeffs: arena dtype must be F32 or BF16");
+  CHECK(n >= 1 && e0 >= 0 && e0 + n <= A->k, "perturb_coeffs: range [%lld, %lld) outside the arena (k=%lld)",
+        (long long)e0, (long long)(e0 + n), (long long)A->k);
+  CHECK(aligned16(out), "perturb_coeffs: out must be 16-byte aligned");
+  return hip_status(zoact::launch_perturb(*A, e0, n, *pert, static_cast<uint16_t*>(out), st(stream)), "perturb_coeffs");
 }
 
 size_t zoact_loss_workspace_bytes(void) { return (size_t)2 * zoact::kLossBlocks * sizeof(double); }

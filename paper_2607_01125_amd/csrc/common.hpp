@@ -15,6 +15,8 @@ __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uin
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 // Internal launchers return hipError_t from hipGetLastError() after the launch.
+hipError_t launch_perturb(const zoact_arena& A, int64_t e0, int64_t n, const zoact_pert& p, uint16_t* out,
+                          hipStream_t s);
 hipError_t launch_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e0, int64_t n, float* out,
                         hipStream_t s);
 hipError_t launch_adam(const zoact_arena& A, const float* loss_pm, const zoact_pert& p, const zoact_adam& h,

@@ -25,6 +25,8 @@ struct GemmArgs {
   int32_t tiles_m_half;  // token tiles per half
   int32_t tiles_n;
   int32_t n_tail;        // depth tiles of the correction block
+  const uint16_t* ch;    // precomputed bf16(C +/- eps Z), [2][N][r] with half stride ch_stride, or null
+  int64_t ch_stride;
 };
 
 __device__ __forceinline__ int swz(int row, int kc) { return (row << 6) + ((kc ^ (row & 7)) << 3); }

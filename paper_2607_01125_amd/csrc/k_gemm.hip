@@ -576,6 +576,8 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
   a.tiles_m_half = (int32_t)((T + BM - 1) / BM);
   a.tiles_n = (int32_t)((L.d_out + BN - 1) / BN);
   a.n_tail = (L.r + 63) / 64;
+  a.ch = static_cast<const uint16_t*>(L.ch);
+  a.ch_stride = L.ch_half_stride;
   const dim3 grid((unsigned)(2 * a.tiles_m_half * a.tiles_n));
   const bool i4 = L.w_dtype == ZOACT_INT4_G128;
   const bool of = y_dtype == ZOACT_F32;

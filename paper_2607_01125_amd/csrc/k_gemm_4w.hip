@@ -16,9 +16,10 @@
 //    land.  The XOR swizzle (16-byte chunk c of row r at chunk c ^ ((r >> 1) & 3)) is
 //    applied on the global side.  Buffer descriptors bound both matrices: rows past the
 //    end read as 0.  One workgroup barrier per step.
-//  * C_h = bf16(C + s_h eps Z) for the tile's 256 features is generated in the prologue,
-//    while the first stages are in flight, into a dedicated 32 KB LDS region; the rank-r
-//    correction runs as one or two extra 32-deep steps against p[h] read from global memory.
+//  * C_h = bf16(C + s_h eps Z) for the tile's 256 features is either read from the
+//    precomputed array (zoact_perturb_coeffs) or generated in the prologue, while the first
+//    stages are in flight, into a dedicated 32 KB LDS region; the rank-r correction runs
+//    as one or two extra 32-deep steps against p[h] read from global memory.
 #include "gemm_common.hpp"
 
 namespace zoact {
@@ -88,7 +89,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
   const uint16_t* xh = a.x + (int64_t)half * a.T * a.K;
   const uint16_t* w = reinterpret_cast<const uint16_t*>(a.w);
 
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: kept in SGPRs
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15, lk = lane >> 4;
   const int wn0 = (wave & 1) * 128;   // features of this wave
@@ -112,7 +113,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
       const bool valid = HAS_R && q < qn && 4 * g < a.r && n < a.N;
       base[q] = valid ? (int)((n * a.r + 4 * g) * esize) : 0x7FFFFF00;
     }
-    if (HAS_R) {
+    if (HAS_R && a.ch == nullptr) {
       if (a.c_bf16) {
 #pragma unroll
         for (int q = 0; q < 16; ++q)
@@ -187,10 +188,29 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
         if (i < 4) dma_run(wrs, a.K, n0 + wave * 64 + i * 16, k0, dst + i * 512);
         else dma_run(xrs, a.K, m0 + wave * 64 + (i - 4) * 16, k0, dst + OP_ELEMS + (i - 4) * 512);
       }
+#ifndef ZO_EARLY_READS
+#define ZO_EARLY_READS 1
+#endif
+#if ZO_EARLY_READS
+      // the next step's 16 fragment reads go out in the first half of the step, so they have
+      // landed by the time the step ends
+      if (has_next && i < 4) {
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+          const int ii = 2 * i + h2;
+          na[ii] = *reinterpret_cast<const bf16x8*>(sp + swz32(wn0 + ii * 16 + lr, lk));
+          nb[ii] = *reinterpret_cast<const bf16x8*>(sp + OP_ELEMS + swz32(wm0 + ii * 16 + lr, lk));
+        }
+      }
+#else
       if (has_next) {
         na[i] = *reinterpret_cast<const bf16x8*>(sp + swz32(wn0 + i * 16 + lr, lk));
         nb[i] = *reinterpret_cast<const bf16x8*>(sp + OP_ELEMS + swz32(wm0 + i * 16 + lr, lk));
       }
+#endif
+      // keep each row's MFMAs, DMA and fragment reads together (the loads stay spread over
+      // the step instead of bunching at its ends)
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
@@ -198,7 +218,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
   // 1 landed, fragments of step 0, then a barrier so that stage 0 may be refilled
   const int npro = S < NSTAGE ? S : NSTAGE;
   for (int st = 0; st < npro; ++st) dma_step(st);
-  if (HAS_R) {
+  if (HAS_R && a.ch == nullptr) {
 #pragma unroll
     for (int q = 0; q < 16; ++q)
       if (q < qn) gen_chunk(q);
@@ -215,13 +235,13 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
   // ---- main loop, two steps per iteration (static fragment buffers).  At the end of step
   // s every wave has waited for the stage of step s + 2 (its own DMA two steps old), so
   // the barrier makes stage s + 2 visible before step s + 1 reads it.
+  // Every step issues its DMA and its next-fragment reads, the last four included: their
+  // stages are never read again (a DMA past the end of a row reads the next row, and past
+  // the end of the matrix reads zeros), and the epilogue waits for all of them.  Constant
+  // predicates leave the step free of branches.
   auto one_step = [&](int s, bf16x8 (&fa)[8], bf16x8 (&fb)[8], bf16x8 (&na)[8], bf16x8 (&nb)[8]) {
-    const bool dma = s + 4 < S;
-    step_body(fa, fb, na, nb, s + 1, s + 1 < S, s + 4, dma);
-    const bool d1 = s + 3 < S;   // DMA issued in step s - 1 still allowed in flight
-    if (dma && d1) __builtin_amdgcn_s_waitcnt(WAIT_VM16);
-    else if (dma || d1) __builtin_amdgcn_s_waitcnt(WAIT_VM8);
-    else __builtin_amdgcn_s_waitcnt(WAIT_VM0);
+    step_body(fa, fb, na, nb, s + 1, true, s + 4, true);
+    __builtin_amdgcn_s_waitcnt(WAIT_VM16);   // the DMA of steps s - 1 and s may stay in flight
     __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
     barrier();
   };
@@ -244,7 +264,14 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
           m = m > a.T - 1 ? a.T - 1 : m;
           const int col = t * 32 + lk * 8;
           fb0[j] = col < a.r ? *reinterpret_cast<const bf16x8*>(ph + m * a.r + col) : zero8;
-          fa0[j] = *reinterpret_cast<const bf16x8*>(chreg + swz(wn0 + j * 16 + lr, t * 4 + lk));
+          if (a.ch != nullptr) {
+            int64_t n = n0 + wn0 + j * 16 + lr;
+            n = n > a.N - 1 ? a.N - 1 : n;
+            fa0[j] = col < a.r ? *reinterpret_cast<const bf16x8*>(a.ch + (int64_t)half * a.ch_stride + n * a.r + col)
+                               : zero8;
+          } else {
+            fa0[j] = *reinterpret_cast<const bf16x8*>(chreg + swz(wn0 + j * 16 + lr, t * 4 + lk));
+          }
         }
 #pragma unroll
         for (int i = 0; i < 8; ++i)

@@ -141,6 +141,27 @@ __global__ void __launch_bounds__(256) sgd_kernel(void* __restrict__ cptr, int64
   }
 }
 
+// out[h][e - e0] = bf16(C[e] + s_h eps Z(e)); one Philox block (4 arena indices) per thread.
+template <bool BF16C>
+__global__ void __launch_bounds__(256) perturb_kernel(const void* __restrict__ cptr, int64_t e0, int64_t n,
+                                                      uint64_t seed, uint32_t step, uint32_t query, float eps,
+                                                      uint16_t* __restrict__ out) {
+#pragma clang fp contract(off)
+  const int64_t b0 = e0 >> 2, b1 = (e0 + n - 1) >> 2;
+  for (int64_t b = b0 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b <= b1; b += (int64_t)gridDim.x * blockDim.x) {
+    const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
+#pragma unroll
+    for (int l = 0; l < 4; ++l) {
+      const int64_t e = 4 * b + l;
+      if (e < e0 || e >= e0 + n) continue;
+      const float c = BF16C ? bf2f(reinterpret_cast<const uint16_t*>(cptr)[e]) : reinterpret_cast<const float*>(cptr)[e];
+      const float ez = eps * rng::lane_of(z, l);
+      out[e - e0] = f2bf(c + ez);
+      out[n + e - e0] = f2bf(c - ez);
+    }
+  }
+}
+
 int64_t grid_for(int64_t blocks_of_four) {
   int64_t g = (blocks_of_four + 255) / 256;
   return g < 1 ? 1 : (g > (1 << 20) ? (1 << 20) : g);
@@ -153,6 +174,17 @@ hipError_t launch_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e0
   if (n == 0) return hipSuccess;
   const int64_t nb = ((e0 + n - 1) >> 2) - (e0 >> 2) + 1;
   gen_z_kernel<<<dim3((unsigned)grid_for(nb)), dim3(256), 0, s>>>(seed, step, query, e0, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_perturb(const zoact_arena& A, int64_t e0, int64_t n, const zoact_pert& p, uint16_t* out,
+                          hipStream_t s) {
+  const int64_t nb = ((e0 + n - 1) >> 2) - (e0 >> 2) + 1;
+  const dim3 grid((unsigned)grid_for(nb));
+  if (A.c_dtype == ZOACT_BF16)
+    perturb_kernel<true><<<grid, dim3(256), 0, s>>>(A.c, e0, n, p.seed, p.step, p.query, p.eps, out);
+  else
+    perturb_kernel<false><<<grid, dim3(256), 0, s>>>(A.c, e0, n, p.seed, p.step, p.query, p.eps, out);
   return hipGetLastError();
 }
 

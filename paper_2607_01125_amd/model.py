@@ -128,6 +128,7 @@ class Decoder:
         self.loss_ws = torch.empty(Z.loss_workspace_bytes(), dtype=torch.uint8, device=self.dev)
         self._bufs = {}
         self._rope = {}
+        self._ch = self._ch_all = None   # per-step C +/- eps Z of the whole arena (bf16 modes)
 
     # ---------------------------------------------------------------- weights
     def _t(self, a, dtype=None):
@@ -238,9 +239,13 @@ class Decoder:
         B = self._cur
         if adapt and blk is not None and site_ut is not None:
             lin.r, lin.ut = self.r, site_ut
+            if self._ch is not None:
+                lin.ch, lin.ch_stride = self._ch[blk.offset:], self.k
+            else:
+                lin.ch, lin.ch_stride = None, 0
             Z.linear_fwd_pm(lin, self.arena, x, T, B["p"], y, pert, residual, flags)
         else:
-            lin.r, lin.ut = 0, None
+            lin.r, lin.ut, lin.ch, lin.ch_stride = 0, None, None, 0
             Z.linear_fwd_pm(lin, None, x, T, None, y, pert, residual, flags)
 
     def forward(self, tokens: torch.Tensor, pert: Z.Pert, *, calibrate=None, distinct_halves=False):
@@ -256,6 +261,14 @@ class Decoder:
         T = n_seq * seq
         B = self._cur = self._buffers(n_seq, seq)
         adapt = calibrate is None
+        # C +/- eps Z for the whole arena in one streaming pass; every adapted GEMM reads its
+        # slice instead of regenerating Z per workgroup
+        self._ch = None
+        if adapt and self.act == torch.bfloat16 and self.k > 0 and self.r % 8 == 0:
+            if self._ch_all is None:
+                self._ch_all = torch.empty(2 * self.k, dtype=torch.bfloat16, device=self.dev)
+            Z.perturb_coeffs(self.arena, 0, self.k, pert, self._ch_all)
+            self._ch = self._ch_all
         Z.embed(tokens, self.emb, B["h0"], seq, self.pos, pos_offset=2, distinct_halves=distinct_halves)
         h, h_alt = B["h0"], B["h1"]
         cos_sin = self._rope_tables(seq) if s.family == "llama" else None

@@ -36,7 +36,8 @@ class Pert(ctypes.Structure):
 class LinearDesc(ctypes.Structure):
     _fields_ = [("w_dtype", ctypes.c_int32), ("w", ctypes.c_void_p), ("w_scales", ctypes.c_void_p),
                 ("bias", ctypes.c_void_p), ("ut", ctypes.c_void_p), ("d_in", ctypes.c_int64),
-                ("d_out", ctypes.c_int64), ("r", ctypes.c_int32), ("coef_offset", ctypes.c_int64)]
+                ("d_out", ctypes.c_int64), ("r", ctypes.c_int32), ("coef_offset", ctypes.c_int64),
+                ("ch", ctypes.c_void_p), ("ch_half_stride", ctypes.c_int64)]
 
 
 class ArenaDesc(ctypes.Structure):
@@ -67,6 +68,7 @@ SIGNATURES = {
     "zoact_project": ([_P, _I32, _I64, _I64, _P, _I32, _P, _P], _I32),
     "zoact_linear_fwd_pm": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I32, _I64, _P, _P, _U32,
                              ctypes.POINTER(Pert), _P, _I32, _P], _I32),
+    "zoact_perturb_coeffs": ([ctypes.POINTER(ArenaDesc), _I64, _I64, ctypes.POINTER(Pert), _P, _P], _I32),
     "zoact_loss_workspace_bytes": ([], _SZ),
     "zoact_mse_pm": ([_P, _I32, _P, _I64, _I64, _P, _P, _SZ, _P], _I32),
     "zoact_xent_pm": ([_P, _P, _I64, _I64, _I64, _P, _P, _SZ, _P], _I32),
@@ -140,13 +142,15 @@ class Linear:
     coef_offset: int = 0
     bias: torch.Tensor | None = None
     w_scales: torch.Tensor | None = None
+    ch: torch.Tensor | None = None      # precomputed bf16(C +/- eps Z): half 0 at ch, half 1 at ch + ch_stride
+    ch_stride: int = 0
 
     def desc(self) -> LinearDesc:
         wd = INT4_G128 if self.w.dtype == torch.uint8 else dtype_code(self.w)
         return LinearDesc(wd, self.w.data_ptr(), self.w_scales.data_ptr() if self.w_scales is not None else None,
                           self.bias.data_ptr() if self.bias is not None else None,
                           self.ut.data_ptr() if self.ut is not None else None, self.d_in, self.d_out, self.r,
-                          self.coef_offset)
+                          self.coef_offset, self.ch.data_ptr() if self.ch is not None else None, self.ch_stride)
 
 
 @dataclass
@@ -185,6 +189,12 @@ def linear_fwd_pm(layer: Linear, arena: Arena | None, x: torch.Tensor, T: int, p
     _check(lib().zoact_linear_fwd_pm(ctypes.byref(d), ctypes.byref(a) if a is not None else None, _ptr(x),
                                      dtype_code(x), T, _ptr(p), _ptr(residual), flags, ctypes.byref(pert), _ptr(y),
                                      dtype_code(y), _stream(stream)))
+
+
+def perturb_coeffs(arena: Arena, e0: int, n: int, pert: Pert, out: torch.Tensor, stream=None):
+    """out bf16 [2][n]: bf16(C[e] +/- eps Z(e)) for arena indices e0 .. e0 + n - 1."""
+    a = arena.desc()
+    _check(lib().zoact_perturb_coeffs(ctypes.byref(a), e0, n, ctypes.byref(pert), _ptr(out), _stream(stream)))
 
 
 def loss_workspace_bytes() -> int:

@@ -123,7 +123,7 @@ def _layer_inputs(T, K, N, r, seed, bias=True, int4=False):
 
 
 def _run_gpu_linear(x, w, b, ut, c_arena, off, r, eps, seed, step, T, K, N, flags=0, resid=None, packed=None,
-                    scales=None, c_bf16=False, out_f32=False):
+                    scales=None, c_bf16=False, out_f32=False, precomputed=False):
     xt = t_bf16(x.reshape(2 * T, K))
     p = None
     if r:
@@ -138,6 +138,10 @@ def _run_gpu_linear(x, w, b, ut, c_arena, off, r, eps, seed, step, T, K, N, flag
     if r:
         ct = t_bf16(c_arena) if c_bf16 else t_f32(c_arena)
         arena = Z.Arena(ct, torch.zeros_like(ct, dtype=torch.float32), torch.zeros_like(ct, dtype=torch.float32))
+    if precomputed:
+        ch = torch.empty(2 * N * r, dtype=torch.bfloat16, device=dev())
+        Z.perturb_coeffs(arena, off, N * r, Z.Pert(seed, step, 0, eps), ch)
+        layer.ch, layer.ch_stride = ch, N * r
     nout = N // 2 if flags & Z.EPI_SWIGLU else N
     y = torch.full((2 * T, nout), float("nan"), dtype=torch.float32 if out_f32 else torch.bfloat16, device=dev())
     rt = t_bf16(resid.reshape(2 * T, nout)) if resid is not None else None
@@ -183,6 +187,45 @@ def test_linear_pm_bf16(T, K, N, r, off):
     got = _run_gpu_linear(x, w, b, ut, c, off, r, eps, seed, step, T, K, N)
     ref = _oracle_linear(x, w, b, ut, c[off:off + N * r].reshape(N, r), off, r, eps, seed, step)
     assert_bf16_close(got, ref, what="linear_pm")
+
+
+@pytest.mark.parametrize("c_bf16", [False, True])
+@pytest.mark.parametrize("e0,n", [(0, 4096), (3, 1001), (44_040_192 - 777, 777)])
+def test_perturb_coeffs_bitwise(c_bf16, e0, n):
+    """bf16(C + eps Z) and bf16(C - eps Z) over an unaligned arena range, bit for bit."""
+    announce("perturb_coeffs", c_bf16, e0, n)
+    k = e0 + n + 3
+    c = synth.normal((k,), 0.01, 3, k % 1000)
+    if c_bf16:
+        c = synth.bf16_round(c)
+    ct = t_bf16(c) if c_bf16 else t_f32(c)
+    arena = Z.Arena(ct, torch.zeros(k, device=dev()), torch.zeros(k, device=dev()))
+    out = torch.empty(2 * n, dtype=torch.bfloat16, device=dev())
+    Z.perturb_coeffs(arena, e0, n, Z.Pert(77, 5, 0, 1e-3), out)
+    z = orng.gauss_range(77, 5, 0, e0, n)
+    got = host(out).reshape(2, n)
+    for h, sign in ((0, 1), (1, -1)):
+        want = olin.perturbed_coeffs(c[e0:e0 + n], z, 1e-3, sign, "bf16")
+        np.testing.assert_array_equal(got[h], want)
+
+
+@pytest.mark.parametrize("T,K,N,r,off,flags", [
+    (300, 512, 336, 32, 0, 0),
+    (64, 384, 256, 64, 8, 0),
+    (513, 2048, 768, 40, 16, 0),
+    (257, 256, 512, 32, 0, 1),
+])
+def test_linear_pm_precomputed_coefficients(T, K, N, r, off, flags):
+    """Reading the precomputed C +/- eps Z gives the same bits as forming it in the kernel."""
+    announce("linear_pm precomputed", T, K, N, r, off, flags)
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=T + 3 * K)
+    c = synth.normal((off + N * r + 9,), 0.01, 8, T)
+    eps, seed, step = 1e-3, 99, 4
+    inline = _run_gpu_linear(x, w, b, ut, c, off, r, eps, seed, step, T, K, N, flags=flags)
+    pre = _run_gpu_linear(x, w, b, ut, c, off, r, eps, seed, step, T, K, N, flags=flags, precomputed=True)
+    np.testing.assert_array_equal(pre, inline)
+    ref = _oracle_linear(x, w, b, ut, c[off:off + N * r].reshape(N, r), off, r, eps, seed, step, flags=flags)
+    assert_bf16_close(pre, ref, what="linear_pm precomputed")
 
 
 def test_linear_pm_zero_coeffs_reproduce_base_and_determinism():
