@@ -98,6 +98,87 @@ __global__ void __launch_bounds__(256) layernorm_kernel(const T* __restrict__ x,
     st_act(yr, c, ((ld_act(xr, c) - mu) * inv) * ld_act(w, c) + ld_act(b, c));
 }
 
+// bf16 RMSNorm with 16-byte accesses: each thread keeps its VPT values of the row in
+// registers between the two passes (d = 256 * 8 * VPT8).
+template <int VPT8>
+__global__ void __launch_bounds__(256) rmsnorm_bf16_vec_kernel(const uint16_t* __restrict__ x,
+                                                               const uint16_t* __restrict__ w, int64_t d, float eps,
+                                                               uint16_t* __restrict__ y) {
+  __shared__ float sh[4];
+  const uint16_t* xr = x + (int64_t)blockIdx.x * d;
+  uint16_t* yr = y + (int64_t)blockIdx.x * d;
+  uint4 v[VPT8];
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < VPT8; ++u) {
+    v[u] = *reinterpret_cast<const uint4*>(xr + (int64_t)(u * 256 + threadIdx.x) * 8);
+    const uint32_t wv[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float a = bf2f((uint16_t)(wv[e] & 0xFFFF)), b = bf2f((uint16_t)(wv[e] >> 16));
+      ss += a * a;
+      ss += b * b;
+    }
+  }
+  const float inv = rsqrtf(block_sum(ss, sh) / (float)d + eps);
+#pragma unroll
+  for (int u = 0; u < VPT8; ++u) {
+    const int64_t c = (int64_t)(u * 256 + threadIdx.x) * 8;
+    const uint4 g = *reinterpret_cast<const uint4*>(w + c);
+    const uint32_t xv[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+    const uint32_t gv[4] = {g.x, g.y, g.z, g.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float a = (bf2f((uint16_t)(xv[e] & 0xFFFF)) * inv) * bf2f((uint16_t)(gv[e] & 0xFFFF));
+      const float b = (bf2f((uint16_t)(xv[e] >> 16)) * inv) * bf2f((uint16_t)(gv[e] >> 16));
+      o[e] = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+    }
+    *reinterpret_cast<uint4*>(yr + c) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+// bf16 rotary embedding with 16-byte accesses: one thread rotates 8 pairs (j .. j + 7 with
+// their partners j + half .. j + half + 7) of one head of one row.
+__global__ void rope_bf16_vec_kernel(uint16_t* __restrict__ x, int64_t rows, int64_t ld, int64_t col0, int heads,
+                                     int hd, int64_t seq, const float* __restrict__ ct, const float* __restrict__ st) {
+  const int half = hd / 2, g8 = half / 8;
+  const int64_t total = rows * heads * g8;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int j = (int)(i % g8) * 8;
+    const int h = (int)((i / g8) % heads);
+    const int64_t r = i / ((int64_t)g8 * heads);
+    const int64_t pos = r % seq;
+    uint16_t* p = x + r * ld + col0 + (int64_t)h * hd;
+    const uint4 lo4 = *reinterpret_cast<const uint4*>(p + j);
+    const uint4 hi4 = *reinterpret_cast<const uint4*>(p + j + half);
+    const float4 c0 = *reinterpret_cast<const float4*>(ct + pos * half + j);
+    const float4 c1 = *reinterpret_cast<const float4*>(ct + pos * half + j + 4);
+    const float4 s0 = *reinterpret_cast<const float4*>(st + pos * half + j);
+    const float4 s1 = *reinterpret_cast<const float4*>(st + pos * half + j + 4);
+    const float cv[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+    const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+    const uint32_t lw[4] = {lo4.x, lo4.y, lo4.z, lo4.w}, hw[4] = {hi4.x, hi4.y, hi4.z, hi4.w};
+    uint32_t lo_o[4], hi_o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      uint16_t lo_r[2], hi_r[2];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const float lo = bf2f((uint16_t)(q ? lw[e] >> 16 : lw[e] & 0xFFFF));
+        const float hi = bf2f((uint16_t)(q ? hw[e] >> 16 : hw[e] & 0xFFFF));
+        const float c = cv[2 * e + q], sn = sv[2 * e + q];
+        lo_r[q] = f2bf(lo * c - hi * sn);
+        hi_r[q] = f2bf(hi * c + lo * sn);
+      }
+      lo_o[e] = (uint32_t)lo_r[0] | ((uint32_t)lo_r[1] << 16);
+      hi_o[e] = (uint32_t)hi_r[0] | ((uint32_t)hi_r[1] << 16);
+    }
+    *reinterpret_cast<uint4*>(p + j) = make_uint4(lo_o[0], lo_o[1], lo_o[2], lo_o[3]);
+    *reinterpret_cast<uint4*>(p + j + half) = make_uint4(hi_o[0], hi_o[1], hi_o[2], hi_o[3]);
+  }
+}
+
 template <typename T>
 __global__ void rope_kernel(T* __restrict__ x, int64_t rows, int64_t ld, int64_t col0, int heads, int hd, int64_t seq,
                             const float* __restrict__ ct, const float* __restrict__ st) {
@@ -356,7 +437,16 @@ extern "C" zoact_status zoact_rmsnorm(const void* x, const void* w, int64_t rows
   ZO_CHECK(rows >= 1 && d >= 1 && rows <= 0x7FFFFFFF, "rmsnorm: bad shape");
   ZO_CHECK(dtype == ZOACT_F32 || dtype == ZOACT_BF16, "rmsnorm: dtype must be F32 or BF16");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (dtype == ZOACT_BF16)
+  const bool vec = dtype == ZOACT_BF16 && ((uintptr_t)x % 16) == 0 && ((uintptr_t)w % 16) == 0 && ((uintptr_t)y % 16) == 0;
+  if (vec && d == 2048)
+    rmsnorm_bf16_vec_kernel<1><<<(unsigned)rows, 256, 0, s>>>((const uint16_t*)x, (const uint16_t*)w, d, eps, (uint16_t*)y);
+  else if (vec && d == 4096)
+    rmsnorm_bf16_vec_kernel<2><<<(unsigned)rows, 256, 0, s>>>((const uint16_t*)x, (const uint16_t*)w, d, eps, (uint16_t*)y);
+  else if (vec && d == 6144)
+    rmsnorm_bf16_vec_kernel<3><<<(unsigned)rows, 256, 0, s>>>((const uint16_t*)x, (const uint16_t*)w, d, eps, (uint16_t*)y);
+  else if (vec && d == 8192)
+    rmsnorm_bf16_vec_kernel<4><<<(unsigned)rows, 256, 0, s>>>((const uint16_t*)x, (const uint16_t*)w, d, eps, (uint16_t*)y);
+  else if (dtype == ZOACT_BF16)
     rmsnorm_kernel<uint16_t><<<(unsigned)rows, 256, 0, s>>>((const uint16_t*)x, (const uint16_t*)w, d, eps, (uint16_t*)y);
   else
     rmsnorm_kernel<float><<<(unsigned)rows, 256, 0, s>>>((const float*)x, (const float*)w, d, eps, (float*)y);
@@ -387,7 +477,12 @@ extern "C" zoact_status zoact_rope(void* x, int32_t dtype, int64_t rows, int64_t
   ZO_CHECK(dtype == ZOACT_F32 || dtype == ZOACT_BF16, "rope: dtype must be F32 or BF16");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int64_t total = rows * n_heads * (head_dim / 2);
-  if (dtype == ZOACT_BF16)
+  const bool vec = dtype == ZOACT_BF16 && (head_dim / 2) % 8 == 0 && ld % 8 == 0 && col0 % 8 == 0 &&
+                   ((uintptr_t)x % 16) == 0 && ((uintptr_t)cos_t % 16) == 0 && ((uintptr_t)sin_t % 16) == 0;
+  if (vec)
+    rope_bf16_vec_kernel<<<grid1d(total / 8), 256, 0, s>>>((uint16_t*)x, rows, ld, col0, n_heads, head_dim, seq, cos_t,
+                                                           sin_t);
+  else if (dtype == ZOACT_BF16)
     rope_kernel<uint16_t><<<grid1d(total), 256, 0, s>>>((uint16_t*)x, rows, ld, col0, n_heads, head_dim, seq, cos_t, sin_t);
   else
     rope_kernel<float><<<grid1d(total), 256, 0, s>>>((float*)x, rows, ld, col0, n_heads, head_dim, seq, cos_t, sin_t);

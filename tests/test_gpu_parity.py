@@ -271,6 +271,30 @@ def test_linear_pm_int4(c_bf16):
     assert_bf16_close(got, ref, what="int4")
 
 
+@pytest.mark.parametrize("T,K,N,r,flags,c_bf16", [
+    (200, 512, 384, 32, 0, True),      # ragged tokens and features
+    (300, 1024, 512, 64, 0, False),
+    (257, 256, 512, 32, 1, True),      # SwiGLU epilogue
+    (64, 4096, 256, 16, 2, True),      # ReLU epilogue, 32 groups per row
+])
+def test_linear_pm_int4_precomputed(T, K, N, r, flags, c_bf16):
+    """INT4 weights with the precomputed C +/- eps Z (the four-wave INT4 schedule): against
+    the oracle on the dequantised weights, and bitwise against the same layer in bf16
+    holding those dequantised weights."""
+    announce("linear_pm int4 precomputed", T, K, N, r, flags, c_bf16)
+    x, w, b, ut, packed, scales = _layer_inputs(T, K, N, r, seed=K + N, bias=True, int4=True)
+    c = synth.normal((N * r,), 0.02, 4, 5)
+    if c_bf16:
+        c = rne_bf16(c)
+    wq = olin.dequant_int4(packed, scales).astype(np.float32)
+    got = _run_gpu_linear(x, w, b, ut, c, 0, r, 1e-3, 9, 4, T, K, N, flags=flags, packed=packed, scales=scales,
+                          c_bf16=c_bf16, precomputed=True)
+    same = _run_gpu_linear(x, wq, b, ut, c, 0, r, 1e-3, 9, 4, T, K, N, flags=flags, c_bf16=c_bf16, precomputed=True)
+    np.testing.assert_array_equal(got, same)
+    ref = _oracle_linear(x, wq, b, ut, c.reshape(N, r), 0, r, 1e-3, 9, 4, flags=flags)
+    assert_bf16_close(got, ref, what="int4 precomputed")
+
+
 def test_linear_pm_r0_fp32_logits():
     announce("linear_pm logits")
     T, K, N = 100, 256, 528
