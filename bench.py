@@ -194,7 +194,8 @@ def bench_single_linear(args, dev):
 
 # ------------------------------------------------------------------ adapted linear at the 8B layer shapes
 def bench_linear_shapes(dev, reps=10):
-    """projection + fused +/- GEMM per Llama-3-8B layer shape, M = 8192 stacked rows, r = 32."""
+    """perturbed coefficients + projection + fused +/- GEMM per Llama-3-8B layer shape,
+    M = 8192 stacked rows, r = 32."""
     import torch
 
     import synth
@@ -221,8 +222,12 @@ def bench_linear_shapes(dev, reps=10):
             p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev)
             y = torch.empty(2 * T, N // 2 if flags else N, dtype=torch.bfloat16, device=dev)
             pert = Z.Pert(3, 1, 0, 1e-3)
+            # C +/- eps Z formed once per step for the layer's slice, as the model step does
+            ch = torch.empty(2 * N * r, dtype=torch.bfloat16, device=dev)
+            layer.ch, layer.ch_stride = ch, N * r
 
             def call():
+                Z.perturb_coeffs(arena, 0, N * r, pert, ch)
                 Z.project(x, ut, p)
                 Z.linear_fwd_pm(layer, arena, x, T, p, y, pert, flags=flags)
 
@@ -240,7 +245,7 @@ def bench_linear_shapes(dev, reps=10):
             res[name] = {"M": M, "N": N, "K": K, "us": round(sec * 1e6, 1), "tflops": round(flop / sec / 1e12, 1)}
             tot_flop += flop
             tot_s += sec
-            del x, layer, arena, p, y
+            del x, layer, arena, p, y, ch
             torch.cuda.empty_cache()
         mean = tot_flop / tot_s / 1e12
         out[mode] = {"shapes": res, "flop_weighted_tflops": round(mean, 1),
