@@ -251,7 +251,52 @@ def bench_linear_shapes(dev, reps=10):
         out[mode] = {"shapes": res, "flop_weighted_tflops": round(mean, 1),
                      "frac_of_bf16_peak": round(mean / PEAK_BF16_TFLOPS, 4)}
         log(f"8B shapes {mode}: {mean:.1f} TFLOP/s")
+    out["ranks_o_shape_bf16"] = bench_ranks(dev, reps)
     return out
+
+
+def bench_ranks(dev, reps, ranks=(1, 8, 32, 64, 128, 256)):
+    """perturbed coefficients + projection + fused GEMM of the o-projection shape
+    (M = 8192 stacked rows, N = K = 4096) across adapter ranks."""
+    import torch
+
+    import synth
+    from paper_2607_01125_amd import zoact as Z
+
+    T, K, N = 4096, 4096, 4096
+    x = synth.device_normal((2 * T, K), 1.0, 9, K, device=dev, dtype=torch.bfloat16)
+    w = synth.device_normal((N, K), 0.02, 9, N, K, device=dev, dtype=torch.bfloat16)
+    y = torch.empty(2 * T, N, dtype=torch.bfloat16, device=dev)
+    res = {}
+    for r in ranks:
+        ut = synth.device_normal((r, K), 1.0 / math.sqrt(K), 9, r, K, device=dev, dtype=torch.bfloat16)
+        layer = Z.Linear(w, K, N, r, ut, 0)
+        arena = Z.Arena(torch.zeros(N * r, device=dev), torch.zeros(N * r, device=dev), torch.zeros(N * r, device=dev))
+        p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev)
+        ch = torch.empty(2 * N * r, dtype=torch.bfloat16, device=dev)
+        layer.ch, layer.ch_stride = ch, N * r
+        pert = Z.Pert(3, 1, 0, 1e-3)
+
+        def call():
+            Z.perturb_coeffs(arena, 0, N * r, pert, ch)
+            Z.project(x, ut, p)
+            Z.linear_fwd_pm(layer, arena, x, T, p, y, pert)
+
+        call()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        sec = e0.elapsed_time(e1) / reps * 1e-3
+        M = 2 * T
+        flop = 2 * M * N * K + 2 * M * K * r + 2 * M * r * N
+        res[str(r)] = {"us": round(sec * 1e6, 1), "tflops": round(flop / sec / 1e12, 1)}
+        del ut, layer, arena, p, ch
+    log("ranks (o shape): " + ", ".join(f"r={k} {v['tflops']}" for k, v in res.items()))
+    return res
 
 
 # ------------------------------------------------------------------ full models

@@ -98,7 +98,9 @@ typedef struct {
   const void* ch;       /* optional (BF16 activations): the perturbed coefficients
                            bf16(C +/- eps Z) of this layer from zoact_perturb_coeffs,
                            half 0 [d_out][r] at ch, half 1 at ch + ch_half_stride
-                           elements; NULL = formed inside the kernel (same values)  */
+                           elements; NULL = formed inside the kernel (same values).
+                           r % 8 == 0: 16-byte aligned, stride a multiple of 8;
+                           otherwise 2-byte alignment suffices                     */
   int64_t ch_half_stride;
 } zoact_linear;
 

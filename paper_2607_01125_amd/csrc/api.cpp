@@ -108,10 +108,12 @@ zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, co
   }
   if (flags & ZOACT_EPI_SWIGLU) CHECK(L->d_out % 32 == 0, "linear_fwd_pm: SWIGLU needs d_out %% 32 == 0");
   if (L->ch != nullptr) {
-    CHECK(x_dtype == ZOACT_BF16 && L->r > 0 && L->r % 8 == 0,
-          "linear_fwd_pm: precomputed coefficients need BF16 activations and r %% 8 == 0");
-    CHECK(aligned16(L->ch) && L->ch_half_stride % 8 == 0 && L->ch_half_stride >= L->d_out * (int64_t)L->r,
-          "linear_fwd_pm: ch must be 16-byte aligned with a half stride >= d_out * r, multiple of 8");
+    CHECK(x_dtype == ZOACT_BF16 && L->r > 0, "linear_fwd_pm: precomputed coefficients need BF16 activations and r > 0");
+    CHECK(L->ch_half_stride >= L->d_out * (int64_t)L->r && (reinterpret_cast<uintptr_t>(L->ch) & 1) == 0,
+          "linear_fwd_pm: ch must be 2-byte aligned with a half stride >= d_out * r");
+    if (L->r % 8 == 0)
+      CHECK(aligned16(L->ch) && L->ch_half_stride % 8 == 0,
+            "linear_fwd_pm: with r %% 8 == 0, ch must be 16-byte aligned with a half stride that is a multiple of 8");
   }
   if (x_dtype == ZOACT_F32) {
     CHECK(L->w_dtype == ZOACT_F32 && y_dtype == ZOACT_F32, "linear_fwd_pm: F32 activations need F32 weights and output");

@@ -1,5 +1,6 @@
 // Fused +/- adapted GEMM, four-wave software-pipelined schedule for gfx950
-// (bf16 or group-128 INT4 weights, 0 <= r <= 64, r % 8 == 0).
+// (bf16 or group-128 INT4 weights; 0 <= r <= 256 with precomputed C_h, else r <= 64,
+// r % 8 == 0).
 //
 // Same contraction as the other kernels: y[h] = x[h] W^T + b + p[h] (C + s_h eps Z)^T
 // (Section 3, factored perturbed forward), over a 256-feature x 256-token tile.
@@ -19,7 +20,7 @@
 //  * C_h = bf16(C + s_h eps Z) for the tile's 256 features is either read from the
 //    precomputed array (zoact_perturb_coeffs) or generated in the prologue, while the first
 //    stages are in flight, into a dedicated 32 KB LDS region; the rank-r correction runs
-//    as one or two extra 32-deep steps against p[h] read from global memory.
+//    as ceil(r / 32) extra 32-deep steps against p[h] read from global memory.
 //  * INT4 weights: the packed row and group scale of each lane's feature arrive by the
 //    direct path six stages ahead; during step s every lane turns its row of stage s + 2
 //    into bf16(q * s) in eight slices, one after each row of MFMAs, and writes it into the
@@ -373,34 +374,43 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
     if (s + 1 < S) one_step(s + 1, fa1, fb1, fa0, fb0);
   }
 
-  // ---- rank-r correction: [p[h] | C_h] as ceil(r/32) extra 32-deep steps
+  // ---- rank-r correction: [p[h] | C_h] as ceil(r/32) extra 32-deep steps.  Operands come
+  // straight from global memory (p[h] rows, and C_h rows when precomputed; otherwise the
+  // C_h region in LDS, r <= 64); a rank that is not a multiple of 8 is gathered element
+  // by element, zero past r.
   if (HAS_R) {
     const int kts = (a.r + 31) >> 5;
     const uint16_t* ph = a.p + (int64_t)half * a.T * a.r;
+    const uint16_t* chh = a.ch + (int64_t)half * a.ch_stride;
+    const bool vec = (a.r & 7) == 0;
     const bf16x8 zero8 = {};
+    auto row8 = [&](const uint16_t* rowp, int col) -> bf16x8 {
+      if (vec) return col < a.r ? *reinterpret_cast<const bf16x8*>(rowp + col) : zero8;
+      uint16_t e[8];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      if (t < kts) {
+      for (int q = 0; q < 8; ++q) e[q] = col + q < a.r ? rowp[col + q] : (uint16_t)0;
+      const uint4 u = make_uint4(pack2(e[0], e[1]), pack2(e[2], e[3]), pack2(e[4], e[5]), pack2(e[6], e[7]));
+      return __builtin_bit_cast(bf16x8, u);
+    };
+    for (int t = 0; t < kts; ++t) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          int64_t m = m0 + wm0 + j * 16 + lr;
-          m = m > a.T - 1 ? a.T - 1 : m;
-          const int col = t * 32 + lk * 8;
-          fb0[j] = col < a.r ? *reinterpret_cast<const bf16x8*>(ph + m * a.r + col) : zero8;
-          if (I4 || a.ch != nullptr) {
-            int64_t n = n0 + wn0 + j * 16 + lr;
-            n = n > a.N - 1 ? a.N - 1 : n;
-            fa0[j] = col < a.r ? *reinterpret_cast<const bf16x8*>(a.ch + (int64_t)half * a.ch_stride + n * a.r + col)
-                               : zero8;
-          } else {
-            fa0[j] = *reinterpret_cast<const bf16x8*>(chreg + swz(wn0 + j * 16 + lr, t * 4 + lk));
-          }
+      for (int j = 0; j < 8; ++j) {
+        int64_t m = m0 + wm0 + j * 16 + lr;
+        m = m > a.T - 1 ? a.T - 1 : m;
+        const int col = t * 32 + lk * 8;
+        fb0[j] = row8(ph + m * a.r, col);
+        if (I4 || a.ch != nullptr) {
+          int64_t n = n0 + wn0 + j * 16 + lr;
+          n = n > a.N - 1 ? a.N - 1 : n;
+          fa0[j] = row8(chh + n * a.r, col);
+        } else {
+          fa0[j] = *reinterpret_cast<const bf16x8*>(chreg + swz(wn0 + j * 16 + lr, t * 4 + lk));
         }
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-#pragma unroll
-          for (int j = 0; j < 8; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa0[i], fb0[j], acc[i][j], 0, 0, 0);
       }
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa0[i], fb0[j], acc[i][j], 0, 0, 0);
     }
   }
 
@@ -536,12 +546,14 @@ hipError_t launch_4w(const GemmArgs& a, hipStream_t s) {
 }  // namespace
 
 // Returns hipErrorNotSupported outside this kernel's coverage: bf16 weights, or INT4 weights
-// with the precomputed C_h (depth a multiple of 128); r <= 64, r % 8 == 0; depth a multiple
-// of 32; a half of x or the weights below 2 GiB.
+// with the precomputed C_h (depth a multiple of 128); r <= 256 with the precomputed C_h,
+// else r <= 64 and r % 8 == 0; depth a multiple of 32; a half of x or the weights below 2 GiB.
 hipError_t launch_linear_pm_4w(const GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s) {
   const bool i4 = w_dtype == ZOACT_INT4_G128;
   if (!(w_dtype == ZOACT_BF16 || (i4 && a.ch != nullptr && a.r > 0 && a.K % 128 == 0))) return hipErrorNotSupported;
-  if (a.r > 64 || (a.r % 8) != 0 || (a.K % 32) != 0) return hipErrorNotSupported;
+  // ranks up to 256 and of any size read C_h precomputed; the in-kernel C_h covers r <= 64, r % 8 == 0
+  if (a.ch == nullptr && (a.r > 64 || (a.r % 8) != 0)) return hipErrorNotSupported;
+  if (a.r > 256 || (a.K % 32) != 0) return hipErrorNotSupported;
   if (a.T * a.K * 2 >= (int64_t(1) << 31) || a.N * a.K * 2 >= (int64_t(1) << 31)) return hipErrorNotSupported;
   // The correction-enabled instantiation also serves r = 0 (no chunks, no correction
   // steps): it is the one whose register assignment keeps the accumulators in AGPRs.

@@ -264,7 +264,7 @@ class Decoder:
         # C +/- eps Z for the whole arena in one streaming pass; every adapted GEMM reads its
         # slice instead of regenerating Z per workgroup
         self._ch = None
-        if adapt and self.act == torch.bfloat16 and self.k > 0 and self.r % 8 == 0:
+        if adapt and self.act == torch.bfloat16 and self.k > 0:
             if self._ch_all is None:
                 self._ch_all = torch.empty(2 * self.k, dtype=torch.bfloat16, device=self.dev)
             Z.perturb_coeffs(self.arena, 0, self.k, pert, self._ch_all)

@@ -109,6 +109,9 @@ def test_tiny_fp32_twenty_steps():
     ("llama-bf16-ragged", LLAMA_S, "bf16", 3, 50),
     ("opt-bf16", OPT_S, "bf16", 2, 40),
     ("llama-int4", LLAMA_S, "int4", 2, 64),
+    ("llama-bf16-r1", synth.shrink(LLAMA_S, rank=1), "bf16", 2, 64),
+    ("llama-bf16-r128", synth.shrink(LLAMA_S, rank=128), "bf16", 2, 48),
+    ("llama-int4-r1", synth.shrink(LLAMA_S, rank=1), "int4", 2, 40),
 ])
 def test_forward_pm_matches_oracle(name, shape, mode, B, S):
     announce("forward pm", name)

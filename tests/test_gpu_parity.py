@@ -228,6 +228,29 @@ def test_linear_pm_precomputed_coefficients(T, K, N, r, off, flags):
     assert_bf16_close(pre, ref, what="linear_pm precomputed")
 
 
+@pytest.mark.parametrize("T,K,N,r,off,flags", [
+    (300, 512, 336, 1, 3, 0),
+    (200, 256, 272, 3, 0, 0),
+    (257, 512, 512, 128, 5, 0),
+    (130, 1024, 256, 256, 0, 0),
+    (200, 512, 512, 128, 0, 1),
+    (64, 256, 256, 200, 7, 2),
+])
+def test_linear_pm_ranks(T, K, N, r, off, flags):
+    """Ranks 1, 3, 128, 200 and 256, with C +/- eps Z formed in the kernel and read
+    precomputed (the four-wave schedule covers every rank up to 256 from the precomputed
+    array; the correction gathers element by element when r % 8 != 0)."""
+    announce("linear_pm ranks", T, K, N, r, off, flags)
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=T + r)
+    c = synth.normal((off + N * r + 3,), 0.01, 8, r)
+    eps, seed, step = 1e-3, 42, 6
+    ref = _oracle_linear(x, w, b, ut, c[off:off + N * r].reshape(N, r), off, r, eps, seed, step, flags=flags)
+    inline = _run_gpu_linear(x, w, b, ut, c, off, r, eps, seed, step, T, K, N, flags=flags)
+    assert_bf16_close(inline, ref, what=f"linear_pm r={r}")
+    pre = _run_gpu_linear(x, w, b, ut, c, off, r, eps, seed, step, T, K, N, flags=flags, precomputed=True)
+    assert_bf16_close(pre, ref, what=f"linear_pm precomputed r={r}")
+
+
 def test_linear_pm_zero_coeffs_reproduce_base_and_determinism():
     announce("linear_pm base")
     T, K, N, r = 200, 256, 256, 32
