@@ -72,8 +72,14 @@ def zo_adam(c: np.ndarray, m: np.ndarray, v: np.ndarray, g, z: np.ndarray, hp: A
     g = _F(g)
     if not np.isfinite(g):
         return c.copy(), m.copy(), v.copy(), 1
+    return adam_on_estimate(c, m, v, g * np.asarray(z, dtype=np.float32), hp, c_bf16)
+
+
+def adam_on_estimate(c: np.ndarray, m: np.ndarray, v: np.ndarray, gh: np.ndarray, hp: AdamScalars,
+                     c_bf16: bool = False):
+    """Adam on a given per-coefficient estimate gh (fp32), in the order stated above."""
     c32 = np.asarray(c, dtype=np.float32)
-    gh = g * np.asarray(z, dtype=np.float32)
+    gh = np.asarray(gh, dtype=np.float32)
     if hp.weight_decay != 0.0:
         gh = gh + _F(hp.weight_decay) * c32
     m1 = _F(hp.beta1) * np.asarray(m, dtype=np.float32) + hp.one_minus_beta1 * gh
@@ -91,4 +97,42 @@ def zo_sgd(c: np.ndarray, g, z: np.ndarray, lr: float, c_bf16: bool = False):
     if not np.isfinite(g):
         return np.asarray(c).copy(), 1
     c1 = np.asarray(c, dtype=np.float32) - _F(lr) * (g * np.asarray(z, dtype=np.float32))
+    return (rne_bf16(c1) if c_bf16 else c1).astype(np.float32), 0
+
+
+# ------------------------------------------------------------------ one-sided, q queries
+# Section 3's averaged forward-difference estimate and the inner loop of Algorithm 2:
+# with the unperturbed loss L and L_j = L(B + mu Z^(j)) for j = 1..q,
+#     a_j = (L_j - L) / mu,    g_B = (1/q) sum_j a_j Z^(j),
+# accumulated in the algorithm's order (j ascending, then one division by q).  Reading of
+# the precision: fp32, one rounding per operation; Z^(j) is Z(seed, t, query j).
+
+def query_coeffs(losses, eps: float) -> np.ndarray:
+    """a_j = (L_j - L_0) / eps for j = 1..q in fp32 (losses = [L, L_1, .., L_q])."""
+    ls = np.asarray(losses, dtype=np.float32)
+    return (ls[1:] - ls[0]) / _F(eps)
+
+
+def query_estimate(a: np.ndarray, zs: np.ndarray) -> np.ndarray:
+    """g = (sum_j a_j Z^(j)) / q for zs [q][k] (fp32, j ascending)."""
+    acc = np.zeros(zs.shape[1], np.float32)
+    for j in range(zs.shape[0]):
+        acc = acc + _F(a[j]) * zs[j].astype(np.float32)
+    return acc / _F(zs.shape[0])
+
+
+def zo_adam_q(c, m, v, losses, zs, eps: float, hp: AdamScalars, c_bf16: bool = False):
+    """One-sided q-query ZO-Adam update.  Returns (c, m, v, status)."""
+    a = query_coeffs(losses, eps)
+    if not np.all(np.isfinite(a)):
+        return np.asarray(c).copy(), np.asarray(m).copy(), np.asarray(v).copy(), 1
+    return adam_on_estimate(c, m, v, query_estimate(a, zs), hp, c_bf16)
+
+
+def zo_sgd_q(c, losses, zs, eps: float, lr: float, c_bf16: bool = False):
+    """One-sided q-query ZO-SGD update: c = c - lr * g.  Returns (c, status)."""
+    a = query_coeffs(losses, eps)
+    if not np.all(np.isfinite(a)):
+        return np.asarray(c).copy(), 1
+    c1 = np.asarray(c, dtype=np.float32) - _F(lr) * query_estimate(a, zs)
     return (rne_bf16(c1) if c_bf16 else c1).astype(np.float32), 0

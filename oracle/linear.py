@@ -42,11 +42,18 @@ def z_block(seed: int, step: int, query: int, off: int, n_rows: int, r: int, row
 
 
 def perturbed_coeffs(c: np.ndarray, z: np.ndarray, eps: float, sign: int, mode: str) -> np.ndarray:
-    """C +/- eps Z: fp32 ops (eps*z first) then bf16 rounding in bf16 mode; float64 in fp32 mode."""
+    """C + sign eps Z for sign in {-1, 0, +1}: fp32 ops (eps*z first) then bf16 rounding in
+    bf16 mode; float64 in fp32 mode.  Sign 0 is the unperturbed C (Algorithm 2's reference
+    loss in the one-sided form)."""
     if mode == "bf16":
+        c32 = c.astype(np.float32)
+        if sign == 0:
+            return rne_bf16(c32).astype(np.float64)
         ez = np.float32(eps) * z.astype(np.float32)
-        ch = (c.astype(np.float32) + ez) if sign > 0 else (c.astype(np.float32) - ez)
+        ch = (c32 + ez) if sign > 0 else (c32 - ez)
         return rne_bf16(ch.astype(np.float32)).astype(np.float64)
+    if sign == 0:
+        return c.astype(np.float64)
     return c.astype(np.float64) + sign * float(np.float32(eps)) * z.astype(np.float64)
 
 

@@ -283,3 +283,20 @@ def zo_step(model: Model, tokens, c, m, v, t: int, eps: float, lr: float, seed: 
     z = olin.rng.gauss_range(seed, t, 0, 0, c.size)
     c1, m1, v1, st = oadam.zo_adam(c, m, v, g, z, oadam.adam_scalars(lr, t), c_bf16=c_bf16)
     return c1, m1, v1, (lp, lm, float(g))
+
+
+def zo_step_q(model: Model, tokens, c, m, v, t: int, eps: float, lr: float, seed: int, q: int, c_bf16=False,
+              optimizer: str = "adam"):
+    """One step of Algorithm 2 in its one-sided q-query form: the unperturbed loss L, the
+    losses L_j under B + mu Z^(j) (Z^(j) = Z(seed, t, query j)), the averaged estimate and
+    the optimiser update."""
+    losses = [model.loss(tokens, c, 0, eps, (seed, t, 0))]
+    for j in range(1, q + 1):
+        losses.append(model.loss(tokens, c, +1, eps, (seed, t, j)))
+    zs = np.stack([olin.rng.gauss_range(seed, t, j, 0, c.size) for j in range(1, q + 1)])
+    if optimizer == "adam":
+        c1, m1, v1, st = oadam.zo_adam_q(c, m, v, losses, zs, eps, oadam.adam_scalars(lr, t), c_bf16=c_bf16)
+    else:
+        c1, st = oadam.zo_sgd_q(c, losses, zs, eps, lr, c_bf16=c_bf16)
+        m1, v1 = m, v
+    return c1, m1, v1, losses
