@@ -83,6 +83,19 @@ typedef struct {
   float eps;      /* perturbation scale (the paper's mu)                  */
 } zoact_pert;
 
+/* Perturbations of the two stacked halves of one evaluation, in general form: half h
+ * evaluates C + sign[h] * eps * Z(seed, step, query[h]) with sign[h] in {-1, 0, +1}.
+ * The two-sided pair is {query, query} with signs {+1, -1}; the one-sided multi-query
+ * form of Algorithm 2 (Section 3's q-query average) evaluates the unperturbed model
+ * (sign 0) and C + eps Z^(j) for queries j = 1..q, two per evaluation. */
+typedef struct {
+  uint64_t seed;
+  uint32_t step;
+  uint32_t query[2];
+  int32_t sign[2];
+  float eps;
+} zoact_pert_pair;
+
 /* One adapted (or plain, r = 0) linear layer. */
 typedef struct {
   int32_t w_dtype;      /* ZOACT_F32, ZOACT_BF16 or ZOACT_INT4_G128               */
@@ -173,6 +186,14 @@ zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, co
                                  int32_t x_dtype, int64_t T, const void* p, const void* residual,
                                  uint32_t flags, const zoact_pert* pert, void* y, int32_t y_dtype,
                                  zoact_stream stream);
+/* The same contraction with the general pair: half h uses C + pp->sign[h] eps
+ * Z(pp->seed, pp->step, pp->query[h]).  zoact_linear_fwd_pm(pert) is this call with
+ * {pert->query, pert->query} and signs {+1, -1}.  A precomputed L->ch must hold the
+ * same pair (zoact_perturb_coeffs_pair with *pp). */
+zoact_status zoact_linear_fwd_pair(const zoact_linear* L, const zoact_arena* A, const void* x,
+                                   int32_t x_dtype, int64_t T, const void* p, const void* residual,
+                                   uint32_t flags, const zoact_pert_pair* pp, void* y, int32_t y_dtype,
+                                   zoact_stream stream);
 
 /* ------------------------------------------------------ perturbed coefficients
  * out[h][e - e0] = bf16(fp32(C[e]) + s_h fp32(eps Z(e))), s = (+1, -1), for arena
@@ -183,6 +204,10 @@ zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, co
  * out bf16 [2][n], 16-byte aligned.  Errors: range outside the arena, n < 1. */
 zoact_status zoact_perturb_coeffs(const zoact_arena* A, int64_t e0, int64_t n, const zoact_pert* pert, void* out,
                                   zoact_stream stream);
+/* The general pair: out[h][e - e0] = bf16(fp32(C[e]) + sign[h] fp32(eps Z(e; query[h])))
+ * (sign 0: bf16(C[e])). */
+zoact_status zoact_perturb_coeffs_pair(const zoact_arena* A, int64_t e0, int64_t n, const zoact_pert_pair* pp,
+                                       void* out, zoact_stream stream);
 
 /* ------------------------------------------------------ losses of both halves
  * Algorithm 2 needs the loss under each perturbation; the two-sided step needs
@@ -212,6 +237,21 @@ zoact_status zoact_step(const zoact_arena* A, const float* loss_pm, const zoact_
                         const zoact_adam* h, uint32_t* dev_status, zoact_stream stream);
 zoact_status zoact_step_sgd(const zoact_arena* A, const float* loss_pm, const zoact_pert* pert, float lr,
                             uint32_t* dev_status, zoact_stream stream);
+
+/* ------------------------------------------------------ one-sided multi-query step
+ * Algorithm 2 with q queries (Section 3's averaged forward-difference estimate):
+ * losses (device, fp32 [q + 1]) holds the unperturbed loss L at losses[0] and the
+ * loss under C + eps Z^(j) at losses[j], Z^(j) = Z(seed, step, query j), j = 1..q.
+ * Per query a_j = (L_j - L) / eps in fp32; per arena index e, in fp32 with one
+ * rounding per operation and j ascending,
+ *   acc = 0; acc = acc + a_j * Z^(j)(e) for j = 1..q;  gh = acc / q,
+ * then the Adam update of zoact_step on gh (zoact_step_q) or c = c - lr * gh
+ * (zoact_step_q_sgd).  1 <= q <= 256.  A non-finite a_j leaves the arena unchanged
+ * and ORs bit 0 into *dev_status (device, nullable). */
+zoact_status zoact_step_q(const zoact_arena* A, const float* losses, int32_t q, uint64_t seed, uint32_t step,
+                          float eps, const zoact_adam* h, uint32_t* dev_status, zoact_stream stream);
+zoact_status zoact_step_q_sgd(const zoact_arena* A, const float* losses, int32_t q, uint64_t seed, uint32_t step,
+                              float eps, float lr, uint32_t* dev_status, zoact_stream stream);
 
 /* ------------------------------------------------------ one-shot basis (Algorithm 1)
  * Top-r right singular vectors of the calibration activations X_l, i.e. the top-r

@@ -87,10 +87,12 @@ zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t 
   return hip_status(zoact::launch_project(x, dtype, n_tok, d_in, ut, r, p, st(stream)), "project");
 }
 
-zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
-                                 const void* p, const void* residual, uint32_t flags, const zoact_pert* pert, void* y,
-                                 int32_t y_dtype, zoact_stream stream) {
+zoact_status zoact_linear_fwd_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int32_t x_dtype,
+                                   int64_t T, const void* p, const void* residual, uint32_t flags,
+                                   const zoact_pert_pair* pert, void* y, int32_t y_dtype, zoact_stream stream) {
   CHECK(L != nullptr && pert != nullptr, "linear_fwd_pm: NULL layer or perturbation");
+  for (int h = 0; h < 2; ++h)
+    CHECK(pert->sign[h] >= -1 && pert->sign[h] <= 1, "linear_fwd_pm: sign[%d]=%d outside {-1, 0, 1}", h, pert->sign[h]);
   CHECK(x && y && L->w, "linear_fwd_pm: NULL x, y or w");
   CHECK(T >= 1, "linear_fwd_pm: T=%lld < 1", (long long)T);
   CHECK(L->d_in >= 1 && L->d_out >= 1, "linear_fwd_pm: empty layer");
@@ -134,14 +136,42 @@ zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, co
                     "linear_fwd_pm");
 }
 
-zoact_status zoact_perturb_coeffs(const zoact_arena* A, int64_t e0, int64_t n, const zoact_pert* pert, void* out,
-                                  zoact_stream stream) {
-  CHECK(A != nullptr && pert != nullptr && out != nullptr && A->c != nullptr, "perturb_coeffs: NULL argument");
+static zoact_pert_pair pm_pair(const zoact_pert& p) {
+  zoact_pert_pair pp{};
+  pp.seed = p.seed;
+  pp.step = p.step;
+  pp.query[0] = pp.query[1] = p.query;
+  pp.sign[0] = 1;
+  pp.sign[1] = -1;
+  pp.eps = p.eps;
+  return pp;
+}
+
+zoact_status zoact_linear_fwd_pm(const zoact_linear* L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
+                                 const void* p, const void* residual, uint32_t flags, const zoact_pert* pert, void* y,
+                                 int32_t y_dtype, zoact_stream stream) {
+  CHECK(pert != nullptr, "linear_fwd_pm: NULL perturbation");
+  const zoact_pert_pair pp = pm_pair(*pert);
+  return zoact_linear_fwd_pair(L, A, x, x_dtype, T, p, residual, flags, &pp, y, y_dtype, stream);
+}
+
+zoact_status zoact_perturb_coeffs_pair(const zoact_arena* A, int64_t e0, int64_t n, const zoact_pert_pair* pp,
+                                       void* out, zoact_stream stream) {
+  CHECK(A != nullptr && pp != nullptr && out != nullptr && A->c != nullptr, "perturb_coeffs: NULL argument");
   CHECK(float_type(A->c_dtype), "perturb_coeffs: arena dtype must be F32 or BF16");
   CHECK(n >= 1 && e0 >= 0 && e0 + n <= A->k, "perturb_coeffs: range [%lld, %lld) outside the arena (k=%lld)",
         (long long)e0, (long long)(e0 + n), (long long)A->k);
   CHECK(aligned16(out), "perturb_coeffs: out must be 16-byte aligned");
-  return hip_status(zoact::launch_perturb(*A, e0, n, *pert, static_cast<uint16_t*>(out), st(stream)), "perturb_coeffs");
+  for (int h = 0; h < 2; ++h)
+    CHECK(pp->sign[h] >= -1 && pp->sign[h] <= 1, "perturb_coeffs: sign[%d]=%d outside {-1, 0, 1}", h, pp->sign[h]);
+  return hip_status(zoact::launch_perturb(*A, e0, n, *pp, static_cast<uint16_t*>(out), st(stream)), "perturb_coeffs");
+}
+
+zoact_status zoact_perturb_coeffs(const zoact_arena* A, int64_t e0, int64_t n, const zoact_pert* pert, void* out,
+                                  zoact_stream stream) {
+  CHECK(pert != nullptr, "perturb_coeffs: NULL argument");
+  const zoact_pert_pair pp = pm_pair(*pert);
+  return zoact_perturb_coeffs_pair(A, e0, n, &pp, out, stream);
 }
 
 size_t zoact_loss_workspace_bytes(void) { return (size_t)2 * zoact::kLossBlocks * sizeof(double); }
@@ -190,6 +220,32 @@ zoact_status zoact_step_sgd(const zoact_arena* A, const float* loss_pm, const zo
   CHECK(A->k >= 0 && float_type(A->c_dtype), "step_sgd: bad arena");
   CHECK(A->k == 0 || A->c != nullptr, "step_sgd: NULL coefficients");
   return hip_status(zoact::launch_sgd(*A, loss_pm, *p, lr, dev_status, st(stream)), "step_sgd");
+}
+
+static zoact_status check_step_q(const zoact_arena* A, const float* losses, int32_t q, const char* who) {
+  CHECK(A != nullptr && losses != nullptr, "%s: NULL arena or losses", who);
+  CHECK(q >= 1 && q <= 256, "%s: q=%d outside [1, 256]", who, q);
+  CHECK(A->k >= 0 && float_type(A->c_dtype), "%s: bad arena", who);
+  CHECK(A->k == 0 || A->c != nullptr, "%s: NULL coefficients", who);
+  CHECK(aligned16(A->c) && aligned16(A->m) && aligned16(A->v), "%s: arena buffers must be 16-byte aligned", who);
+  return ZOACT_OK;
+}
+
+zoact_status zoact_step_q(const zoact_arena* A, const float* losses, int32_t q, uint64_t seed, uint32_t step,
+                          float eps, const zoact_adam* h, uint32_t* dev_status, zoact_stream stream) {
+  zoact_status s = check_step_q(A, losses, q, "step_q");
+  if (s != ZOACT_OK) return s;
+  CHECK(h != nullptr, "step_q: NULL Adam scalars");
+  CHECK(A->k == 0 || (A->m != nullptr && A->v != nullptr), "step_q: NULL moments");
+  return hip_status(zoact::launch_step_q(*A, losses, q, seed, step, eps, h, 0.f, dev_status, st(stream)), "step_q");
+}
+
+zoact_status zoact_step_q_sgd(const zoact_arena* A, const float* losses, int32_t q, uint64_t seed, uint32_t step,
+                              float eps, float lr, uint32_t* dev_status, zoact_stream stream) {
+  zoact_status s = check_step_q(A, losses, q, "step_q_sgd");
+  if (s != ZOACT_OK) return s;
+  return hip_status(zoact::launch_step_q(*A, losses, q, seed, step, eps, nullptr, lr, dev_status, st(stream)),
+                    "step_q_sgd");
 }
 
 static void eig_defaults(int32_t r, const zoact_eig_opts* o, int32_t& p, int32_t& iters, uint64_t& seed) {

@@ -15,7 +15,7 @@ __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uin
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 // Internal launchers return hipError_t from hipGetLastError() after the launch.
-hipError_t launch_perturb(const zoact_arena& A, int64_t e0, int64_t n, const zoact_pert& p, uint16_t* out,
+hipError_t launch_perturb(const zoact_arena& A, int64_t e0, int64_t n, const zoact_pert_pair& p, uint16_t* out,
                           hipStream_t s);
 hipError_t launch_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e0, int64_t n, float* out,
                         hipStream_t s);
@@ -23,11 +23,14 @@ hipError_t launch_adam(const zoact_arena& A, const float* loss_pm, const zoact_p
                        uint32_t* status, hipStream_t s);
 hipError_t launch_sgd(const zoact_arena& A, const float* loss_pm, const zoact_pert& p, float lr,
                       uint32_t* status, hipStream_t s);
+// one-sided multi-query update: Adam when h != nullptr, else SGD with rate lr
+hipError_t launch_step_q(const zoact_arena& A, const float* losses, int32_t q, uint64_t seed, uint32_t step, float eps,
+                         const zoact_adam* h, float lr, uint32_t* status, hipStream_t s);
 hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut, int32_t r,
                           void* p, hipStream_t s);
 hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
-                            const void* p, const void* residual, uint32_t flags, const zoact_pert& pert, void* y,
-                            int32_t y_dtype, hipStream_t s);
+                            const void* p, const void* residual, uint32_t flags, const zoact_pert_pair& pert,
+                            void* y, int32_t y_dtype, hipStream_t s);
 hipError_t launch_mse_pm(const void* y, int32_t dtype, const void* target, int64_t T, int64_t N, float* loss_pm,
                          void* ws, hipStream_t s);
 hipError_t launch_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V,

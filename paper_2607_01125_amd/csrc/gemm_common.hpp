@@ -20,12 +20,14 @@ struct GemmArgs {
   int32_t c_bf16;
   int64_t coef_offset;
   uint64_t seed;
-  uint32_t step, query;
+  uint32_t step;
+  uint32_t query_h[2];   // query index of half 0 / half 1
+  int32_t sign_h[2];     // -1, 0 or +1: half h uses C + sign_h[h] eps Z(query_h[h])
   float eps;
   int32_t tiles_m_half;  // token tiles per half
   int32_t tiles_n;
   int32_t n_tail;        // depth tiles of the correction block
-  const uint16_t* ch;    // precomputed bf16(C +/- eps Z), [2][N][r] with half stride ch_stride, or null
+  const uint16_t* ch;    // precomputed bf16(C + sign_h eps Z), [2][N][r] with half stride ch_stride, or null
   int64_t ch_stride;
 };
 
@@ -41,11 +43,12 @@ __device__ __forceinline__ float4 gauss4(uint64_t seed, uint32_t step, uint32_t 
   return make_float4(v[o], v[o + 1], v[o + 2], v[o + 3]);
 }
 
-// fp32 (C + sign*eps*z) rounded to bf16; the product eps*z is rounded before the sum.
-__device__ __forceinline__ uint16_t perturbed_bf16(float c, float z, float eps, bool plus) {
+// fp32 (C + sign*eps*z) rounded to bf16; the product eps*z is rounded before the sum
+// (sign 0: C itself).
+__device__ __forceinline__ uint16_t perturbed_bf16(float c, float z, float eps, int sign) {
 #pragma clang fp contract(off)
   const float ez = eps * z;
-  return f2bf(plus ? c + ez : c - ez);
+  return f2bf(sign > 0 ? c + ez : (sign < 0 ? c - ez : c));
 }
 
 __device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) { return (uint32_t)lo | ((uint32_t)hi << 16); }

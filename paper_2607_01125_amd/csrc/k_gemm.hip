@@ -115,7 +115,7 @@ __device__ __forceinline__ void store_main(uint16_t* wl, uint16_t* xl, const uin
 // Correction-block tile `tt`: W side = bf16(C + s eps Z) for coefficient columns
 // tt*64 .. tt*64+63 of each feature row, x side = p[h] for the same columns.
 __device__ __forceinline__ void load_tail(const GemmArgs& a, int64_t n0, const uint16_t* ph, int64_t m0, int64_t T,
-                                          bool plus, int tt, uint4 (&ws)[4], uint4 (&xs)[4]) {
+                                          int hf, int tt, uint4 (&ws)[4], uint4 (&xs)[4]) {
   const int t = threadIdx.x;
   const int row = t >> 1, half = t & 1;
   const int col0 = tt * 64 + half * 32;
@@ -132,7 +132,7 @@ __device__ __forceinline__ void load_tail(const GemmArgs& a, int64_t n0, const u
       const bool any = (n < a.N) && (col < a.r);
       if (any) {
         const uint64_t e = (uint64_t)(a.coef_offset + n * a.r + col);
-        z = gauss4(a.seed, a.step, a.query, e);
+        z = gauss4(a.seed, a.step, a.query_h[hf], e);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           if (col + j < a.r)
@@ -144,7 +144,7 @@ __device__ __forceinline__ void load_tail(const GemmArgs& a, int64_t n0, const u
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const bool ok = any && (col + j < a.r);
-        wv[g * 4 + j] = ok ? perturbed_bf16(cv[j], zz[j], a.eps, plus) : (uint16_t)0;
+        wv[g * 4 + j] = ok ? perturbed_bf16(cv[j], zz[j], a.eps, a.sign_h[hf]) : (uint16_t)0;
         xv[g * 4 + j] = (col + j < a.r && m < T) ? ph[m * a.r + col + j] : (uint16_t)0;
       }
     }
@@ -208,7 +208,6 @@ __global__ void __launch_bounds__(NTHR, 1) gemm_pm_kernel(GemmArgs a) {
   const int half = tm / a.tiles_m_half;
   const int64_t m0 = (int64_t)(tm % a.tiles_m_half) * BM;
   const int64_t n0 = (int64_t)tn * BN;
-  const bool plus = half == 0;
   const uint16_t* xh = a.x + (int64_t)half * a.T * a.K;
   const uint16_t* ph = a.p ? a.p + (int64_t)half * a.T * a.r : nullptr;
 
@@ -236,7 +235,7 @@ __global__ void __launch_bounds__(NTHR, 1) gemm_pm_kernel(GemmArgs a) {
   }
   // correction block: [p[h] | C + s eps Z], 64 coefficient columns per tile
   for (int tt = 0; tt < a.n_tail; ++tt) {
-    load_tail(a, n0, ph, m0, a.T, plus, tt, ws, xs);
+    load_tail(a, n0, ph, m0, a.T, half, tt, ws, xs);
     store_tail(WL(tt & 1), XL(tt & 1), ws, xs);
     __syncthreads();
     const int rem = a.r - tt * 64;
@@ -318,7 +317,9 @@ struct GemmArgsF32 {
   int32_t r;
   int64_t coef_offset;
   uint64_t seed;
-  uint32_t step, query;
+  uint32_t step;
+  uint32_t query_h[2];
+  int32_t sign_h[2];
   float eps;
   int32_t tiles_m_half;
 };
@@ -336,7 +337,6 @@ __global__ void __launch_bounds__(256) gemm_pm_f32_kernel(GemmArgsF32 a) {
   const int half = tm / a.tiles_m_half;
   const int64_t m0 = (int64_t)(tm % a.tiles_m_half) * 64;
   const int64_t n0 = (int64_t)blockIdx.x * 64;
-  const bool plus = half == 0;
   const float* xh = a.x + (int64_t)half * a.T * a.K;
   const float* ph = a.p ? a.p + (int64_t)half * a.T * a.r : nullptr;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
@@ -357,9 +357,10 @@ __global__ void __launch_bounds__(256) gemm_pm_f32_kernel(GemmArgsF32 a) {
         if (n < a.N) {
 #pragma clang fp contract(off)
           const int64_t e = a.coef_offset + n * a.r + i2;
-          const float z = rng::gauss_at(a.seed, a.step, a.query, (uint64_t)e);
+          const float z = rng::gauss_at(a.seed, a.step, a.query_h[half], (uint64_t)e);
           const float ez = a.eps * z;
-          wv = plus ? a.c[e] + ez : a.c[e] - ez;
+          const int sg = a.sign_h[half];
+          wv = sg > 0 ? a.c[e] + ez : (sg < 0 ? a.c[e] - ez : a.c[e]);
         }
       }
       xs[kk][rr] = xv;
@@ -525,7 +526,7 @@ hipError_t launch_linear_pm_pp(const gemm::GemmArgs& a, int w_dtype, int epi, bo
 hipError_t launch_linear_pm_4w(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
 
 hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
-                            const void* p, const void* residual, uint32_t flags, const zoact_pert& pert, void* y,
+                            const void* p, const void* residual, uint32_t flags, const zoact_pert_pair& pert, void* y,
                             int32_t y_dtype, hipStream_t s) {
   const int epi = (flags & ZOACT_EPI_SWIGLU) ? ZOACT_EPI_SWIGLU : (flags & ZOACT_EPI_RELU) ? ZOACT_EPI_RELU : 0;
   if (x_dtype == ZOACT_F32) {
@@ -542,7 +543,7 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
     a.coef_offset = L.coef_offset;
     a.seed = pert.seed;
     a.step = pert.step;
-    a.query = pert.query;
+    for (int h = 0; h < 2; ++h) a.query_h[h] = pert.query[h], a.sign_h[h] = pert.sign[h];
     a.eps = pert.eps;
     a.tiles_m_half = (int32_t)((T + 63) / 64);
     dim3 grid((unsigned)((L.d_out + 63) / 64), (unsigned)(2 * a.tiles_m_half));
@@ -571,7 +572,7 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
   a.coef_offset = L.coef_offset;
   a.seed = pert.seed;
   a.step = pert.step;
-  a.query = pert.query;
+  for (int h = 0; h < 2; ++h) a.query_h[h] = pert.query[h], a.sign_h[h] = pert.sign[h];
   a.eps = pert.eps;
   a.tiles_m_half = (int32_t)((T + BM - 1) / BM);
   a.tiles_n = (int32_t)((L.d_out + BN - 1) / BN);

@@ -101,7 +101,8 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
   const int half = tm / a.tiles_m_half;
   const int64_t m0 = (int64_t)(tm % a.tiles_m_half) * 256;
   const int64_t n0 = (int64_t)tn * 256;
-  const bool plus = half == 0;
+  const int sgn = a.sign_h[half];          // perturbation sign of this half
+  const uint32_t qry = a.query_h[half];   // and its query index
   const uint16_t* xh = a.x + (int64_t)half * a.T * a.K;
   const uint16_t* w = reinterpret_cast<const uint16_t*>(a.w);
 
@@ -151,12 +152,12 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
     uint2 packed = make_uint2(0u, 0u);
     if (4 * g < a.r && n < a.N) {
       const uint64_t e = (uint64_t)(a.coef_offset + n * a.r + 4 * g);
-      const float4 z = gauss4(a.seed, a.step, a.query, e);
+      const float4 z = gauss4(a.seed, a.step, qry, e);
       float cv[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) cv[j] = a.c_bf16 ? bf2f((uint16_t)cbits[q][j]) : __uint_as_float(cbits[q][j]);
-      packed.x = pack2(perturbed_bf16(cv[0], z.x, a.eps, plus), perturbed_bf16(cv[1], z.y, a.eps, plus));
-      packed.y = pack2(perturbed_bf16(cv[2], z.z, a.eps, plus), perturbed_bf16(cv[3], z.w, a.eps, plus));
+      packed.x = pack2(perturbed_bf16(cv[0], z.x, a.eps, sgn), perturbed_bf16(cv[1], z.y, a.eps, sgn));
+      packed.y = pack2(perturbed_bf16(cv[2], z.z, a.eps, sgn), perturbed_bf16(cv[3], z.w, a.eps, sgn));
     }
     *reinterpret_cast<uint2*>(chreg + swz(f, g >> 1) + (g & 1) * 4) = packed;
   };

@@ -141,23 +141,111 @@ __global__ void __launch_bounds__(256) sgd_kernel(void* __restrict__ cptr, int64
   }
 }
 
-// out[h][e - e0] = bf16(C[e] + s_h eps Z(e)); one Philox block (4 arena indices) per thread.
+// out[h][e - e0] = bf16(C[e] + s_h eps Z(e; q_h)) (s_h = 0: bf16(C[e])); one Philox block
+// (4 arena indices) per thread and half.
 template <bool BF16C>
 __global__ void __launch_bounds__(256) perturb_kernel(const void* __restrict__ cptr, int64_t e0, int64_t n,
-                                                      uint64_t seed, uint32_t step, uint32_t query, float eps,
-                                                      uint16_t* __restrict__ out) {
+                                                      uint64_t seed, uint32_t step, uint32_t q0, uint32_t q1,
+                                                      int32_t s0, int32_t s1, float eps, uint16_t* __restrict__ out) {
 #pragma clang fp contract(off)
   const int64_t b0 = e0 >> 2, b1 = (e0 + n - 1) >> 2;
+  const bool same = q0 == q1;
   for (int64_t b = b0 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b <= b1; b += (int64_t)gridDim.x * blockDim.x) {
-    const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
+    const float4 za = rng::gauss_block(seed, step, q0, (uint64_t)b);
+    const float4 zb = same ? za : rng::gauss_block(seed, step, q1, (uint64_t)b);
 #pragma unroll
     for (int l = 0; l < 4; ++l) {
       const int64_t e = 4 * b + l;
       if (e < e0 || e >= e0 + n) continue;
       const float c = BF16C ? bf2f(reinterpret_cast<const uint16_t*>(cptr)[e]) : reinterpret_cast<const float*>(cptr)[e];
-      const float ez = eps * rng::lane_of(z, l);
-      out[e - e0] = f2bf(c + ez);
-      out[n + e - e0] = f2bf(c - ez);
+      const float ea = eps * rng::lane_of(za, l), eb = eps * rng::lane_of(zb, l);
+      out[e - e0] = f2bf(s0 > 0 ? c + ea : (s0 < 0 ? c - ea : c));
+      out[n + e - e0] = f2bf(s1 > 0 ? c + eb : (s1 < 0 ? c - eb : c));
+    }
+  }
+}
+
+// One-sided multi-query estimate of Algorithm 2: gh = (sum_j a_j Z^(j)) / q with
+// a_j = (L_j - L_0) / eps, accumulated in fp32 with j ascending; then Adam (ADAM) or
+// SGD on gh.  Returns false (no update anywhere) when some a_j is not finite.
+__device__ __forceinline__ bool query_coeffs_finite(const float* losses, int q, float eps) {
+#pragma clang fp contract(off)
+  const float l0 = losses[0];
+  for (int j = 1; j <= q; ++j)
+    if (!__builtin_isfinite((losses[j] - l0) / eps)) return false;
+  return true;
+}
+
+template <bool BF16C, bool ADAM>
+__global__ void __launch_bounds__(256) step_q_kernel(void* __restrict__ cptr, float* __restrict__ mptr,
+                                                     float* __restrict__ vptr, int64_t k, const float* losses, int q,
+                                                     uint64_t seed, uint32_t step, float eps, AdamConst h, float lr,
+                                                     uint32_t* status) {
+#pragma clang fp contract(off)
+  if (!query_coeffs_finite(losses, q, eps)) {
+    if (status != nullptr && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, 1u);
+    return;
+  }
+  const float l0 = losses[0];
+  const float qf = (float)q;
+  const int64_t nb = (k + 3) >> 2;
+  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb; b += (int64_t)gridDim.x * blockDim.x) {
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int j = 1; j <= q; ++j) {
+      const float aj = (losses[j] - l0) / eps;
+      const float4 z = rng::gauss_block(seed, step, (uint32_t)j, (uint64_t)b);
+      acc[0] = acc[0] + aj * z.x;
+      acc[1] = acc[1] + aj * z.y;
+      acc[2] = acc[2] + aj * z.z;
+      acc[3] = acc[3] + aj * z.w;
+    }
+    const int64_t e = 4 * b;
+    if (e + 4 <= k) {
+      float cv[4], mv[4] = {0.f, 0.f, 0.f, 0.f}, vv[4] = {0.f, 0.f, 0.f, 0.f};
+      if (BF16C) {
+        const vu2 cb = __builtin_nontemporal_load(reinterpret_cast<const vu2*>(reinterpret_cast<const uint16_t*>(cptr) + e));
+        cv[0] = bf2f((uint16_t)(cb.x & 0xFFFFu)); cv[1] = bf2f((uint16_t)(cb.x >> 16));
+        cv[2] = bf2f((uint16_t)(cb.y & 0xFFFFu)); cv[3] = bf2f((uint16_t)(cb.y >> 16));
+      } else {
+        const vf4 cf = ld_nt(reinterpret_cast<const float*>(cptr) + e);
+        cv[0] = cf.x; cv[1] = cf.y; cv[2] = cf.z; cv[3] = cf.w;
+      }
+      if (ADAM) {
+        const vf4 m4 = ld_nt(mptr + e), v4 = ld_nt(vptr + e);
+        mv[0] = m4.x; mv[1] = m4.y; mv[2] = m4.z; mv[3] = m4.w;
+        vv[0] = v4.x; vv[1] = v4.y; vv[2] = v4.z; vv[3] = v4.w;
+      }
+#pragma unroll
+      for (int l = 0; l < 4; ++l) {
+        const float gh = acc[l] / qf;
+        cv[l] = ADAM ? adam_one(cv[l], mv[l], vv[l], gh, h) : cv[l] - lr * gh;
+      }
+      if (ADAM) {
+        st_nt(mptr + e, vf4{mv[0], mv[1], mv[2], mv[3]});
+        st_nt(vptr + e, vf4{vv[0], vv[1], vv[2], vv[3]});
+      }
+      if (BF16C) {
+        const vu2 cb = {(uint32_t)f2bf(cv[0]) | ((uint32_t)f2bf(cv[1]) << 16),
+                        (uint32_t)f2bf(cv[2]) | ((uint32_t)f2bf(cv[3]) << 16)};
+        __builtin_nontemporal_store(cb, reinterpret_cast<vu2*>(reinterpret_cast<uint16_t*>(cptr) + e));
+      } else {
+        st_nt(reinterpret_cast<float*>(cptr) + e, vf4{cv[0], cv[1], cv[2], cv[3]});
+      }
+    } else {
+      for (int l = 0; l < 4 && e + l < k; ++l) {
+        const float gh = acc[l] / qf;
+        float c = BF16C ? bf2f(reinterpret_cast<const uint16_t*>(cptr)[e + l]) : reinterpret_cast<const float*>(cptr)[e + l];
+        if (ADAM) {
+          float m = mptr[e + l], v = vptr[e + l];
+          c = adam_one(c, m, v, gh, h);
+          mptr[e + l] = m;
+          vptr[e + l] = v;
+        } else {
+          c = c - lr * gh;
+        }
+        if (BF16C) reinterpret_cast<uint16_t*>(cptr)[e + l] = f2bf(c);
+        else reinterpret_cast<float*>(cptr)[e + l] = c;
+      }
     }
   }
 }
@@ -177,14 +265,34 @@ hipError_t launch_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e0
   return hipGetLastError();
 }
 
-hipError_t launch_perturb(const zoact_arena& A, int64_t e0, int64_t n, const zoact_pert& p, uint16_t* out,
+hipError_t launch_perturb(const zoact_arena& A, int64_t e0, int64_t n, const zoact_pert_pair& p, uint16_t* out,
                           hipStream_t s) {
   const int64_t nb = ((e0 + n - 1) >> 2) - (e0 >> 2) + 1;
   const dim3 grid((unsigned)grid_for(nb));
   if (A.c_dtype == ZOACT_BF16)
-    perturb_kernel<true><<<grid, dim3(256), 0, s>>>(A.c, e0, n, p.seed, p.step, p.query, p.eps, out);
+    perturb_kernel<true><<<grid, dim3(256), 0, s>>>(A.c, e0, n, p.seed, p.step, p.query[0], p.query[1], p.sign[0],
+                                                    p.sign[1], p.eps, out);
   else
-    perturb_kernel<false><<<grid, dim3(256), 0, s>>>(A.c, e0, n, p.seed, p.step, p.query, p.eps, out);
+    perturb_kernel<false><<<grid, dim3(256), 0, s>>>(A.c, e0, n, p.seed, p.step, p.query[0], p.query[1], p.sign[0],
+                                                     p.sign[1], p.eps, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_step_q(const zoact_arena& A, const float* losses, int32_t q, uint64_t seed, uint32_t step, float eps,
+                         const zoact_adam* h, float lr, uint32_t* status, hipStream_t s) {
+  if (A.k == 0) return hipSuccess;
+  AdamConst c{};
+  if (h) c = AdamConst{h->beta1, h->beta2, h->eps, h->weight_decay, h->step_size, h->inv_sqrt_bc2, h->one_minus_beta1,
+                       h->one_minus_beta2};
+  const dim3 grid((unsigned)grid_for((A.k + 3) >> 2));
+  const bool bf = A.c_dtype == ZOACT_BF16;
+#define ZO_Q(BF, AD) step_q_kernel<BF, AD><<<grid, dim3(256), 0, s>>>(A.c, A.m, A.v, A.k, losses, q, seed, step, eps, c, lr, status)
+  if (h) {
+    if (bf) ZO_Q(true, true); else ZO_Q(false, true);
+  } else {
+    if (bf) ZO_Q(true, false); else ZO_Q(false, false);
+  }
+#undef ZO_Q
   return hipGetLastError();
 }
 

@@ -248,11 +248,12 @@ class Decoder:
             lin.r, lin.ut, lin.ch, lin.ch_stride = 0, None, None, 0
             Z.linear_fwd_pm(lin, None, x, T, None, y, pert, residual, flags)
 
-    def forward(self, tokens: torch.Tensor, pert: Z.Pert, *, calibrate=None, distinct_halves=False):
+    def forward(self, tokens: torch.Tensor, pert: Z.Pert | Z.PertPair, *, calibrate=None, distinct_halves=False):
         """Both halves of the forward; logits fp32 [2][n_seq][seq][V] in the buffer set.
 
-        tokens int32 [n_seq][seq] (or [2][n_seq][seq] with distinct_halves).  Half 0 uses
-        C + eps Z, half 1 C - eps Z.  With `calibrate` (a callable taking (layer, site, x))
+        tokens int32 [n_seq][seq] (or [2][n_seq][seq] with distinct_halves).  With a Pert,
+        half 0 uses C + eps Z and half 1 C - eps Z; with a PertPair, half h uses
+        C + sign[h] eps Z(query[h]).  With `calibrate` (a callable taking (layer, site, x))
         the linears are not adapted and each site's input [2 T][d_in] is handed over
         before it is consumed (Algorithm 1's calibration forward).
         """
@@ -382,3 +383,29 @@ class Decoder:
         else:
             raise ValueError(optimizer)
         return self.loss_pm
+
+    def step_q(self, tokens: torch.Tensor, seed: int, eps: float, lr: float, q: int, optimizer: str = "adam"):
+        """One step of Algorithm 2 in its one-sided q-query form: the unperturbed loss L and
+        L_j under C + eps Z^(j), j = 1..q (Z^(j) = Z(seed, t, query j)), evaluated two per
+        stacked forward (ceil((q + 1) / 2) forwards; a spare half re-evaluates L), then the
+        averaged estimate drives Adam or SGD.  Returns the device losses [L, L_1 .. L_q, spare]."""
+        if not 1 <= q <= 256:
+            raise ValueError("q must be in [1, 256]")
+        self.t += 1
+        n_fwd = (q + 2) // 2
+        losses = torch.zeros(2 * n_fwd, dtype=torch.float32, device=self.dev)
+
+        def spec(e):            # evaluation e: 0 = unperturbed, 1..q = query e, beyond = spare (unperturbed)
+            return (e, 1) if 1 <= e <= q else (0, 0)
+
+        for i in range(n_fwd):
+            (q0, s0), (q1, s1) = spec(2 * i), spec(2 * i + 1)
+            self.forward(tokens, Z.pert_pair(seed, self.t, (q0, q1), (s0, s1), eps))
+            Z.xent_pm(self._cur["logits"], tokens, losses[2 * i:2 * i + 2], self.loss_ws)
+        if optimizer == "adam":
+            Z.step_q(self.arena, losses, q, seed, self.t, eps, Z.adam_desc(lr, self.t), self.status)
+        elif optimizer == "sgd":
+            Z.step_q_sgd(self.arena, losses, q, seed, self.t, eps, lr, self.status)
+        else:
+            raise ValueError(optimizer)
+        return losses

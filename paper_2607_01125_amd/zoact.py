@@ -33,6 +33,16 @@ class Pert(ctypes.Structure):
                 ("eps", ctypes.c_float)]
 
 
+class PertPair(ctypes.Structure):
+    """General pair: half h evaluates C + sign[h] eps Z(seed, step, query[h]), sign in {-1, 0, 1}."""
+    _fields_ = [("seed", ctypes.c_uint64), ("step", ctypes.c_uint32), ("query", ctypes.c_uint32 * 2),
+                ("sign", ctypes.c_int32 * 2), ("eps", ctypes.c_float)]
+
+
+def pert_pair(seed: int, step: int, queries, signs, eps: float) -> PertPair:
+    return PertPair(seed, step, (ctypes.c_uint32 * 2)(*queries), (ctypes.c_int32 * 2)(*signs), eps)
+
+
 class LinearDesc(ctypes.Structure):
     _fields_ = [("w_dtype", ctypes.c_int32), ("w", ctypes.c_void_p), ("w_scales", ctypes.c_void_p),
                 ("bias", ctypes.c_void_p), ("ut", ctypes.c_void_p), ("d_in", ctypes.c_int64),
@@ -69,6 +79,11 @@ SIGNATURES = {
     "zoact_linear_fwd_pm": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I32, _I64, _P, _P, _U32,
                              ctypes.POINTER(Pert), _P, _I32, _P], _I32),
     "zoact_perturb_coeffs": ([ctypes.POINTER(ArenaDesc), _I64, _I64, ctypes.POINTER(Pert), _P, _P], _I32),
+    "zoact_linear_fwd_pair": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I32, _I64, _P, _P, _U32,
+                               ctypes.POINTER(PertPair), _P, _I32, _P], _I32),
+    "zoact_perturb_coeffs_pair": ([ctypes.POINTER(ArenaDesc), _I64, _I64, ctypes.POINTER(PertPair), _P, _P], _I32),
+    "zoact_step_q": ([ctypes.POINTER(ArenaDesc), _P, _I32, _U64, _U32, _F, ctypes.POINTER(AdamDesc), _P, _P], _I32),
+    "zoact_step_q_sgd": ([ctypes.POINTER(ArenaDesc), _P, _I32, _U64, _U32, _F, _F, _P, _P], _I32),
     "zoact_loss_workspace_bytes": ([], _SZ),
     "zoact_mse_pm": ([_P, _I32, _P, _I64, _I64, _P, _P, _SZ, _P], _I32),
     "zoact_xent_pm": ([_P, _P, _I64, _I64, _I64, _P, _P, _SZ, _P], _I32),
@@ -183,18 +198,23 @@ def project(x: torch.Tensor, ut: torch.Tensor, p: torch.Tensor, stream=None):
 
 
 def linear_fwd_pm(layer: Linear, arena: Arena | None, x: torch.Tensor, T: int, p: torch.Tensor | None,
-                  y: torch.Tensor, pert: Pert, residual: torch.Tensor | None = None, flags: int = 0, stream=None):
+                  y: torch.Tensor, pert: Pert | PertPair, residual: torch.Tensor | None = None, flags: int = 0,
+                  stream=None):
+    """Both halves of the adapted linear: the +/- pair for a Pert (zoact_linear_fwd_pm), the
+    general pair for a PertPair (zoact_linear_fwd_pair)."""
     d = layer.desc()
     a = arena.desc() if arena is not None else None
-    _check(lib().zoact_linear_fwd_pm(ctypes.byref(d), ctypes.byref(a) if a is not None else None, _ptr(x),
-                                     dtype_code(x), T, _ptr(p), _ptr(residual), flags, ctypes.byref(pert), _ptr(y),
-                                     dtype_code(y), _stream(stream)))
+    fn = lib().zoact_linear_fwd_pair if isinstance(pert, PertPair) else lib().zoact_linear_fwd_pm
+    _check(fn(ctypes.byref(d), ctypes.byref(a) if a is not None else None, _ptr(x), dtype_code(x), T, _ptr(p),
+              _ptr(residual), flags, ctypes.byref(pert), _ptr(y), dtype_code(y), _stream(stream)))
 
 
-def perturb_coeffs(arena: Arena, e0: int, n: int, pert: Pert, out: torch.Tensor, stream=None):
-    """out bf16 [2][n]: bf16(C[e] +/- eps Z(e)) for arena indices e0 .. e0 + n - 1."""
+def perturb_coeffs(arena: Arena, e0: int, n: int, pert: Pert | PertPair, out: torch.Tensor, stream=None):
+    """out bf16 [2][n]: bf16(C[e] + s_h eps Z(e)) for arena indices e0 .. e0 + n - 1 (s = (+1, -1)
+    for a Pert; the pair's signs and queries for a PertPair)."""
     a = arena.desc()
-    _check(lib().zoact_perturb_coeffs(ctypes.byref(a), e0, n, ctypes.byref(pert), _ptr(out), _stream(stream)))
+    fn = lib().zoact_perturb_coeffs_pair if isinstance(pert, PertPair) else lib().zoact_perturb_coeffs
+    _check(fn(ctypes.byref(a), e0, n, ctypes.byref(pert), _ptr(out), _stream(stream)))
 
 
 def loss_workspace_bytes() -> int:
@@ -226,6 +246,21 @@ def step_sgd(arena: Arena, loss_pm: torch.Tensor, pert: Pert, lr: float, status:
     a = arena.desc()
     _check(lib().zoact_step_sgd(ctypes.byref(a), _ptr(loss_pm), ctypes.byref(pert), lr, _ptr(status),
                                 _stream(stream)))
+
+
+def step_q(arena: Arena, losses: torch.Tensor, q: int, seed: int, step: int, eps: float, adam: AdamDesc,
+           status: torch.Tensor | None = None, stream=None):
+    """One-sided q-query update (Adam): losses fp32 [q + 1] = (L, L_1 .. L_q) on the device."""
+    a = arena.desc()
+    _check(lib().zoact_step_q(ctypes.byref(a), _ptr(losses), q, seed, step, eps, ctypes.byref(adam), _ptr(status),
+                              _stream(stream)))
+
+
+def step_q_sgd(arena: Arena, losses: torch.Tensor, q: int, seed: int, step: int, eps: float, lr: float,
+               status: torch.Tensor | None = None, stream=None):
+    a = arena.desc()
+    _check(lib().zoact_step_q_sgd(ctypes.byref(a), _ptr(losses), q, seed, step, eps, lr, _ptr(status),
+                                  _stream(stream)))
 
 
 def basis_workspace_bytes(d: int, r: int, opts: EigOpts | None = None) -> int:

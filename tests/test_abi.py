@@ -92,3 +92,26 @@ def test_basis_init_workspace_holds_the_gram():
     for d in (129, 4096):
         g = (d * d * 4 + 255) // 256 * 256
         assert Z.basis_init_workspace_bytes(d, 8) == g + Z.basis_workspace_bytes(d, 8)
+
+
+def test_pair_and_query_step_validation():
+    L = Z.lib()
+    a = Z.ArenaDesc(Z.F32, 16, 16, 16, 100)
+    bad = Z.pert_pair(1, 1, (0, 1), (1, 2), 1e-3)
+    d = Z.LinearDesc(Z.BF16, 16, None, None, None, 64, 64, 0, 0)
+    st = L.zoact_linear_fwd_pair(ctypes.byref(d), None, ctypes.c_void_p(16), Z.BF16, 4, None, None, 0,
+                                 ctypes.byref(bad), ctypes.c_void_p(16), Z.BF16, None)
+    assert st == Z.E_INVALID and b"sign" in L.zoact_last_error()
+    st = L.zoact_perturb_coeffs_pair(ctypes.byref(a), 0, 10, ctypes.byref(bad), ctypes.c_void_p(16), None)
+    assert st == Z.E_INVALID and b"sign" in L.zoact_last_error()
+    adam = Z.adam_desc(1e-3, 1)
+    for q in (0, 257):
+        st = L.zoact_step_q(ctypes.byref(a), ctypes.c_void_p(16), q, 1, 1, 1e-3, ctypes.byref(adam), None, None)
+        assert st == Z.E_INVALID and b"q=" in L.zoact_last_error()
+        st = L.zoact_step_q_sgd(ctypes.byref(a), ctypes.c_void_p(16), q, 1, 1, 1e-3, 1e-4, None, None)
+        assert st == Z.E_INVALID
+    st = L.zoact_step_q(ctypes.byref(a), None, 4, 1, 1, 1e-3, ctypes.byref(adam), None, None)
+    assert st == Z.E_INVALID
+    # the two-sided pair written as a general pair is accepted (fails later only for want of a GPU)
+    good = Z.pert_pair(1, 1, (0, 0), (1, -1), 1e-3)
+    assert tuple(good.sign) == (1, -1) and tuple(good.query) == (0, 0)
