@@ -390,9 +390,33 @@ def bench_model(dev, which, warmup=2, steps=5):
         rec["adam"] = {"coefficients": g.k, "bytes_per_coefficient": per, "us": round(us, 1),
                        "achieved_GBps": round(gbs, 1), "peak_GBps": PEAK_HBM_GBS,
                        "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        # Algorithm 2's one-sided form with q = 8 queries: L and L_1..L_8 in five stacked
+        # forwards, then the update that regenerates eight Gaussians per coefficient
+        q = 8
+        g.step_q(tok, 1, 1e-3, lr, q)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(2):
+            g.step_q(tok, 1, 1e-3, lr, q)
+        e1.record()
+        torch.cuda.synchronize()
+        qms = e0.elapsed_time(e1) / 2
+        losses = torch.full((q + 1,), 2.0, dtype=torch.float32, device=dev)
+        Z.step_q(g.arena, losses, q, 1, 99, 1e-3, adam, g.status)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            Z.step_q(g.arena, losses, q, 1, 99, 1e-3, adam, g.status)
+        e1.record()
+        torch.cuda.synchronize()
+        qus = e0.elapsed_time(e1) / reps * 1e3
+        rec["one_sided_q8"] = {"ms_per_step": round(qms, 2), "forwards_per_step": (q + 2) // 2,
+                               "steps_per_s": round(1e3 / qms, 3), "update_us": round(qus, 1),
+                               "update_GBps": round(g.k * per / (qus * 1e-6) / 1e9, 1)}
     del g
     torch.cuda.empty_cache()
-    log(f"{which}: {rec['steps_per_s']} steps/s, {rec['model_tflops']} TFLOP/s, init {rec['basis_init_s']} s")
+    log(f"{which}: {rec['steps_per_s']} steps/s, {rec['model_tflops']} TFLOP/s, init {rec['basis_init_s']} s"
+        + (f", one-sided q=8 {rec['one_sided_q8']['ms_per_step']} ms/step" if "one_sided_q8" in rec else ""))
     return rec
 
 
