@@ -5,19 +5,21 @@ d_in = d_out = 4096, rank r = 32, 8192 tokens per perturbation half, activations
 with a planted low-rank structure (64 directions carrying 90% of the variance),
 W ~ N(0, 0.02^2).  One step is the whole hot path of a +/- ZO step:
     C +/- eps Z (one pass over C)  ->  P = x U (both halves)  ->  fused +/- adapted GEMM
-    ->  MSE of both halves against a fixed in-subspace teacher  ->  ZO-Adam on C.
+    whose epilogue sums the squared errors of both halves against a fixed in-subspace
+    teacher (y is never stored)  ->  ZO-Adam on C.
 The activation basis U comes from the one-shot basis initialisation (timed
 separately, outside the step).  Inputs are resident in HBM before timing starts.
 
 Besides the headline line the run measures (unless --quick):
-  * the fused +/- adapted linear (projection + fused GEMM) at the Llama-3-8B layer
-    shapes, M = 8192 stacked rows, bf16 and INT4 weights: TFLOP/s per shape and
-    the FLOP-weighted mean;
+  * the fused +/- adapted linear (coefficient pass + projection + fused GEMM) at the
+    Llama-3-8B layer shapes, M = 8192 stacked rows, bf16 and INT4 weights: TFLOP/s per
+    shape and the FLOP-weighted mean; the o-projection shape across ranks 1..256;
   * full ZO steps of random-initialised decoders: Llama-3-8B shape in bf16 and with
     INT4 weights (16 x 256 tokens, r = 32 on all seven projections) and OPT-13B
     shape in bf16 (8 x 512 tokens, r = 64 on q, v, out, fc1, fc2, basis
     initialisation from 32 x 512 calibration tokens timed): steps/s, model TFLOP/s;
-  * ZO-Adam over the Llama-3-8B arena (44,040,192 coefficients): GB/s against HBM.
+  * ZO-Adam over the Llama-3-8B arena (44,040,192 coefficients): GB/s against HBM;
+  * the one-sided q = 8 form of the Llama step (five stacked forwards) and its update.
 
 Prints one JSON line.  `roofline` is the fused GEMM of the headline workload:
 algorithmic FLOPs per launch over its mean duration (HIP events on its stream),
@@ -141,9 +143,8 @@ def bench_single_linear(args, dev):
     arena = Z.Arena(c, torch.zeros_like(c), torch.zeros_like(c))
     layer = Z.Linear(w, K, N, r, ut, 0)
     p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev)
-    y = torch.empty(2 * T, N, dtype=torch.bfloat16, device=dev)
     loss = torch.zeros(2, dtype=torch.float32, device=dev)
-    ws_l = torch.empty(Z.loss_workspace_bytes(), dtype=torch.uint8, device=dev)
+    ws_l = torch.empty(Z.linear_mse_workspace_bytes(T, N), dtype=torch.uint8, device=dev)
     status = torch.zeros(1, dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream()
 
@@ -156,10 +157,11 @@ def bench_single_linear(args, dev):
         Z.project(x_pm, ut, p)
         if ev is not None:
             ev[0].record(stream)
-        Z.linear_fwd_pm(layer, arena, x_pm, T, p, y, pert)
+        # both halves' forward with the regression loss summed in the GEMM epilogue (y is
+        # never stored), then the fixed-order sum of the per-tile partials
+        Z.linear_mse(layer, arena, x_pm, T, p, pert, tgt, loss, ws_l)
         if ev is not None:
             ev[1].record(stream)
-        Z.mse_pm(y, tgt, loss, ws_l)
         Z.step(arena, loss, pert, Z.adam_desc(lr, t), status)
 
     for t in range(1, args.warmup + 1):
@@ -182,7 +184,8 @@ def bench_single_linear(args, dev):
     assert int(status.item()) == 0, "non-finite projected gradient"
     return {
         "ms_per_step": ms_per_step, "init_ms": init_ms, "flops": flops,
-        "roofline": {"kernel": f"{DOMINANT_KERNEL} (fused ± adapted GEMM, M=16384, N=K=4096, r=32)",
+        "roofline": {"kernel": f"{DOMINANT_KERNEL} (fused ± adapted GEMM with the MSE epilogue, M=16384, "
+                               f"N=K=4096, r=32; timed with the tile-sum kernel that follows it)",
                      "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic_record(DOMINANT_KERNEL, "single_linear_4096", DOMINANT_SOURCES),
@@ -459,7 +462,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (planted low-rank activations, random-init W, seeded)",
         "config": {"workload": "single adapted linear, bf16, d_in=d_out=4096, r=32, 8192 tokens per ± half "
-                               "(projection + fused ± forward + MSE + ZO-Adam)",
+                               "(C±εZ pass + projection + fused ± forward with the MSE in its epilogue + ZO-Adam)",
                    **head["config"], "parallelism": "single GPU"},
         "adapted_linear_tflops": round(head["flops"] / (ms * 1e-3) / 1e12, 1),
         "basis_init_ms": round(head["init_ms"], 1),

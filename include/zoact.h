@@ -219,6 +219,19 @@ zoact_status zoact_perturb_coeffs_pair(const zoact_arena* A, int64_t e0, int64_t
  *   tokens int32 [B][S] (host-validated range is the caller's duty; ids outside
  *   [0, V) are clamped). */
 size_t zoact_loss_workspace_bytes(void);
+/* Fused form of the single-layer regression loss: the adapted linear of both halves
+ * (as zoact_linear_fwd_pair computes it, bias included, no residual or activation)
+ * followed by loss_pm[h] = mean over T x d_out of (bf16(y[h]) - target)^2, without
+ * storing y.  The sum of squares runs in the GEMM's epilogue (fp32 per lane, fp64
+ * across the tile) and a fixed-order fp64 sum over tiles; it differs from
+ * zoact_linear_fwd_pair + zoact_mse_pm by summation order only.  BF16 activations,
+ * bf16 target [T][d_out] (16-byte aligned); BF16 or INT4 weights (INT4 with L->ch).
+ * ws: at least zoact_linear_mse_workspace_bytes(T, d_out) bytes (16-byte aligned).
+ * Errors: shapes the fused kernel does not cover -> ZOACT_E_UNSUPPORTED. */
+size_t zoact_linear_mse_workspace_bytes(int64_t T, int64_t d_out);
+zoact_status zoact_linear_mse_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t T,
+                                   const void* p, const zoact_pert_pair* pp, const void* target, float* loss_pm,
+                                   void* ws, size_t ws_bytes, zoact_stream stream);
 zoact_status zoact_mse_pm(const void* y, int32_t dtype, const void* target, int64_t T, int64_t N,
                           float* loss_pm, void* ws, size_t ws_bytes, zoact_stream stream);
 zoact_status zoact_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V,

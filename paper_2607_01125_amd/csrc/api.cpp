@@ -87,9 +87,9 @@ zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t 
   return hip_status(zoact::launch_project(x, dtype, n_tok, d_in, ut, r, p, st(stream)), "project");
 }
 
-zoact_status zoact_linear_fwd_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int32_t x_dtype,
-                                   int64_t T, const void* p, const void* residual, uint32_t flags,
-                                   const zoact_pert_pair* pert, void* y, int32_t y_dtype, zoact_stream stream) {
+static zoact_status validate_linear(const zoact_linear* L, const zoact_arena* A, const void* x, int32_t x_dtype,
+                                    int64_t T, const void* p, const void* residual, uint32_t flags,
+                                    const zoact_pert_pair* pert, const void* y, int32_t y_dtype) {
   CHECK(L != nullptr && pert != nullptr, "linear_fwd_pm: NULL layer or perturbation");
   for (int h = 0; h < 2; ++h)
     CHECK(pert->sign[h] >= -1 && pert->sign[h] <= 1, "linear_fwd_pm: sign[%d]=%d outside {-1, 0, 1}", h, pert->sign[h]);
@@ -132,6 +132,14 @@ zoact_status zoact_linear_fwd_pair(const zoact_linear* L, const zoact_arena* A, 
       CHECK(L->w_scales != nullptr, "linear_fwd_pm: INT4 needs w_scales");
     }
   }
+  return ZOACT_OK;
+}
+
+zoact_status zoact_linear_fwd_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int32_t x_dtype,
+                                   int64_t T, const void* p, const void* residual, uint32_t flags,
+                                   const zoact_pert_pair* pert, void* y, int32_t y_dtype, zoact_stream stream) {
+  const zoact_status v = validate_linear(L, A, x, x_dtype, T, p, residual, flags, pert, y, y_dtype);
+  if (v != ZOACT_OK) return v;
   return hip_status(zoact::launch_linear_pm(*L, A, x, x_dtype, T, p, residual, flags, *pert, y, y_dtype, st(stream)),
                     "linear_fwd_pm");
 }
@@ -185,6 +193,27 @@ zoact_status zoact_mse_pm(const void* y, int32_t dtype, const void* target, int6
   if (ws == nullptr || ws_bytes < zoact_loss_workspace_bytes())
     return fail(ZOACT_E_WORKSPACE, "mse_pm: workspace needs %zu bytes", zoact_loss_workspace_bytes());
   return hip_status(zoact::launch_mse_pm(y, dtype, target, T, N, loss_pm, ws, st(stream)), "mse_pm");
+}
+
+size_t zoact_linear_mse_workspace_bytes(int64_t T, int64_t d_out) {
+  if (T < 1 || d_out < 1) return 0;
+  return (size_t)2 * (size_t)((T + 255) / 256) * (size_t)((d_out + 255) / 256) * sizeof(double);
+}
+
+zoact_status zoact_linear_mse_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t T,
+                                   const void* p, const zoact_pert_pair* pp, const void* target, float* loss_pm,
+                                   void* ws, size_t ws_bytes, zoact_stream stream) {
+  CHECK(target != nullptr && loss_pm != nullptr, "linear_mse: NULL target or loss");
+  CHECK(L != nullptr && aligned16(target), "linear_mse: NULL layer or misaligned target");
+  // the shared validation of the layer, with y standing in for the unused output
+  const zoact_status v = validate_linear(L, A, x, ZOACT_BF16, T, p, nullptr, 0, pp, target, ZOACT_BF16);
+  if (v != ZOACT_OK) return v;
+  const size_t need = zoact_linear_mse_workspace_bytes(T, L->d_out);
+  if (ws == nullptr || ws_bytes < need || !aligned16(ws))
+    return fail(ZOACT_E_WORKSPACE, "linear_mse: workspace needs %zu bytes, 16-byte aligned", need);
+  return hip_status(zoact::launch_linear_mse(*L, A, x, T, p, *pp, target, static_cast<double*>(ws), loss_pm,
+                                             st(stream)),
+                    "linear_mse");
 }
 
 zoact_status zoact_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V, float* loss_pm,

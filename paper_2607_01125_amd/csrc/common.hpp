@@ -31,6 +31,12 @@ hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d
 hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
                             const void* p, const void* residual, uint32_t flags, const zoact_pert_pair& pert,
                             void* y, int32_t y_dtype, hipStream_t s);
+// Adapted linear of both halves with the regression loss fused into the epilogue (y not
+// stored): per-tile sums into part [2][tiles], then loss_pm[h] = sum / (T * d_out).
+hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, const void* p,
+                             const zoact_pert_pair& pert, const void* target, double* part, float* loss_pm,
+                             hipStream_t s);
+hipError_t launch_sum_mean(const double* part, int64_t n, double count, float* loss_pm, hipStream_t s);
 hipError_t launch_mse_pm(const void* y, int32_t dtype, const void* target, int64_t T, int64_t N, float* loss_pm,
                          void* ws, hipStream_t s);
 hipError_t launch_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V,

@@ -29,7 +29,13 @@ struct GemmArgs {
   int32_t n_tail;        // depth tiles of the correction block
   const uint16_t* ch;    // precomputed bf16(C + sign_h eps Z), [2][N][r] with half stride ch_stride, or null
   int64_t ch_stride;
+  const uint16_t* tgt;   // EPI_MSE: regression target [T][N] (bf16); y is not stored
+  double* part;          // EPI_MSE: per-tile sums of squared errors [2][tiles_m_half * tiles_n]
 };
+
+// Internal epilogue selector (not a public flag): the tile's squared errors against tgt
+// are summed instead of storing y.
+constexpr int EPI_MSE = 1 << 8;
 
 __device__ __forceinline__ int swz(int row, int kc) { return (row << 6) + ((kc ^ (row & 7)) << 3); }
 

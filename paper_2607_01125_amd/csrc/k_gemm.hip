@@ -525,6 +525,36 @@ int schedule_choice() {
 hipError_t launch_linear_pm_pp(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
 hipError_t launch_linear_pm_4w(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
 
+// Arguments of the bf16-activation kernels for one call.
+static GemmArgs bf16_args(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, const void* p,
+                   const void* residual, const zoact_pert_pair& pert, void* y) {
+  GemmArgs a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.w = L.w;
+  a.wsc = static_cast<const uint16_t*>(L.w_scales);
+  a.bias = static_cast<const uint16_t*>(L.bias);
+  a.p = static_cast<const uint16_t*>(p);
+  a.c = (L.r > 0 && A) ? A->c : nullptr;
+  a.resid = static_cast<const uint16_t*>(residual);
+  a.y = y;
+  a.T = T;
+  a.N = L.d_out;
+  a.K = L.d_in;
+  a.r = L.r;
+  a.c_bf16 = (A && A->c_dtype == ZOACT_BF16) ? 1 : 0;
+  a.coef_offset = L.coef_offset;
+  a.seed = pert.seed;
+  a.step = pert.step;
+  for (int h = 0; h < 2; ++h) a.query_h[h] = pert.query[h], a.sign_h[h] = pert.sign[h];
+  a.eps = pert.eps;
+  a.tiles_m_half = (int32_t)((T + BM - 1) / BM);
+  a.tiles_n = (int32_t)((L.d_out + BN - 1) / BN);
+  a.n_tail = (L.r + 63) / 64;
+  a.ch = static_cast<const uint16_t*>(L.ch);
+  a.ch_stride = L.ch_half_stride;
+  return a;
+}
+
 hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
                             const void* p, const void* residual, uint32_t flags, const zoact_pert_pair& pert, void* y,
                             int32_t y_dtype, hipStream_t s) {
@@ -555,30 +585,7 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
     return hipGetLastError();
   }
 
-  GemmArgs a{};
-  a.x = static_cast<const uint16_t*>(x);
-  a.w = L.w;
-  a.wsc = static_cast<const uint16_t*>(L.w_scales);
-  a.bias = static_cast<const uint16_t*>(L.bias);
-  a.p = static_cast<const uint16_t*>(p);
-  a.c = (L.r > 0 && A) ? A->c : nullptr;
-  a.resid = static_cast<const uint16_t*>(residual);
-  a.y = y;
-  a.T = T;
-  a.N = L.d_out;
-  a.K = L.d_in;
-  a.r = L.r;
-  a.c_bf16 = (A && A->c_dtype == ZOACT_BF16) ? 1 : 0;
-  a.coef_offset = L.coef_offset;
-  a.seed = pert.seed;
-  a.step = pert.step;
-  for (int h = 0; h < 2; ++h) a.query_h[h] = pert.query[h], a.sign_h[h] = pert.sign[h];
-  a.eps = pert.eps;
-  a.tiles_m_half = (int32_t)((T + BM - 1) / BM);
-  a.tiles_n = (int32_t)((L.d_out + BN - 1) / BN);
-  a.n_tail = (L.r + 63) / 64;
-  a.ch = static_cast<const uint16_t*>(L.ch);
-  a.ch_stride = L.ch_half_stride;
+  GemmArgs a = bf16_args(L, A, x, T, p, residual, pert, y);
   const dim3 grid((unsigned)(2 * a.tiles_m_half * a.tiles_n));
   const bool i4 = L.w_dtype == ZOACT_INT4_G128;
   const bool of = y_dtype == ZOACT_F32;
@@ -603,6 +610,17 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
   ZO_DISPATCH(true, ZOACT_EPI_RELU, false)
 #undef ZO_DISPATCH
   return hipErrorNotSupported;
+}
+
+hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, const void* p,
+                             const zoact_pert_pair& pert, const void* target, double* part, float* loss_pm,
+                             hipStream_t s) {
+  GemmArgs a = bf16_args(L, A, x, T, p, nullptr, pert, nullptr);
+  a.tgt = static_cast<const uint16_t*>(target);
+  a.part = part;
+  const hipError_t e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
+  if (e != hipSuccess) return e;
+  return launch_sum_mean(part, (int64_t)a.tiles_m_half * a.tiles_n, (double)T * (double)L.d_out, loss_pm, s);
 }
 
 hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut, int32_t r, void* p,

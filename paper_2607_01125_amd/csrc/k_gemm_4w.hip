@@ -422,6 +422,21 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
   barrier();
   float* ep = reinterpret_cast<float*>(lds) + wave * (64 * 132);
   constexpr int LDR = 132;  // padded fp32 row
+  float sq_acc = 0.f;       // EPI_MSE: this lane's sum of squared errors
+  // EPI_MSE: the target rows this lane meets in both passes, loaded up front so their
+  // latency overlaps the staging instead of stalling every row (clamped in bounds; rows
+  // past the ends are skipped below)
+  uint4 tpre[2][16];
+  if constexpr (EPI == EPI_MSE) {
+    const int64_t nc = min((int64_t)(n0 + wn0 + (lane & 15) * 8), a.N - 8);
+#pragma unroll
+    for (int ps = 0; ps < 2; ++ps)
+#pragma unroll
+      for (int it = 0; it < 16; ++it) {
+        const int64_t m = min((int64_t)(m0 + wm0 + ps * 64 + (lane >> 4) + 4 * it), a.T - 1);
+        tpre[ps][it] = *reinterpret_cast<const uint4*>(a.tgt + m * a.N + nc);
+      }
+  }
   const int64_t nout = (EPI == ZOACT_EPI_SWIGLU) ? a.N / 2 : a.N;
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
@@ -501,7 +516,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
           o[e] = v_lo[e] + bb[e];
           o[e + 4] = v_hi[e] + bb[e + 4];
         }
-        if (a.resid) {
+        if (EPI != EPI_MSE && a.resid) {
           const uint4 rv = *reinterpret_cast<const uint4*>(a.resid + row * nout + n);
           const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
 #pragma unroll
@@ -513,6 +528,19 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
         if (EPI == ZOACT_EPI_RELU) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) o[e] = fmaxf(o[e], 0.0f);
+        }
+        if constexpr (EPI == EPI_MSE) {
+          // squared error of the bf16-rounded output against the target, summed in fp32
+          const uint4 tv = tpre[pass][it];
+          const uint32_t tw[4] = {tv.x, tv.y, tv.z, tv.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float d0 = bf2f(f2bf(o[2 * e])) - bf2f((uint16_t)(tw[e] & 0xFFFF));
+            const float d1 = bf2f(f2bf(o[2 * e + 1])) - bf2f((uint16_t)(tw[e] >> 16));
+            sq_acc += d0 * d0;
+            sq_acc += d1 * d1;
+          }
+          continue;
         }
         if (OUT_F32) {
           float* yp = reinterpret_cast<float*>(a.y) + row * nout + n;
@@ -526,6 +554,18 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w_kernel(GemmArgs a) {
       }
     }
     __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
+  }
+  if constexpr (EPI == EPI_MSE) {
+    // tile sum in a fixed order: lanes (fp64 butterfly), then the four waves in order
+    double v = (double)sq_acc;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    double* red = reinterpret_cast<double*>(reinterpret_cast<char*>(lds) + 4 * 64 * LDR * 4);
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    if (threadIdx.x == 0)
+      a.part[(int64_t)half * a.tiles_m_half * a.tiles_n + (int64_t)(tm % a.tiles_m_half) * a.tiles_n + tn] =
+          ((red[0] + red[1]) + red[2]) + red[3];
   }
 }
 
@@ -565,6 +605,7 @@ hipError_t launch_linear_pm_4w(const GemmArgs& a, int w_dtype, int epi, bool out
   ZO_4W(0, true)
   ZO_4W(ZOACT_EPI_SWIGLU, false)
   ZO_4W(ZOACT_EPI_RELU, false)
+  ZO_4W(EPI_MSE, false)
 #undef ZO_4W
   return hipErrorNotSupported;
 }

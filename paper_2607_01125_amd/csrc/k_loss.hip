@@ -68,6 +68,19 @@ __global__ void __launch_bounds__(256) mse_partial(const void* __restrict__ y, c
   if (threadIdx.x == 0) part[h * kLossBlocks + blockIdx.x] = s;
 }
 
+// Sum n partials per half ([2][n]) in a fixed order and scale: the per-tile squared errors
+// of the fused regression-loss epilogue.
+__global__ void __launch_bounds__(256) sum_mean(const double* __restrict__ part, int64_t n, double count,
+                                                float* loss_pm) {
+  __shared__ double sh[4];
+  for (int h = 0; h < 2; ++h) {
+    double v = 0.0;
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) v += part[h * n + i];
+    const double s = block_sum_d(v, sh);
+    if (threadIdx.x == 0) loss_pm[h] = (float)(s / count);
+  }
+}
+
 // Sum kLossBlocks partials per half in a fixed order and scale.
 __global__ void __launch_bounds__(256) finish_mean(const double* __restrict__ part, double count, float* loss_pm) {
   __shared__ double sh[4];
@@ -131,6 +144,11 @@ __global__ void __launch_bounds__(256) xent_partial(const float* __restrict__ lo
 }
 
 }  // namespace
+
+hipError_t launch_sum_mean(const double* part, int64_t n, double count, float* loss_pm, hipStream_t s) {
+  sum_mean<<<dim3(1), dim3(256), 0, s>>>(part, n, count, loss_pm);
+  return hipGetLastError();
+}
 
 hipError_t launch_mse_pm(const void* y, int32_t dtype, const void* target, int64_t T, int64_t N, float* loss_pm,
                          void* ws, hipStream_t s) {

@@ -85,6 +85,9 @@ SIGNATURES = {
     "zoact_step_q": ([ctypes.POINTER(ArenaDesc), _P, _I32, _U64, _U32, _F, ctypes.POINTER(AdamDesc), _P, _P], _I32),
     "zoact_step_q_sgd": ([ctypes.POINTER(ArenaDesc), _P, _I32, _U64, _U32, _F, _F, _P, _P], _I32),
     "zoact_loss_workspace_bytes": ([], _SZ),
+    "zoact_linear_mse_workspace_bytes": ([_I64, _I64], _SZ),
+    "zoact_linear_mse_pair": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I64, _P,
+                               ctypes.POINTER(PertPair), _P, _P, _P, _SZ, _P], _I32),
     "zoact_mse_pm": ([_P, _I32, _P, _I64, _I64, _P, _P, _SZ, _P], _I32),
     "zoact_xent_pm": ([_P, _P, _I64, _I64, _I64, _P, _P, _SZ, _P], _I32),
     "zoact_step": ([ctypes.POINTER(ArenaDesc), _P, ctypes.POINTER(Pert), ctypes.POINTER(AdamDesc), _P, _P], _I32),
@@ -215,6 +218,29 @@ def perturb_coeffs(arena: Arena, e0: int, n: int, pert: Pert | PertPair, out: to
     a = arena.desc()
     fn = lib().zoact_perturb_coeffs_pair if isinstance(pert, PertPair) else lib().zoact_perturb_coeffs
     _check(fn(ctypes.byref(a), e0, n, ctypes.byref(pert), _ptr(out), _stream(stream)))
+
+
+def as_pair(pert: Pert | PertPair) -> PertPair:
+    """The general pair of a perturbation (the +/- pair for a Pert)."""
+    if isinstance(pert, PertPair):
+        return pert
+    return pert_pair(pert.seed, pert.step, (pert.query, pert.query), (1, -1), pert.eps)
+
+
+def linear_mse_workspace_bytes(T: int, d_out: int) -> int:
+    return int(lib().zoact_linear_mse_workspace_bytes(T, d_out))
+
+
+def linear_mse(layer: Linear, arena: Arena | None, x: torch.Tensor, T: int, p: torch.Tensor | None,
+               pert: Pert | PertPair, target: torch.Tensor, loss_pm: torch.Tensor, ws: torch.Tensor, stream=None):
+    """Adapted linear of both halves with the regression loss fused into its epilogue:
+    loss_pm[h] = mean (bf16(y[h]) - target)^2, y not stored."""
+    d = layer.desc()
+    a = arena.desc() if arena is not None else None
+    pp = as_pair(pert)
+    _check(lib().zoact_linear_mse_pair(ctypes.byref(d), ctypes.byref(a) if a is not None else None, _ptr(x), T,
+                                       _ptr(p), ctypes.byref(pp), _ptr(target), _ptr(loss_pm), _ptr(ws),
+                                       ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def loss_workspace_bytes() -> int:

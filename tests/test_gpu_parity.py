@@ -460,3 +460,62 @@ def test_single_layer_4096_sampled():
     assert_bf16_close(yh[:, rows], ref, what="single layer sampled")
     # P rows as well
     assert_bf16_close(host(p)[rows], olin.project(xs, ut, "bf16"), what="P sampled")
+    # the fused regression loss at full size: the same y, summed in the epilogue
+    tgt = t_bf16(synth.normal((T, N), 1.0, 0, 5))
+    lpm = torch.zeros(2, dtype=torch.float32, device=dev())
+    Z.mse_pm(y, tgt, lpm, torch.empty(Z.loss_workspace_bytes(), dtype=torch.uint8, device=dev()))
+    fused = torch.full((2,), float("nan"), dtype=torch.float32, device=dev())
+    ws = torch.empty(Z.linear_mse_workspace_bytes(T, N), dtype=torch.uint8, device=dev())
+    Z.linear_mse(layer, arena, xt, T, p, Z.Pert(seed, step, 0, eps), tgt, fused, ws)
+    np.testing.assert_allclose(host(fused), host(lpm), rtol=2e-6)
+
+
+# ------------------------------------------------------------------ fused regression loss
+@pytest.mark.parametrize("T,K,N,r,mode", [
+    (300, 512, 336, 32, "bf16"),       # ragged tokens and features
+    (257, 256, 512, 128, "bf16-pre"),  # precomputed coefficients, r > 64
+    (200, 512, 384, 32, "int4"),
+    (64, 1024, 256, 0, "bf16"),        # plain layer
+])
+def test_linear_mse_fused(T, K, N, r, mode):
+    """The fused loss equals the stored-output path (linear + zoact_mse_pm) up to summation
+    order, and the oracle's MSE of its own bf16 outputs within the bf16 bar."""
+    announce("linear mse fused", T, K, N, r, mode)
+    x, w, b, ut, packed, scales = _layer_inputs(T, K, N, max(r, 1), seed=T + N, int4=(mode == "int4"))
+    if r == 0:
+        ut = None
+    c = synth.normal((N * max(r, 1),), 0.02, 3, 3)
+    eps, seed, step = 1e-3, 5, 2
+    xt = t_bf16(x.reshape(2 * T, K))
+    p = None
+    if r:
+        p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev())
+        Z.project(xt, t_bf16(ut), p)
+    if mode == "int4":
+        layer = Z.Linear(t_u8(packed), K, N, r, t_bf16(ut), 0, t_bf16(b), t_bf16(scales))
+    else:
+        layer = Z.Linear(t_bf16(w), K, N, r, t_bf16(ut) if r else None, 0, t_bf16(b))
+    arena = Z.Arena(t_f32(c), torch.zeros(c.size, device=dev()), torch.zeros(c.size, device=dev())) if r else None
+    pert = Z.Pert(seed, step, 0, eps)
+    if mode in ("int4", "bf16-pre"):
+        ch = torch.empty(2 * N * r, dtype=torch.bfloat16, device=dev())
+        Z.perturb_coeffs(arena, 0, N * r, pert, ch)
+        layer.ch, layer.ch_stride = ch, N * r
+    tgt_np = synth.bf16_round(synth.normal((T, N), 1.0, 4, 4))
+    tgt = t_bf16(tgt_np)
+    y = torch.empty(2 * T, N, dtype=torch.bfloat16, device=dev())
+    Z.linear_fwd_pm(layer, arena, xt, T, p, y, pert)
+    lpm = torch.zeros(2, dtype=torch.float32, device=dev())
+    Z.mse_pm(y, tgt, lpm, torch.empty(Z.loss_workspace_bytes(), dtype=torch.uint8, device=dev()))
+    fused = torch.full((2,), float("nan"), dtype=torch.float32, device=dev())
+    ws = torch.empty(Z.linear_mse_workspace_bytes(T, N), dtype=torch.uint8, device=dev())
+    Z.linear_mse(layer, arena, xt, T, p, pert, tgt, fused, ws)
+    np.testing.assert_allclose(host(fused), host(lpm), rtol=2e-6)
+    wq = olin.dequant_int4(packed, scales) if mode == "int4" else w
+    if r:
+        ref = _oracle_linear(x, wq, b, ut, c.reshape(N, r), 0, r, eps, seed, step)
+    else:
+        ref = np.stack([rne_bf16((x[h].astype(np.float64) @ wq.astype(np.float64).T + b).astype(np.float32))
+                        for h in range(2)]).astype(np.float64)
+    want = [oloss.mse(ref[h], tgt_np) for h in range(2)]
+    assert_rel_close(host(fused), want, 1e-3, "fused mse vs oracle")
