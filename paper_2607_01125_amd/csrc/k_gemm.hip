@@ -506,8 +506,9 @@ hipError_t launch_bf16(const GemmArgs& a, dim3 grid, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Schedule of the bf16 fused GEMM: 0 = four-wave pipelined (default, fastest measured),
-// 1 = eight-wave ping-pong, 2 = generic.  ZOACT_GEMM_SCHEDULE selects one for A/B
+// Schedule of the bf16 fused GEMM: 0 = four-wave pipelined (default, fastest measured: the
+// 64-deep stages where they apply, else the 32-deep ones), 1 = eight-wave ping-pong,
+// 2 = generic, 3 = the 32-deep four-wave schedule only.  ZOACT_GEMM_SCHEDULE selects one for A/B
 // measurements; the generic kernel is the fallback for shapes outside the others' coverage.
 int schedule_choice() {
   static const int v = [] {
@@ -515,6 +516,7 @@ int schedule_choice() {
     if (e == nullptr) return 0;
     if (e[0] == '1') return 1;
     if (e[0] == '2') return 2;
+    if (e[0] == '3') return 3;   // the 32-deep four-wave schedule only
     return 0;
   }();
   return v;
@@ -524,6 +526,7 @@ int schedule_choice() {
 
 hipError_t launch_linear_pm_pp(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
 hipError_t launch_linear_pm_4w(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
+hipError_t launch_linear_pm_4w64(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
 
 // Arguments of the bf16-activation kernels for one call.
 static GemmArgs bf16_args(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, const void* p,
@@ -590,11 +593,13 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
   const bool i4 = L.w_dtype == ZOACT_INT4_G128;
   const bool of = y_dtype == ZOACT_F32;
   const int sched = schedule_choice();
-  if (sched == 0) {
-    const hipError_t e = launch_linear_pm_4w(a, L.w_dtype, epi, of, s);
+  if (sched == 0 || sched == 3) {
+    hipError_t e = sched == 0 ? launch_linear_pm_4w64(a, L.w_dtype, epi, of, s) : hipErrorNotSupported;
+    if (e != hipErrorNotSupported) return e;
+    e = launch_linear_pm_4w(a, L.w_dtype, epi, of, s);
     if (e != hipErrorNotSupported) return e;
   }
-  if (sched <= 1) {
+  if (sched <= 1 || sched == 3) {
     const hipError_t e = launch_linear_pm_pp(a, L.w_dtype, epi, of, s);
     if (e != hipErrorNotSupported) return e;
   }
@@ -618,7 +623,8 @@ hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const 
   GemmArgs a = bf16_args(L, A, x, T, p, nullptr, pert, nullptr);
   a.tgt = static_cast<const uint16_t*>(target);
   a.part = part;
-  const hipError_t e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
+  hipError_t e = schedule_choice() == 0 ? launch_linear_pm_4w64(a, L.w_dtype, EPI_MSE, false, s) : hipErrorNotSupported;
+  if (e == hipErrorNotSupported) e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
   if (e != hipSuccess) return e;
   return launch_sum_mean(part, (int64_t)a.tiles_m_half * a.tiles_n, (double)T * (double)L.d_out, loss_pm, s);
 }
