@@ -17,7 +17,7 @@
 //    stage S+2 goes into the slot stage S-1's x has left (during 2S) and its x into the
 //    slot stage S's W leaves after 2S (during 2S+1); both are waited for at the end of
 //    2S+2, one and a half to two and a half sub-steps later.  Eight loads per wave per
-//    sub-step, as in the 32-deep schedule.
+//    sub-step, as in the 32-deep schedule, and one workgroup barrier per stage.
 //  * The fifth slot is the 32 KB the 32-deep schedule spends on C_h, so this schedule
 //    reads C_h precomputed (zoact_perturb_coeffs) for the ceil(r/32) correction steps.
 #include "gemm_4w_epi.hpp"
@@ -169,11 +169,13 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a) {
     __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
     barrier();
     if (j + 1 < nsub) {
-      // sub-step 2S + 1: k-half 1 of stage S; reads k-half 0 of stage S + 1; loads x of S + 2
+      // sub-step 2S + 1: k-half 1 of stage S; reads k-half 0 of stage S + 1; loads x of S + 2.
+      // No barrier after it: sub-step 2S + 2 reads stage S + 1 (complete since the barrier
+      // above) and loads into stage S's x slot (last read during 2S), so nothing it touches
+      // can still be in use by a slower wave.
       sub_step(fa1, fb1, fa0, fb0, sw1, sx1, fo0, true, st + 2, s5);
-      __builtin_amdgcn_s_waitcnt(WAIT_VM16);
       __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
-      barrier();
+      __builtin_amdgcn_sched_barrier(0);
     }
     s5 = sw1;
   }
