@@ -41,8 +41,9 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 METRIC = "ZO steps/sec (±ε forwards + Adam) and adapted-linear TFLOP/s at 8B shapes"
-DOMINANT_KERNEL = "gemm_4w_kernel"
-DOMINANT_SOURCES = [os.path.join("paper_2607_01125_amd", "csrc", f) for f in ("k_gemm_4w.hip", "gemm_common.hpp")]
+DOMINANT_KERNEL = "gemm_4w64_kernel"
+DOMINANT_SOURCES = [os.path.join("paper_2607_01125_amd", "csrc", f)
+                    for f in ("k_gemm_4w64.hip", "gemm_4w_epi.hpp", "gemm_common.hpp")]
 
 
 def log(*a):
