@@ -389,6 +389,233 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(const uint16_t* __r
   }
 }
 
+// ---------------------------------------------------------------- attention, bf16 MFMA, shared K/V
+// Same two-pass definition as attention_bf16_kernel (P = exp(s - final max) rounded to bf16,
+// normaliser from the unrounded P), organised for grouped-query heads: a workgroup takes one
+// key/value head of one sequence and HG = min(G, 4) of the G query heads that read it, each
+// wave 16 * QB queries of one head (QT = 64 QB / HG queries per workgroup tile), so every
+// K/V block staged in LDS serves four waves' worth of queries; K and V blocks travel
+// global -> registers one block ahead of their use.  QB = 2 keeps a thread within 256
+// registers, two workgroups per CU.  Scores are formed transposed,
+// S^T[key][query] (K as the MFMA A operand, Q as B): a lane then holds four keys of one
+// query, its probabilities are already the B operand of O^T = V^T P^T, and V^T is read in
+// the same key order (the order of the 32 keys inside one MFMA does not change the sum
+// beyond rounding), so P never goes through LDS.
+template <int HD, int QB>
+__global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* __restrict__ q, int64_t ldq,
+                                                            const uint16_t* __restrict__ k, int64_t ldk,
+                                                            const uint16_t* __restrict__ v, int64_t ldv, int64_t seq,
+                                                            int heads, int kv_heads, float scale,
+                                                            uint16_t* __restrict__ out) {
+  constexpr int KC = HD / 8;   // 16-byte chunks per row
+  constexpr int KS = HD / 32;  // 32-deep steps over the head dimension
+  constexpr int ND = HD / 16;  // 16-row blocks of the head dimension
+  __shared__ __align__(16) uint16_t ks[64 * HD];   // K block [key][hd], chunk-swizzled
+  __shared__ __align__(16) uint32_t vt[HD * 36];   // V block transposed [d][key], key pairs per word, padded
+  const int G = heads / kv_heads;
+  const int HG = G < 4 ? G : 4;
+  const int QT = 64 * QB / HG;                             // queries per workgroup tile
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lr = lane & 15, lk = lane >> 4;
+  const int sub = G / HG;                                   // workgroups per key/value head
+  const int hk = blockIdx.y / sub;
+  const int h = hk * G + (blockIdx.y % sub) * HG + (wave % HG);
+  const int64_t r0 = (int64_t)blockIdx.z * seq;
+  const int64_t qt0 = (int64_t)blockIdx.x * QT;
+  const int64_t q0 = qt0 + (int64_t)(wave / HG) * (16 * QB);   // this wave's first query
+  const int64_t wq_last = q0 + 16 * QB - 1 < seq - 1 ? q0 + 16 * QB - 1 : seq - 1;
+  const int64_t tq_last = qt0 + QT - 1 < seq - 1 ? qt0 + QT - 1 : seq - 1;
+  const int nkb = (int)(tq_last / 64) + 1;
+
+  // Q fragments (B operand): q-block b, row lr, depth kk*32 + lk*8
+  bf16x8 qf[QB][KS];
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    int64_t qr = q0 + b * 16 + lr;
+    qr = qr < seq ? qr : seq - 1;
+    const uint16_t* qp = q + (r0 + qr) * ldq + (int64_t)h * HD;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) qf[b][kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + lk * 8);
+  }
+  // S^T of key block kb against q-block b: lane holds S^T[key = j*16 + 4*lk + i][query = b*16 + lr]
+  auto scores_t = [&](int b, floatx4 (&st)[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      st[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        const int key = j * 16 + lr;
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + key * HD + (((kk * 4 + lk) ^ (key & 7)) * 8));
+        st[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[b][kk], st[j], 0, 0, 0);
+      }
+    }
+  };
+
+  // keys of block kb this lane's query of q-block b may see: key offset within the block
+  // <= the returned limit (causal: key <= query; and key < seq)
+  auto key_limit = [&](int b, int kb) -> int {
+    int64_t last = q0 + b * 16 + lr;
+    last = last < seq - 1 ? last : seq - 1;
+    return (int)(last - (int64_t)kb * 64);
+  };
+
+  // pass 1: row maxima of the scaled, masked scores
+  float mq[QB];
+#pragma unroll
+  for (int b = 0; b < QB; ++b) mq[b] = -INFINITY;
+  // K and V blocks go global -> registers one block ahead (their latency hides behind the
+  // current block's MFMAs), then registers -> LDS between two barriers
+  constexpr int KPT = 64 * KC / 256;   // 16-byte K chunks per thread and block
+  constexpr int VPT = 32 * KC / 256;   // V items (key pair x 8 columns) per thread and block
+  uint4 kreg[KPT], vreg[VPT][2];
+  auto load_k = [&](int kb) {
+#pragma unroll
+    for (int t = 0; t < KPT; ++t) {
+      const int cidx = threadIdx.x + t * 256, key = cidx / KC, ch = cidx % KC;
+      int64_t kr = (int64_t)kb * 64 + key;
+      kr = kr < seq ? kr : seq - 1;
+      kreg[t] = *reinterpret_cast<const uint4*>(k + (r0 + kr) * ldk + (int64_t)hk * HD + ch * 8);
+    }
+  };
+  auto store_k = [&]() {
+#pragma unroll
+    for (int t = 0; t < KPT; ++t) {
+      const int cidx = threadIdx.x + t * 256, key = cidx / KC, ch = cidx % KC;
+      *reinterpret_cast<uint4*>(ks + key * HD + ((ch ^ (key & 7)) * 8)) = kreg[t];
+    }
+  };
+  auto load_v = [&](int kb) {
+#pragma unroll
+    for (int t = 0; t < VPT; ++t) {
+      const int it = threadIdx.x + t * 256, kp = it & 31, dc = it >> 5;
+      int64_t k0r = (int64_t)kb * 64 + 2 * kp, k1r = k0r + 1;
+      k0r = k0r < seq ? k0r : seq - 1;
+      k1r = k1r < seq ? k1r : seq - 1;
+      vreg[t][0] = *reinterpret_cast<const uint4*>(v + (r0 + k0r) * ldv + (int64_t)hk * HD + dc * 8);
+      vreg[t][1] = *reinterpret_cast<const uint4*>(v + (r0 + k1r) * ldv + (int64_t)hk * HD + dc * 8);
+    }
+  };
+  // V^T: item (key pair kp, 8-column chunk dc) -> eight words (V[2kp][d], V[2kp+1][d])
+  auto store_vt = [&]() {
+#pragma unroll
+    for (int t = 0; t < VPT; ++t) {
+      const int it = threadIdx.x + t * 256, kp = it & 31, dc = it >> 5;
+      const uint32_t aw[4] = {vreg[t][0].x, vreg[t][0].y, vreg[t][0].z, vreg[t][0].w};
+      const uint32_t cw[4] = {vreg[t][1].x, vreg[t][1].y, vreg[t][1].z, vreg[t][1].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        vt[(dc * 8 + 2 * e) * 36 + kp] = (aw[e] & 0xFFFFu) | (cw[e] << 16);
+        vt[(dc * 8 + 2 * e + 1) * 36 + kp] = (aw[e] >> 16) | (cw[e] & 0xFFFF0000u);
+      }
+    }
+  };
+
+  load_k(0);
+  for (int kb = 0; kb < nkb; ++kb) {
+    __syncthreads();
+    store_k();
+    if (kb + 1 < nkb) load_k(kb + 1);
+    else load_k(0);                              // pass 2 starts again at block 0
+    __syncthreads();
+    if ((int64_t)kb * 64 > wq_last) continue;   // wave-uniform: this block is masked for all its queries
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      floatx4 st[4];
+      scores_t(b, st);
+      const int lim = key_limit(b, kb);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (j * 16 + lk * 4 + i <= lim) mq[b] = fmaxf(mq[b], st[j][i] * scale);
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    mq[b] = fmaxf(mq[b], __shfl_xor(mq[b], 16, 64));
+    mq[b] = fmaxf(mq[b], __shfl_xor(mq[b], 32, 64));
+  }
+
+  // pass 2: P = exp(s - max) rounded to bf16, O^T += V^T P^T, l += P (unrounded)
+  floatx4 o[ND][QB];
+#pragma unroll
+  for (int n = 0; n < ND; ++n)
+#pragma unroll
+    for (int b = 0; b < QB; ++b) o[n][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float lq[QB];
+#pragma unroll
+  for (int b = 0; b < QB; ++b) lq[b] = 0.f;
+  load_v(0);
+  for (int kb = 0; kb < nkb; ++kb) {
+    __syncthreads();
+    store_k();
+    store_vt();
+    if (kb + 1 < nkb) {
+      load_k(kb + 1);
+      load_v(kb + 1);
+    }
+    __syncthreads();
+    if ((int64_t)kb * 64 > wq_last) continue;
+    // probabilities of the four q-blocks as B operands: 32-key step c holds keys
+    // c*32 + 4*lk + i (block j = 2c) and c*32 + 16 + 4*lk + i (block j = 2c + 1)
+    bf16x8 pb[QB][2];
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      floatx4 st[4];
+      scores_t(b, st);
+      const int lim = key_limit(b, kb);
+      uint16_t pbits[4][4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float p = (j * 16 + lk * 4 + i <= lim) ? expf(st[j][i] * scale - mq[b]) : 0.f;
+          lq[b] += p;
+          pbits[j][i] = f2bf(p);
+        }
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const uint4 u = make_uint4((uint32_t)pbits[2 * c][0] | ((uint32_t)pbits[2 * c][1] << 16),
+                                   (uint32_t)pbits[2 * c][2] | ((uint32_t)pbits[2 * c][3] << 16),
+                                   (uint32_t)pbits[2 * c + 1][0] | ((uint32_t)pbits[2 * c + 1][1] << 16),
+                                   (uint32_t)pbits[2 * c + 1][2] | ((uint32_t)pbits[2 * c + 1][3] << 16));
+        pb[b][c] = __builtin_bit_cast(bf16x8, u);
+      }
+    }
+    // A operand: V^T rows d = n*16 + lr, the same keys (two 8-byte reads per step)
+#pragma unroll
+    for (int n = 0; n < ND; ++n)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const uint32_t* vr = vt + (n * 16 + lr) * 36 + c * 16 + lk * 2;
+        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
+        const bf16x8 va = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+#pragma unroll
+        for (int b = 0; b < QB; ++b) o[n][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[b][c], o[n][b], 0, 0, 0);
+      }
+  }
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    lq[b] += __shfl_xor(lq[b], 16, 64);
+    lq[b] += __shfl_xor(lq[b], 32, 64);
+  }
+  // O^T[d = n*16 + 4*lk + i][query = b*16 + lr] / l -> four consecutive columns per store
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+    const int64_t qi = q0 + b * 16 + lr;
+    if (qi >= seq) continue;
+    const float inv = 1.f / lq[b];
+    uint16_t* op = out + (r0 + qi) * (int64_t)heads * HD + (int64_t)h * HD;
+#pragma unroll
+    for (int n = 0; n < ND; ++n) {
+      const uint2 w2 = make_uint2((uint32_t)f2bf(o[n][b][0] * inv) | ((uint32_t)f2bf(o[n][b][1] * inv) << 16),
+                                  (uint32_t)f2bf(o[n][b][2] * inv) | ((uint32_t)f2bf(o[n][b][3] * inv) << 16));
+      *reinterpret_cast<uint2*>(op + n * 16 + lk * 4) = w2;
+    }
+  }
+}
+
 unsigned grid1d(int64_t n) {
   int64_t g = (n + 255) / 256;
   return (unsigned)(g < 1 ? 1 : (g > 65535 ? 65535 : g));
@@ -503,6 +730,22 @@ extern "C" zoact_status zoact_attention(const void* q, int64_t ldq, const void* 
   if (dtype == ZOACT_BF16) {
     ZO_CHECK(head_dim == 64 || head_dim == 128, "attention: bf16 head_dim must be 64 or 128");
     ZO_CHECK(ldq % 8 == 0 && ldk % 8 == 0 && ldv % 8 == 0, "attention: bf16 strides must be multiples of 8");
+    const int G = n_heads / n_kv_heads;
+    if ((G == 1 || G == 2 || G % 4 == 0) && (int64_t)n_kv_heads * (G < 4 ? 1 : G / 4) <= 65535) {
+      constexpr int QB = 2;                     // 16-query blocks per wave
+      const int HG = G < 4 ? G : 4;
+      const int QT = 64 * QB / HG;
+      const dim3 g2((unsigned)((seq + QT - 1) / QT), (unsigned)(n_kv_heads * (G / HG)), (unsigned)n_seq);
+      if (head_dim == 128)
+        attention_gqa_kernel<128, QB><<<g2, 256, 0, s>>>((const uint16_t*)q, ldq, (const uint16_t*)k, ldk,
+                                                         (const uint16_t*)v, ldv, seq, n_heads, n_kv_heads, scale,
+                                                         (uint16_t*)out);
+      else
+        attention_gqa_kernel<64, QB><<<g2, 256, 0, s>>>((const uint16_t*)q, ldq, (const uint16_t*)k, ldk,
+                                                        (const uint16_t*)v, ldv, seq, n_heads, n_kv_heads, scale,
+                                                        (uint16_t*)out);
+      return launched("attention");
+    }
     const dim3 grid((unsigned)((seq + 63) / 64), (unsigned)n_heads, (unsigned)n_seq);
     if (head_dim == 128)
       attention_bf16_kernel<128><<<grid, 256, 0, s>>>((const uint16_t*)q, ldq, (const uint16_t*)k, ldk,

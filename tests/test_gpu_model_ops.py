@@ -128,7 +128,8 @@ def _attn_case(bf16, B, S, H, Hkv, hd, seed):
 
 
 @pytest.mark.parametrize("B,S,H,Hkv,hd", [(2, 64, 4, 2, 128), (3, 100, 4, 4, 64), (1, 257, 8, 2, 128),
-                                          (2, 1, 2, 1, 64), (1, 512, 2, 2, 128)])
+                                          (2, 1, 2, 1, 64), (1, 512, 2, 2, 128), (1, 130, 16, 2, 128),
+                                          (1, 70, 6, 2, 64), (2, 256, 32, 8, 128)])
 def test_attention_bf16(B, S, H, Hkv, hd):
     """Bound: the output's own bf16 rounding (2^-7 |o|) plus one bf16 ulp (<= 2^-7 p) on
     every rounded probability, which fp32 scores (GPU) and float64 scores (oracle) can
