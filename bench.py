@@ -209,19 +209,25 @@ def bench_linear_shapes(dev, reps=10):
     shapes = [("qkv", 4096, 6144, 0), ("o", 4096, 4096, 0), ("gate|up", 4096, 28672, Z.EPI_SWIGLU),
               ("down", 14336, 4096, 0)]
     out = {}
-    for mode in ("bf16", "int4"):
+    # int4: the in-register INT4 GEMM; int4_dequant: one dequantisation pass into a bf16
+    # buffer, then the bf16 schedule (what the decoder runs), the pass inside the timed call
+    for mode in ("bf16", "int4", "int4_dequant"):
         res, tot_flop, tot_s = {}, 0.0, 0.0
         for name, K, N, flags in shapes:
             x = synth.device_normal((2 * T, K), 1.0, 9, K, device=dev, dtype=torch.bfloat16)
             w = synth.device_normal((N, K), 0.02, 9, N, K, device=dev, dtype=torch.bfloat16)
             ut = synth.device_normal((r, K), 1.0 / math.sqrt(K), 9, r, K, device=dev, dtype=torch.bfloat16)
+            packed = scales = None
             if mode == "int4":
                 packed, scales = synth.device_quantize_int4_g128(w)
                 layer = Z.Linear(packed, K, N, r, ut, 0, w_scales=scales)
                 del w
+            elif mode == "int4_dequant":
+                packed, scales = synth.device_quantize_int4_g128(w)
+                layer = Z.Linear(w, K, N, r, ut, 0)      # w: the buffer the pass fills
             else:
                 layer = Z.Linear(w, K, N, r, ut, 0)
-            c = torch.zeros(N * r, dtype=torch.bfloat16 if mode == "int4" else torch.float32, device=dev)
+            c = torch.zeros(N * r, dtype=torch.float32 if mode == "bf16" else torch.bfloat16, device=dev)
             arena = Z.Arena(c, torch.zeros(N * r, device=dev), torch.zeros(N * r, device=dev))
             p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev)
             y = torch.empty(2 * T, N // 2 if flags else N, dtype=torch.bfloat16, device=dev)
@@ -231,6 +237,8 @@ def bench_linear_shapes(dev, reps=10):
             layer.ch, layer.ch_stride = ch, N * r
 
             def call():
+                if mode == "int4_dequant":
+                    Z.dequant_int4(packed, scales, layer.w)
                 Z.perturb_coeffs(arena, 0, N * r, pert, ch)
                 Z.project(x, ut, p)
                 Z.linear_fwd_pm(layer, arena, x, T, p, y, pert, flags=flags)
@@ -249,7 +257,7 @@ def bench_linear_shapes(dev, reps=10):
             res[name] = {"M": M, "N": N, "K": K, "us": round(sec * 1e6, 1), "tflops": round(flop / sec / 1e12, 1)}
             tot_flop += flop
             tot_s += sec
-            del x, layer, arena, p, y, ch
+            del x, layer, arena, p, y, ch, packed, scales
             torch.cuda.empty_cache()
         mean = tot_flop / tot_s / 1e12
         out[mode] = {"shapes": res, "flop_weighted_tflops": round(mean, 1),

@@ -195,6 +195,14 @@ zoact_status zoact_linear_fwd_pair(const zoact_linear* L, const zoact_arena* A, 
                                    uint32_t flags, const zoact_pert_pair* pp, void* y, int32_t y_dtype,
                                    zoact_stream stream);
 
+/* INT4 weights to bf16: out[n][k] = bf16(q[n][k] * s[n][k / 128]), the dequantised weight
+ * the INT4 GEMM forms in registers (same packing as zoact_linear.w).  At large token counts
+ * a caller dequantises each INT4 layer once per forward into a bf16 buffer of its own and
+ * runs the bf16 schedule on it: the in-register path converts every weight once per
+ * 256-token tile.  w and out 16-byte aligned, out bf16 [d_out][d_in]; d_in % 128 == 0. */
+zoact_status zoact_dequant_int4(const void* w, const void* w_scales, int64_t d_out, int64_t d_in, void* out,
+                                zoact_stream stream);
+
 /* ------------------------------------------------------ perturbed coefficients
  * out[h][e - e0] = bf16(fp32(C[e]) + s_h fp32(eps Z(e))), s = (+1, -1), for arena
  * indices e0 <= e < e0 + n: the C +/- eps Z of Section 3's perturbed forward, exactly

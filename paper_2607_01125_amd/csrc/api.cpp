@@ -87,6 +87,14 @@ zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t 
   return hip_status(zoact::launch_project(x, dtype, n_tok, d_in, ut, r, p, st(stream)), "project");
 }
 
+zoact_status zoact_dequant_int4(const void* w, const void* w_scales, int64_t d_out, int64_t d_in, void* out,
+                                zoact_stream stream) {
+  CHECK(w && w_scales && out, "dequant_int4: NULL pointer");
+  CHECK(d_out >= 1 && d_in >= 128 && d_in % 128 == 0, "dequant_int4: need d_out >= 1 and d_in %% 128 == 0");
+  CHECK(aligned16(w) && aligned16(out), "dequant_int4: w and out must be 16-byte aligned");
+  return hip_status(zoact::launch_dequant_int4(w, w_scales, d_out, d_in, out, st(stream)), "dequant_int4");
+}
+
 static zoact_status validate_linear(const zoact_linear* L, const zoact_arena* A, const void* x, int32_t x_dtype,
                                     int64_t T, const void* p, const void* residual, uint32_t flags,
                                     const zoact_pert_pair* pert, const void* y, int32_t y_dtype) {

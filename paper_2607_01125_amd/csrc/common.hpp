@@ -26,6 +26,8 @@ hipError_t launch_sgd(const zoact_arena& A, const float* loss_pm, const zoact_pe
 // one-sided multi-query update: Adam when h != nullptr, else SGD with rate lr
 hipError_t launch_step_q(const zoact_arena& A, const float* losses, int32_t q, uint64_t seed, uint32_t step, float eps,
                          const zoact_adam* h, float lr, uint32_t* status, hipStream_t s);
+hipError_t launch_dequant_int4(const void* w, const void* scales, int64_t d_out, int64_t d_in, void* out,
+                               hipStream_t s);
 hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut, int32_t r,
                           void* p, hipStream_t s);
 hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,

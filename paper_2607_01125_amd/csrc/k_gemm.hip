@@ -522,6 +522,24 @@ int schedule_choice() {
   return v;
 }
 
+// INT4 weights to bf16 in one streaming pass: thread = 16 packed bytes (32 weights of one
+// row, inside one group of 128) -> 64 bytes out.
+__global__ void __launch_bounds__(256) dequant_int4_kernel(const uint4* __restrict__ w, const uint16_t* __restrict__ sc,
+                                                           int64_t n_units, int64_t units_per_row, int64_t groups,
+                                                           uint4* __restrict__ out) {
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < n_units; u += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = u / units_per_row, cu = u % units_per_row;     // 32 weights per unit
+    const float s = bf2f(sc[row * groups + (cu >> 2)]);
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 qv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(w + u));
+    const uint4 q = make_uint4(qv.x, qv.y, qv.z, qv.w);
+    out[4 * u + 0] = dequant8(q.x, s);
+    out[4 * u + 1] = dequant8(q.y, s);
+    out[4 * u + 2] = dequant8(q.z, s);
+    out[4 * u + 3] = dequant8(q.w, s);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_linear_pm_pp(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
@@ -627,6 +645,17 @@ hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const 
   if (e == hipErrorNotSupported) e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
   if (e != hipSuccess) return e;
   return launch_sum_mean(part, (int64_t)a.tiles_m_half * a.tiles_n, (double)T * (double)L.d_out, loss_pm, s);
+}
+
+hipError_t launch_dequant_int4(const void* w, const void* scales, int64_t d_out, int64_t d_in, void* out,
+                               hipStream_t s) {
+  const int64_t units = d_out * (d_in / 32);
+  int64_t g = (units + 255) / 256;
+  g = g > (1 << 20) ? (1 << 20) : g;
+  dequant_int4_kernel<<<dim3((unsigned)g), dim3(256), 0, s>>>(static_cast<const uint4*>(w),
+                                                               static_cast<const uint16_t*>(scales), units, d_in / 32,
+                                                               d_in / 128, static_cast<uint4*>(out));
+  return hipGetLastError();
 }
 
 hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut, int32_t r, void* p,

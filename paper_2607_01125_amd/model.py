@@ -31,6 +31,8 @@ everything else, bf16 coefficients by default).
 """
 from __future__ import annotations
 
+import dataclasses
+
 import math
 from dataclasses import dataclass
 
@@ -102,7 +104,8 @@ class Decoder:
     [N][K/2], scales [N][K/128]) in the library's INT4 format.
     """
 
-    def __init__(self, shape, W: dict, mode: str, *, c_bf16: bool | None = None, device="cuda"):
+    def __init__(self, shape, W: dict, mode: str, *, c_bf16: bool | None = None, device="cuda",
+                 int4_dequant: bool = True):
         if mode not in ("fp32", "bf16", "int4"):
             raise ValueError(f"unknown mode {mode!r}")
         self.s, self.mode, self.dev = shape, mode, torch.device(device)
@@ -129,6 +132,13 @@ class Decoder:
         self._bufs = {}
         self._rope = {}
         self._ch = self._ch_all = None   # per-step C +/- eps Z of the whole arena (bf16 modes)
+        # INT4 layers: dequantised once per forward into one bf16 buffer (the largest layer's
+        # size) and run on the bf16 schedule; False keeps the in-register INT4 GEMM
+        self._wdq = None
+        if mode == "int4" and int4_dequant:
+            n = max(lin.d_out * lin.d_in for P in self.layers for lin, _ in
+                    (v for k, v in P.items() if isinstance(v, tuple)) if lin.w.dtype == torch.uint8)
+            self._wdq = torch.empty(n, dtype=torch.bfloat16, device=self.dev)
 
     # ---------------------------------------------------------------- weights
     def _t(self, a, dtype=None):
@@ -237,6 +247,10 @@ class Decoder:
     def _apply(self, lin_blk, x, T, y, pert, site_ut, residual=None, flags=0, adapt=True):
         lin, blk = lin_blk
         B = self._cur
+        if self._wdq is not None and lin.w.dtype == torch.uint8:
+            wdq = self._wdq[:lin.d_out * lin.d_in].view(lin.d_out, lin.d_in)
+            Z.dequant_int4(lin.w, lin.w_scales, wdq)
+            lin = dataclasses.replace(lin, w=wdq, w_scales=None)
         if adapt and blk is not None and site_ut is not None:
             lin.r, lin.ut = self.r, site_ut
             if self._ch is not None:

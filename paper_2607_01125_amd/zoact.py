@@ -79,6 +79,7 @@ SIGNATURES = {
     "zoact_linear_fwd_pm": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I32, _I64, _P, _P, _U32,
                              ctypes.POINTER(Pert), _P, _I32, _P], _I32),
     "zoact_perturb_coeffs": ([ctypes.POINTER(ArenaDesc), _I64, _I64, ctypes.POINTER(Pert), _P, _P], _I32),
+    "zoact_dequant_int4": ([_P, _P, _I64, _I64, _P, _P], _I32),
     "zoact_linear_fwd_pair": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I32, _I64, _P, _P, _U32,
                                ctypes.POINTER(PertPair), _P, _I32, _P], _I32),
     "zoact_perturb_coeffs_pair": ([ctypes.POINTER(ArenaDesc), _I64, _I64, ctypes.POINTER(PertPair), _P, _P], _I32),
@@ -218,6 +219,12 @@ def perturb_coeffs(arena: Arena, e0: int, n: int, pert: Pert | PertPair, out: to
     a = arena.desc()
     fn = lib().zoact_perturb_coeffs_pair if isinstance(pert, PertPair) else lib().zoact_perturb_coeffs
     _check(fn(ctypes.byref(a), e0, n, ctypes.byref(pert), _ptr(out), _stream(stream)))
+
+
+def dequant_int4(w: torch.Tensor, scales: torch.Tensor, out: torch.Tensor, stream=None):
+    """bf16 [d_out][d_in] = bf16(q * s) of INT4 weights (packed uint8 [d_out][d_in/2])."""
+    d_out, d_in = w.shape[0], w.shape[1] * 2
+    _check(lib().zoact_dequant_int4(_ptr(w), _ptr(scales), d_out, d_in, _ptr(out), _stream(stream)))
 
 
 def as_pair(pert: Pert | PertPair) -> PertPair:

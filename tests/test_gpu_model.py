@@ -63,13 +63,17 @@ def _dequant(packed, scales):
 
 
 def _models(shape, mode, seed=0, perturb=False):
+    """mode "int4-inreg": INT4 weights on the in-register INT4 GEMM instead of the
+    dequantise-then-bf16 path the decoder takes by default."""
+    inreg = mode == "int4-inreg"
+    mode = "int4" if inreg else mode
     W = synth.model_weights(shape, seed, "fp32" if mode == "fp32" else "bf16")
     if perturb:
         W = _perturb_params(W, shape, seed)
     Wg, Wo = _int4(W, shape) if mode == "int4" else (W, W)
     om_m = om.Model(shape, seed, "fp32" if mode == "fp32" else "bf16", weights=Wo)
     om_m.basis_init(synth.uniform_tokens(4, 32, shape.vocab, seed, 1))
-    g = gm.Decoder(shape, Wg, mode)
+    g = gm.Decoder(shape, Wg, mode, int4_dequant=not inreg)
     g.set_basis({k: om_m.U[k].T for k in g.site_dims()})
     return om_m, g
 
@@ -109,6 +113,7 @@ def test_tiny_fp32_twenty_steps():
     ("llama-bf16-ragged", LLAMA_S, "bf16", 3, 50),
     ("opt-bf16", OPT_S, "bf16", 2, 40),
     ("llama-int4", LLAMA_S, "int4", 2, 64),
+    ("llama-int4-inreg", LLAMA_S, "int4-inreg", 2, 64),
     ("llama-bf16-r1", synth.shrink(LLAMA_S, rank=1), "bf16", 2, 64),
     ("llama-bf16-r128", synth.shrink(LLAMA_S, rank=128), "bf16", 2, 48),
     ("llama-int4-r1", synth.shrink(LLAMA_S, rank=1), "int4", 2, 40),

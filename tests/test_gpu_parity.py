@@ -471,6 +471,20 @@ def test_single_layer_4096_sampled():
 
 
 # ------------------------------------------------------------------ fused regression loss
+@pytest.mark.parametrize("d_out,d_in", [(384, 512), (16, 128), (1000, 4096)])
+def test_dequant_int4_bitwise(d_out, d_in):
+    """bf16(q * s) of packed INT4 weights, bit for bit against the oracle's dequantisation,
+    and the layer on the dequantised weights equals the in-register INT4 layer."""
+    announce("dequant int4", d_out, d_in)
+    w = synth.bf16_round(synth.normal((d_out, d_in), 0.02, d_out, d_in))
+    packed, scales = synth.quantize_int4_g128(w)
+    out = torch.empty(d_out, d_in, dtype=torch.bfloat16, device=dev())
+    Z.dequant_int4(t_u8(packed), t_bf16(scales), out)
+    want = olin.dequant_int4(packed, scales)
+    np.testing.assert_array_equal(host(out).astype(np.float32).view(np.uint32),
+                                  want.astype(np.float32).view(np.uint32))
+
+
 @pytest.mark.parametrize("T,K,N,r,mode", [
     (300, 512, 336, 32, "bf16"),       # ragged tokens and features
     (257, 256, 512, 128, "bf16-pre"),  # precomputed coefficients, r > 64
