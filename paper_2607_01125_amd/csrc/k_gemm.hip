@@ -413,52 +413,82 @@ __global__ void __launch_bounds__(256) gemm_pm_f32_kernel(GemmArgsF32 a) {
 
 // ------------------------------------------------------------------ projection
 // p = x U for x [n_tok][d_in], U^T [r][d_in]: HBM-bound (r FLOP per byte of x), so the
-// design goal is to keep enough of x in flight.  A workgroup owns 32 tokens and splits the
-// depth over its 4 waves; each wave reads its x fragments straight from global memory
-// (16 bytes per lane per 32-deep step, 4 steps in flight) and U^T fragments from L2, runs
-// v_mfma_f32_16x16x32_bf16 into fp32 partials, and the 4 partials are summed in a fixed
-// order through LDS before the single rounding to bf16.
-constexpr int PROJ_TOK = 32;
+// design goal is to keep enough of x in flight.  A workgroup owns 16 TB tokens and splits
+// the depth over its 4 waves; each wave reads its x fragments straight from global memory
+// and its U^T fragments from L2 (16 bytes per lane per 32-deep step, the next 128-deep
+// step's loads issued before this step's MFMAs), runs v_mfma_f32_16x16x32_bf16 into fp32
+// partials, and the 4 partials are summed in a fixed order through LDS before the single
+// rounding to bf16.
 
-template <int RB>
+template <int RB, int TB>
 __global__ void __launch_bounds__(256) project_bf16_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ ut,
                                                           uint16_t* __restrict__ p, int64_t n_tok, int64_t d, int r,
                                                           int64_t dq) {
+  constexpr int PROJ_TOK = 16 * TB;
   __shared__ float part[4][PROJ_TOK][RB * 16 + 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t t0 = (int64_t)blockIdx.x * PROJ_TOK;
   const int lr = lane & 15, lk = lane >> 4;
-  floatx4 acc[2][RB];
+  floatx4 acc[TB][RB];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TB; ++i)
 #pragma unroll
     for (int j = 0; j < RB; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const uint16_t* xr[2];
+  const uint16_t* xr[TB];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < TB; ++i) {
     int64_t t = t0 + i * 16 + lr;
     t = t < n_tok ? t : n_tok - 1;
     xr[i] = x + t * d + lk * 8;
   }
   const bf16x8 zero8 = {};
   const int64_t k_begin = (int64_t)wave * dq, k_end = k_begin + dq < d ? k_begin + dq : d;
+  // the x and U^T chunks of the next 128-deep step are loaded while this step's MFMAs run
+  // (the pass is bound by the bytes each wave keeps in flight; U^T comes from L2); with
+  // r > 64 the U^T chunks are loaded step by step instead
+  constexpr bool PRE_B = RB <= 4;
+  bf16x8 a[4][TB], an[4][TB];
+  bf16x8 bq[PRE_B ? 4 : 1][PRE_B ? RB : 1], bn[PRE_B ? 4 : 1][PRE_B ? RB : 1];
+  auto load_b = [&](int64_t k, int u, int j) -> bf16x8 {
+    const int rc = j * 16 + lr;
+    return (rc < r && k + u * 32 < k_end) ? *reinterpret_cast<const bf16x8*>(ut + (int64_t)rc * d + k + u * 32 + lk * 8)
+                                         : zero8;
+  };
+  auto load_ab = [&](int64_t k) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+#pragma unroll
+      for (int i = 0; i < TB; ++i)
+        an[u][i] = (k + u * 32 < k_end) ? *reinterpret_cast<const bf16x8*>(xr[i] + k + u * 32) : zero8;
+      if constexpr (PRE_B) {
+#pragma unroll
+        for (int j = 0; j < RB; ++j) bn[u][j] = load_b(k, u, j);
+      }
+    }
+  };
+  if (k_begin < k_end) load_ab(k_begin);
   for (int64_t k = k_begin; k < k_end; k += 128) {
-    bf16x8 a[4][2];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < 4; ++u) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) a[u][i] = (k + u * 32 < k_end) ? *reinterpret_cast<const bf16x8*>(xr[i] + k + u * 32) : zero8;
+      for (int i = 0; i < TB; ++i) a[u][i] = an[u][i];
+      if constexpr (PRE_B) {
+#pragma unroll
+        for (int j = 0; j < RB; ++j) bq[u][j] = bn[u][j];
+      }
+    }
+    if (k + 128 < k_end) load_ab(k + 128);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       if (k + u * 32 < k_end) {
         bf16x8 b[RB];
 #pragma unroll
         for (int j = 0; j < RB; ++j) {
-          const int rc = j * 16 + lr;
-          b[j] = rc < r ? *reinterpret_cast<const bf16x8*>(ut + (int64_t)rc * d + k + u * 32 + lk * 8) : zero8;
+          if constexpr (PRE_B) b[j] = bq[u][j];
+          else b[j] = load_b(k, u, j);
         }
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < TB; ++i)
 #pragma unroll
           for (int j = 0; j < RB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][i], b[j], acc[i][j], 0, 0, 0);
       }
@@ -466,7 +496,7 @@ __global__ void __launch_bounds__(256) project_bf16_kernel(const uint16_t* __res
   }
   // D[token = 4*lk + q][col = lr] of each 16 x 16 block -> LDS partials
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TB; ++i)
 #pragma unroll
     for (int j = 0; j < RB; ++j)
 #pragma unroll
@@ -668,7 +698,10 @@ hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d
                                                                n_tok, d_in, r);
     return hipGetLastError();
   }
-  const dim3 grid((unsigned)((n_tok + PROJ_TOK - 1) / PROJ_TOK));
+  // 32 tokens per workgroup (two 16-token blocks per wave): fewer would multiply the U^T
+  // reads per token
+  constexpr int TB = 2;
+  const dim3 grid((unsigned)((n_tok + 16 * TB - 1) / (16 * TB)));
   // depth quarter per wave, a multiple of 32 (the last wave may get less or nothing)
   int64_t dq = (d_in + 3) / 4;
   dq = (dq + 31) / 32 * 32;
@@ -676,11 +709,13 @@ hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d
   const uint16_t* uu = static_cast<const uint16_t*>(ut);
   uint16_t* pp = static_cast<uint16_t*>(p);
   const int rb = (r + 15) / 16;
-  if (rb <= 1) project_bf16_kernel<1><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq);
-  else if (rb <= 2) project_bf16_kernel<2><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq);
-  else if (rb <= 4) project_bf16_kernel<4><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq);
-  else if (rb <= 8) project_bf16_kernel<8><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq);
-  else project_bf16_kernel<16><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq);
+#define ZO_PROJ(RB) project_bf16_kernel<RB, TB><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, dq)
+  if (rb <= 1) ZO_PROJ(1);
+  else if (rb <= 2) ZO_PROJ(2);
+  else if (rb <= 4) ZO_PROJ(4);
+  else if (rb <= 8) ZO_PROJ(8);
+  else ZO_PROJ(16);
+#undef ZO_PROJ
   return hipGetLastError();
 }
 
