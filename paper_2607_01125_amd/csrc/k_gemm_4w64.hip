@@ -126,6 +126,20 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a) {
           nb[ii] = frag(nxs, wm0 + ii * 16, nfo);
         }
       }
+      // issue order inside the row: each memory instruction right after an MFMA, so its
+      // issue cycles fall in the shadow of that MFMA instead of between two rows
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);    // the direct-to-LDS load
+      if (i < 4) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one fragment read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x008, 7, 0);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
   };
