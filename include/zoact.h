@@ -236,6 +236,19 @@ size_t zoact_loss_workspace_bytes(void);
  * bf16 target [T][d_out] (16-byte aligned); BF16 or INT4 weights (INT4 with L->ch).
  * ws: at least zoact_linear_mse_workspace_bytes(T, d_out) bytes (16-byte aligned).
  * Errors: shapes the fused kernel does not cover -> ZOACT_E_UNSUPPORTED. */
+/* Fused LM head and next-token cross entropy: the linear of both halves (as
+ * zoact_linear_fwd_pair computes it, logits in fp32, no residual or activation) followed by
+ * zoact_xent_pm's loss, without storing the logits: the GEMM's epilogue keeps, per row and
+ * 128-column block, the maximum and the sum of exp(logit - maximum) and the next token's
+ * logit; a second pass merges the blocks per row (the online log-sum-exp rule) and sums
+ * the rows in a fixed order.  x [2][B*S][d_in] bf16, tokens int32 [B][S] shared by both
+ * halves (ids clamped to [0, d_out)), S >= 2.  BF16 activations and weights.
+ * ws: zoact_linear_xent_workspace_bytes(B*S, d_out) bytes, 16-byte aligned.
+ * Errors: shapes the fused kernel does not cover -> ZOACT_E_UNSUPPORTED. */
+size_t zoact_linear_xent_workspace_bytes(int64_t T, int64_t d_out);
+zoact_status zoact_linear_xent_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t B, int64_t S,
+                                    const void* p, const zoact_pert_pair* pp, const int32_t* tokens, float* loss_pm,
+                                    void* ws, size_t ws_bytes, zoact_stream stream);
 size_t zoact_linear_mse_workspace_bytes(int64_t T, int64_t d_out);
 zoact_status zoact_linear_mse_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t T,
                                    const void* p, const zoact_pert_pair* pp, const void* target, float* loss_pm,

@@ -203,6 +203,27 @@ zoact_status zoact_mse_pm(const void* y, int32_t dtype, const void* target, int6
   return hip_status(zoact::launch_mse_pm(y, dtype, target, T, N, loss_pm, ws, st(stream)), "mse_pm");
 }
 
+size_t zoact_linear_xent_workspace_bytes(int64_t T, int64_t d_out) {
+  if (T < 1 || d_out < 1) return 0;
+  return zoact::linear_xent_ws_bytes(T, d_out);
+}
+
+zoact_status zoact_linear_xent_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t B, int64_t S,
+                                    const void* p, const zoact_pert_pair* pp, const int32_t* tokens, float* loss_pm,
+                                    void* ws, size_t ws_bytes, zoact_stream stream) {
+  CHECK(tokens != nullptr && loss_pm != nullptr, "linear_xent: NULL tokens or loss");
+  CHECK(B >= 1 && S >= 2, "linear_xent: need B >= 1 and S >= 2");
+  CHECK(L != nullptr && L->w_dtype == ZOACT_BF16, "linear_xent: needs a BF16 layer");
+  // the shared validation of the layer, with x standing in for the unused output
+  const zoact_status v = validate_linear(L, A, x, ZOACT_BF16, B * S, p, nullptr, 0, pp, x, ZOACT_F32);
+  if (v != ZOACT_OK) return v;
+  const size_t need = zoact_linear_xent_workspace_bytes(B * S, L->d_out);
+  if (ws == nullptr || ws_bytes < need || !aligned16(ws))
+    return fail(ZOACT_E_WORKSPACE, "linear_xent: workspace needs %zu bytes, 16-byte aligned", need);
+  return hip_status(zoact::launch_linear_xent(*L, A, x, B * S, p, *pp, tokens, S, loss_pm, ws, st(stream)),
+                    "linear_xent");
+}
+
 size_t zoact_linear_mse_workspace_bytes(int64_t T, int64_t d_out) {
   if (T < 1 || d_out < 1) return 0;
   return (size_t)2 * (size_t)((T + 255) / 256) * (size_t)((d_out + 255) / 256) * sizeof(double);

@@ -39,6 +39,14 @@ hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const 
                              const zoact_pert_pair& pert, const void* target, double* part, float* loss_pm,
                              hipStream_t s);
 hipError_t launch_sum_mean(const double* part, int64_t n, double count, float* loss_pm, hipStream_t s);
+// LM head of both halves with the next-token cross entropy fused into its epilogue (logits
+// not stored); ws holds the per-row block partials, target logits and loss partials.
+hipError_t launch_linear_xent(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, const void* p,
+                              const zoact_pert_pair& pert, const int32_t* tokens, int64_t S, float* loss_pm, void* ws,
+                              hipStream_t s);
+size_t linear_xent_ws_bytes(int64_t T, int64_t d_out);
+hipError_t launch_xent_combine(const float2* xpart, const float* xtgt, int64_t T, int64_t S, int nblk, int64_t B,
+                               double* part, float* loss_pm, hipStream_t s);
 hipError_t launch_mse_pm(const void* y, int32_t dtype, const void* target, int64_t T, int64_t N, float* loss_pm,
                          void* ws, hipStream_t s);
 hipError_t launch_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V,

@@ -3,6 +3,8 @@
 // wave's 128 x 128 accumulator tile through LDS and applies bias, residual, activation
 // (or the fused regression loss) with one rounding.
 #pragma once
+#include <math.h>
+
 #include "gemm_common.hpp"
 
 namespace zoact {
@@ -125,7 +127,8 @@ __device__ __forceinline__ void epilogue_4w(const GemmArgs& a, floatx4 (&acc)[8]
       for (int it = 0; it < 16; ++it) {
         const int tl = (lane >> 4) + 4 * it;
         const int64_t m = m0 + wm0 + pass * 64 + tl;
-        if (m >= a.T || n >= a.N) continue;
+        // (the cross-entropy reduction runs over the 16 lanes of a row: they skip together)
+        if (m >= a.T || (EPI != EPI_XENT && n >= a.N)) continue;
         const int64_t row = (int64_t)half * a.T + m;
         const floatx4 v_lo = *reinterpret_cast<const floatx4*>(ep + tl * LDR + c * 8);
         const floatx4 v_hi = *reinterpret_cast<const floatx4*>(ep + tl * LDR + c * 8 + 4);
@@ -134,6 +137,36 @@ __device__ __forceinline__ void epilogue_4w(const GemmArgs& a, floatx4 (&acc)[8]
         for (int e = 0; e < 4; ++e) {
           o[e] = v_lo[e] + bb[e];
           o[e + 4] = v_hi[e] + bb[e + 4];
+        }
+        if constexpr (EPI == EPI_XENT) {
+          // this row's 128 columns: maximum and sum of exp over the 16 lanes (8 each), then
+          // the next token's logit from the lane that holds it
+          float mx = -INFINITY;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (n + e < a.N) mx = fmaxf(mx, o[e]);
+#pragma unroll
+          for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+          float se = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (n + e < a.N) se += __expf(o[e] - mx);
+#pragma unroll
+          for (int off = 1; off < 16; off <<= 1) se += __shfl_xor(se, off, 64);
+          if (c == 0) a.xpart[row * a.xnblk + (n0 + wn0) / 128] = make_float2(mx, se);
+          const int64_t pos = m % a.seq;
+          if (pos < a.seq - 1) {
+            int64_t t = a.tok[m + 1];
+            t = t < 0 ? 0 : (t >= a.N ? a.N - 1 : t);
+            if (t >= n && t < n + 8) {
+              float tv = o[0];
+#pragma unroll
+              for (int e = 1; e < 8; ++e)
+                if (t - n == e) tv = o[e];
+              a.xtgt[row] = tv;
+            }
+          }
+          continue;
         }
         if (EPI != EPI_MSE && a.resid) {
           const uint4 rv = *reinterpret_cast<const uint4*>(a.resid + row * nout + n);

@@ -31,11 +31,19 @@ struct GemmArgs {
   int64_t ch_stride;
   const uint16_t* tgt;   // EPI_MSE: regression target [T][N] (bf16); y is not stored
   double* part;          // EPI_MSE: per-tile sums of squared errors [2][tiles_m_half * tiles_n]
+  const int32_t* tok;    // EPI_XENT: token ids [T / seq][seq] shared by both halves
+  int64_t seq;           // EPI_XENT: sequence length
+  float2* xpart;         // EPI_XENT: (max, sum of exp) per row and 128-column block [2 T][xnblk]
+  float* xtgt;           // EPI_XENT: the logit of each row's next token [2 T]
+  int32_t xnblk;         // EPI_XENT: ceil(N / 128)
 };
 
 // Internal epilogue selector (not a public flag): the tile's squared errors against tgt
 // are summed instead of storing y.
 constexpr int EPI_MSE = 1 << 8;
+// Internal epilogue selector: per row and 128-column block, the maximum and the sum of
+// exp(logit - maximum), plus the logit of the row's next token; logits are not stored.
+constexpr int EPI_XENT = 1 << 9;
 
 __device__ __forceinline__ int swz(int row, int kc) { return (row << 6) + ((kc ^ (row & 7)) << 3); }
 

@@ -677,6 +677,33 @@ hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const 
   return launch_sum_mean(part, (int64_t)a.tiles_m_half * a.tiles_n, (double)T * (double)L.d_out, loss_pm, s);
 }
 
+size_t linear_xent_ws_bytes(int64_t T, int64_t d_out) {
+  const int64_t nblk = (d_out + 127) / 128;
+  const size_t a = (size_t)2 * T * nblk * sizeof(float2);
+  const size_t b = ((size_t)2 * T * sizeof(float) + 255) / 256 * 256;
+  return (a + 255) / 256 * 256 + b + (size_t)2 * kLossBlocks * sizeof(double);
+}
+
+hipError_t launch_linear_xent(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, const void* p,
+                              const zoact_pert_pair& pert, const int32_t* tokens, int64_t S, float* loss_pm, void* ws,
+                              hipStream_t s) {
+  GemmArgs a = bf16_args(L, A, x, T, p, nullptr, pert, nullptr);
+  const int64_t nblk = (L.d_out + 127) / 128;
+  char* w = static_cast<char*>(ws);
+  a.xpart = reinterpret_cast<float2*>(w);
+  w += ((size_t)2 * T * nblk * sizeof(float2) + 255) / 256 * 256;
+  a.xtgt = reinterpret_cast<float*>(w);
+  w += ((size_t)2 * T * sizeof(float) + 255) / 256 * 256;
+  double* part = reinterpret_cast<double*>(w);
+  a.tok = tokens;
+  a.seq = S;
+  a.xnblk = (int32_t)nblk;
+  const hipError_t e = schedule_choice() == 0 ? launch_linear_pm_4w64(a, L.w_dtype, EPI_XENT, false, s)
+                                              : hipErrorNotSupported;
+  if (e != hipSuccess) return e;
+  return launch_xent_combine(a.xpart, a.xtgt, T, S, (int)nblk, T / S, part, loss_pm, s);
+}
+
 hipError_t launch_dequant_int4(const void* w, const void* scales, int64_t d_out, int64_t d_in, void* out,
                                hipStream_t s) {
   const int64_t units = d_out * (d_in / 32);

@@ -262,6 +262,7 @@ hipError_t launch_linear_pm_4w64(const GemmArgs& a, int w_dtype, int epi, bool o
   ZO_4W64(ZOACT_EPI_SWIGLU, false)
   ZO_4W64(ZOACT_EPI_RELU, false)
   ZO_4W64(EPI_MSE, false)
+  ZO_4W64(EPI_XENT, false)
 #undef ZO_4W64
   return hipErrorNotSupported;
 }

@@ -81,6 +81,39 @@ __global__ void __launch_bounds__(256) sum_mean(const double* __restrict__ part,
   }
 }
 
+// Cross entropy from the fused LM-head epilogue's per-block (max, sum of exp): one wave per
+// row merges its nblk blocks (lanes strided, then a butterfly, in the online-softmax rule of
+// xent_partial), and lane 0 adds max + log(sum) - next-token logit; kLossBlocks fixed
+// partial sums per half as in xent_partial.
+__global__ void __launch_bounds__(256) xent_combine(const float2* __restrict__ xpart, const float* __restrict__ xtgt,
+                                                    int64_t T, int64_t S, int nblk, double* __restrict__ part) {
+  __shared__ double sh[4];
+  const int h = blockIdx.y;
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  double acc = 0.0;
+  for (int64_t m = (int64_t)blockIdx.x * 4 + w; m < T; m += (int64_t)gridDim.x * 4) {
+    if (m % S == S - 1) continue;              // the last position has no next token
+    const float2* pr = xpart + ((int64_t)h * T + m) * nblk;
+    float mm = -INFINITY, se = 0.f;
+    for (int i = l; i < nblk; i += 64) {
+      const float2 q = pr[i];
+      const float m2 = fmaxf(mm, q.x);
+      se = (m2 == -INFINITY) ? 0.f : se * __expf(mm - m2) + q.y * __expf(q.x - m2);
+      mm = m2;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float m2 = __shfl_xor(mm, o, 64), s2 = __shfl_xor(se, o, 64);
+      const float mx = fmaxf(mm, m2);
+      se = (mx == -INFINITY) ? 0.f : se * __expf(mm - mx) + s2 * __expf(m2 - mx);
+      mm = mx;
+    }
+    if (l == 0) acc += (double)mm + log((double)se) - (double)xtgt[(int64_t)h * T + m];
+  }
+  const double s = block_sum_d(l == 0 ? acc : 0.0, sh);
+  if (threadIdx.x == 0) part[h * kLossBlocks + blockIdx.x] = s;
+}
+
 // Sum kLossBlocks partials per half in a fixed order and scale.
 __global__ void __launch_bounds__(256) finish_mean(const double* __restrict__ part, double count, float* loss_pm) {
   __shared__ double sh[4];
@@ -144,6 +177,13 @@ __global__ void __launch_bounds__(256) xent_partial(const float* __restrict__ lo
 }
 
 }  // namespace
+
+hipError_t launch_xent_combine(const float2* xpart, const float* xtgt, int64_t T, int64_t S, int nblk, int64_t B,
+                               double* part, float* loss_pm, hipStream_t s) {
+  xent_combine<<<dim3(kLossBlocks, 2), dim3(256), 0, s>>>(xpart, xtgt, T, S, nblk, part);
+  finish_mean<<<dim3(1), dim3(256), 0, s>>>(part, (double)(B * (S - 1)), loss_pm);
+  return hipGetLastError();
+}
 
 hipError_t launch_sum_mean(const double* part, int64_t n, double count, float* loss_pm, hipStream_t s) {
   sum_mean<<<dim3(1), dim3(256), 0, s>>>(part, n, count, loss_pm);

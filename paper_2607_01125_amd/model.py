@@ -222,7 +222,7 @@ class Decoder:
             "k": None if fused else e(2 * T, self.dkv),
             "att": e(2 * T, self.d), "ff": e(2 * T, s.d_ff),
             "p": e(2 * T, max(self.r, 1)),
-            "logits": e(2 * T, s.vocab, dt=torch.float32),
+            "logits": None,          # fp32 [2 T][vocab], allocated when a forward returns logits
         }
         self._bufs[key] = B
         return B
@@ -262,7 +262,8 @@ class Decoder:
             lin.r, lin.ut, lin.ch, lin.ch_stride = 0, None, None, 0
             Z.linear_fwd_pm(lin, None, x, T, None, y, pert, residual, flags)
 
-    def forward(self, tokens: torch.Tensor, pert: Z.Pert | Z.PertPair, *, calibrate=None, distinct_halves=False):
+    def forward(self, tokens: torch.Tensor, pert: Z.Pert | Z.PertPair, *, calibrate=None, distinct_halves=False,
+                head: bool = True):
         """Both halves of the forward; logits fp32 [2][n_seq][seq][V] in the buffer set.
 
         tokens int32 [n_seq][seq] (or [2][n_seq][seq] with distinct_halves).  With a Pert,
@@ -320,6 +321,10 @@ class Decoder:
             self._apply(P["down"], B["ff"], T, h_alt, pert, ut, residual=h, adapt=adapt)
             h, h_alt = h_alt, h
         self._norm(h, self.nf, getattr(self, "nfb", None), B["a"])
+        if not head:                 # the caller runs the LM head (fused with the loss)
+            return B["a"]
+        if B["logits"] is None:
+            B["logits"] = torch.empty(2 * T, s.vocab, dtype=torch.float32, device=self.dev)
         Z.linear_fwd_pm(self.head, None, B["a"], T, None, B["logits"], pert)
         return B["logits"].view(2, n_seq, seq, s.vocab)
 
@@ -378,12 +383,24 @@ class Decoder:
             self.ut[key] = self._t(u).reshape(self.r, d_in).contiguous()
 
     # ---------------------------------------------------------------- Algorithm 2 step
+    def _loss_pair(self, tokens: torch.Tensor, pert, out: torch.Tensor):
+        """Forward both halves and write their next-token cross entropies into out[0:2]; in
+        bf16 modes the LM head and the loss run fused (logits not stored)."""
+        if self.act == torch.bfloat16:
+            a = self.forward(tokens, pert, head=False)
+            T = tokens.numel()
+            need = Z.linear_xent_workspace_bytes(T, self.s.vocab)
+            if getattr(self, "_xent_ws", None) is None or self._xent_ws.numel() < need:
+                self._xent_ws = torch.empty(need, dtype=torch.uint8, device=self.dev)
+            Z.linear_xent(self.head, None, a, tokens, None, pert, out, self._xent_ws)
+        else:
+            self.forward(tokens, pert)
+            Z.xent_pm(self._cur["logits"], tokens, out, self.loss_ws)
+        return out
+
     def losses(self, tokens: torch.Tensor, seed: int, t: int, eps: float):
         """Forward both halves at step t and write (L+, L-) into self.loss_pm."""
-        self.forward(tokens, Z.Pert(seed, t, 0, eps))
-        B = self._cur
-        Z.xent_pm(B["logits"], tokens, self.loss_pm, self.loss_ws)
-        return self.loss_pm
+        return self._loss_pair(tokens, Z.Pert(seed, t, 0, eps), self.loss_pm)
 
     def step(self, tokens: torch.Tensor, seed: int, eps: float, lr: float, optimizer: str = "adam"):
         """One two-sided ZO step: L+ and L-, g = (L+ - L-) / (2 eps), update C with Z regenerated."""
@@ -414,8 +431,7 @@ class Decoder:
 
         for i in range(n_fwd):
             (q0, s0), (q1, s1) = spec(2 * i), spec(2 * i + 1)
-            self.forward(tokens, Z.pert_pair(seed, self.t, (q0, q1), (s0, s1), eps))
-            Z.xent_pm(self._cur["logits"], tokens, losses[2 * i:2 * i + 2], self.loss_ws)
+            self._loss_pair(tokens, Z.pert_pair(seed, self.t, (q0, q1), (s0, s1), eps), losses[2 * i:2 * i + 2])
         if optimizer == "adam":
             Z.step_q(self.arena, losses, q, seed, self.t, eps, Z.adam_desc(lr, self.t), self.status)
         elif optimizer == "sgd":

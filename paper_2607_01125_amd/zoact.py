@@ -86,6 +86,9 @@ SIGNATURES = {
     "zoact_step_q": ([ctypes.POINTER(ArenaDesc), _P, _I32, _U64, _U32, _F, ctypes.POINTER(AdamDesc), _P, _P], _I32),
     "zoact_step_q_sgd": ([ctypes.POINTER(ArenaDesc), _P, _I32, _U64, _U32, _F, _F, _P, _P], _I32),
     "zoact_loss_workspace_bytes": ([], _SZ),
+    "zoact_linear_xent_workspace_bytes": ([_I64, _I64], _SZ),
+    "zoact_linear_xent_pair": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I64, _I64, _P,
+                                ctypes.POINTER(PertPair), _P, _P, _P, _SZ, _P], _I32),
     "zoact_linear_mse_workspace_bytes": ([_I64, _I64], _SZ),
     "zoact_linear_mse_pair": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I64, _P,
                                ctypes.POINTER(PertPair), _P, _P, _P, _SZ, _P], _I32),
@@ -232,6 +235,23 @@ def as_pair(pert: Pert | PertPair) -> PertPair:
     if isinstance(pert, PertPair):
         return pert
     return pert_pair(pert.seed, pert.step, (pert.query, pert.query), (1, -1), pert.eps)
+
+
+def linear_xent_workspace_bytes(T: int, d_out: int) -> int:
+    return int(lib().zoact_linear_xent_workspace_bytes(T, d_out))
+
+
+def linear_xent(layer: Linear, arena: Arena | None, x: torch.Tensor, tokens: torch.Tensor, p: torch.Tensor | None,
+                pert: Pert | PertPair, loss_pm: torch.Tensor, ws: torch.Tensor, stream=None):
+    """LM head of both halves with the next-token cross entropy in its epilogue:
+    loss_pm[h] = mean over B (S - 1) positions, logits not stored (tokens int32 [B][S])."""
+    d = layer.desc()
+    a = arena.desc() if arena is not None else None
+    B, S = tokens.shape
+    pp = as_pair(pert)
+    _check(lib().zoact_linear_xent_pair(ctypes.byref(d), ctypes.byref(a) if a is not None else None, _ptr(x), B, S,
+                                        _ptr(p), ctypes.byref(pp), _ptr(tokens), _ptr(loss_pm), _ptr(ws),
+                                        ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def linear_mse_workspace_bytes(T: int, d_out: int) -> int:

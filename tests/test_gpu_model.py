@@ -217,3 +217,22 @@ def test_basis_init_over_model(shape, mode):
     for key, u in ut.items():
         um = host(u).T
         assert np.max(np.abs(um.T @ um - np.eye(shape.rank))) <= (1e-5 if mode == "fp32" else 2e-2)
+
+
+# ------------------------------------------------------------------ fused LM head + cross entropy
+@pytest.mark.parametrize("shape,B,S", [(LLAMA_S, 2, 64), (OPT_S, 3, 40)], ids=["llama", "opt"])
+def test_fused_head_xent_matches_stored_logits(shape, B, S):
+    """The LM head with the cross entropy in its epilogue (logits never stored) gives the
+    losses of the stored-logits path up to summation order."""
+    announce("fused head xent", shape.name, B, S)
+    om_m, g = _models(shape, "bf16", seed=6, perturb=True)
+    g.arena.c.copy_(torch.from_numpy(synth.normal((om_m.k,), 0.05, 6, 9)).to(g.arena.c.dtype))
+    tok = t_i32(synth.uniform_tokens(B, S, shape.vocab, 6, 4))
+    pert = Z.Pert(3, 2, 0, 1e-2)
+    logits = g.forward(tok, pert)
+    stored = torch.zeros(2, dtype=torch.float32, device=dev())
+    Z.xent_pm(logits.reshape(2 * B * S, -1), tok, stored, g.loss_ws)
+    fused = torch.full((2,), float("nan"), dtype=torch.float32, device=dev())
+    g._loss_pair(tok, pert, fused)
+    np.testing.assert_allclose(host(fused), host(stored), rtol=2e-6)
+    assert host(fused)[0] != host(fused)[1]
