@@ -138,6 +138,64 @@ __global__ void __launch_bounds__(256) rmsnorm_bf16_vec_kernel(const uint16_t* _
   }
 }
 
+// bf16 LayerNorm with 16-byte accesses, the same arrangement (row chunks of 8 in registers,
+// chunk u * 256 + thread, d % 8 == 0, d <= 2048 * VPT8): mean, then the centred second
+// moment, then ((x - mean) * inv) * w + b with one rounding.
+template <int VPT8>
+__global__ void __launch_bounds__(256) layernorm_bf16_vec_kernel(const uint16_t* __restrict__ x,
+                                                                 const uint16_t* __restrict__ w,
+                                                                 const uint16_t* __restrict__ bias, int64_t d,
+                                                                 float eps, uint16_t* __restrict__ y) {
+  __shared__ float sh[4];
+  const uint16_t* xr = x + (int64_t)blockIdx.x * d;
+  uint16_t* yr = y + (int64_t)blockIdx.x * d;
+  const int nch = (int)(d / 8);
+  float f[VPT8][8];
+  float s = 0.f;
+#pragma unroll
+  for (int u = 0; u < VPT8; ++u) {
+    const int ch = u * 256 + threadIdx.x;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (ch < nch) v = *reinterpret_cast<const uint4*>(xr + (int64_t)ch * 8);
+    const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      f[u][2 * e] = bf2f((uint16_t)(wv[e] & 0xFFFF));
+      f[u][2 * e + 1] = bf2f((uint16_t)(wv[e] >> 16));
+      s += f[u][2 * e];
+      s += f[u][2 * e + 1];
+    }
+  }
+  const float mu = block_sum(s, sh) / (float)d;
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < VPT8; ++u) {
+    if (u * 256 + (int)threadIdx.x >= nch) continue;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float c = f[u][e] - mu;
+      ss += c * c;
+    }
+  }
+  const float inv = rsqrtf(block_sum(ss, sh) / (float)d + eps);
+#pragma unroll
+  for (int u = 0; u < VPT8; ++u) {
+    const int ch = u * 256 + threadIdx.x;
+    if (ch >= nch) continue;
+    const uint4 g = *reinterpret_cast<const uint4*>(w + (int64_t)ch * 8);
+    const uint4 bb = *reinterpret_cast<const uint4*>(bias + (int64_t)ch * 8);
+    const uint32_t gv[4] = {g.x, g.y, g.z, g.w}, bv[4] = {bb.x, bb.y, bb.z, bb.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float a = ((f[u][2 * e] - mu) * inv) * bf2f((uint16_t)(gv[e] & 0xFFFF)) + bf2f((uint16_t)(bv[e] & 0xFFFF));
+      const float b = ((f[u][2 * e + 1] - mu) * inv) * bf2f((uint16_t)(gv[e] >> 16)) + bf2f((uint16_t)(bv[e] >> 16));
+      o[e] = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+    }
+    *reinterpret_cast<uint4*>(yr + (int64_t)ch * 8) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
 // bf16 rotary embedding with 16-byte accesses: one thread rotates 8 pairs (j .. j + 7 with
 // their partners j + half .. j + half + 7) of one head of one row.
 __global__ void rope_bf16_vec_kernel(uint16_t* __restrict__ x, int64_t rows, int64_t ld, int64_t col0, int heads,
@@ -394,9 +452,8 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(const uint16_t* __r
 // normaliser from the unrounded P), organised for grouped-query heads: a workgroup takes one
 // key/value head of one sequence and HG = min(G, 4) of the G query heads that read it, each
 // wave 16 * QB queries of one head (QT = 64 QB / HG queries per workgroup tile), so every
-// K/V block staged in LDS serves four waves' worth of queries; K and V blocks travel
-// global -> registers one block ahead of their use.  QB = 2 keeps a thread within 256
-// registers, two workgroups per CU.  Scores are formed transposed,
+// K/V block staged in LDS serves four waves' worth of queries.  QB = 2 keeps a thread within
+// 256 registers, two workgroups per CU.  Scores are formed transposed,
 // S^T[key][query] (K as the MFMA A operand, Q as B): a lane then holds four keys of one
 // query, its probabilities are already the B operand of O^T = V^T P^T, and V^T is read in
 // the same key order (the order of the 32 keys inside one MFMA does not change the sum
@@ -463,12 +520,12 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
   float mq[QB];
 #pragma unroll
   for (int b = 0; b < QB; ++b) mq[b] = -INFINITY;
-  // K and V blocks go global -> registers one block ahead (their latency hides behind the
-  // current block's MFMAs), then registers -> LDS between two barriers
+  // K and V blocks go global -> registers -> LDS between two barriers: all loads of a block
+  // are issued before the first LDS write
   constexpr int KPT = 64 * KC / 256;   // 16-byte K chunks per thread and block
   constexpr int VPT = 32 * KC / 256;   // V items (key pair x 8 columns) per thread and block
-  uint4 kreg[KPT], vreg[VPT][2];
-  auto load_k = [&](int kb) {
+  auto stage = [&](int kb, bool with_v) {
+    uint4 kreg[KPT], vreg[VPT][2];
 #pragma unroll
     for (int t = 0; t < KPT; ++t) {
       const int cidx = threadIdx.x + t * 256, key = cidx / KC, ch = cidx % KC;
@@ -476,46 +533,41 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
       kr = kr < seq ? kr : seq - 1;
       kreg[t] = *reinterpret_cast<const uint4*>(k + (r0 + kr) * ldk + (int64_t)hk * HD + ch * 8);
     }
-  };
-  auto store_k = [&]() {
+    if (with_v) {
+#pragma unroll
+      for (int t = 0; t < VPT; ++t) {
+        const int it = threadIdx.x + t * 256, kp = it & 31, dc = it >> 5;
+        int64_t k0r = (int64_t)kb * 64 + 2 * kp, k1r = k0r + 1;
+        k0r = k0r < seq ? k0r : seq - 1;
+        k1r = k1r < seq ? k1r : seq - 1;
+        vreg[t][0] = *reinterpret_cast<const uint4*>(v + (r0 + k0r) * ldv + (int64_t)hk * HD + dc * 8);
+        vreg[t][1] = *reinterpret_cast<const uint4*>(v + (r0 + k1r) * ldv + (int64_t)hk * HD + dc * 8);
+      }
+    }
 #pragma unroll
     for (int t = 0; t < KPT; ++t) {
       const int cidx = threadIdx.x + t * 256, key = cidx / KC, ch = cidx % KC;
       *reinterpret_cast<uint4*>(ks + key * HD + ((ch ^ (key & 7)) * 8)) = kreg[t];
     }
-  };
-  auto load_v = [&](int kb) {
+    if (with_v) {
+      // V^T: item (key pair kp, 8-column chunk dc) -> eight words (V[2kp][d], V[2kp+1][d])
 #pragma unroll
-    for (int t = 0; t < VPT; ++t) {
-      const int it = threadIdx.x + t * 256, kp = it & 31, dc = it >> 5;
-      int64_t k0r = (int64_t)kb * 64 + 2 * kp, k1r = k0r + 1;
-      k0r = k0r < seq ? k0r : seq - 1;
-      k1r = k1r < seq ? k1r : seq - 1;
-      vreg[t][0] = *reinterpret_cast<const uint4*>(v + (r0 + k0r) * ldv + (int64_t)hk * HD + dc * 8);
-      vreg[t][1] = *reinterpret_cast<const uint4*>(v + (r0 + k1r) * ldv + (int64_t)hk * HD + dc * 8);
-    }
-  };
-  // V^T: item (key pair kp, 8-column chunk dc) -> eight words (V[2kp][d], V[2kp+1][d])
-  auto store_vt = [&]() {
+      for (int t = 0; t < VPT; ++t) {
+        const int it = threadIdx.x + t * 256, kp = it & 31, dc = it >> 5;
+        const uint32_t aw[4] = {vreg[t][0].x, vreg[t][0].y, vreg[t][0].z, vreg[t][0].w};
+        const uint32_t cw[4] = {vreg[t][1].x, vreg[t][1].y, vreg[t][1].z, vreg[t][1].w};
 #pragma unroll
-    for (int t = 0; t < VPT; ++t) {
-      const int it = threadIdx.x + t * 256, kp = it & 31, dc = it >> 5;
-      const uint32_t aw[4] = {vreg[t][0].x, vreg[t][0].y, vreg[t][0].z, vreg[t][0].w};
-      const uint32_t cw[4] = {vreg[t][1].x, vreg[t][1].y, vreg[t][1].z, vreg[t][1].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vt[(dc * 8 + 2 * e) * 36 + kp] = (aw[e] & 0xFFFFu) | (cw[e] << 16);
-        vt[(dc * 8 + 2 * e + 1) * 36 + kp] = (aw[e] >> 16) | (cw[e] & 0xFFFF0000u);
+        for (int e = 0; e < 4; ++e) {
+          vt[(dc * 8 + 2 * e) * 36 + kp] = (aw[e] & 0xFFFFu) | (cw[e] << 16);
+          vt[(dc * 8 + 2 * e + 1) * 36 + kp] = (aw[e] >> 16) | (cw[e] & 0xFFFF0000u);
+        }
       }
     }
   };
 
-  load_k(0);
   for (int kb = 0; kb < nkb; ++kb) {
     __syncthreads();
-    store_k();
-    if (kb + 1 < nkb) load_k(kb + 1);
-    else load_k(0);                              // pass 2 starts again at block 0
+    stage(kb, false);
     __syncthreads();
     if ((int64_t)kb * 64 > wq_last) continue;   // wave-uniform: this block is masked for all its queries
 #pragma unroll
@@ -545,15 +597,9 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
   float lq[QB];
 #pragma unroll
   for (int b = 0; b < QB; ++b) lq[b] = 0.f;
-  load_v(0);
   for (int kb = 0; kb < nkb; ++kb) {
     __syncthreads();
-    store_k();
-    store_vt();
-    if (kb + 1 < nkb) {
-      load_k(kb + 1);
-      load_v(kb + 1);
-    }
+    stage(kb, true);
     __syncthreads();
     if ((int64_t)kb * 64 > wq_last) continue;
     // probabilities of the four q-blocks as B operands: 32-key step c holds keys
@@ -686,7 +732,18 @@ extern "C" zoact_status zoact_layernorm(const void* x, const void* w, const void
   ZO_CHECK(rows >= 1 && d >= 1 && rows <= 0x7FFFFFFF, "layernorm: bad shape");
   ZO_CHECK(dtype == ZOACT_F32 || dtype == ZOACT_BF16, "layernorm: dtype must be F32 or BF16");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (dtype == ZOACT_BF16)
+  const bool vec = dtype == ZOACT_BF16 && d % 8 == 0 && d <= 8192 && ((uintptr_t)x % 16) == 0 &&
+                   ((uintptr_t)w % 16) == 0 && ((uintptr_t)b % 16) == 0 && ((uintptr_t)y % 16) == 0;
+  const int vpt = (int)((d / 8 + 255) / 256);
+#define ZO_LN(V)                                                                                     \
+  layernorm_bf16_vec_kernel<V><<<(unsigned)rows, 256, 0, s>>>((const uint16_t*)x, (const uint16_t*)w, \
+                                                               (const uint16_t*)b, d, eps, (uint16_t*)y)
+  if (vec && vpt <= 1) ZO_LN(1);
+  else if (vec && vpt == 2) ZO_LN(2);
+  else if (vec && vpt == 3) ZO_LN(3);
+  else if (vec) ZO_LN(4);
+#undef ZO_LN
+  else if (dtype == ZOACT_BF16)
     layernorm_kernel<uint16_t><<<(unsigned)rows, 256, 0, s>>>((const uint16_t*)x, (const uint16_t*)w,
                                                               (const uint16_t*)b, d, eps, (uint16_t*)y);
   else

@@ -67,7 +67,7 @@ def test_rmsnorm(bf16, rows, d):
 
 
 @pytest.mark.parametrize("bf16", [False, True])
-@pytest.mark.parametrize("rows,d", [(5, 128), (129, 5120)])
+@pytest.mark.parametrize("rows,d", [(5, 128), (129, 5120), (7, 2056), (3, 8192), (2, 100)])
 def test_layernorm(bf16, rows, d):
     announce("layernorm", bf16, rows, d)
     x = synth.normal((rows, d), 2.0, 3, rows) + np.float32(0.5)
