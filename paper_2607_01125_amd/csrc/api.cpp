@@ -226,7 +226,8 @@ zoact_status zoact_linear_xent_pair(const zoact_linear* L, const zoact_arena* A,
 
 size_t zoact_linear_mse_workspace_bytes(int64_t T, int64_t d_out) {
   if (T < 1 || d_out < 1) return 0;
-  return (size_t)2 * (size_t)((T + 255) / 256) * (size_t)((d_out + 255) / 256) * sizeof(double);
+  // one fp64 partial sum per 256 x 256 tile and wave (four per tile)
+  return (size_t)2 * (size_t)((T + 255) / 256) * (size_t)((d_out + 255) / 256) * 4 * sizeof(double);
 }
 
 zoact_status zoact_linear_mse_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t T,

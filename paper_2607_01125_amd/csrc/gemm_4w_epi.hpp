@@ -1,7 +1,8 @@
 // Pieces shared by the four-wave fused GEMM schedules (32-deep and 64-deep stages): wait
 // counts, the workgroup barrier, buffer descriptors, and the epilogue that stages each
 // wave's 128 x 128 accumulator tile through LDS and applies bias, residual, activation
-// (or the fused regression loss) with one rounding.
+// (or the fused regression loss) with one rounding, and the same operations straight from
+// the accumulators.
 #pragma once
 #include <math.h>
 
@@ -28,6 +29,12 @@ __device__ __forceinline__ void barrier() {
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Tile index of the regression loss's partial sums (four per tile, one per wave):
+// half-major, then token tile, then feature tile.
+__device__ __forceinline__ int64_t mse_slot(const GemmArgs& a, int half, int tm, int tn) {
+  return (int64_t)half * a.tiles_m_half * a.tiles_n + (int64_t)(tm % a.tiles_m_half) * a.tiles_n + tn;
 }
 
 template <int EPI, bool OUT_F32>
@@ -153,7 +160,7 @@ __device__ __forceinline__ void epilogue_4w(const GemmArgs& a, floatx4 (&acc)[8]
             if (n + e < a.N) se += __expf(o[e] - mx);
 #pragma unroll
           for (int off = 1; off < 16; off <<= 1) se += __shfl_xor(se, off, 64);
-          if (c == 0) a.xpart[row * a.xnblk + (n0 + wn0) / 128] = make_float2(mx, se);
+          if (c == 0 && n0 + wn0 < a.N) a.xpart[row * a.xnblk + (n0 + wn0) / 128] = make_float2(mx, se);
           const int64_t pos = m % a.seq;
           if (pos < a.seq - 1) {
             int64_t t = a.tok[m + 1];
@@ -208,17 +215,376 @@ __device__ __forceinline__ void epilogue_4w(const GemmArgs& a, floatx4 (&acc)[8]
     __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
   }
   if constexpr (EPI == EPI_MSE) {
-    // tile sum in a fixed order: lanes (fp64 butterfly), then the four waves in order
+    // this wave's sum (fp64 butterfly over lanes) into its own slot: four per tile
     double v = (double)sq_acc;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    double* red = reinterpret_cast<double*>(reinterpret_cast<char*>(lds) + 4 * 64 * LDR * 4);
-    if (lane == 0) red[wave] = v;
-    __syncthreads();
-    if (threadIdx.x == 0)
-      a.part[(int64_t)half * a.tiles_m_half * a.tiles_n + (int64_t)(tm % a.tiles_m_half) * a.tiles_n + tn] =
-          ((red[0] + red[1]) + red[2]) + red[3];
+    if (lane == 0) a.part[mse_slot(a, half, tm, tn) * 4 + wave] = v;
   }
+}
+
+// Epilogue straight from the accumulators, for the persistent schedule whose operand ring
+// stays busy with the next tile's first stages: no LDS.  Lane (lr, lk) holds, for every
+// 16 x 16 block (i, j), features i*16 + lk*4 .. +3 of token j*16 + lr (the MFMA output
+// layout), so each store writes 4 consecutive features of one row; the row reductions of
+// the cross entropy run over the 4 lanes that share lr.  Rows go through buffer
+// descriptors based at the wave's first token and feature, sized to its tokens below T:
+// the per-lane part of an address is one register, the block's part is scalar, and rows
+// past T fall outside the range (loads read zeros, stores are dropped).  N is a multiple
+// of 16, so a 16-feature block lies wholly below N or past it: those tests are uniform.
+
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// Descriptor over `rows` rows of `ld` elements of `esz` bytes from element `first` (all
+// wave-uniform: read from the first lane so that the compiler keeps the descriptor in
+// scalar registers rather than looping over lanes at every access).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void* base, int64_t first, int64_t ld, int rows,
+                                                           int esz) {
+  const uint64_t p = reinterpret_cast<uint64_t>(base) + (uint64_t)(first * esz);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)p);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(p >> 32));
+  const uint32_t n = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(rows * ld * esz));
+  return buffer_rsrc(reinterpret_cast<const void*>(((uint64_t)hi << 32) | lo), n);
+}
+
+// Tokens of this wave below T (0 .. 128).
+__device__ __forceinline__ int wave_rows(const GemmArgs& a, int64_t mw) {
+  const int64_t r = a.T - mw;
+  return r <= 0 ? 0 : (r >= 128 ? 128 : (int)r);
+}
+
+// One accumulator element read into a VGPR where it is used: kept in order with the block
+// fences, so a block's values are read with the block instead of all 256 at once.
+__device__ __forceinline__ float acc_read(float x) {
+  float r;
+  asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(r) : "a"(x));
+  return r;
+}
+
+// Per-lane byte offset past any descriptor's range: a store through it is dropped.
+constexpr int OFF_NONE = (int)0x80000000u;
+
+// Operand rows the epilogue reads, for this lane's blocks in token blocks J0 .. J0 + 3:
+// the regression target (EPI_MSE) or the residual (stored outputs with a residual; block b
+// is output block b).  Rows past T read zeros; blocks past N are not read (a descriptor
+// starts at the wave's first feature, so in its last row such a block would still be in
+// its range but past the end of the tensor).
+template <int EPI, int J0>
+__device__ __forceinline__ void epi_prefetch(const GemmArgs& a, uint2 (&tv)[8][8], int wave, int lane, int64_t m0,
+                                             int64_t n0, int half) {
+  const int lr = lane & 15, lk = lane >> 4;
+  const int64_t nw = n0 + (wave & 1) * 128, mw = m0 + (wave >> 1) * 128;
+  if constexpr (EPI == EPI_MSE) {
+    const __amdgpu_buffer_rsrc_t rs = rows_rsrc(a.tgt, mw * a.N + nw, a.N, wave_rows(a, mw), 2);
+    const int vo = (int)((lr * a.N + lk * 4) * 2);
+#pragma unroll
+    for (int j = J0; j < J0 + 4; ++j)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        u32x2_t u = {0u, 0u};
+        if (nw + i * 16 < a.N) u = __builtin_amdgcn_raw_buffer_load_b64(rs, vo, (int)(j * 16 * a.N * 2) + i * 32, 0);
+        tv[j][i] = make_uint2(u.x, u.y);
+      }
+  } else if constexpr (EPI != EPI_XENT) {
+    if (a.resid == nullptr) return;
+    constexpr bool SW = EPI == ZOACT_EPI_SWIGLU;
+    constexpr int NB = SW ? 4 : 8;
+    const int64_t nout = SW ? a.N / 2 : a.N;
+    const int64_t first = ((int64_t)half * a.T + mw) * nout + (SW ? nw / 2 : nw);
+    const __amdgpu_buffer_rsrc_t rs = rows_rsrc(a.resid, first, nout, wave_rows(a, mw), 2);
+    const int vo = (int)((lr * nout + lk * 4) * 2);
+#pragma unroll
+    for (int j = J0; j < J0 + 4; ++j)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        u32x2_t u = {0u, 0u};
+        if (nw + b * (SW ? 32 : 16) < a.N)
+          u = __builtin_amdgcn_raw_buffer_load_b64(rs, vo, (int)(j * 16 * nout * 2) + b * 32, 0);
+        tv[j][b] = make_uint2(u.x, u.y);
+      }
+  }
+}
+
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded to bf16 (round to nearest even) in one conversion, lo in the low half.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Epilogues that use the interleaved W-row order of the 64-deep schedule, in which lane
+// (lr, lk) holds features q * 32 + lk * 8 .. +7 of block pair q (blocks 2q, 2q + 1): those
+// with one output per feature, whose rows are then read and written 16 bytes per lane.
+// (SwiGLU needs gate and up in one lane; the cross entropy reduces over whole rows.)
+constexpr bool epi_perm(int epi) { return epi == 0 || epi == ZOACT_EPI_RELU || epi == EPI_MSE; }
+
+// Per-lane offset of a lane's 8 features of block pair q, or an offset past the range where
+// they lie past N (N is a multiple of 8, so 8 features lie wholly on one side).
+__device__ __forceinline__ int pair_off(const GemmArgs& a, int64_t nw, int q, int lk, int vo) {
+  return nw + q * 32 + lk * 8 < a.N ? vo : OFF_NONE;
+}
+
+// Interleaved order: the 8 bf16 values of each lane's block pair q in token blocks 0 .. 7 of
+// `src` (the regression target, or the residual), 16 bytes per lane; rows past T and
+// features past N read zeros.
+__device__ __forceinline__ void epi_prefetch8(const GemmArgs& a, const uint16_t* src, int64_t ld, uint4 (&tq)[8][4],
+                                              int wave, int lane, int64_t m0, int64_t n0, int half) {
+  const int lr = lane & 15, lk = lane >> 4;
+  const int64_t nw = n0 + (wave & 1) * 128, mw = m0 + (wave >> 1) * 128;
+  const __amdgpu_buffer_rsrc_t rs = rows_rsrc(src, ((int64_t)half * a.T + mw) * ld + nw, ld, wave_rows(a, mw), 2);
+  const int vo = (int)((lr * ld + lk * 8) * 2);
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const u32x4_t u = __builtin_amdgcn_raw_buffer_load_b128(rs, pair_off(a, nw, q, lk, vo),
+                                                              (int)((j * 16 * ld + q * 32) * 2), 0);
+      tq[j][q] = make_uint4(u.x, u.y, u.z, u.w);
+    }
+}
+
+template <int EPI, bool OUT_F32, bool BIAS>
+__device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&acc)[8][8], int wave, int lane,
+                                                   int64_t m0, int64_t n0, int half, int tm, int tn) {
+  const int lr = lane & 15, lk = lane >> 4;
+  const int64_t nw = n0 + (wave & 1) * 128;   // first feature of this wave
+  const int64_t mw = m0 + (wave >> 1) * 128;  // first token of this wave
+  const int rows = wave_rows(a, mw);
+  constexpr bool PERM = epi_perm(EPI);
+  // the rows this epilogue reads (regression target or residual), all requested up front:
+  // in the interleaved order 16 bytes per lane and block pair, else 8 per block
+  uint4 tq[8][4];
+  uint2 tv[8][8];
+  if constexpr (EPI == EPI_MSE) {
+    epi_prefetch8(a, a.tgt, a.N, tq, wave, lane, m0, n0, 0);
+  } else if constexpr (PERM) {
+    if (a.resid) epi_prefetch8(a, a.resid, a.N, tq, wave, lane, m0, n0, half);
+  } else {
+    epi_prefetch<EPI, 0>(a, tv, wave, lane, m0, n0, half);
+    epi_prefetch<EPI, 4>(a, tv, wave, lane, m0, n0, half);
+  }
+  // bias of the lane's 32 features as bf16 pairs (per block pair, or per block), zero past N
+  uint32_t bw[16];
+  if constexpr (BIAS) {
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(a.bias, (uint32_t)(a.N * 2));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if constexpr (PERM) {
+        const u32x4_t u = __builtin_amdgcn_raw_buffer_load_b128(rs, pair_off(a, nw, q, lk, lk * 16),
+                                                                (int)((nw + q * 32) * 2), 0);
+        bw[4 * q] = u.x, bw[4 * q + 1] = u.y, bw[4 * q + 2] = u.z, bw[4 * q + 3] = u.w;
+      } else {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const u32x2_t u = __builtin_amdgcn_raw_buffer_load_b64(rs, lk * 8, (int)((nw + (2 * q + h) * 16) * 2), 0);
+          bw[4 * q + 2 * h] = u.x, bw[4 * q + 2 * h + 1] = u.y;
+        }
+      }
+    }
+  }
+  // accumulator element e of block (i, j), plus the bias (none added without one).  Either
+  // order keeps block i's 4 bias values in words 2i, 2i + 1.
+  auto val = [&](int i, int j, int e) -> float {
+    const float v = acc_read(acc[i][j][e]);
+    if constexpr (BIAS) {
+      const uint32_t w = bw[2 * i + (e >> 1)];
+      return v + (e & 1 ? bf_hi(w) : bf_lo(w));
+    }
+    return v;
+  };
+  if constexpr (EPI == EPI_MSE) {
+    float sq = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      float sj = 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (nw + q * 32 >= a.N) continue;   // uniform
+        // squared error of the bf16-rounded outputs (features lk*8 .. +7) against the target
+        const uint32_t t[4] = {tq[j][q].x, tq[j][q].y, tq[j][q].z, tq[j][q].w};
+        float sp = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const int i = 2 * q + (w >> 1), e = 2 * (w & 1);
+          const uint32_t o = pack_bf16x2(val(i, j, e), val(i, j, e + 1));
+          const float d0 = bf_lo(o) - bf_lo(t[w]), d1 = bf_hi(o) - bf_hi(t[w]);
+          sp = fmaf(d0, d0, sp);
+          sp = fmaf(d1, d1, sp);
+        }
+        sj += nw + q * 32 + lk * 8 < a.N ? sp : 0.f;
+      }
+      sq += j * 16 + lr < rows ? sj : 0.f;   // rows past T add nothing
+      __builtin_amdgcn_sched_barrier(0);     // one token block at a time: bounded registers
+    }
+    double v = (double)sq;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    if (lane == 0) a.part[mse_slot(a, half, tm, tn) * 4 + wave] = v;
+  } else if constexpr (EPI == EPI_XENT) {
+    // branch-free per token block (stores through an offset outside the range where a lane
+    // must not write) so that the block's values stay the only ones in registers
+    const __amdgpu_buffer_rsrc_t trs = buffer_rsrc(a.tok, (uint32_t)(a.T * 4));
+    const __amdgpu_buffer_rsrc_t xps = buffer_rsrc(a.xpart, (uint32_t)(2 * a.T * a.xnblk * 8));
+    const __amdgpu_buffer_rsrc_t xts = buffer_rsrc(a.xtgt, (uint32_t)(2 * a.T * 4));
+    const int seq = (int)a.seq;
+    int nxt[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int m = (int)mw + j * 16 + lr;
+      const bool has = j * 16 + lr < rows && m % seq < seq - 1;
+      // (m + 1 = T reads zero: past the range)
+      const int t = (int)__builtin_amdgcn_raw_buffer_load_b32(trs, (m + 1) * 4, 0, 0);
+      nxt[j] = has ? (t < 0 ? 0 : (t >= a.N ? (int)a.N - 1 : t)) : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      float v[8][4];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[i][e] = val(i, j, e);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (nw + i * 16 < a.N) mx = fmaxf(mx, v[i][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      float se = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (nw + i * 16 < a.N) se += __expf(v[i][e] - mx);
+      se += __shfl_xor(se, 16, 64);
+      se += __shfl_xor(se, 32, 64);
+      const bool mv = j * 16 + lr < rows;
+      const int row = half * (int)a.T + (int)mw + j * 16 + lr;
+      // (a wave wholly past N has no block of its own: index xnblk would be the next row's)
+      const int vxp = (mv && lk == 0 && nw < a.N) ? (row * a.xnblk + (int)(nw >> 7)) * 8 : OFF_NONE;
+      __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{__float_as_uint(mx), __float_as_uint(se)}, xps, vxp, 0, 0);
+      const int d = nxt[j] - (int)nw;   // the next token's offset in this wave's block
+      float tvv = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (d == i * 16 + lk * 4 + e) tvv = v[i][e];
+      const bool own = mv && d >= 0 && d < 128 && ((d >> 2) & 3) == lk;
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(tvv), xts, own ? row * 4 : OFF_NONE, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else if constexpr (PERM) {
+    constexpr int ESZ = OUT_F32 ? 4 : 2;
+    const bool res = a.resid != nullptr;
+    const __amdgpu_buffer_rsrc_t ys = rows_rsrc(a.y, ((int64_t)half * a.T + mw) * a.N + nw, a.N, rows, ESZ);
+    const int vy = (int)((lr * a.N + lk * 8) * ESZ);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (nw + q * 32 >= a.N) continue;   // uniform
+        float o[8];
+#pragma unroll
+        for (int f = 0; f < 8; ++f) o[f] = val(2 * q + (f >> 2), j, f & 3);
+        if (res) {
+          const uint32_t t[4] = {tq[j][q].x, tq[j][q].y, tq[j][q].z, tq[j][q].w};
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            o[2 * w] += bf_lo(t[w]);
+            o[2 * w + 1] += bf_hi(t[w]);
+          }
+        }
+        if (EPI == ZOACT_EPI_RELU) {
+#pragma unroll
+          for (int f = 0; f < 8; ++f) o[f] = fmaxf(o[f], 0.0f);
+        }
+        // 8 consecutive features: one 16-byte store (two in fp32); none past N
+        const int vo = pair_off(a, nw, q, lk, vy);
+        const int so = (int)((j * 16 * a.N + q * 32) * ESZ);
+        if (OUT_F32) {
+          __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{__float_as_uint(o[0]), __float_as_uint(o[1]),
+                                                         __float_as_uint(o[2]), __float_as_uint(o[3])},
+                                                 ys, vo, so, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{__float_as_uint(o[4]), __float_as_uint(o[5]),
+                                                         __float_as_uint(o[6]), __float_as_uint(o[7])},
+                                                 ys, vo, so + 16, 0);
+        } else {
+          __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]),
+                                                         pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7])},
+                                                 ys, vo, so, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+    constexpr bool SW = EPI == ZOACT_EPI_SWIGLU;
+    constexpr int ESZ = OUT_F32 ? 4 : 2;
+    const bool res = a.resid != nullptr;
+    const int64_t nout = SW ? a.N / 2 : a.N;
+    const int64_t first = ((int64_t)half * a.T + mw) * nout + (SW ? nw / 2 : nw);
+    const __amdgpu_buffer_rsrc_t ys = rows_rsrc(a.y, first, nout, rows, ESZ);
+    const int vy = (int)((lr * nout + lk * 4) * ESZ);
+    // output block b of token block j: the residual added, one store per lane (none for a
+    // block past N)
+    auto emit = [&](int j, int b, float (&o)[4]) {
+      if (res) {
+        o[0] += bf_lo(tv[j][b].x);
+        o[1] += bf_hi(tv[j][b].x);
+        o[2] += bf_lo(tv[j][b].y);
+        o[3] += bf_hi(tv[j][b].y);
+      }
+      if (EPI == ZOACT_EPI_RELU) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = fmaxf(o[e], 0.0f);
+      }
+      const int so = (int)((j * 16 * nout + b * 16) * ESZ);
+      if (OUT_F32)
+        __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{__float_as_uint(o[0]), __float_as_uint(o[1]),
+                                                       __float_as_uint(o[2]), __float_as_uint(o[3])},
+                                               ys, vy, so, 0);
+      else
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])}, ys, vy,
+                                              so, 0);
+    };
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if constexpr (SW) {
+        // blocks 2q (gate) and 2q + 1 (up) of the 16-interleaved fused projection give
+        // output block q
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (nw + q * 32 >= a.N) continue;   // uniform
+          float o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = silu(val(2 * q, j, e)) * val(2 * q + 1, j, e);
+          emit(j, q, o);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          if (nw + i * 16 >= a.N) continue;   // uniform
+          float o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = val(i, j, e);
+          emit(j, i, o);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+template <int EPI, bool OUT_F32>
+__device__ __forceinline__ void epilogue_regs(const GemmArgs& a, floatx4 (&acc)[8][8], int wave, int lane,
+                                              int64_t m0, int64_t n0, int half, int tm, int tn) {
+  if (a.bias) epilogue_regs_impl<EPI, OUT_F32, true>(a, acc, wave, lane, m0, n0, half, tm, tn);
+  else epilogue_regs_impl<EPI, OUT_F32, false>(a, acc, wave, lane, m0, n0, half, tm, tn);
 }
 
 }  // namespace gemm

@@ -30,7 +30,7 @@ struct GemmArgs {
   const uint16_t* ch;    // precomputed bf16(C + sign_h eps Z), [2][N][r] with half stride ch_stride, or null
   int64_t ch_stride;
   const uint16_t* tgt;   // EPI_MSE: regression target [T][N] (bf16); y is not stored
-  double* part;          // EPI_MSE: per-tile sums of squared errors [2][tiles_m_half * tiles_n]
+  double* part;          // EPI_MSE: sums of squared errors per tile and wave [2][tiles_m_half * tiles_n][4]
   const int32_t* tok;    // EPI_XENT: token ids [T / seq][seq] shared by both halves
   int64_t seq;           // EPI_XENT: sequence length
   float2* xpart;         // EPI_XENT: (max, sum of exp) per row and 128-column block [2 T][xnblk]
@@ -79,7 +79,10 @@ __device__ __forceinline__ uint4 dequant8(uint32_t q, float s) {
 }
 
 
-__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+// g * sigmoid(g) with the hardware reciprocal (1 ulp) in place of an IEEE divide: the
+// result is rounded to bf16 (or carries fp32 GEMM rounding), far coarser than the
+// reciprocal's error.
+__device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 }  // namespace gemm
 }  // namespace zoact

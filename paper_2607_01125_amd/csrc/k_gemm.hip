@@ -674,7 +674,7 @@ hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const 
   hipError_t e = schedule_choice() == 0 ? launch_linear_pm_4w64(a, L.w_dtype, EPI_MSE, false, s) : hipErrorNotSupported;
   if (e == hipErrorNotSupported) e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
   if (e != hipSuccess) return e;
-  return launch_sum_mean(part, (int64_t)a.tiles_m_half * a.tiles_n, (double)T * (double)L.d_out, loss_pm, s);
+  return launch_sum_mean(part, (int64_t)a.tiles_m_half * a.tiles_n * 4, (double)T * (double)L.d_out, loss_pm, s);
 }
 
 size_t linear_xent_ws_bytes(int64_t T, int64_t d_out) {

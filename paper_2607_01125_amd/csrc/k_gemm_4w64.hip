@@ -20,6 +20,10 @@
 //    sub-step, as in the 32-deep schedule, and one workgroup barrier per stage.
 //  * The fifth slot is the 32 KB the 32-deep schedule spends on C_h, so this schedule
 //    reads C_h precomputed (zoact_perturb_coeffs) for the ceil(r/32) correction steps.
+//  * Persistent workgroups (one per CU) walk their tiles back to back with the ring running
+//    on: a tile's last two stages load the next tile's first two, so the next tile needs
+//    no prologue, and the epilogue works from the accumulators without LDS while those
+//    loads land.
 #include "gemm_4w_epi.hpp"
 
 namespace zoact {
@@ -27,6 +31,8 @@ namespace zoact {
 namespace {
 
 using namespace gemm;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int NT = 256;
 constexpr int SLOT_ELEMS = 256 * 64;                 // one operand tile, 64 deep (bf16 elements, 32 KB)
@@ -36,94 +42,106 @@ constexpr int LDS_BYTES = NSLOT * SLOT_ELEMS * 2;    // 160 KB
 // Byte offset of (row, 16-byte chunk c) in a 64-deep operand tile (rows of 128 bytes).
 __device__ __forceinline__ int swz64(int row, int c) { return (row << 7) + ((c ^ (row & 7)) << 4); }
 
-// One 1 KB load: rows row0 .. row0+7 (row0 % 8 == 0), depth k0 .. k0+63 -> LDS at dst.
-// Lane l lands at dst + 16 l, i.e. row l >> 3, LDS chunk l & 7, which holds global
-// chunk (l & 7) ^ (l >> 3).  The per-lane part of the address (`lane_off`, the same for
+// One 1 KB load moves rows row0 .. row0+7 (row0 % 8 == 0), depth k0 .. k0+63 to LDS at
+// dst: lane l lands at dst + 16 l, i.e. row l >> 3, LDS chunk l & 7, which holds global
+// chunk (l & 7) ^ (l >> 3).  The per-lane part of the address (this offset, the same for
 // every load of a wave) goes in the vector offset, the uniform part in the scalar one.
 __device__ __forceinline__ int dma8_lane_off(int64_t ld) {
   const int lane = threadIdx.x & 63;
   return (int)((lane >> 3) * ld * 2 + (((lane & 7) ^ (lane >> 3)) << 4));
 }
-__device__ __forceinline__ void dma8(__amdgpu_buffer_rsrc_t src, int lane_off, int64_t ld, int64_t row0, int64_t k0,
-                                     char* dst) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_void_t*)dst, 16, lane_off, (int)((row0 * ld + k0) * 2), 0, 0);
-}
 
 __device__ __forceinline__ int mod5(int v) { return v >= 5 ? v - 5 : v; }
 
-template <int EPI, bool OUT_F32>
-__global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a) {
-  extern __shared__ __align__(16) uint16_t lds[];
-  char* const lb = reinterpret_cast<char*>(lds);
-
-  // ---- tile assignment (XCD-contiguous runs, grouped token-major order)
-  const int ntiles = gridDim.x;
-  int lin = blockIdx.x;
-  if ((ntiles & 7) == 0) lin = (blockIdx.x & 7) * (ntiles >> 3) + (blockIdx.x >> 3);
+// Token tile, feature tile and half of virtual tile v of ntiles (XCD-contiguous runs,
+// grouped token-major order: a workgroup's tiles v, v + grid, ... stay on its XCD when the
+// grid is a multiple of 8).
+struct TileGeom {
+  int tm, tn, half;
+  int64_t m0, n0;
+};
+__device__ __forceinline__ TileGeom tile_geom(const GemmArgs& a, int ntiles, int v) {
+  int lin = v;
+  if ((ntiles & 7) == 0) lin = (v & 7) * (ntiles >> 3) + (v >> 3);
   const int tiles_m = 2 * a.tiles_m_half;
   const int per_group = 4 * a.tiles_n;
-  const int grp_t = lin / per_group;
-  const int first_m = grp_t * 4;
+  const int first_m = (lin / per_group) * 4;
   const int gsz = min(4, tiles_m - first_m);
-  const int tm = first_m + (lin % per_group) % gsz;
-  const int tn = (lin % per_group) / gsz;
-  const int half = tm / a.tiles_m_half;
-  const int64_t m0 = (int64_t)(tm % a.tiles_m_half) * 256;
-  const int64_t n0 = (int64_t)tn * 256;
-  const uint16_t* xh = a.x + (int64_t)half * a.T * a.K;
-  const uint16_t* w = reinterpret_cast<const uint16_t*>(a.w);
+  TileGeom g;
+  g.tm = first_m + (lin % per_group) % gsz;
+  g.tn = (lin % per_group) / gsz;
+  g.half = g.tm / a.tiles_m_half;
+  g.m0 = (int64_t)(g.tm % a.tiles_m_half) * 256;
+  g.n0 = (int64_t)g.tn * 256;
+  return g;
+}
+
+// Persistent: the grid holds one workgroup per CU and each walks tiles v = blockIdx.x,
+// + gridDim.x, ...  The stage ring runs on across tiles: the last two stages of a tile
+// load the next tile's stages 0 and 1, and its last sub-step reads the next tile's first
+// fragments, so the next tile starts without a prologue while this one finishes (rank
+// correction, epilogue straight from the accumulators, no LDS).
+template <int EPI, bool OUT_F32>
+__global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles) {
+  constexpr bool PERM = epi_perm(EPI);
+  extern __shared__ __align__(16) uint16_t lds[];
+  char* const lb = reinterpret_cast<char*>(lds);
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: kept in SGPRs
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15, lk = lane >> 4;
   const int wn0 = (wave & 1) * 128;   // features of this wave
   const int wm0 = (wave >> 1) * 128;  // tokens of this wave
-  const int NS = (int)(a.K >> 6);     // 64-deep stages
+  const int NS = (int)(a.K >> 6);     // 64-deep stages (at least 2)
+  const uint32_t xbytes = (uint32_t)(a.T * a.K * 2);
 
-  const __amdgpu_buffer_rsrc_t wrs = buffer_rsrc(w, (uint32_t)(a.N * a.K * 2));
-  const __amdgpu_buffer_rsrc_t xrs = buffer_rsrc(xh, (uint32_t)(a.T * a.K * 2));
-  // this wave's 64 rows of one operand of stage st into slot `slot` (8 loads); `i` picks one
+  const __amdgpu_buffer_rsrc_t wrs = buffer_rsrc(a.w, (uint32_t)(a.N * a.K * 2));
   const int loff = dma8_lane_off(a.K);
-  auto dma_w = [&](int st, int slot, int i) {
-    dma8(wrs, loff, a.K, n0 + wave * 64 + i * 8, (int64_t)st * 64,
-         lb + slot * (SLOT_ELEMS * 2) + (wave * 64 + i * 8) * 128);
+  // Load i (rows 8i .. 8i+7) of this wave's 64 rows of one operand into slot `slot`; `base`
+  // is the byte offset of the wave's first row at the stage's depth (see src_base).
+  const int row8_bytes = (int)(a.K * 16);   // 8 rows
+  auto dma = [&](__amdgpu_buffer_rsrc_t rs, int base, int slot, int i) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(lb + slot * (SLOT_ELEMS * 2) + (wave * 64 + i * 8) * 128),
+                                             16, loff, base + i * row8_bytes, 0, 0);
   };
-  auto dma_x = [&](int st, int slot, int i) {
-    dma8(xrs, loff, a.K, m0 + wave * 64 + i * 8, (int64_t)st * 64,
-         lb + slot * (SLOT_ELEMS * 2) + (wave * 64 + i * 8) * 128);
-  };
+  auto src_base = [&](int64_t rows, int64_t k0) -> int { return (int)(((rows + wave * 64) * a.K + k0) * 2); };
 
   floatx4 acc[8][8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
   bf16x8 fa0[8], fb0[8], fa1[8], fb1[8];
 
-  // fragment offsets inside a slot: row (base + i * 16 + lr), chunk 4 h + lk; the swizzle
-  // term depends on lr only, so k-half h has one per-lane offset
+  // fragment offsets inside a slot.  x block j: row (wm0 + j * 16 + lr), chunk 4 kh + lk; the
+  // swizzle term depends on lr only, so k-half kh has one per-lane offset.  W block i: the
+  // same, or with PERM the rows of block pair q = i / 2 interleaved so that the outputs of
+  // lane (lr, lk) in blocks 2q and 2q + 1 are 8 consecutive features: A-row r of block 2q + h
+  // is feature q * 32 + (r / 4) * 8 + h * 4 + r % 4 (row r % 4 + 4 h modulo 8 for the swizzle).
   const int fo0 = swz64(lr, lk), fo1 = swz64(lr, 4 + lk);
+  const int prow = (lr >> 2) * 8 + (lr & 3);
+  const int fw[2][2] = {{PERM ? swz64(prow, lk) : fo0, PERM ? swz64(prow, 4 + lk) : fo1},
+                        {PERM ? swz64(prow + 4, lk) : fo0, PERM ? swz64(prow + 4, 4 + lk) : fo1}};
   auto frag = [&](int slot, int row0, int fo) -> bf16x8 {
     return *reinterpret_cast<const bf16x8*>(lb + slot * (SLOT_ELEMS * 2) + row0 * 128 + fo);
   };
+  // W fragment of block i, k-half kh
+  auto wfrag = [&](int slot, int i, int kh) -> bf16x8 {
+    return frag(slot, PERM ? wn0 + (i >> 1) * 32 : wn0 + i * 16, fw[i & 1][kh]);
+  };
 
   // One 32-deep sub-step: 64 MFMAs on (fa, fb); the next sub-step's 16 fragments (slots
-  // nws / nxs, k-half offset nfo) are read in the first four rows; one load of operand
-  // `dma_x_side ? x : W` of stage dst_st into slot dslot after each row of MFMAs.
-  auto sub_step = [&](bf16x8 (&fa)[8], bf16x8 (&fb)[8], bf16x8 (&na)[8], bf16x8 (&nb)[8], int nws, int nxs, int nfo,
-                      bool dma_x_side, int dst_st, int dslot) {
+  // nws / nxs, k-half nkh) are read in the first four rows; one load of operand
+  // `rs` from byte offset `base` into slot dslot after each row of MFMAs.
+  auto sub_step = [&](bf16x8 (&fa)[8], bf16x8 (&fb)[8], bf16x8 (&na)[8], bf16x8 (&nb)[8], int nws, int nxs, int nkh,
+                      __amdgpu_buffer_rsrc_t rs, int base, int dslot) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-      if (dma_x_side) dma_x(dst_st, dslot, i);
-      else dma_w(dst_st, dslot, i);
+      dma(rs, base, dslot, i);
       if (i < 4) {
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2) {
           const int ii = 2 * i + h2;
-          na[ii] = frag(nws, wn0 + ii * 16, nfo);
-          nb[ii] = frag(nxs, wm0 + ii * 16, nfo);
+          na[ii] = wfrag(nws, ii, nkh);
+          nb[ii] = frag(nxs, wm0 + ii * 16, nkh ? fo1 : fo0);
         }
       }
       // issue order inside the row: each memory instruction right after an MFMA, so its
@@ -144,91 +162,158 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a) {
     }
   };
 
-  // ---- prologue: stages 0 and 1 in flight (slots 0..3), stage 0 landed, fragments of
-  // sub-step 0, then a barrier so that no slot is refilled before every wave has read it
+  int v = blockIdx.x;
+  TileGeom g = tile_geom(a, ntiles, v);
+  __amdgpu_buffer_rsrc_t xrs = buffer_rsrc(a.x + (int64_t)g.half * a.T * a.K, xbytes);
+
+  // ---- prologue of the first tile: stages 0 and 1 in flight (slots 0..3), stage 0
+  // landed in every wave's rows (the barrier)
 #pragma unroll
-  for (int i = 0; i < 8; ++i) dma_w(0, 0, i);
+  for (int i = 0; i < 8; ++i) dma(wrs, src_base(g.n0, 0), 0, i);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) dma_x(0, 1, i);
+  for (int i = 0; i < 8; ++i) dma(xrs, src_base(g.m0, 0), 1, i);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) dma_w(1, 2, i);
+  for (int i = 0; i < 8; ++i) dma(wrs, src_base(g.n0, 64), 2, i);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) dma_x(1, 3, i);
+  for (int i = 0; i < 8; ++i) dma(xrs, src_base(g.m0, 64), 3, i);
   __builtin_amdgcn_s_waitcnt(WAIT_VM16);
   barrier();
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    fa0[i] = frag(0, wn0 + i * 16, fo0);
-    fb0[i] = frag(1, wm0 + i * 16, fo0);
-  }
-  __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
-  barrier();
 
-  // ---- main loop: one stage (two sub-steps) per iteration.  s5 = 2S mod 5: stage S has
-  // W in slot s5 and x in s5 + 1, stage S + 1 in s5 + 2 / s5 + 3, and stage S + 2 goes to
-  // s5 + 4 (W, during sub-step 2S) and s5 (x, during 2S + 1).  Loads past the last stage
-  // read the next rows or zeros into slots nobody reads again; the epilogue waits for them.
-  // (The second sub-step sits under a test that always holds: written this way the
-  // register allocator keeps every accumulator in place across the loop.)
+  // s5 = 2S mod 5 over the whole sequence of stages (tiles back to back): stage S has W in
+  // slot s5 and x in s5 + 1, stage S + 1 in s5 + 2 / s5 + 3, and stage S + 2 goes to
+  // s5 + 4 (W, during sub-step 2S) and s5 (x, during 2S + 1).
   int s5 = 0;
-  const int nsub = 2 * NS;
-  for (int j = 0; j < nsub; j += 2) {
-    const int st = j >> 1;
-    const int sw1 = mod5(s5 + 2), sx1 = mod5(s5 + 3), sw2 = mod5(s5 + 4);
-    // sub-step 2S: k-half 0 of stage S; reads k-half 1 of stage S; loads W of stage S + 2
-    sub_step(fa0, fb0, fa1, fb1, s5, mod5(s5 + 1), fo1, false, st + 2, sw2);
-    // stage S + 1 (issued during sub-steps 2S - 2 and 2S - 1) must have landed: the
-    // eight loads of this sub-step may stay in flight
-    __builtin_amdgcn_s_waitcnt(WAIT_VM8);
+  for (;;) {
+    // fragments of the tile's first sub-step: stage 0 has landed (the prologue's barrier,
+    // or the previous tile's barrier after its second-last sub-step) and its slots are
+    // not refilled before sub-step 1.  (The previous tile's last sub-step read them too;
+    // reading them again here keeps those registers free through its epilogue.)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      fa0[i] = wfrag(s5, i, 0);
+      fb0[i] = frag(mod5(s5 + 1), wm0 + i * 16, fo0);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // nothing from LDS in flight when the main loop starts (as at the end of each of its
+    // iterations), so the compiler places no LDS waits inside it
     __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
-    barrier();
-    if (j + 1 < nsub) {
-      // sub-step 2S + 1: k-half 1 of stage S; reads k-half 0 of stage S + 1; loads x of S + 2.
-      // No barrier after it: sub-step 2S + 2 reads stage S + 1 (complete since the barrier
-      // above) and loads into stage S's x slot (last read during 2S), so nothing it touches
-      // can still be in use by a slower wave.
-      sub_step(fa1, fb1, fa0, fb0, sw1, sx1, fo0, true, st + 2, s5);
+    const int vn = v + (int)gridDim.x;
+    const bool has_next = vn < ntiles;
+    const TileGeom gn = tile_geom(a, ntiles, has_next ? vn : v);
+    const __amdgpu_buffer_rsrc_t xrs_n = buffer_rsrc(a.x + (int64_t)gn.half * a.T * a.K, xbytes);
+
+    // ---- main loop: one stage (two sub-steps) per iteration.  Stages S + 2 past this
+    // tile's end are the next tile's stages 0 and 1; after the last tile they re-read the
+    // rows past the end (or zeros) into slots nobody reads again.
+    // (The second sub-step sits under a test that always holds: written this way the
+    // register allocator keeps every accumulator in place across the loop.)
+    const int nsub = 2 * NS;
+    for (int j = 0; j < nsub; j += 2) {
+      const int st = j >> 1;
+      const bool nx = has_next && st + 2 >= NS;
+      const int64_t kd = (int64_t)(nx ? st + 2 - NS : st + 2) * 64;
+      const int wb = src_base(nx ? gn.n0 : g.n0, kd), xb = src_base(nx ? gn.m0 : g.m0, kd);
+      const __amdgpu_buffer_rsrc_t xr = nx ? xrs_n : xrs;
+      const int sw1 = mod5(s5 + 2), sx1 = mod5(s5 + 3), sw2 = mod5(s5 + 4);
+      // sub-step 2S: k-half 0 of stage S; reads k-half 1 of stage S; loads W of stage S + 2
+      sub_step(fa0, fb0, fa1, fb1, s5, mod5(s5 + 1), 1, wrs, wb, sw2);
+      // stage S + 1 (issued during sub-steps 2S - 2 and 2S - 1) must have landed: the
+      // eight loads of this sub-step may stay in flight
+      __builtin_amdgcn_s_waitcnt(WAIT_VM8);
       __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    s5 = sw1;
-  }
-
-  // ---- rank-r correction: [p[h] | C_h] as ceil(r/32) extra 32-deep steps, operands from
-  // global memory (C_h precomputed); ranks not a multiple of 8 are gathered element-wise
-  if (a.r > 0) {
-    const int kts = (a.r + 31) >> 5;
-    const uint16_t* ph = a.p + (int64_t)half * a.T * a.r;
-    const uint16_t* chh = a.ch + (int64_t)half * a.ch_stride;
-    const bool vec = (a.r & 7) == 0;
-    const bf16x8 zero8 = {};
-    auto row8 = [&](const uint16_t* rowp, int col) -> bf16x8 {
-      if (vec) return col < a.r ? *reinterpret_cast<const bf16x8*>(rowp + col) : zero8;
-      uint16_t e[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) e[q] = col + q < a.r ? rowp[col + q] : (uint16_t)0;
-      const uint4 u = make_uint4(pack2(e[0], e[1]), pack2(e[2], e[3]), pack2(e[4], e[5]), pack2(e[6], e[7]));
-      return __builtin_bit_cast(bf16x8, u);
-    };
-    for (int t = 0; t < kts; ++t) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        int64_t m = m0 + wm0 + j * 16 + lr;
-        m = m > a.T - 1 ? a.T - 1 : m;
-        int64_t n = n0 + wn0 + j * 16 + lr;
-        n = n > a.N - 1 ? a.N - 1 : n;
-        const int col = t * 32 + lk * 8;
-        fb0[j] = row8(ph + m * a.r, col);
-        fa0[j] = row8(chh + n * a.r, col);
+      barrier();
+      if (j + 1 < nsub) {
+        // sub-step 2S + 1: k-half 1 of stage S; reads k-half 0 of stage S + 1 (the next
+        // tile's stage 0 after the last stage); loads x of S + 2.  No barrier after it:
+        // sub-step 2S + 2 reads stage S + 1 (complete since the barrier above) and loads
+        // into stage S's x slot (last read during 2S), so nothing it touches can still be
+        // in use by a slower wave.
+        sub_step(fa1, fb1, fa0, fb0, sw1, sx1, 0, xr, xb, s5);
+        __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
+        __builtin_amdgcn_sched_barrier(0);
       }
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa0[i], fb0[j], acc[i][j], 0, 0, 0);
+      s5 = sw1;
     }
-  }
 
-  epilogue_4w<EPI, OUT_F32>(a, acc, lds, wave, lane, m0, n0, half, tm, tn);
+    // ---- rank-r correction: [p[h] | C_h] as ceil(r/32) extra 32-deep steps, operands from
+    // global memory (C_h precomputed) through buffer loads: rows past T or N read zeros
+    // (their outputs are not stored), columns past r are zeroed, element-wise when r is
+    // not a multiple of 8.
+    if (a.r > 0) {
+      const int kts = (a.r + 31) >> 5;
+      const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(a.p + (int64_t)g.half * a.T * a.r, (uint32_t)(a.T * a.r * 2));
+      const __amdgpu_buffer_rsrc_t crs = buffer_rsrc(a.ch + (int64_t)g.half * a.ch_stride, (uint32_t)(a.N * a.r * 2));
+      const bool vec = (a.r & 7) == 0;
+      const int pvo = ((wm0 + lr) * a.r + lk * 8) * 2, cvo = ((wn0 + (PERM ? prow : lr)) * a.r + lk * 8) * 2;
+      // C_h rows of W block i (the permuted order with PERM): first row's byte offset
+      auto crow = [&](int i) -> int {
+        return (int)((g.n0 + (PERM ? (i >> 1) * 32 + (i & 1) * 4 : i * 16)) * a.r * 2);
+      };
+      for (int t = 0; t < kts; ++t) {
+        const int col = t * 32 + lk * 8;
+        // every load issued before any result is used (one wait), then columns past r zeroed
+        if (vec) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            fb1[j] = __builtin_bit_cast(
+                bf16x8, __builtin_amdgcn_raw_buffer_load_b128(prs, pvo, (int)((g.m0 + j * 16) * a.r * 2) + t * 64, 0));
+            fa1[j] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(crs, cvo, crow(j) + t * 64, 0));
+          }
+          if (col >= a.r) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) fb1[j] = fa1[j] = bf16x8{};
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            uint16_t ep[8], ec[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              ep[q] = __builtin_amdgcn_raw_buffer_load_b16(prs, pvo, (int)((g.m0 + j * 16) * a.r * 2) + t * 64 + 2 * q, 0);
+              ec[q] = __builtin_amdgcn_raw_buffer_load_b16(crs, cvo, crow(j) + t * 64 + 2 * q, 0);
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+              if (col + q >= a.r) ep[q] = ec[q] = 0;
+            fb1[j] = __builtin_bit_cast(bf16x8, make_uint4(pack2(ep[0], ep[1]), pack2(ep[2], ep[3]), pack2(ep[4], ep[5]),
+                                                           pack2(ep[6], ep[7])));
+            fa1[j] = __builtin_bit_cast(bf16x8, make_uint4(pack2(ec[0], ec[1]), pack2(ec[2], ec[3]), pack2(ec[4], ec[5]),
+                                                           pack2(ec[6], ec[7])));
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa1[i], fb1[j], acc[i][j], 0, 0, 0);
+      }
+    }
+
+    epilogue_regs<EPI, OUT_F32>(a, acc, wave, lane, g.m0, g.n0, g.half, g.tm, g.tn);
+    if (!has_next) break;
+    v = vn;
+    g = gn;
+    xrs = xrs_n;
+  }
+  // the loads past the last stage must land before the workgroup ends
+  __builtin_amdgcn_s_waitcnt(WAIT_VM0);
+}
+
+// Compute units of the current device (cached per device; every caller stores the same
+// value, so concurrent first calls are harmless).  -1 on error.
+int cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return -1;
+  static int cache[64] = {};
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return -1;
+    cache[dev] = n;
+  }
+  return cache[dev];
 }
 
 template <int EPI, bool OUT_F32>
@@ -240,21 +325,26 @@ hipError_t launch_4w64(const GemmArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  const dim3 grid((unsigned)(2 * a.tiles_m_half * a.tiles_n));
-  gemm_4w64_kernel<EPI, OUT_F32><<<grid, dim3(NT), LDS_BYTES, s>>>(a);
+  const int ntiles = 2 * a.tiles_m_half * a.tiles_n;
+  const int ncu = cu_count();
+  if (ncu <= 0) return hipErrorInvalidDevice;
+  const unsigned grid = (unsigned)(ntiles < ncu ? ntiles : ncu);
+  gemm_4w64_kernel<EPI, OUT_F32><<<dim3(grid), dim3(NT), LDS_BYTES, s>>>(a, ntiles);
   return hipGetLastError();
 }
 
 }  // namespace
 
 // Returns hipErrorNotSupported outside this schedule's coverage: bf16 weights; C_h
-// precomputed (or r = 0), r <= 256; depth a multiple of 64; a half of x or the weights
-// below 2 GiB.
+// precomputed (or r = 0), r <= 256; depth a multiple of 64, at least 128; a half of x,
+// of p or of C_h, the weights, and the cross entropy's block partials, below 2 GiB.
 hipError_t launch_linear_pm_4w64(const GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s) {
   if (w_dtype != ZOACT_BF16) return hipErrorNotSupported;
   if (a.r > 0 && a.ch == nullptr) return hipErrorNotSupported;
-  if (a.r > 256 || (a.K % 64) != 0) return hipErrorNotSupported;
+  if (a.r > 256 || (a.K % 64) != 0 || a.K < 128) return hipErrorNotSupported;
   if (a.T * a.K * 2 >= (int64_t(1) << 31) || a.N * a.K * 2 >= (int64_t(1) << 31)) return hipErrorNotSupported;
+  if (a.T * a.r * 2 >= (int64_t(1) << 31) || a.N * a.r * 2 >= (int64_t(1) << 31)) return hipErrorNotSupported;
+  if (epi == EPI_XENT && 2 * a.T * (int64_t)a.xnblk * 8 >= (int64_t(1) << 31)) return hipErrorNotSupported;
 #define ZO_4W64(EP, OF) \
   if (epi == EP && out_f32 == OF) return launch_4w64<EP, OF>(a, s);
   ZO_4W64(0, false)

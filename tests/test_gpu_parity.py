@@ -468,6 +468,19 @@ def test_single_layer_4096_sampled():
     ws = torch.empty(Z.linear_mse_workspace_bytes(T, N), dtype=torch.uint8, device=dev())
     Z.linear_mse(layer, arena, xt, T, p, Z.Pert(seed, step, 0, eps), tgt, fused, ws)
     np.testing.assert_allclose(host(fused), host(lpm), rtol=2e-6)
+    # and with the coefficients precomputed: the 64-deep persistent schedule (1024 tiles,
+    # four per workgroup), stored and fused, in the launch configuration the benchmark times
+    ch = torch.empty(2 * N * r, dtype=torch.bfloat16, device=dev())
+    Z.perturb_coeffs(arena, 0, N * r, Z.Pert(seed, step, 0, eps), ch)
+    layer.ch, layer.ch_stride = ch, N * r
+    y2 = torch.empty_like(y)
+    Z.linear_fwd_pm(layer, arena, xt, T, p, y2, Z.Pert(seed, step, 0, eps))
+    assert_bf16_close(host(y2).reshape(2, T, N)[:, rows], ref, what="single layer sampled, 64-deep")
+    fused2 = torch.full((2,), float("nan"), dtype=torch.float32, device=dev())
+    Z.linear_mse(layer, arena, xt, T, p, Z.Pert(seed, step, 0, eps), tgt, fused2, ws)
+    lpm2 = torch.zeros(2, dtype=torch.float32, device=dev())
+    Z.mse_pm(y2, tgt, lpm2, torch.empty(Z.loss_workspace_bytes(), dtype=torch.uint8, device=dev()))
+    np.testing.assert_allclose(host(fused2), host(lpm2), rtol=2e-6)
 
 
 # ------------------------------------------------------------------ fused regression loss
@@ -533,3 +546,81 @@ def test_linear_mse_fused(T, K, N, r, mode):
                         for h in range(2)]).astype(np.float64)
     want = [oloss.mse(ref[h], tgt_np) for h in range(2)]
     assert_rel_close(host(fused), want, 1e-3, "fused mse vs oracle")
+
+
+# ------------------------------------------------------------------ more tiles than workgroups
+@pytest.mark.parametrize("T,K,N,r,flags,out_f32", [
+    (2050, 128, 4112, 32, 0, False),              # 306 tiles, two stages per tile
+    (4100, 192, 4112, 8, Z.EPI_RELU, False),      # 578 tiles, ragged tokens and features
+    (2050, 256, 4128, 16, Z.EPI_SWIGLU, False),   # last feature tile: one gate|up group
+    (2050, 128, 4112, 0, 0, True),                # plain layer, fp32 out
+])
+def test_linear_pm_persistent_tiles(T, K, N, r, flags, out_f32):
+    """More 256 x 256 tiles than the GPU has CUs: each workgroup of the 64-deep schedule
+    walks several tiles with its stage ring running from one tile into the next.  Bias and
+    residual on, against the oracle element by element."""
+    announce("linear_pm persistent", T, K, N, r, flags, out_f32)
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=T + K + N)
+    nout = N // 2 if flags & Z.EPI_SWIGLU else N
+    resid = None if out_f32 else synth.bf16_round(synth.normal((2, T, nout), 0.5, 12, T))
+    c = synth.normal((N * max(r, 1),), 0.02, 12, 1)
+    eps, seed, step = 1e-2, 17, 3
+    got = _run_gpu_linear(x, w, b, ut, c, 0, r, eps, seed, step, T, K, N, flags=flags, resid=resid,
+                          out_f32=out_f32, precomputed=r > 0)
+    if r:
+        ref = _oracle_linear(x, w, b, ut, c.reshape(N, r), 0, r, eps, seed, step, flags=flags, resid=resid)
+        assert_bf16_close(got, ref, atol_rel_rms=2e-3, what="persistent tiles")
+    else:
+        ref = np.stack([x[h].astype(np.float64) @ w.astype(np.float64).T + b for h in range(2)])
+        assert np.max(np.abs(got - ref)) <= 1e-5 * np.sqrt(np.mean(ref**2)) * 10
+
+
+def test_linear_mse_fused_persistent_tiles():
+    """The fused regression loss over 578 tiles (ragged both ways) with the precomputed
+    coefficients: equal to the stored-output path up to summation order, and to the
+    oracle's MSE within the bf16 bar."""
+    T, K, N, r = 4100, 192, 4112, 32
+    announce("linear mse persistent", T, K, N, r)
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=7)
+    c = synth.normal((N * r,), 0.02, 7, 7)
+    eps, seed, step = 1e-3, 8, 2
+    xt = t_bf16(x.reshape(2 * T, K))
+    p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev())
+    Z.project(xt, t_bf16(ut), p)
+    layer = Z.Linear(t_bf16(w), K, N, r, t_bf16(ut), 0, t_bf16(b))
+    arena = Z.Arena(t_f32(c), torch.zeros(c.size, device=dev()), torch.zeros(c.size, device=dev()))
+    pert = Z.Pert(seed, step, 0, eps)
+    ch = torch.empty(2 * N * r, dtype=torch.bfloat16, device=dev())
+    Z.perturb_coeffs(arena, 0, N * r, pert, ch)
+    layer.ch, layer.ch_stride = ch, N * r
+    tgt_np = synth.bf16_round(synth.normal((T, N), 1.0, 7, 8))
+    tgt = t_bf16(tgt_np)
+    y = torch.empty(2 * T, N, dtype=torch.bfloat16, device=dev())
+    Z.linear_fwd_pm(layer, arena, xt, T, p, y, pert)
+    lpm = torch.zeros(2, dtype=torch.float32, device=dev())
+    Z.mse_pm(y, tgt, lpm, torch.empty(Z.loss_workspace_bytes(), dtype=torch.uint8, device=dev()))
+    fused = torch.full((2,), float("nan"), dtype=torch.float32, device=dev())
+    ws = torch.empty(Z.linear_mse_workspace_bytes(T, N), dtype=torch.uint8, device=dev())
+    Z.linear_mse(layer, arena, xt, T, p, pert, tgt, fused, ws)
+    np.testing.assert_allclose(host(fused), host(lpm), rtol=2e-6)
+    ref = _oracle_linear(x, w, b, ut, c.reshape(N, r), 0, r, eps, seed, step)
+    assert_rel_close(host(fused), [oloss.mse(ref[h], tgt_np) for h in range(2)], 1e-3, "persistent mse vs oracle")
+
+
+@pytest.mark.parametrize("B,S,K,V", [(8, 130, 256, 8000), (3, 7, 128, 50272)])
+def test_linear_xent_fused_vs_oracle(B, S, K, V):
+    """The LM head with the cross entropy in its epilogue against the oracle's next-token
+    cross entropy of the float64 logits: 320 tiles with a ragged last vocabulary tile, and
+    a short batch over the OPT vocabulary (197 feature tiles, 50272 = 196 x 256 + 96)."""
+    announce("linear xent fused", B, S, K, V)
+    T = B * S
+    x, w, b, _, _, _ = _layer_inputs(T, K, V, 0, seed=B + S + V, bias=False)
+    tok = synth.uniform_tokens(B, S, V, 5, B)
+    layer = Z.Linear(t_bf16(w), K, V, 0, None, 0)
+    loss = torch.full((2,), float("nan"), dtype=torch.float32, device=dev())
+    ws = torch.empty(Z.linear_xent_workspace_bytes(T, V), dtype=torch.uint8, device=dev())
+    Z.linear_xent(layer, None, t_bf16(x.reshape(2 * T, K)), t_i32(tok), None, Z.Pert(1, 1, 0, 0.0), loss, ws)
+    want = [oloss.next_token_ce((x[h].astype(np.float64) @ w.astype(np.float64).T).reshape(B, S, V), tok)
+            for h in range(2)]
+    # fp32 logits (summation order) and fp32 exp/log in the per-block partials
+    assert_rel_close(host(loss), want, 1e-5, "fused xent vs oracle")
