@@ -347,23 +347,32 @@ __device__ __forceinline__ void epi_prefetch8(const GemmArgs& a, const uint16_t*
     }
 }
 
+// EPI_MSE: the regression target's rows, requested before the rank correction so that
+// their latency overlaps it.  (A residual is requested in the epilogue: beside the
+// correction's operands it would not fit in registers with the stores' working set.)
+template <int EPI>
+__device__ __forceinline__ void epi_rows_early(const GemmArgs& a, uint4 (&tq)[8][4], int wave, int lane, int64_t m0,
+                                               int64_t n0) {
+  if constexpr (EPI == EPI_MSE) epi_prefetch8(a, a.tgt, a.N, tq, wave, lane, m0, n0, 0);
+}
+
 template <int EPI, bool OUT_F32, bool BIAS>
-__device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&acc)[8][8], int wave, int lane,
-                                                   int64_t m0, int64_t n0, int half, int tm, int tn) {
+__device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&acc)[8][8], uint4 (&tq)[8][4],
+                                                   int wave, int lane, int64_t m0, int64_t n0, int half, int tm,
+                                                   int tn) {
   const int lr = lane & 15, lk = lane >> 4;
   const int64_t nw = n0 + (wave & 1) * 128;   // first feature of this wave
   const int64_t mw = m0 + (wave >> 1) * 128;  // first token of this wave
   const int rows = wave_rows(a, mw);
   constexpr bool PERM = epi_perm(EPI);
-  // the rows this epilogue reads (regression target or residual), all requested up front:
-  // in the interleaved order 16 bytes per lane and block pair, else 8 per block
-  uint4 tq[8][4];
+  // the rows this epilogue reads: in the interleaved order 16 bytes per lane and block pair
+  // (the regression target was requested before the rank correction, a residual is now),
+  // else 8 bytes per block
   uint2 tv[8][8];
-  if constexpr (EPI == EPI_MSE) {
-    epi_prefetch8(a, a.tgt, a.N, tq, wave, lane, m0, n0, 0);
-  } else if constexpr (PERM) {
-    if (a.resid) epi_prefetch8(a, a.resid, a.N, tq, wave, lane, m0, n0, half);
-  } else {
+  uint4 tr[8][4];   // a residual in the interleaved order
+  if constexpr (PERM && EPI != EPI_MSE) {
+    if (a.resid) epi_prefetch8(a, a.resid, a.N, tr, wave, lane, m0, n0, half);
+  } else if constexpr (!PERM) {
     epi_prefetch<EPI, 0>(a, tv, wave, lane, m0, n0, half);
     epi_prefetch<EPI, 4>(a, tv, wave, lane, m0, n0, half);
   }
@@ -493,7 +502,7 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
 #pragma unroll
         for (int f = 0; f < 8; ++f) o[f] = val(2 * q + (f >> 2), j, f & 3);
         if (res) {
-          const uint32_t t[4] = {tq[j][q].x, tq[j][q].y, tq[j][q].z, tq[j][q].w};
+          const uint32_t t[4] = {tr[j][q].x, tr[j][q].y, tr[j][q].z, tr[j][q].w};
 #pragma unroll
           for (int w = 0; w < 4; ++w) {
             o[2 * w] += bf_lo(t[w]);
@@ -581,10 +590,10 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
 }
 
 template <int EPI, bool OUT_F32>
-__device__ __forceinline__ void epilogue_regs(const GemmArgs& a, floatx4 (&acc)[8][8], int wave, int lane,
-                                              int64_t m0, int64_t n0, int half, int tm, int tn) {
-  if (a.bias) epilogue_regs_impl<EPI, OUT_F32, true>(a, acc, wave, lane, m0, n0, half, tm, tn);
-  else epilogue_regs_impl<EPI, OUT_F32, false>(a, acc, wave, lane, m0, n0, half, tm, tn);
+__device__ __forceinline__ void epilogue_regs(const GemmArgs& a, floatx4 (&acc)[8][8], uint4 (&tq)[8][4], int wave,
+                                              int lane, int64_t m0, int64_t n0, int half, int tm, int tn) {
+  if (a.bias) epilogue_regs_impl<EPI, OUT_F32, true>(a, acc, tq, wave, lane, m0, n0, half, tm, tn);
+  else epilogue_regs_impl<EPI, OUT_F32, false>(a, acc, tq, wave, lane, m0, n0, half, tm, tn);
 }
 
 }  // namespace gemm

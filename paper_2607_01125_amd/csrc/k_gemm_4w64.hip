@@ -238,6 +238,10 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
       s5 = sw1;
     }
 
+    // EPI_MSE: the target rows, requested now so that their latency overlaps the correction's
+    uint4 tq[8][4];
+    epi_rows_early<EPI>(a, tq, wave, lane, g.m0, g.n0);
+
     // ---- rank-r correction: [p[h] | C_h] as ceil(r/32) extra 32-deep steps, operands from
     // global memory (C_h precomputed) through buffer loads: rows past T or N read zeros
     // (their outputs are not stored), columns past r are zeroed, element-wise when r is
@@ -292,7 +296,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
       }
     }
 
-    epilogue_regs<EPI, OUT_F32>(a, acc, wave, lane, g.m0, g.n0, g.half, g.tm, g.tn);
+    epilogue_regs<EPI, OUT_F32>(a, acc, tq, wave, lane, g.m0, g.n0, g.half, g.tm, g.tn);
     if (!has_next) break;
     v = vn;
     g = gn;
