@@ -233,8 +233,8 @@ size_t zoact_loss_workspace_bytes(void);
  * storing y.  The sum of squares runs in the GEMM's epilogue (fp32 per lane, fp64
  * per wave: four partial sums per 256 x 256 tile) and a fixed-order fp64 sum over them;
  * it differs from zoact_linear_fwd_pair + zoact_mse_pm by summation order only.  BF16
- * activations,
- * bf16 target [T][d_out] (16-byte aligned); BF16 or INT4 weights (INT4 with L->ch).
+ * activations, bf16 target [T][d_out] (16-byte aligned); BF16 or INT4 weights (INT4
+ * with L->ch).
  * ws: at least zoact_linear_mse_workspace_bytes(T, d_out) bytes (16-byte aligned).
  * Errors: shapes the fused kernel does not cover -> ZOACT_E_UNSUPPORTED. */
 /* Fused LM head and next-token cross entropy: the linear of both halves (as
