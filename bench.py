@@ -121,7 +121,10 @@ def bench_single_linear(args, dev):
     eps, lr, seed = 1e-3, 1e-4, 1
     x, q = synth.planted_lowrank(T, K, seed=0)
     xb = torch.from_numpy(synth.bf16_round(x)).to(dev).to(torch.bfloat16)
-    x_pm = torch.cat([xb, xb], dim=0).contiguous()                 # [2][T][K], halves share x here
+    # both halves read this x: the step forms x W^T and P = x U once and each half adds its
+    # own rank-r correction (ZOACT_SHARED_X, the same bits as giving x twice); the stacked
+    # form [2][T][K] is timed beside it for reference
+    x_pm = torch.cat([xb, xb], dim=0).contiguous()
     w = torch.from_numpy(synth.bf16_round(synth.normal((N, K), 0.02, 0, 2))).to(dev).to(torch.bfloat16)
     # in-subspace teacher: Y = x (W + C* Q_r^T)^T, C* ~ N(0, 0.05^2), planted directions Q_r
     cstar = torch.from_numpy(synth.normal((N, r), 0.05, 0, 4)).to(dev)
@@ -143,7 +146,8 @@ def bench_single_linear(args, dev):
     c = torch.zeros(N * r, dtype=torch.float32, device=dev)
     arena = Z.Arena(c, torch.zeros_like(c), torch.zeros_like(c))
     layer = Z.Linear(w, K, N, r, ut, 0)
-    p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev)
+    p = torch.empty(T, r, dtype=torch.bfloat16, device=dev)
+    p_pm = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev)
     loss = torch.zeros(2, dtype=torch.float32, device=dev)
     ws_l = torch.empty(Z.linear_mse_workspace_bytes(T, N), dtype=torch.uint8, device=dev)
     status = torch.zeros(1, dtype=torch.int32, device=dev)
@@ -152,47 +156,66 @@ def bench_single_linear(args, dev):
     ch = torch.empty(2 * N * r, dtype=torch.bfloat16, device=dev)
     layer.ch, layer.ch_stride = ch, N * r
 
-    def zo_step(t, ev=None):
+    def zo_step(t, ev=None, shared=True):
         pert = Z.Pert(seed, t, 0, eps)
         Z.perturb_coeffs(arena, 0, N * r, pert, ch)
-        Z.project(x_pm, ut, p)
+        if shared:
+            Z.project(xb, ut, p)
+        else:
+            Z.project(x_pm, ut, p_pm)
         if ev is not None:
             ev[0].record(stream)
         # both halves' forward with the regression loss summed in the GEMM epilogue (y is
         # never stored), then the fixed-order sum of the per-tile partials
-        Z.linear_mse(layer, arena, x_pm, T, p, pert, tgt, loss, ws_l)
+        if shared:
+            Z.linear_mse(layer, arena, xb, T, p, pert, tgt, loss, ws_l, flags=Z.SHARED_X)
+        else:
+            Z.linear_mse(layer, arena, x_pm, T, p_pm, pert, tgt, loss, ws_l)
         if ev is not None:
             ev[1].record(stream)
         Z.step(arena, loss, pert, Z.adam_desc(lr, t), status)
 
+    def timed(t0, n, shared):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for i in range(n):
+            zo_step(t0 + i, evs[i], shared)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / n, sum(a.elapsed_time(b) for a, b in evs) / n
+
     for t in range(1, args.warmup + 1):
         zo_step(t)
     torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(args.steps):
-        zo_step(args.warmup + 1 + i, evs[i])
-    stop.record(stream)
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(stop)
-    gemm_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
-    ms_per_step = total_ms / args.steps
-    flops = 2 * (2 * T) * N * K + 2 * (2 * T) * K * r + 2 * (2 * T) * r * N   # base + projection + correction
-    gemm_flops = 2 * (2 * T) * N * K + 2 * (2 * T) * r * N
+    ms_per_step, gemm_ms = timed(args.warmup + 1, args.steps, True)
+    losses = [float(v) for v in loss.cpu().numpy()]
+    # the stacked form (x given twice, base formed per half), same steps continued
+    t_next = args.warmup + 1 + args.steps
+    zo_step(t_next, shared=False)
+    st_steps = max(args.steps // 2, 5)
+    st_ms, st_gemm_ms = timed(t_next + 1, st_steps, False)
+    flops = 2 * T * N * K + 2 * T * K * r + 2 * (2 * T) * r * N      # base once + projection once + two corrections
+    gemm_flops = 2 * T * N * K + 2 * (2 * T) * r * N
+    st_gemm_flops = 2 * (2 * T) * N * K + 2 * (2 * T) * r * N
     achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
     assert int(status.item()) == 0, "non-finite projected gradient"
     return {
         "ms_per_step": ms_per_step, "init_ms": init_ms, "flops": flops,
-        "roofline": {"kernel": f"{DOMINANT_KERNEL} (fused ± adapted GEMM with the MSE epilogue, M=16384, "
-                               f"N=K=4096, r=32; timed with the tile-sum kernel that follows it)",
+        "roofline": {"kernel": f"{DOMINANT_KERNEL} (fused ± adapted GEMM, shared input, MSE epilogue: "
+                               f"M=8192 base rows, N=K=4096, r=32 per half; timed with the tile-sum kernel "
+                               f"that follows it)",
                      "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic_record(DOMINANT_KERNEL, "single_linear_4096", DOMINANT_SOURCES),
                      "flops_per_launch": gemm_flops, "mean_launch_us": round(gemm_ms * 1e3, 1)},
-        "losses": [float(v) for v in loss.cpu().numpy()],
-        "config": {"tokens_per_half": T, "d_in": K, "d_out": N, "rank": r, "eps": eps},
+        "stacked_form": {"steps_per_s": round(1e3 / st_ms, 3), "ms_per_step": round(st_ms, 4),
+                         "gemm_us": round(st_gemm_ms * 1e3, 1),
+                         "gemm_tflops": round(st_gemm_flops / (st_gemm_ms * 1e-3) / 1e12, 1),
+                         "note": "x given for both halves (M=16384 stacked rows)"},
+        "losses": losses,
+        "config": {"tokens_per_half": T, "d_in": K, "d_out": N, "rank": r, "eps": eps, "shared_x": True},
     }
 
 
@@ -471,14 +494,17 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (planted low-rank activations, random-init W, seeded)",
         "config": {"workload": "single adapted linear, bf16, d_in=d_out=4096, r=32, 8192 tokens per ± half "
-                               "(C±εZ pass + projection + fused ± forward with the MSE in its epilogue + ZO-Adam)",
+                               "(C±εZ pass + projection + fused ± forward with the MSE in its epilogue + ZO-Adam; "
+                               "both halves read the same x, so x W^T and x U are formed once)",
                    **head["config"], "parallelism": "single GPU"},
         "adapted_linear_tflops": round(head["flops"] / (ms * 1e-3) / 1e12, 1),
         "basis_init_ms": round(head["init_ms"], 1),
         "roofline": head["roofline"],
+        "stacked_form": head["stacked_form"],
         "losses": head["losses"],
     }
-    log(f"headline: {out['value']} steps/s, fused GEMM {head['roofline']['achieved']} TFLOP/s")
+    log(f"headline: {out['value']} steps/s, fused GEMM {head['roofline']['achieved']} TFLOP/s "
+        f"(stacked form {head['stacked_form']['steps_per_s']} steps/s)")
     if not args.quick:
         if not args.no_shapes:
             out["adapted_linear_8b_shapes"] = bench_linear_shapes(dev)

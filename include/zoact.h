@@ -70,7 +70,15 @@ enum {
                                  16j..16j+15 and rows 32j+16..32j+31 the matching
                                  up features; output y[t][f] = silu(gate)*up,
                                  width d_out/2                                    */
-  ZOACT_EPI_RELU = 1u << 1    /* y = max(0, .) before the store                   */
+  ZOACT_EPI_RELU = 1u << 1,   /* y = max(0, .) before the store                   */
+  ZOACT_SHARED_X = 1u << 2    /* both halves read the same input: x [T][d_in] and
+                                 p [T][r] hold one copy; the base x W^T is formed
+                                 once and each half adds its own rank-r correction
+                                 to it (the same operations in the same order as
+                                 with the input given twice, so the outputs are
+                                 the same bits).  BF16 weights with L->ch (or
+                                 r == 0), d_in % 64 == 0 and >= 128; not with
+                                 ZOACT_EPI_SWIGLU.  Else ZOACT_E_UNSUPPORTED.      */
 };
 
 typedef void* zoact_stream; /* hipStream_t */
@@ -170,7 +178,8 @@ zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t 
 /* ------------------------------------------------------ fused +/- adapted linear
  * Section 3's perturbed forward evaluated for both signs in one pass over W:
  *   y[h] = epilogue(residual[h] + x[h] W^T + b + p[h] (C + s_h eps Z)^T),  s = (+1, -1)
- * x [2][T][d_in] and p [2][T][r] (from zoact_project on x) in the activation
+ * x [2][T][d_in] and p [2][T][r] (from zoact_project on x; one copy of each,
+ * [T][d_in] and [T][r], with ZOACT_SHARED_X) in the activation
  * dtype x_dtype (BF16 with BF16 or INT4 weights; F32 with F32 weights);
  * residual NULL or [2][T][d_out] in y's layout; y [2][T][d_out'] in y_dtype
  * (x_dtype, or F32 for logits), d_out' = d_out/2 with ZOACT_EPI_SWIGLU.
@@ -234,7 +243,8 @@ size_t zoact_loss_workspace_bytes(void);
  * per wave: four partial sums per 256 x 256 tile) and a fixed-order fp64 sum over them;
  * it differs from zoact_linear_fwd_pair + zoact_mse_pm by summation order only.  BF16
  * activations, bf16 target [T][d_out] (16-byte aligned); BF16 or INT4 weights (INT4
- * with L->ch).
+ * with L->ch).  flags: 0, or ZOACT_SHARED_X when both halves' inputs are the same (x and p
+ * then hold one copy, as in zoact_linear_fwd_pair).
  * ws: at least zoact_linear_mse_workspace_bytes(T, d_out) bytes (16-byte aligned).
  * Errors: shapes the fused kernel does not cover -> ZOACT_E_UNSUPPORTED. */
 /* Fused LM head and next-token cross entropy: the linear of both halves (as
@@ -252,8 +262,8 @@ zoact_status zoact_linear_xent_pair(const zoact_linear* L, const zoact_arena* A,
                                     void* ws, size_t ws_bytes, zoact_stream stream);
 size_t zoact_linear_mse_workspace_bytes(int64_t T, int64_t d_out);
 zoact_status zoact_linear_mse_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t T,
-                                   const void* p, const zoact_pert_pair* pp, const void* target, float* loss_pm,
-                                   void* ws, size_t ws_bytes, zoact_stream stream);
+                                   uint32_t flags, const void* p, const zoact_pert_pair* pp, const void* target,
+                                   float* loss_pm, void* ws, size_t ws_bytes, zoact_stream stream);
 zoact_status zoact_mse_pm(const void* y, int32_t dtype, const void* target, int64_t T, int64_t N,
                           float* loss_pm, void* ws, size_t ws_bytes, zoact_stream stream);
 zoact_status zoact_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V,

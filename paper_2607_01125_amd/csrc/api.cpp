@@ -105,7 +105,9 @@ static zoact_status validate_linear(const zoact_linear* L, const zoact_arena* A,
   CHECK(T >= 1, "linear_fwd_pm: T=%lld < 1", (long long)T);
   CHECK(L->d_in >= 1 && L->d_out >= 1, "linear_fwd_pm: empty layer");
   CHECK(L->r >= 0 && L->r <= 256, "linear_fwd_pm: r=%d outside [0, 256]", L->r);
-  CHECK((flags & ~(uint32_t)(ZOACT_EPI_SWIGLU | ZOACT_EPI_RELU)) == 0, "linear_fwd_pm: unknown flags 0x%x", flags);
+  CHECK((flags & ~(uint32_t)(ZOACT_EPI_SWIGLU | ZOACT_EPI_RELU | ZOACT_SHARED_X)) == 0,
+        "linear_fwd_pm: unknown flags 0x%x", flags);
+  CHECK(!(flags & ZOACT_SHARED_X) || x_dtype == ZOACT_BF16, "linear_fwd_pm: SHARED_X needs BF16 activations");
   CHECK(!((flags & ZOACT_EPI_SWIGLU) && (flags & ZOACT_EPI_RELU)), "linear_fwd_pm: SWIGLU and RELU are exclusive");
   CHECK(float_type(x_dtype) && float_type(y_dtype), "linear_fwd_pm: activation types must be F32 or BF16");
   if (L->r > 0) {
@@ -231,17 +233,18 @@ size_t zoact_linear_mse_workspace_bytes(int64_t T, int64_t d_out) {
 }
 
 zoact_status zoact_linear_mse_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t T,
-                                   const void* p, const zoact_pert_pair* pp, const void* target, float* loss_pm,
-                                   void* ws, size_t ws_bytes, zoact_stream stream) {
+                                   uint32_t flags, const void* p, const zoact_pert_pair* pp, const void* target,
+                                   float* loss_pm, void* ws, size_t ws_bytes, zoact_stream stream) {
   CHECK(target != nullptr && loss_pm != nullptr, "linear_mse: NULL target or loss");
   CHECK(L != nullptr && aligned16(target), "linear_mse: NULL layer or misaligned target");
+  CHECK((flags & ~(uint32_t)ZOACT_SHARED_X) == 0, "linear_mse: flags 0x%x (only ZOACT_SHARED_X applies)", flags);
   // the shared validation of the layer, with y standing in for the unused output
-  const zoact_status v = validate_linear(L, A, x, ZOACT_BF16, T, p, nullptr, 0, pp, target, ZOACT_BF16);
+  const zoact_status v = validate_linear(L, A, x, ZOACT_BF16, T, p, nullptr, flags, pp, target, ZOACT_BF16);
   if (v != ZOACT_OK) return v;
   const size_t need = zoact_linear_mse_workspace_bytes(T, L->d_out);
   if (ws == nullptr || ws_bytes < need || !aligned16(ws))
     return fail(ZOACT_E_WORKSPACE, "linear_mse: workspace needs %zu bytes, 16-byte aligned", need);
-  return hip_status(zoact::launch_linear_mse(*L, A, x, T, p, *pp, target, static_cast<double*>(ws), loss_pm,
+  return hip_status(zoact::launch_linear_mse(*L, A, x, T, flags, p, *pp, target, static_cast<double*>(ws), loss_pm,
                                              st(stream)),
                     "linear_mse");
 }

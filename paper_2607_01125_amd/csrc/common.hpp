@@ -35,7 +35,7 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
                             void* y, int32_t y_dtype, hipStream_t s);
 // Adapted linear of both halves with the regression loss fused into the epilogue (y not
 // stored): per-tile sums into part [2][tiles], then loss_pm[h] = sum / (T * d_out).
-hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, const void* p,
+hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, uint32_t flags, const void* p,
                              const zoact_pert_pair& pert, const void* target, double* part, float* loss_pm,
                              hipStream_t s);
 hipError_t launch_sum_mean(const double* part, int64_t n, double count, float* loss_pm, hipStream_t s);

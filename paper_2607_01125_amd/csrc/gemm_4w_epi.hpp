@@ -356,7 +356,15 @@ __device__ __forceinline__ void epi_rows_early(const GemmArgs& a, uint4 (&tq)[8]
   if constexpr (EPI == EPI_MSE) epi_prefetch8(a, a.tgt, a.N, tq, wave, lane, m0, n0, 0);
 }
 
-template <int EPI, bool OUT_F32, bool BIAS>
+// CORR (shared input, half 0): the accumulators hold the base x W^T only, and each block's
+// value is the rank-r correction MFMA of C_0's and p's slices with that base block as its
+// accumulator input (r <= 32, one slice): the stacked form's correction step, the base left
+// in place for the other half.  The MFMAs are issued in their VGPR form (inline assembly):
+// in the accumulator form they would need free accumulator registers, and every one holds
+// the tile.  The assembly carries its own wait states, as the compiler does not look inside
+// it: 2 before (a VALU result read as MFMA input) and 20 after (an 8-pass MFMA result read
+// by a VALU or memory instruction needs fewer).
+template <int EPI, bool OUT_F32, bool BIAS, bool CORR>
 __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&acc)[8][8], uint4 (&tq)[8][4],
                                                    int wave, int lane, int64_t m0, int64_t n0, int half, int tm,
                                                    int tn) {
@@ -405,6 +413,61 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
     }
     return v;
   };
+  // CORR: correction operands (p [T][r] shared by both halves, C_0 in the interleaved row
+  // order), their slices read one pair / one token block ahead of use
+  [[maybe_unused]] const int r = a.r;
+  [[maybe_unused]] const int lrow = (lr >> 2) * 8 + (lr & 3);
+  [[maybe_unused]] const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(a.p, (uint32_t)(a.T * a.r * 2));
+  [[maybe_unused]] const __amdgpu_buffer_rsrc_t crs = buffer_rsrc(a.ch, (uint32_t)(a.N * a.r * 2));
+  [[maybe_unused]] const int pvo = (int)(((mw - m0) + lr) * a.r + lk * 8) * 2;
+  [[maybe_unused]] const int cvo = (int)(((nw - n0) + lrow) * a.r + lk * 8) * 2;
+  auto cfrag = [&](__amdgpu_buffer_rsrc_t rs, int vo, int so) -> bf16x8 {
+    const u32x4_t u = __builtin_amdgcn_raw_buffer_load_b128(rs, vo, so, 0);
+    return __builtin_bit_cast(bf16x8, lk * 8 < r ? u : u32x4_t{0u, 0u, 0u, 0u});   // columns past r: zero
+  };
+  auto cblk = [&](int i) -> bf16x8 { return cfrag(crs, cvo, (int)((n0 + (i >> 1) * 32 + (i & 1) * 4) * r * 2)); };
+  auto pblk = [&](int j) -> bf16x8 { return cfrag(prs, pvo, (int)((m0 + j * 16) * r * 2)); };
+  bf16x8 cn0 = {}, cn1 = {}, pn = {};
+  if constexpr (CORR) {
+    cn0 = cblk(0), cn1 = cblk(1), pn = pblk(0);
+  }
+  // values of block pair q in token block j (features lk*8 .. +7, blocks 2q and 2q + 1), bias
+  // added; pairs are visited in the order j, q
+  auto pair_vals = [&](int q, int j, float (&v)[8]) {
+    if constexpr (CORR) {
+      const bf16x8 c0 = cn0, c1 = cn1, pf = pn;
+      const int k = 4 * j + q + 1;   // the next pair
+      if (k < 32) {
+        cn0 = cblk(2 * (k & 3)), cn1 = cblk(2 * (k & 3) + 1);
+        if ((k & 3) == 0) pn = pblk(k >> 2);
+      }
+      floatx4 b0, b1, y0, y1;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) b0[e] = acc_read(acc[2 * q][j][e]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) b1[e] = acc_read(acc[2 * q + 1][j][e]);
+      asm volatile(
+          "s_nop 1\n\t"
+          "v_mfma_f32_16x16x32_bf16 %0, %2, %4, %5\n\t"
+          "v_mfma_f32_16x16x32_bf16 %1, %3, %4, %6\n\t"
+          "s_nop 15\n\t"
+          "s_nop 3"
+          : "=&v"(y0), "=&v"(y1)
+          : "v"(c0), "v"(c1), "v"(pf), "v"(b0), "v"(b1));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = y0[e], v[4 + e] = y1[e];
+      if constexpr (BIAS) {
+#pragma unroll
+        for (int f = 0; f < 8; ++f) {
+          const uint32_t w = bw[4 * q + (f >> 1)];
+          v[f] += f & 1 ? bf_hi(w) : bf_lo(w);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int f = 0; f < 8; ++f) v[f] = val(2 * q + (f >> 2), j, f & 3);
+    }
+  };
   if constexpr (EPI == EPI_MSE) {
     float sq = 0.f;
 #pragma unroll
@@ -412,14 +475,15 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
       float sj = 0.f;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        if (nw + q * 32 >= a.N) continue;   // uniform
-        // squared error of the bf16-rounded outputs (features lk*8 .. +7) against the target
+        // squared error of the bf16-rounded outputs (features lk*8 .. +7) against the target;
+        // a pair past N is computed too and its terms dropped
+        float v[8];
+        pair_vals(q, j, v);
         const uint32_t t[4] = {tq[j][q].x, tq[j][q].y, tq[j][q].z, tq[j][q].w};
         float sp = 0.f;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-          const int i = 2 * q + (w >> 1), e = 2 * (w & 1);
-          const uint32_t o = pack_bf16x2(val(i, j, e), val(i, j, e + 1));
+          const uint32_t o = pack_bf16x2(v[2 * w], v[2 * w + 1]);
           const float d0 = bf_lo(o) - bf_lo(t[w]), d1 = bf_hi(o) - bf_hi(t[w]);
           sp = fmaf(d0, d0, sp);
           sp = fmaf(d1, d1, sp);
@@ -497,10 +561,9 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
     for (int j = 0; j < 8; ++j) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        if (nw + q * 32 >= a.N) continue;   // uniform
+        // (a pair past N is computed too; its store goes through an offset past the range)
         float o[8];
-#pragma unroll
-        for (int f = 0; f < 8; ++f) o[f] = val(2 * q + (f >> 2), j, f & 3);
+        pair_vals(q, j, o);
         if (res) {
           const uint32_t t[4] = {tr[j][q].x, tr[j][q].y, tr[j][q].z, tr[j][q].w};
 #pragma unroll
@@ -589,11 +652,11 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
   }
 }
 
-template <int EPI, bool OUT_F32>
+template <int EPI, bool OUT_F32, bool CORR = false>
 __device__ __forceinline__ void epilogue_regs(const GemmArgs& a, floatx4 (&acc)[8][8], uint4 (&tq)[8][4], int wave,
                                               int lane, int64_t m0, int64_t n0, int half, int tm, int tn) {
-  if (a.bias) epilogue_regs_impl<EPI, OUT_F32, true>(a, acc, tq, wave, lane, m0, n0, half, tm, tn);
-  else epilogue_regs_impl<EPI, OUT_F32, false>(a, acc, tq, wave, lane, m0, n0, half, tm, tn);
+  if (a.bias) epilogue_regs_impl<EPI, OUT_F32, true, CORR>(a, acc, tq, wave, lane, m0, n0, half, tm, tn);
+  else epilogue_regs_impl<EPI, OUT_F32, false, CORR>(a, acc, tq, wave, lane, m0, n0, half, tm, tn);
 }
 
 }  // namespace gemm

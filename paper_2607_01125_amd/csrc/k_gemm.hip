@@ -574,7 +574,8 @@ __global__ void __launch_bounds__(256) dequant_int4_kernel(const uint4* __restri
 
 hipError_t launch_linear_pm_pp(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
 hipError_t launch_linear_pm_4w(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
-hipError_t launch_linear_pm_4w64(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
+hipError_t launch_linear_pm_4w64(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, bool shared,
+                                 hipStream_t s);
 
 // Arguments of the bf16-activation kernels for one call.
 static GemmArgs bf16_args(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, const void* p,
@@ -640,9 +641,11 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
   const dim3 grid((unsigned)(2 * a.tiles_m_half * a.tiles_n));
   const bool i4 = L.w_dtype == ZOACT_INT4_G128;
   const bool of = y_dtype == ZOACT_F32;
+  // one half's x and p read by both halves: the 64-deep schedule's shared-input form only
+  if (flags & ZOACT_SHARED_X) return launch_linear_pm_4w64(a, L.w_dtype, epi, of, true, s);
   const int sched = schedule_choice();
   if (sched == 0 || sched == 3) {
-    hipError_t e = sched == 0 ? launch_linear_pm_4w64(a, L.w_dtype, epi, of, s) : hipErrorNotSupported;
+    hipError_t e = sched == 0 ? launch_linear_pm_4w64(a, L.w_dtype, epi, of, false, s) : hipErrorNotSupported;
     if (e != hipErrorNotSupported) return e;
     e = launch_linear_pm_4w(a, L.w_dtype, epi, of, s);
     if (e != hipErrorNotSupported) return e;
@@ -665,14 +668,16 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
   return hipErrorNotSupported;
 }
 
-hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, const void* p,
-                             const zoact_pert_pair& pert, const void* target, double* part, float* loss_pm,
-                             hipStream_t s) {
+hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, uint32_t flags,
+                             const void* p, const zoact_pert_pair& pert, const void* target, double* part,
+                             float* loss_pm, hipStream_t s) {
   GemmArgs a = bf16_args(L, A, x, T, p, nullptr, pert, nullptr);
   a.tgt = static_cast<const uint16_t*>(target);
   a.part = part;
-  hipError_t e = schedule_choice() == 0 ? launch_linear_pm_4w64(a, L.w_dtype, EPI_MSE, false, s) : hipErrorNotSupported;
-  if (e == hipErrorNotSupported) e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
+  const bool shared = (flags & ZOACT_SHARED_X) != 0;
+  hipError_t e = (schedule_choice() == 0 || shared) ? launch_linear_pm_4w64(a, L.w_dtype, EPI_MSE, false, shared, s)
+                                                   : hipErrorNotSupported;
+  if (e == hipErrorNotSupported && !shared) e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
   if (e != hipSuccess) return e;
   return launch_sum_mean(part, (int64_t)a.tiles_m_half * a.tiles_n * 4, (double)T * (double)L.d_out, loss_pm, s);
 }
@@ -698,7 +703,7 @@ hipError_t launch_linear_xent(const zoact_linear& L, const zoact_arena* A, const
   a.tok = tokens;
   a.seq = S;
   a.xnblk = (int32_t)nblk;
-  const hipError_t e = schedule_choice() == 0 ? launch_linear_pm_4w64(a, L.w_dtype, EPI_XENT, false, s)
+  const hipError_t e = schedule_choice() == 0 ? launch_linear_pm_4w64(a, L.w_dtype, EPI_XENT, false, false, s)
                                               : hipErrorNotSupported;
   if (e != hipSuccess) return e;
   return launch_xent_combine(a.xpart, a.xtgt, T, S, (int)nblk, T / S, part, loss_pm, s);

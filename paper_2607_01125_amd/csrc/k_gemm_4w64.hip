@@ -60,17 +60,17 @@ struct TileGeom {
   int tm, tn, half;
   int64_t m0, n0;
 };
-__device__ __forceinline__ TileGeom tile_geom(const GemmArgs& a, int ntiles, int v) {
+__device__ __forceinline__ TileGeom tile_geom(const GemmArgs& a, int ntiles, int v, bool shared) {
   int lin = v;
   if ((ntiles & 7) == 0) lin = (v & 7) * (ntiles >> 3) + (v >> 3);
-  const int tiles_m = 2 * a.tiles_m_half;
+  const int tiles_m = shared ? a.tiles_m_half : 2 * a.tiles_m_half;   // (shared input: one half's tokens)
   const int per_group = 4 * a.tiles_n;
   const int first_m = (lin / per_group) * 4;
   const int gsz = min(4, tiles_m - first_m);
   TileGeom g;
   g.tm = first_m + (lin % per_group) % gsz;
   g.tn = (lin % per_group) / gsz;
-  g.half = g.tm / a.tiles_m_half;
+  g.half = shared ? 0 : g.tm / a.tiles_m_half;
   g.m0 = (int64_t)(g.tm % a.tiles_m_half) * 256;
   g.n0 = (int64_t)g.tn * 256;
   return g;
@@ -81,7 +81,7 @@ __device__ __forceinline__ TileGeom tile_geom(const GemmArgs& a, int ntiles, int
 // load the next tile's stages 0 and 1, and its last sub-step reads the next tile's first
 // fragments, so the next tile starts without a prologue while this one finishes (rank
 // correction, epilogue straight from the accumulators, no LDS).
-template <int EPI, bool OUT_F32>
+template <int EPI, bool OUT_F32, bool SHARED>
 __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles) {
   constexpr bool PERM = epi_perm(EPI);
   extern __shared__ __align__(16) uint16_t lds[];
@@ -163,7 +163,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
   };
 
   int v = blockIdx.x;
-  TileGeom g = tile_geom(a, ntiles, v);
+  TileGeom g = tile_geom(a, ntiles, v, SHARED);
   __amdgpu_buffer_rsrc_t xrs = buffer_rsrc(a.x + (int64_t)g.half * a.T * a.K, xbytes);
 
   // ---- prologue of the first tile: stages 0 and 1 in flight (slots 0..3), stage 0
@@ -202,7 +202,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
     __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
     const int vn = v + (int)gridDim.x;
     const bool has_next = vn < ntiles;
-    const TileGeom gn = tile_geom(a, ntiles, has_next ? vn : v);
+    const TileGeom gn = tile_geom(a, ntiles, has_next ? vn : v, SHARED);
     const __amdgpu_buffer_rsrc_t xrs_n = buffer_rsrc(a.x + (int64_t)gn.half * a.T * a.K, xbytes);
 
     // ---- main loop: one stage (two sub-steps) per iteration.  Stages S + 2 past this
@@ -238,18 +238,25 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
       s5 = sw1;
     }
 
-    // EPI_MSE: the target rows, requested now so that their latency overlaps the correction's
+    // EPI_MSE: the target rows, requested now so that their latency overlaps what follows
     uint4 tq[8][4];
     epi_rows_early<EPI>(a, tq, wave, lane, g.m0, g.n0);
+    if constexpr (SHARED) {
+      // shared input: half 0 first, from the base with its correction applied in VGPR-form
+      // MFMAs so that the base stays in the accumulators; half 1 then as in the stacked form
+      epilogue_regs<EPI, OUT_F32, true>(a, acc, tq, wave, lane, g.m0, g.n0, 0, g.tm, g.tn);
+      epi_rows_early<EPI>(a, tq, wave, lane, g.m0, g.n0);   // (the same target rows again)
+    }
+    const int p_half = SHARED ? 0 : g.half, c_half = SHARED ? 1 : g.half;
 
     // ---- rank-r correction: [p[h] | C_h] as ceil(r/32) extra 32-deep steps, operands from
     // global memory (C_h precomputed) through buffer loads: rows past T or N read zeros
     // (their outputs are not stored), columns past r are zeroed, element-wise when r is
-    // not a multiple of 8.
+    // not a multiple of 8.  With the shared input: the shared p and C_1, for half 1.
     if (a.r > 0) {
       const int kts = (a.r + 31) >> 5;
-      const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(a.p + (int64_t)g.half * a.T * a.r, (uint32_t)(a.T * a.r * 2));
-      const __amdgpu_buffer_rsrc_t crs = buffer_rsrc(a.ch + (int64_t)g.half * a.ch_stride, (uint32_t)(a.N * a.r * 2));
+      const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(a.p + (int64_t)p_half * a.T * a.r, (uint32_t)(a.T * a.r * 2));
+      const __amdgpu_buffer_rsrc_t crs = buffer_rsrc(a.ch + (int64_t)c_half * a.ch_stride, (uint32_t)(a.N * a.r * 2));
       const bool vec = (a.r & 7) == 0;
       const int pvo = ((wm0 + lr) * a.r + lk * 8) * 2, cvo = ((wn0 + (PERM ? prow : lr)) * a.r + lk * 8) * 2;
       // C_h rows of W block i (the permuted order with PERM): first row's byte offset
@@ -296,7 +303,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
       }
     }
 
-    epilogue_regs<EPI, OUT_F32>(a, acc, tq, wave, lane, g.m0, g.n0, g.half, g.tm, g.tn);
+    epilogue_regs<EPI, OUT_F32>(a, acc, tq, wave, lane, g.m0, g.n0, SHARED ? 1 : g.half, g.tm, g.tn);
     if (!has_next) break;
     v = vn;
     g = gn;
@@ -320,20 +327,20 @@ int cu_count() {
   return cache[dev];
 }
 
-template <int EPI, bool OUT_F32>
+template <int EPI, bool OUT_F32, bool SHARED>
 hipError_t launch_4w64(const GemmArgs& a, hipStream_t s) {
   static bool attr_set = false;  // benign race: every thread sets the same value
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_4w64_kernel<EPI, OUT_F32>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_4w64_kernel<EPI, OUT_F32, SHARED>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  const int ntiles = 2 * a.tiles_m_half * a.tiles_n;
+  const int ntiles = (SHARED ? 1 : 2) * a.tiles_m_half * a.tiles_n;
   const int ncu = cu_count();
   if (ncu <= 0) return hipErrorInvalidDevice;
   const unsigned grid = (unsigned)(ntiles < ncu ? ntiles : ncu);
-  gemm_4w64_kernel<EPI, OUT_F32><<<dim3(grid), dim3(NT), LDS_BYTES, s>>>(a, ntiles);
+  gemm_4w64_kernel<EPI, OUT_F32, SHARED><<<dim3(grid), dim3(NT), LDS_BYTES, s>>>(a, ntiles);
   return hipGetLastError();
 }
 
@@ -342,21 +349,28 @@ hipError_t launch_4w64(const GemmArgs& a, hipStream_t s) {
 // Returns hipErrorNotSupported outside this schedule's coverage: bf16 weights; C_h
 // precomputed (or r = 0), r <= 256; depth a multiple of 64, at least 128; a half of x,
 // of p or of C_h, the weights, and the cross entropy's block partials, below 2 GiB.
-hipError_t launch_linear_pm_4w64(const GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s) {
+// `shared`: x and p hold one half's rows, read by both (plain, ReLU or regression-loss
+// epilogues; 8 <= r <= 32, a multiple of 8).
+hipError_t launch_linear_pm_4w64(const GemmArgs& a, int w_dtype, int epi, bool out_f32, bool shared, hipStream_t s) {
   if (w_dtype != ZOACT_BF16) return hipErrorNotSupported;
   if (a.r > 0 && a.ch == nullptr) return hipErrorNotSupported;
   if (a.r > 256 || (a.K % 64) != 0 || a.K < 128) return hipErrorNotSupported;
   if (a.T * a.K * 2 >= (int64_t(1) << 31) || a.N * a.K * 2 >= (int64_t(1) << 31)) return hipErrorNotSupported;
   if (a.T * a.r * 2 >= (int64_t(1) << 31) || a.N * a.r * 2 >= (int64_t(1) << 31)) return hipErrorNotSupported;
   if (epi == EPI_XENT && 2 * a.T * (int64_t)a.xnblk * 8 >= (int64_t(1) << 31)) return hipErrorNotSupported;
-#define ZO_4W64(EP, OF) \
-  if (epi == EP && out_f32 == OF) return launch_4w64<EP, OF>(a, s);
-  ZO_4W64(0, false)
-  ZO_4W64(0, true)
-  ZO_4W64(ZOACT_EPI_SWIGLU, false)
-  ZO_4W64(ZOACT_EPI_RELU, false)
-  ZO_4W64(EPI_MSE, false)
-  ZO_4W64(EPI_XENT, false)
+  if (shared && (a.r < 8 || a.r > 32 || (a.r & 7) != 0)) return hipErrorNotSupported;
+#define ZO_4W64(EP, OF, SH) \
+  if (epi == EP && out_f32 == OF && shared == SH) return launch_4w64<EP, OF, SH>(a, s);
+  ZO_4W64(0, false, false)
+  ZO_4W64(0, true, false)
+  ZO_4W64(ZOACT_EPI_SWIGLU, false, false)
+  ZO_4W64(ZOACT_EPI_RELU, false, false)
+  ZO_4W64(EPI_MSE, false, false)
+  ZO_4W64(EPI_XENT, false, false)
+  ZO_4W64(0, false, true)
+  ZO_4W64(0, true, true)
+  ZO_4W64(ZOACT_EPI_RELU, false, true)
+  ZO_4W64(EPI_MSE, false, true)
 #undef ZO_4W64
   return hipErrorNotSupported;
 }

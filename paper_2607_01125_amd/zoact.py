@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libzoact.so")
 
 F32, BF16, INT4_G128 = 0, 1, 2
 EPI_NONE, EPI_SWIGLU, EPI_RELU = 0, 1, 2
+SHARED_X = 4   # both halves read one copy of x and p
 OK, E_INVALID, E_UNSUPPORTED, E_HIP, E_NOCONVERGE, E_WORKSPACE = range(6)
 
 
@@ -90,7 +91,7 @@ SIGNATURES = {
     "zoact_linear_xent_pair": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I64, _I64, _P,
                                 ctypes.POINTER(PertPair), _P, _P, _P, _SZ, _P], _I32),
     "zoact_linear_mse_workspace_bytes": ([_I64, _I64], _SZ),
-    "zoact_linear_mse_pair": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I64, _P,
+    "zoact_linear_mse_pair": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I64, _U32, _P,
                                ctypes.POINTER(PertPair), _P, _P, _P, _SZ, _P], _I32),
     "zoact_mse_pm": ([_P, _I32, _P, _I64, _I64, _P, _P, _SZ, _P], _I32),
     "zoact_xent_pm": ([_P, _P, _I64, _I64, _I64, _P, _P, _SZ, _P], _I32),
@@ -259,14 +260,16 @@ def linear_mse_workspace_bytes(T: int, d_out: int) -> int:
 
 
 def linear_mse(layer: Linear, arena: Arena | None, x: torch.Tensor, T: int, p: torch.Tensor | None,
-               pert: Pert | PertPair, target: torch.Tensor, loss_pm: torch.Tensor, ws: torch.Tensor, stream=None):
+               pert: Pert | PertPair, target: torch.Tensor, loss_pm: torch.Tensor, ws: torch.Tensor, stream=None,
+               flags: int = 0):
     """Adapted linear of both halves with the regression loss fused into its epilogue:
-    loss_pm[h] = mean (bf16(y[h]) - target)^2, y not stored."""
+    loss_pm[h] = mean (bf16(y[h]) - target)^2, y not stored.  flags: SHARED_X when x and p
+    hold one copy read by both halves."""
     d = layer.desc()
     a = arena.desc() if arena is not None else None
     pp = as_pair(pert)
     _check(lib().zoact_linear_mse_pair(ctypes.byref(d), ctypes.byref(a) if a is not None else None, _ptr(x), T,
-                                       _ptr(p), ctypes.byref(pp), _ptr(target), _ptr(loss_pm), _ptr(ws),
+                                       flags, _ptr(p), ctypes.byref(pp), _ptr(target), _ptr(loss_pm), _ptr(ws),
                                        ws.numel() * ws.element_size(), _stream(stream)))
 
 

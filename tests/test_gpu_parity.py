@@ -624,3 +624,86 @@ def test_linear_xent_fused_vs_oracle(B, S, K, V):
             for h in range(2)]
     # fp32 logits (summation order) and fp32 exp/log in the per-block partials
     assert_rel_close(host(loss), want, 1e-5, "fused xent vs oracle")
+
+
+# ------------------------------------------------------------------ shared input (ZOACT_SHARED_X)
+def _shared_case(T, K, N, r, seed, bias=True):
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=seed, bias=bias)
+    x[1] = x[0]   # both halves read the same input
+    layer = Z.Linear(t_bf16(w), K, N, r, t_bf16(ut), 0, t_bf16(b) if b is not None else None)
+    c = synth.normal((N * r,), 0.02, seed, 5)
+    arena = Z.Arena(t_f32(c), torch.zeros(c.size, device=dev()), torch.zeros(c.size, device=dev()))
+    pert = Z.Pert(seed, 2, 0, 1e-2)
+    ch = torch.empty(2 * N * r, dtype=torch.bfloat16, device=dev())
+    Z.perturb_coeffs(arena, 0, N * r, pert, ch)
+    layer.ch, layer.ch_stride = ch, N * r
+    x1 = t_bf16(x[0])                         # one copy: [T][K]
+    x2 = t_bf16(x.reshape(2 * T, K))          # the stacked form: [2][T][K]
+    p1 = torch.empty(T, r, dtype=torch.bfloat16, device=dev())
+    Z.project(x1, t_bf16(ut), p1)
+    p2 = torch.cat([p1, p1])
+    return x, w, b, ut, c, layer, arena, pert, x1, x2, p1, p2
+
+
+@pytest.mark.parametrize("T,K,N,r,flags,out_f32,resid", [
+    (300, 512, 336, 32, 0, False, False),          # ragged tokens and features
+    (2050, 128, 4112, 16, 0, False, True),         # 153 tiles, two stages, residual
+    (4100, 192, 4112, 8, Z.EPI_RELU, False, True),  # 289 tiles: some workgroups take two
+    (257, 256, 512, 32, 0, True, False),           # fp32 out
+])
+def test_linear_pm_shared_x_bitwise(T, K, N, r, flags, out_f32, resid):
+    """The base x W^T formed once for both halves gives the same bits as the stacked form
+    with the input given twice, for both halves; and the oracle's outputs within the bar."""
+    announce("linear_pm shared x", T, K, N, r, flags, out_f32, resid)
+    x, w, b, ut, c, layer, arena, pert, x1, x2, p1, p2 = _shared_case(T, K, N, r, T + N + r)
+    dt = torch.float32 if out_f32 else torch.bfloat16
+    res = t_bf16(synth.bf16_round(synth.normal((2 * T, N), 0.5, 3, T))) if resid else None
+    ys = torch.full((2 * T, N), float("nan"), dtype=dt, device=dev())
+    yt = torch.full((2 * T, N), float("nan"), dtype=dt, device=dev())
+    Z.linear_fwd_pm(layer, arena, x1, T, p1, ys, pert, residual=res, flags=flags | Z.SHARED_X)
+    Z.linear_fwd_pm(layer, arena, x2, T, p2, yt, pert, residual=res, flags=flags)
+    bits = torch.int32 if out_f32 else torch.int16
+    assert torch.equal(ys.view(bits), yt.view(bits)), "shared x differs from the stacked form"
+    gs = host(ys)
+    if not out_f32 and not resid and flags == 0:
+        ref = _oracle_linear(x, w, b, ut, c.reshape(N, r), 0, r, 1e-2, T + N + r, 2)
+        assert_bf16_close(gs.reshape(2, T, N), ref, what="shared x vs oracle")
+
+
+def test_linear_mse_shared_x_equals_stacked():
+    """The fused regression loss with the shared input: the same per-wave partial sums as the
+    stacked form, so the same losses bit for bit (1024 tiles in the stacked form, 512 shared)."""
+    T, K, N, r = 8192, 256, 4096, 32
+    announce("linear mse shared x", T, K, N, r)
+    x, w, b, ut, c, layer, arena, pert, x1, x2, p1, p2 = _shared_case(T, K, N, r, 11)
+    tgt = t_bf16(synth.bf16_round(synth.normal((T, N), 1.0, 11, 6)))
+    ws = torch.empty(Z.linear_mse_workspace_bytes(T, N), dtype=torch.uint8, device=dev())
+    ls = torch.full((2,), float("nan"), dtype=torch.float32, device=dev())
+    lt = torch.full((2,), float("nan"), dtype=torch.float32, device=dev())
+    Z.linear_mse(layer, arena, x1, T, p1, pert, tgt, ls, ws, flags=Z.SHARED_X)
+    Z.linear_mse(layer, arena, x2, T, p2, pert, tgt, lt, ws)
+    np.testing.assert_array_equal(host(ls), host(lt))
+    assert host(ls)[0] != host(ls)[1]
+
+
+def test_shared_x_unsupported_cases():
+    """Outside the shared form's coverage the call fails with ZOACT_E_UNSUPPORTED (no
+    silent fallback): r = 40 (two slices), r = 4 (not a multiple of 8), SwiGLU, no C_h."""
+    T, K, N = 64, 128, 256
+    x = t_bf16(synth.bf16_round(synth.normal((T, K), 1.0, 1, 1)))
+    w = t_bf16(synth.bf16_round(synth.normal((N, K), 0.02, 1, 2)))
+    y = torch.empty(2 * T, N, dtype=torch.bfloat16, device=dev())
+    for r, flags, with_ch in ((40, 0, True), (4, 0, True), (32, Z.EPI_SWIGLU, True), (32, 0, False)):
+        ut = t_bf16(synth.normal((r, K), 0.1, 1, 3))
+        c = torch.zeros(N * r, device=dev())
+        arena = Z.Arena(c, torch.zeros_like(c), torch.zeros_like(c))
+        layer = Z.Linear(w, K, N, r, ut, 0)
+        if with_ch:
+            ch = torch.zeros(2 * N * r, dtype=torch.bfloat16, device=dev())
+            layer.ch, layer.ch_stride = ch, N * r
+        p = torch.zeros(T, r, dtype=torch.bfloat16, device=dev())
+        yy = torch.empty(2 * T, N // 2 if flags else N, dtype=torch.bfloat16, device=dev())
+        with pytest.raises(Z.ZoactError) as e:
+            Z.linear_fwd_pm(layer, arena, x, T, p, yy, Z.Pert(1, 1, 0, 1e-3), flags=flags | Z.SHARED_X)
+        assert e.value.status == Z.E_UNSUPPORTED, (r, flags, with_ch, e.value)
+    del y
