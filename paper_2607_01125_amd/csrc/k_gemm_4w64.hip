@@ -245,7 +245,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
       // shared input: half 0 first, from the base with its correction applied in VGPR-form
       // MFMAs so that the base stays in the accumulators; half 1 then as in the stacked form
       epilogue_regs<EPI, OUT_F32, true>(a, acc, tq, wave, lane, g.m0, g.n0, 0, g.tm, g.tn);
-      epi_rows_early<EPI>(a, tq, wave, lane, g.m0, g.n0);   // (the same target rows again)
+      // (EPI_MSE: half 1 compares against the same target rows, still in tq)
     }
     const int p_half = SHARED ? 0 : g.half, c_half = SHARED ? 1 : g.half;
 
