@@ -15,6 +15,9 @@ __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uin
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 // Internal launchers return hipError_t from hipGetLastError() after the launch.
+// Compute units of the current device (cached per device); -1 on error.
+int cu_count();
+
 hipError_t launch_perturb(const zoact_arena& A, int64_t e0, int64_t n, const zoact_pert_pair& p, uint16_t* out,
                           hipStream_t s);
 hipError_t launch_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e0, int64_t n, float* out,

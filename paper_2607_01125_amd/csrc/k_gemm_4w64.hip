@@ -313,20 +313,6 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
   __builtin_amdgcn_s_waitcnt(WAIT_VM0);
 }
 
-// Compute units of the current device (cached per device; every caller stores the same
-// value, so concurrent first calls are harmless).  -1 on error.
-int cu_count() {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return -1;
-  static int cache[64] = {};
-  if (cache[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return -1;
-    cache[dev] = n;
-  }
-  return cache[dev];
-}
-
 template <int EPI, bool OUT_F32, bool SHARED>
 hipError_t launch_4w64(const GemmArgs& a, hipStream_t s) {
   static bool attr_set = false;  // benign race: every thread sets the same value
@@ -345,6 +331,21 @@ hipError_t launch_4w64(const GemmArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+// Compute units of the current device (cached per device; every caller stores the same
+// value, so concurrent first calls are harmless).  -1 on error.
+int cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return -1;
+  static int cache[64] = {};
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return -1;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
 
 // Returns hipErrorNotSupported outside this schedule's coverage: bf16 weights; C_h
 // precomputed (or r = 0), r <= 256; depth a multiple of 64, at least 128; a half of x,

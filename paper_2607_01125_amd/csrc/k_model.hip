@@ -467,8 +467,12 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
   constexpr int KC = HD / 8;   // 16-byte chunks per row
   constexpr int KS = HD / 32;  // 32-deep steps over the head dimension
   constexpr int ND = HD / 16;  // 16-row blocks of the head dimension
+  // K chunks XOR-swizzled over 16 rows (8 when a row has only 8 chunks) and V^T rows of 34
+  // words keep the fragment reads free of LDS bank conflicts
+  constexpr int KSW = KC >= 16 ? 15 : 7;
+  constexpr int VW = 34;
   __shared__ __align__(16) uint16_t ks[64 * HD];   // K block [key][hd], chunk-swizzled
-  __shared__ __align__(16) uint32_t vt[HD * 36];   // V block transposed [d][key], key pairs per word, padded
+  __shared__ __align__(16) uint32_t vt[HD * VW];   // V block transposed [d][key], key pairs per word, padded
   const int G = heads / kv_heads;
   const int HG = G < 4 ? G : 4;
   const int QT = 64 * QB / HG;                             // queries per workgroup tile
@@ -502,7 +506,7 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
         const int key = j * 16 + lr;
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + key * HD + (((kk * 4 + lk) ^ (key & 7)) * 8));
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + key * HD + (((kk * 4 + lk) ^ (key & KSW)) * 8));
         st[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[b][kk], st[j], 0, 0, 0);
       }
     }
@@ -516,7 +520,13 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
     return (int)(last - (int64_t)kb * 64);
   };
 
-  // pass 1: row maxima of the scaled, masked scores
+  // a key block needs the causal mask only where it reaches past the q-block's first query
+  // (or past the sequence); the test is uniform over the wave
+  auto masked = [&](int b, int kb) {
+    return (int64_t)kb * 64 + 63 > (q0 + b * 16 < seq - 1 ? q0 + b * 16 : seq - 1);
+  };
+  // pass 1: row maxima of the raw scores over visible keys (scaling by a positive constant
+  // keeps the maximiser, so the scale is applied once, to the maximum)
   float mq[QB];
 #pragma unroll
   for (int b = 0; b < QB; ++b) mq[b] = -INFINITY;
@@ -547,7 +557,7 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
 #pragma unroll
     for (int t = 0; t < KPT; ++t) {
       const int cidx = threadIdx.x + t * 256, key = cidx / KC, ch = cidx % KC;
-      *reinterpret_cast<uint4*>(ks + key * HD + ((ch ^ (key & 7)) * 8)) = kreg[t];
+      *reinterpret_cast<uint4*>(ks + key * HD + ((ch ^ (key & KSW)) * 8)) = kreg[t];
     }
     if (with_v) {
       // V^T: item (key pair kp, 8-column chunk dc) -> eight words (V[2kp][d], V[2kp+1][d])
@@ -558,8 +568,8 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
         const uint32_t cw[4] = {vreg[t][1].x, vreg[t][1].y, vreg[t][1].z, vreg[t][1].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          vt[(dc * 8 + 2 * e) * 36 + kp] = (aw[e] & 0xFFFFu) | (cw[e] << 16);
-          vt[(dc * 8 + 2 * e + 1) * 36 + kp] = (aw[e] >> 16) | (cw[e] & 0xFFFF0000u);
+          vt[(dc * 8 + 2 * e) * VW + kp] = (aw[e] & 0xFFFFu) | (cw[e] << 16);
+          vt[(dc * 8 + 2 * e + 1) * VW + kp] = (aw[e] >> 16) | (cw[e] & 0xFFFF0000u);
         }
       }
     }
@@ -574,18 +584,30 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
     for (int b = 0; b < QB; ++b) {
       floatx4 st[4];
       scores_t(b, st);
-      const int lim = key_limit(b, kb);
+      if (masked(b, kb)) {
+        const int lim = key_limit(b, kb);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (j * 16 + lk * 4 + i <= lim) mq[b] = fmaxf(mq[b], st[j][i] * scale);
+          for (int i = 0; i < 4; ++i)
+            if (j * 16 + lk * 4 + i <= lim) mq[b] = fmaxf(mq[b], st[j][i]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mq[b] = fmaxf(mq[b], st[j][i]);
+      }
     }
   }
+  // exp(s * scale - max) = 2^(s * c - max * c) with c = scale * log2(e): one fma and the
+  // hardware base-2 exponential per score; masked scores become -inf, whose 2^ is 0
+  const float c2 = scale * 1.4426950408889634f;
+  float mc[QB];
 #pragma unroll
   for (int b = 0; b < QB; ++b) {
     mq[b] = fmaxf(mq[b], __shfl_xor(mq[b], 16, 64));
     mq[b] = fmaxf(mq[b], __shfl_xor(mq[b], 32, 64));
+    mc[b] = mq[b] * c2;
   }
 
   // pass 2: P = exp(s - max) rounded to bf16, O^T += V^T P^T, l += P (unrounded)
@@ -609,13 +631,20 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
     for (int b = 0; b < QB; ++b) {
       floatx4 st[4];
       scores_t(b, st);
-      const int lim = key_limit(b, kb);
+      if (masked(b, kb)) {
+        const int lim = key_limit(b, kb);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (j * 16 + lk * 4 + i > lim) st[j][i] = -INFINITY;
+      }
       uint16_t pbits[4][4];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float p = (j * 16 + lk * 4 + i <= lim) ? expf(st[j][i] * scale - mq[b]) : 0.f;
+          const float p = __builtin_amdgcn_exp2f(fmaf(st[j][i], c2, -mc[b]));
           lq[b] += p;
           pbits[j][i] = f2bf(p);
         }
@@ -633,7 +662,7 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
     for (int n = 0; n < ND; ++n)
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const uint32_t* vr = vt + (n * 16 + lr) * 36 + c * 16 + lk * 2;
+        const uint32_t* vr = vt + (n * 16 + lr) * VW + c * 16 + lk * 2;
         const uint2 lo = *reinterpret_cast<const uint2*>(vr);
         const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
         const bf16x8 va = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
@@ -658,6 +687,243 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
       const uint2 w2 = make_uint2((uint32_t)f2bf(o[n][b][0] * inv) | ((uint32_t)f2bf(o[n][b][1] * inv) << 16),
                                   (uint32_t)f2bf(o[n][b][2] * inv) | ((uint32_t)f2bf(o[n][b][3] * inv) << 16));
       *reinterpret_cast<uint2*>(op + n * 16 + lk * 4) = w2;
+    }
+  }
+}
+
+// Whole sequence resident (seq <= 256): one workgroup per (sequence, key/value head, group
+// of up to four of its query heads), WPH = 4 / QB waves per query head.  K and V^T of the
+// sequence go into LDS once (K rows chunk-swizzled, V^T as key-pair words, as above), and
+// both passes of the softmax (row maxima, then P = bf16(exp(s - max)) with l summed
+// unrounded and O^T += V^T P^T) read them from there: nothing is staged twice and no
+// barrier is needed after the load.  A wave takes units of QB 16-query blocks (each K and
+// V^T fragment read from LDS feeds QB MFMAs).  Units are dealt so that every wave of a head
+// gets the same causal work: with QB = 2 the two waves take the units u with u mod 4 in
+// {w, 3 - w}; with QB = 1 wave w takes the units with u mod 4 = w.
+template <int HD, int QB>
+__global__ void __launch_bounds__(1024 / QB, 1) attention_res_kernel(const uint16_t* __restrict__ q, int64_t ldq,
+                                                                   const uint16_t* __restrict__ k, int64_t ldk,
+                                                                   const uint16_t* __restrict__ v, int64_t ldv,
+                                                                   int64_t seq, int heads, int kv_heads, float scale,
+                                                                   uint16_t* __restrict__ out) {
+  constexpr int KC = HD / 8;    // 16-byte chunks per row
+  constexpr int KS = HD / 32;   // 32-deep steps over the head dimension
+  constexpr int ND = HD / 16;   // 16-row blocks of the head dimension
+  constexpr int SMAX = 256;
+  constexpr int WPH = 4 / QB;   // waves per query head
+  // Padding and swizzle keep the fragment reads free of LDS bank conflicts: V^T rows of
+  // 130 words, K chunks XOR-swizzled over 16 rows (8 when a row has only 8 chunks)
+  constexpr int VW = SMAX / 2 + 2;
+  constexpr int KSW = KC >= 16 ? 15 : 7;
+  __shared__ __align__(16) uint16_t ks[SMAX * HD];   // K [key][hd], chunk-swizzled
+  __shared__ __align__(16) uint32_t vt[HD * VW];     // V^T [d][key pair]
+  const int G = heads / kv_heads;
+  const int HG = G < 4 ? G : 4;
+  const int sub = G / HG;
+  const int nthr = 64 * WPH * HG;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lr = lane & 15, lk = lane >> 4;
+  const int hk = blockIdx.y / sub;
+  const int h = hk * G + (blockIdx.y % sub) * HG + (wave % HG);
+  const int hv = wave / HG;   // which of the head's waves
+  const int64_t r0 = (int64_t)blockIdx.x * seq;
+  const int nk = (int)((seq + 63) / 64) * 64;   // keys held (whole 64-key blocks)
+
+  // ---- K and V^T of the sequence into LDS; rows past seq are copies of the last row, so
+  // masked probabilities (exactly zero) never meet non-finite values.  Loads go out in
+  // batches (eight K chunks, then four V key pairs, per thread) before their LDS writes.
+  const int nkc = nk * KC, nvi = (nk / 2) * KC;
+  for (int c0 = threadIdx.x; c0 < nkc; c0 += 8 * nthr) {
+    uint4 kr[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int c = c0 + u * nthr < nkc ? c0 + u * nthr : nkc - 1;   // in range; written only below nkc
+      const int key = c / KC, ch = c % KC;
+      const int64_t row = key < seq ? key : seq - 1;
+      kr[u] = *reinterpret_cast<const uint4*>(k + (r0 + row) * ldk + (int64_t)hk * HD + ch * 8);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int c = c0 + u * nthr;
+      if (c < nkc) {
+        const int key = c / KC, ch = c % KC;
+        *reinterpret_cast<uint4*>(ks + key * HD + ((ch ^ (key & KSW)) * 8)) = kr[u];
+      }
+    }
+  }
+  for (int i0 = threadIdx.x; i0 < nvi; i0 += 4 * nthr) {
+    uint4 va[4], vb[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int it = i0 + u * nthr < nvi ? i0 + u * nthr : nvi - 1;
+      const int kp = it % (nk / 2), dc = it / (nk / 2);
+      int64_t k0r = 2 * kp, k1r = k0r + 1;
+      k0r = k0r < seq ? k0r : seq - 1;
+      k1r = k1r < seq ? k1r : seq - 1;
+      va[u] = *reinterpret_cast<const uint4*>(v + (r0 + k0r) * ldv + (int64_t)hk * HD + dc * 8);
+      vb[u] = *reinterpret_cast<const uint4*>(v + (r0 + k1r) * ldv + (int64_t)hk * HD + dc * 8);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int it = i0 + u * nthr;
+      if (it < nvi) {
+        const int kp = it % (nk / 2), dc = it / (nk / 2);
+        const uint32_t aw[4] = {va[u].x, va[u].y, va[u].z, va[u].w};
+        const uint32_t cw[4] = {vb[u].x, vb[u].y, vb[u].z, vb[u].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          vt[(dc * 8 + 2 * e) * VW + kp] = (aw[e] & 0xFFFFu) | (cw[e] << 16);
+          vt[(dc * 8 + 2 * e + 1) * VW + kp] = (aw[e] >> 16) | (cw[e] & 0xFFFF0000u);
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  const int nunit = (int)((seq + 16 * QB - 1) / (16 * QB));
+  for (int un = 0; un < nunit; ++un) {
+    if (QB == 2 ? ((un & 3) != hv && (un & 3) != 3 - hv) : ((un & 3) != hv)) continue;
+    const int64_t q0 = (int64_t)un * 16 * QB;
+    // Q fragments (B operand): q-block b, row lr, depth kk*32 + lk*8
+    bf16x8 qf[QB][KS];
+    int lastq[QB];   // this lane's query in q-block b, clamped to the sequence
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      int64_t qr = q0 + b * 16 + lr;
+      qr = qr < seq ? qr : seq - 1;
+      lastq[b] = (int)qr;
+      const uint16_t* qp = q + (r0 + qr) * ldq + (int64_t)h * HD;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) qf[b][kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + lk * 8);
+    }
+    const int64_t ulast = q0 + 16 * QB - 1 < seq - 1 ? q0 + 16 * QB - 1 : seq - 1;
+    const int nkb = (int)(ulast / 64) + 1;
+    // S^T of key block kb for the unit's q-blocks: st[b][j] holds S^T[key = j*16 + 4*lk + i][query lr]
+    auto scores_t = [&](int kb, floatx4 (&st)[QB][4]) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int b = 0; b < QB; ++b) st[b][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          const int key = kb * 64 + j * 16 + lr;
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + key * HD + (((kk * 4 + lk) ^ (key & KSW)) * 8));
+#pragma unroll
+          for (int b = 0; b < QB; ++b)
+            st[b][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[b][kk], st[b][j], 0, 0, 0);
+        }
+      }
+    };
+    // a key block needs the causal mask only where it reaches past the q-block's first
+    // query (or past the sequence); the test is uniform over the wave
+    auto masked = [&](int b, int kb) {
+      return (int64_t)kb * 64 + 63 > (q0 + b * 16 < seq - 1 ? q0 + b * 16 : seq - 1);
+    };
+    // pass 1: the row maxima of the raw scores over visible keys (key <= query); scaling by
+    // a positive constant keeps the maximiser, so the scale is applied once, to the maximum
+    float mq[QB];
+#pragma unroll
+    for (int b = 0; b < QB; ++b) mq[b] = -INFINITY;
+    for (int kb = 0; kb < nkb; ++kb) {
+      floatx4 st[QB][4];
+      scores_t(kb, st);
+#pragma unroll
+      for (int b = 0; b < QB; ++b) {
+        if (masked(b, kb)) {
+          const int lim = lastq[b] - kb * 64;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (j * 16 + lk * 4 + i <= lim) mq[b] = fmaxf(mq[b], st[b][j][i]);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mq[b] = fmaxf(mq[b], st[b][j][i]);
+        }
+      }
+    }
+    // exp(s * scale - max) = 2^(s * c - max * c) with c = scale * log2(e): one fma and the
+    // hardware base-2 exponential per score; masked scores become -inf, whose 2^ is 0
+    const float c2 = scale * 1.4426950408889634f;
+    float mc[QB];
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      mq[b] = fmaxf(mq[b], __shfl_xor(mq[b], 16, 64));
+      mq[b] = fmaxf(mq[b], __shfl_xor(mq[b], 32, 64));
+      mc[b] = mq[b] * c2;
+    }
+    // pass 2: P = exp(s - max) rounded to bf16, O^T += V^T P^T, l += P (unrounded)
+    floatx4 o[ND][QB];
+#pragma unroll
+    for (int n = 0; n < ND; ++n)
+#pragma unroll
+      for (int b = 0; b < QB; ++b) o[n][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float lq[QB];
+#pragma unroll
+    for (int b = 0; b < QB; ++b) lq[b] = 0.f;
+    for (int kb = 0; kb < nkb; ++kb) {
+      floatx4 st[QB][4];
+      scores_t(kb, st);
+      // B operands: 32-key step c holds keys c*32 + 4*lk + i (j = 2c) and c*32 + 16 + 4*lk + i
+      bf16x8 pb[QB][2];
+#pragma unroll
+      for (int b = 0; b < QB; ++b) {
+        if (masked(b, kb)) {
+          const int lim = lastq[b] - kb * 64;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (j * 16 + lk * 4 + i > lim) st[b][j][i] = -INFINITY;
+        }
+        uint16_t pbits[4][4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float pv = __builtin_amdgcn_exp2f(fmaf(st[b][j][i], c2, -mc[b]));
+            lq[b] += pv;
+            pbits[j][i] = f2bf(pv);
+          }
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const uint4 u = make_uint4((uint32_t)pbits[2 * c][0] | ((uint32_t)pbits[2 * c][1] << 16),
+                                     (uint32_t)pbits[2 * c][2] | ((uint32_t)pbits[2 * c][3] << 16),
+                                     (uint32_t)pbits[2 * c + 1][0] | ((uint32_t)pbits[2 * c + 1][1] << 16),
+                                     (uint32_t)pbits[2 * c + 1][2] | ((uint32_t)pbits[2 * c + 1][3] << 16));
+          pb[b][c] = __builtin_bit_cast(bf16x8, u);
+        }
+      }
+      // A operand: V^T rows d = n*16 + lr, the same keys (two 8-byte reads per step)
+#pragma unroll
+      for (int n = 0; n < ND; ++n)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const uint32_t* vr = vt + (n * 16 + lr) * VW + kb * 32 + c * 16 + lk * 2;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
+          const bf16x8 va = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+#pragma unroll
+          for (int b = 0; b < QB; ++b) o[n][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[b][c], o[n][b], 0, 0, 0);
+        }
+    }
+    // O^T[d = n*16 + 4*lk + i][query lr] / l -> four consecutive columns per store
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      lq[b] += __shfl_xor(lq[b], 16, 64);
+      lq[b] += __shfl_xor(lq[b], 32, 64);
+      const int64_t qi = q0 + b * 16 + lr;
+      if (qi >= seq) continue;
+      const float inv = 1.f / lq[b];
+      uint16_t* op = out + (r0 + qi) * (int64_t)heads * HD + (int64_t)h * HD;
+#pragma unroll
+      for (int n = 0; n < ND; ++n) {
+        const uint2 w2 = make_uint2((uint32_t)f2bf(o[n][b][0] * inv) | ((uint32_t)f2bf(o[n][b][1] * inv) << 16),
+                                    (uint32_t)f2bf(o[n][b][2] * inv) | ((uint32_t)f2bf(o[n][b][3] * inv) << 16));
+        *reinterpret_cast<uint2*>(op + n * 16 + lk * 4) = w2;
+      }
     }
   }
 }
@@ -788,6 +1054,25 @@ extern "C" zoact_status zoact_attention(const void* q, int64_t ldq, const void* 
     ZO_CHECK(head_dim == 64 || head_dim == 128, "attention: bf16 head_dim must be 64 or 128");
     ZO_CHECK(ldq % 8 == 0 && ldk % 8 == 0 && ldv % 8 == 0, "attention: bf16 strides must be multiples of 8");
     const int G = n_heads / n_kv_heads;
+    // Whole sequence resident in LDS: for groups of four or more query heads per key/value
+    // head (sixteen waves per workgroup), when the grid of one workgroup per (sequence,
+    // key/value head, four query heads) covers every compute unit; smaller grids run the
+    // staged kernel below, which splits the queries over more workgroups
+    const int ncu = cu_count();
+    if (ncu <= 0) return zoact::set_error(ZOACT_E_HIP, "attention: device query failed");
+    if (G % 4 == 0 && seq <= 256 && (int64_t)n_kv_heads * (G / 4) <= 65535 &&
+        n_seq * n_kv_heads * (G / 4) >= ncu) {
+      const dim3 g1((unsigned)n_seq, (unsigned)(n_kv_heads * (G / 4)));
+      if (head_dim == 128)
+        attention_res_kernel<128, 1><<<g1, 1024, 0, s>>>((const uint16_t*)q, ldq, (const uint16_t*)k, ldk,
+                                                         (const uint16_t*)v, ldv, seq, n_heads, n_kv_heads, scale,
+                                                         (uint16_t*)out);
+      else
+        attention_res_kernel<64, 1><<<g1, 1024, 0, s>>>((const uint16_t*)q, ldq, (const uint16_t*)k, ldk,
+                                                        (const uint16_t*)v, ldv, seq, n_heads, n_kv_heads, scale,
+                                                        (uint16_t*)out);
+      return launched("attention");
+    }
     if ((G == 1 || G == 2 || G % 4 == 0) && (int64_t)n_kv_heads * (G < 4 ? 1 : G / 4) <= 65535) {
       constexpr int QB = 2;                     // 16-query blocks per wave
       const int HG = G < 4 ? G : 4;

@@ -127,9 +127,13 @@ def _attn_case(bf16, B, S, H, Hkv, hd, seed):
     return host(out), want, mag
 
 
+# the last three fill the chip with (sequence, key/value head, four query heads) workgroups,
+# which selects the whole-sequence-resident kernel: ragged lengths, both head sizes, and
+# eight query heads per key/value head (two workgroups per key/value head)
 @pytest.mark.parametrize("B,S,H,Hkv,hd", [(2, 64, 4, 2, 128), (3, 100, 4, 4, 64), (1, 257, 8, 2, 128),
                                           (2, 1, 2, 1, 64), (1, 512, 2, 2, 128), (1, 130, 16, 2, 128),
-                                          (1, 70, 6, 2, 64), (2, 256, 32, 8, 128)])
+                                          (1, 70, 6, 2, 64), (2, 256, 32, 8, 128),
+                                          (128, 33, 8, 2, 64), (64, 130, 16, 4, 128), (64, 64, 16, 2, 128)])
 def test_attention_bf16(B, S, H, Hkv, hd):
     """Bound: the output's own bf16 rounding (2^-7 |o|) plus one bf16 ulp (<= 2^-7 p) on
     every rounded probability, which fp32 scores (GPU) and float64 scores (oracle) can
@@ -141,6 +145,32 @@ def test_attention_bf16(B, S, H, Hkv, hd):
     assert not bad.any(), f"{bad.sum()} outside; first {np.argwhere(bad)[0]}"
     # far inside the bound on average: the rounding differences are rare
     assert np.mean(np.abs(got - want)) <= 0.05 * np.mean(tol)
+
+
+def test_attention_llama_shape_sampled():
+    """32 sequences of 256 tokens, 32 query and 8 key/value heads of 128: the attention of
+    the Llama-3-8B step (both perturbation halves).  The oracle runs on three of the
+    sequences; same bound as test_attention_bf16."""
+    B, S, H, Hkv, hd = 32, 256, 32, 8, 128
+    announce("attention bf16 sampled", B, S, H, Hkv, hd)
+    ld = (H + 2 * Hkv) * hd
+    qkv = _vals((B * S, ld), 1.0, 5, 4242, bf16=True)
+    t = t_bf16(qkv)
+    out = torch.empty(B * S, H * hd, dtype=torch.bfloat16, device=dev())
+    Z.attention(t[:, :H * hd], t[:, H * hd:(H + Hkv) * hd], t[:, (H + Hkv) * hd:], out, B, S, H, Hkv, hd,
+                float(np.float32(1.0 / math.sqrt(hd))))
+    got = host(out).reshape(B, S, H * hd)
+    x = qkv.reshape(B, S, ld)
+    for b in (0, 17, 31):
+        q = x[b:b + 1, :, :H * hd].reshape(1, S, H, hd)
+        k = x[b:b + 1, :, H * hd:(H + Hkv) * hd].reshape(1, S, Hkv, hd)
+        v = x[b:b + 1, :, (H + Hkv) * hd:].reshape(1, S, Hkv, hd)
+        want = om.attention(q, k, v, "bf16").reshape(S, H * hd)
+        mag = om.attention(q, k, np.abs(v), "fp32").reshape(S, H * hd)
+        tol = 2.0 ** -7 * (np.abs(want) + mag) + 1e-6
+        bad = np.abs(got[b] - want) > tol
+        assert not bad.any(), f"sequence {b}: {bad.sum()} outside; first {np.argwhere(bad)[0]}"
+        assert np.mean(np.abs(got[b] - want)) <= 0.05 * np.mean(tol)
 
 
 @pytest.mark.parametrize("B,S,H,Hkv,hd", [(4, 64, 4, 4, 32), (2, 17, 4, 2, 16), (1, 1, 1, 1, 8)])
