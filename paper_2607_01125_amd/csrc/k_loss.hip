@@ -69,16 +69,27 @@ __global__ void __launch_bounds__(256) mse_partial(const void* __restrict__ y, c
 }
 
 // Sum n partials per half ([2][n]) in a fixed order and scale: the per-tile squared errors
-// of the fused regression-loss epilogue.
+// of the fused regression-loss epilogue.  One block per half; each thread adds its
+// partials i = t, t + 256, ... in index order, with the loads issued eight at a time (index
+// clamped, value replaced by zero past n) so that they overlap.
 __global__ void __launch_bounds__(256) sum_mean(const double* __restrict__ part, int64_t n, double count,
                                                 float* loss_pm) {
   __shared__ double sh[4];
-  for (int h = 0; h < 2; ++h) {
-    double v = 0.0;
-    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) v += part[h * n + i];
-    const double s = block_sum_d(v, sh);
-    if (threadIdx.x == 0) loss_pm[h] = (float)(s / count);
+  const int h = blockIdx.x;
+  const double* ph = part + (int64_t)h * n;
+  double v = 0.0;
+  for (int64_t i0 = threadIdx.x; i0 < n; i0 += 8 * (int64_t)blockDim.x) {
+    double t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t i = i0 + u * (int64_t)blockDim.x;
+      t[u] = ph[i < n ? i : n - 1];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v += (i0 + u * (int64_t)blockDim.x < n) ? t[u] : 0.0;
   }
+  const double s = block_sum_d(v, sh);
+  if (threadIdx.x == 0) loss_pm[h] = (float)(s / count);
 }
 
 // Cross entropy from the fused LM-head epilogue's per-block (max, sum of exp): one wave per
@@ -114,15 +125,14 @@ __global__ void __launch_bounds__(256) xent_combine(const float2* __restrict__ x
   if (threadIdx.x == 0) part[h * kLossBlocks + blockIdx.x] = s;
 }
 
-// Sum kLossBlocks partials per half in a fixed order and scale.
+// Sum kLossBlocks partials per half in a fixed order and scale (one block per half).
 __global__ void __launch_bounds__(256) finish_mean(const double* __restrict__ part, double count, float* loss_pm) {
   __shared__ double sh[4];
-  for (int h = 0; h < 2; ++h) {
-    double v = 0.0;
-    for (int i = threadIdx.x; i < kLossBlocks; i += blockDim.x) v += part[h * kLossBlocks + i];
-    const double s = block_sum_d(v, sh);
-    if (threadIdx.x == 0) loss_pm[h] = (float)(s / count);
-  }
+  const int h = blockIdx.x;
+  double v = 0.0;
+  for (int i = threadIdx.x; i < kLossBlocks; i += blockDim.x) v += part[h * kLossBlocks + i];
+  const double s = block_sum_d(v, sh);
+  if (threadIdx.x == 0) loss_pm[h] = (float)(s / count);
 }
 
 __global__ void __launch_bounds__(256) xent_partial(const float* __restrict__ logits, const int32_t* __restrict__ tokens,
@@ -181,12 +191,12 @@ __global__ void __launch_bounds__(256) xent_partial(const float* __restrict__ lo
 hipError_t launch_xent_combine(const float2* xpart, const float* xtgt, int64_t T, int64_t S, int nblk, int64_t B,
                                double* part, float* loss_pm, hipStream_t s) {
   xent_combine<<<dim3(kLossBlocks, 2), dim3(256), 0, s>>>(xpart, xtgt, T, S, nblk, part);
-  finish_mean<<<dim3(1), dim3(256), 0, s>>>(part, (double)(B * (S - 1)), loss_pm);
+  finish_mean<<<dim3(2), dim3(256), 0, s>>>(part, (double)(B * (S - 1)), loss_pm);
   return hipGetLastError();
 }
 
 hipError_t launch_sum_mean(const double* part, int64_t n, double count, float* loss_pm, hipStream_t s) {
-  sum_mean<<<dim3(1), dim3(256), 0, s>>>(part, n, count, loss_pm);
+  sum_mean<<<dim3(2), dim3(256), 0, s>>>(part, n, count, loss_pm);
   return hipGetLastError();
 }
 
@@ -198,7 +208,7 @@ hipError_t launch_mse_pm(const void* y, int32_t dtype, const void* target, int64
   else mse_partial<false><<<dim3(kLossBlocks, 2), dim3(256), 0, s>>>(y, target, n, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  finish_mean<<<1, 256, 0, s>>>(part, (double)n, loss_pm);
+  finish_mean<<<2, 256, 0, s>>>(part, (double)n, loss_pm);
   return hipGetLastError();
 }
 
@@ -208,7 +218,7 @@ hipError_t launch_xent_pm(const float* logits, const int32_t* tokens, int64_t B,
   xent_partial<<<dim3(kLossBlocks, 2), dim3(256), 0, s>>>(logits, tokens, B, S, V, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  finish_mean<<<1, 256, 0, s>>>(part, (double)(B * (S - 1)), loss_pm);
+  finish_mean<<<2, 256, 0, s>>>(part, (double)(B * (S - 1)), loss_pm);
   return hipGetLastError();
 }
 
