@@ -46,6 +46,68 @@ DOMINANT_SOURCES = [os.path.join("paper_2607_01125_amd", "csrc", f)
                     for f in ("k_gemm_4w64.hip", "gemm_4w_epi.hpp", "gemm_common.hpp")]
 
 
+class TimingEvent:
+    """A HIP timing event created with hipEventDisableSystemFence, recorded on a torch stream.
+
+    Recording torch's events applies a system-scope release (cache writeback and
+    invalidation), which put about 6 µs of idle time before the next kernel of a step;
+    without the fence the events that bracket one launch add no gap to the step.  The
+    HIP runtime is the one torch has loaded (this library resolves to the same one)."""
+
+    _hip = None
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    @classmethod
+    def _rt(cls):
+        if cls._hip is None:
+            import ctypes
+
+            path = None
+            with open("/proc/self/maps") as f:
+                for line in f:
+                    if "libamdhip64.so" in line:
+                        path = line.split()[-1]
+                        break
+            if path is None:
+                raise RuntimeError("HIP runtime not loaded")
+            h = ctypes.CDLL(path)
+            h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._hip = h
+        return cls._hip
+
+    def __init__(self):
+        import ctypes
+
+        self._ev = ctypes.c_void_p()
+        if self._rt().hipEventCreateWithFlags(ctypes.byref(self._ev), self.DISABLE_SYSTEM_FENCE) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+
+    def record(self, stream):
+        if self._rt().hipEventRecord(self._ev, ctypes_stream(stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, end) -> float:
+        import ctypes
+
+        ms = ctypes.c_float()
+        if self._rt().hipEventElapsedTime(ctypes.byref(ms), self._ev, end._ev) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def __del__(self):
+        if self._hip is not None and self._ev:
+            self._hip.hipEventDestroy(self._ev)
+
+
+def ctypes_stream(stream):
+    import ctypes
+
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
@@ -176,7 +238,7 @@ def bench_single_linear(args, dev):
         Z.step(arena, loss, pert, Z.adam_desc(lr, t), status)
 
     def timed(t0, n, shared):
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        evs = [(TimingEvent(), TimingEvent()) for _ in range(n)]
         start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         start.record(stream)
