@@ -218,9 +218,15 @@ def bench_single_linear(args, dev):
     ch = torch.empty(2 * N * r, dtype=torch.bfloat16, device=dev)
     layer.ch, layer.ch_stride = ch, N * r
 
+    # ch holds C +/- eps Z for step ch_for[0]: each step's update also writes the next step's
+    # perturbed coefficients (zoact_step_perturb: one pass over the arena instead of two
+    # launches); a step whose perturbation is not there yet forms it first
+    ch_for = [None]
+
     def zo_step(t, ev=None, shared=True):
         pert = Z.Pert(seed, t, 0, eps)
-        Z.perturb_coeffs(arena, 0, N * r, pert, ch)
+        if ch_for[0] != t:
+            Z.perturb_coeffs(arena, 0, N * r, pert, ch)
         if shared:
             Z.project(xb, ut, p)
         else:
@@ -235,7 +241,8 @@ def bench_single_linear(args, dev):
             Z.linear_mse(layer, arena, x_pm, T, p_pm, pert, tgt, loss, ws_l)
         if ev is not None:
             ev[1].record(stream)
-        Z.step(arena, loss, pert, Z.adam_desc(lr, t), status)
+        Z.step_perturb(arena, loss, pert, Z.adam_desc(lr, t), Z.Pert(seed, t + 1, 0, eps), ch, status)
+        ch_for[0] = t + 1
 
     def timed(t0, n, shared):
         evs = [(TimingEvent(), TimingEvent()) for _ in range(n)]
@@ -556,7 +563,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (planted low-rank activations, random-init W, seeded)",
         "config": {"workload": "single adapted linear, bf16, d_in=d_out=4096, r=32, 8192 tokens per ± half "
-                               "(C±εZ pass + projection + fused ± forward with the MSE in its epilogue + ZO-Adam; "
+                               "(projection + fused ± forward with the MSE in its epilogue + ZO-Adam, whose pass "
+                               "also forms the next step's C±εZ; "
                                "both halves read the same x, so x W^T and x U are formed once)",
                    **head["config"], "parallelism": "single GPU"},
         "adapted_linear_tflops": round(head["flops"] / (ms * 1e-3) / 1e12, 1),

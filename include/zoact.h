@@ -282,6 +282,15 @@ zoact_status zoact_step(const zoact_arena* A, const float* loss_pm, const zoact_
                         const zoact_adam* h, uint32_t* dev_status, zoact_stream stream);
 zoact_status zoact_step_sgd(const zoact_arena* A, const float* loss_pm, const zoact_pert* pert, float lr,
                             uint32_t* dev_status, zoact_stream stream);
+/* zoact_step, then zoact_perturb_coeffs(A, 0, A->k, next, ch_next) for the next step, in
+ * one pass over the arena: both results bit for bit as the two calls give them (the
+ * perturbation is formed from C as stored, after the update; with a non-finite g C is
+ * unchanged and the perturbation is still written).  Saves one launch and one read of C
+ * per step when a layer's coefficients are the whole arena.  ch_next bf16 [2][A->k],
+ * 16-byte aligned; A->k >= 1. */
+zoact_status zoact_step_perturb(const zoact_arena* A, const float* loss_pm, const zoact_pert* pert,
+                                const zoact_adam* h, uint32_t* dev_status, const zoact_pert* next, void* ch_next,
+                                zoact_stream stream);
 
 /* ------------------------------------------------------ one-sided multi-query step
  * Algorithm 2 with q queries (Section 3's averaged forward-difference estimate):

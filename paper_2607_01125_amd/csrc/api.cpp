@@ -273,7 +273,21 @@ zoact_status zoact_step(const zoact_arena* A, const float* loss_pm, const zoact_
   if (s != ZOACT_OK) return s;
   CHECK(h != nullptr, "step: NULL Adam scalars");
   CHECK(A->k == 0 || (A->m != nullptr && A->v != nullptr), "step: NULL moments");
-  return hip_status(zoact::launch_adam(*A, loss_pm, *p, *h, dev_status, st(stream)), "step");
+  return hip_status(zoact::launch_adam(*A, loss_pm, *p, *h, dev_status, nullptr, nullptr, st(stream)), "step");
+}
+
+zoact_status zoact_step_perturb(const zoact_arena* A, const float* loss_pm, const zoact_pert* p, const zoact_adam* h,
+                                uint32_t* dev_status, const zoact_pert* next, void* ch_next, zoact_stream stream) {
+  zoact_status s = check_arena(A, loss_pm, p, "step_perturb");
+  if (s != ZOACT_OK) return s;
+  CHECK(h != nullptr && next != nullptr && ch_next != nullptr, "step_perturb: NULL Adam scalars, next or ch_next");
+  CHECK(A->k >= 1, "step_perturb: empty arena");
+  CHECK(A->m != nullptr && A->v != nullptr, "step_perturb: NULL moments");
+  CHECK(aligned16(ch_next), "step_perturb: ch_next must be 16-byte aligned");
+  const zoact_pert_pair pp = pm_pair(*next);
+  return hip_status(zoact::launch_adam(*A, loss_pm, *p, *h, dev_status, &pp, static_cast<uint16_t*>(ch_next),
+                                       st(stream)),
+                    "step_perturb");
 }
 
 zoact_status zoact_step_sgd(const zoact_arena* A, const float* loss_pm, const zoact_pert* p, float lr,

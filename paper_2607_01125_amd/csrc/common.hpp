@@ -23,7 +23,7 @@ hipError_t launch_perturb(const zoact_arena& A, int64_t e0, int64_t n, const zoa
 hipError_t launch_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e0, int64_t n, float* out,
                         hipStream_t s);
 hipError_t launch_adam(const zoact_arena& A, const float* loss_pm, const zoact_pert& p, const zoact_adam& h,
-                       uint32_t* status, hipStream_t s);
+                       uint32_t* status, const zoact_pert_pair* next, uint16_t* out, hipStream_t s);
 hipError_t launch_sgd(const zoact_arena& A, const float* loss_pm, const zoact_pert& p, float lr,
                       uint32_t* status, hipStream_t s);
 // one-sided multi-query update: Adam when h != nullptr, else SGD with rate lr

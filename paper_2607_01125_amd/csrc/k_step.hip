@@ -58,23 +58,39 @@ typedef uint32_t vu2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ vf4 ld_nt(const float* p) { return __builtin_nontemporal_load(reinterpret_cast<const vf4*>(p)); }
 __device__ __forceinline__ void st_nt(float* p, vf4 v) { __builtin_nontemporal_store(v, reinterpret_cast<vf4*>(p)); }
 
-template <bool BF16C>
+// With NEXT, the same pass also writes the next step's perturbed coefficients from the C it
+// leaves behind, exactly as perturb_kernel would over the whole arena (out bf16 [2][k]):
+// out[h][e] = bf16(C'[e] + s_h (eps' Z(e; q'_h))), C' the stored value (bf16 C: the rounded
+// one); with a non-finite g C is left unchanged and the perturbation is still written.
+template <bool BF16C, bool NEXT>
 __global__ void __launch_bounds__(256) adam_kernel(void* __restrict__ cptr, float* __restrict__ mptr,
                                                    float* __restrict__ vptr, int64_t k, const float* loss_pm,
                                                    uint64_t seed, uint32_t step, uint32_t query, float eps,
-                                                   AdamConst h, uint32_t* status) {
+                                                   AdamConst h, uint32_t* status, zoact_pert_pair nx,
+                                                   uint16_t* __restrict__ out) {
 #pragma clang fp contract(off)
   const float g = projected_grad(loss_pm, eps);
-  if (!__builtin_isfinite(g)) {
+  const bool upd = __builtin_isfinite(g);
+  if (!upd) {
     if (status != nullptr && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, 1u);
-    return;
+    if (!NEXT) return;
   }
+  // next perturbation of arena indices 4b .. 4b + nl - 1 from their stored values cs
+  auto next_pert = [&](int64_t b, const float* cs, int nl) {
+    const float4 za = rng::gauss_block(nx.seed, nx.step, nx.query[0], (uint64_t)b);
+    const float4 zb = nx.query[0] == nx.query[1] ? za : rng::gauss_block(nx.seed, nx.step, nx.query[1], (uint64_t)b);
+    for (int l = 0; l < nl; ++l) {
+      const int64_t e = 4 * b + l;
+      const float c = cs[l];
+      const float ea = nx.eps * rng::lane_of(za, l), eb = nx.eps * rng::lane_of(zb, l);
+      out[e] = f2bf(nx.sign[0] > 0 ? c + ea : (nx.sign[0] < 0 ? c - ea : c));
+      out[k + e] = f2bf(nx.sign[1] > 0 ? c + eb : (nx.sign[1] < 0 ? c - eb : c));
+    }
+  };
   const int64_t nb = (k + 3) >> 2;
   for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb; b += (int64_t)gridDim.x * blockDim.x) {
     const int64_t e = 4 * b;
     if (e + 4 <= k) {
-      vf4 m4 = ld_nt(mptr + e);
-      vf4 v4 = ld_nt(vptr + e);
       float c0, c1, c2, c3;
       if (BF16C) {
         const vu2 cb = __builtin_nontemporal_load(reinterpret_cast<const vu2*>(reinterpret_cast<const uint16_t*>(cptr) + e));
@@ -84,32 +100,46 @@ __global__ void __launch_bounds__(256) adam_kernel(void* __restrict__ cptr, floa
         const vf4 cf = ld_nt(reinterpret_cast<const float*>(cptr) + e);
         c0 = cf.x; c1 = cf.y; c2 = cf.z; c3 = cf.w;
       }
-      const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
-      float mx = m4.x, my = m4.y, mz = m4.z, mw = m4.w, vx = v4.x, vy = v4.y, vz = v4.z, vw = v4.w;
-      c0 = adam_one(c0, mx, vx, g * z.x, h);
-      c1 = adam_one(c1, my, vy, g * z.y, h);
-      c2 = adam_one(c2, mz, vz, g * z.z, h);
-      c3 = adam_one(c3, mw, vw, g * z.w, h);
-      st_nt(mptr + e, vf4{mx, my, mz, mw});
-      st_nt(vptr + e, vf4{vx, vy, vz, vw});
-      if (BF16C) {
-        const vu2 cb = {(uint32_t)f2bf(c0) | ((uint32_t)f2bf(c1) << 16), (uint32_t)f2bf(c2) | ((uint32_t)f2bf(c3) << 16)};
-        __builtin_nontemporal_store(cb, reinterpret_cast<vu2*>(reinterpret_cast<uint16_t*>(cptr) + e));
-      } else {
-        st_nt(reinterpret_cast<float*>(cptr) + e, vf4{c0, c1, c2, c3});
+      if (upd) {
+        vf4 m4 = ld_nt(mptr + e);
+        vf4 v4 = ld_nt(vptr + e);
+        const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
+        float mx = m4.x, my = m4.y, mz = m4.z, mw = m4.w, vx = v4.x, vy = v4.y, vz = v4.z, vw = v4.w;
+        c0 = adam_one(c0, mx, vx, g * z.x, h);
+        c1 = adam_one(c1, my, vy, g * z.y, h);
+        c2 = adam_one(c2, mz, vz, g * z.z, h);
+        c3 = adam_one(c3, mw, vw, g * z.w, h);
+        st_nt(mptr + e, vf4{mx, my, mz, mw});
+        st_nt(vptr + e, vf4{vx, vy, vz, vw});
+        if (BF16C) {
+          const vu2 cb = {(uint32_t)f2bf(c0) | ((uint32_t)f2bf(c1) << 16), (uint32_t)f2bf(c2) | ((uint32_t)f2bf(c3) << 16)};
+          __builtin_nontemporal_store(cb, reinterpret_cast<vu2*>(reinterpret_cast<uint16_t*>(cptr) + e));
+        } else {
+          st_nt(reinterpret_cast<float*>(cptr) + e, vf4{c0, c1, c2, c3});
+        }
+      }
+      if constexpr (NEXT) {
+        const float cs[4] = {BF16C ? bf2f(f2bf(c0)) : c0, BF16C ? bf2f(f2bf(c1)) : c1, BF16C ? bf2f(f2bf(c2)) : c2,
+                             BF16C ? bf2f(f2bf(c3)) : c3};
+        next_pert(b, cs, 4);
       }
     } else {
       const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
+      float cs[4] = {0.f, 0.f, 0.f, 0.f};
       for (int l = 0; l < 4 && e + l < k; ++l) {
-        float m = mptr[e + l], v = vptr[e + l];
         float c = BF16C ? bf2f(reinterpret_cast<const uint16_t*>(cptr)[e + l])
                         : reinterpret_cast<const float*>(cptr)[e + l];
-        c = adam_one(c, m, v, g * rng::lane_of(z, l), h);
-        mptr[e + l] = m;
-        vptr[e + l] = v;
-        if (BF16C) reinterpret_cast<uint16_t*>(cptr)[e + l] = f2bf(c);
-        else reinterpret_cast<float*>(cptr)[e + l] = c;
+        if (upd) {
+          float m = mptr[e + l], v = vptr[e + l];
+          c = adam_one(c, m, v, g * rng::lane_of(z, l), h);
+          mptr[e + l] = m;
+          vptr[e + l] = v;
+          if (BF16C) reinterpret_cast<uint16_t*>(cptr)[e + l] = f2bf(c);
+          else reinterpret_cast<float*>(cptr)[e + l] = c;
+        }
+        cs[l] = BF16C ? bf2f(f2bf(c)) : c;
       }
+      if constexpr (NEXT) next_pert(b, cs, (int)(k - e));
     }
   }
 }
@@ -297,17 +327,22 @@ hipError_t launch_step_q(const zoact_arena& A, const float* losses, int32_t q, u
 }
 
 hipError_t launch_adam(const zoact_arena& A, const float* loss_pm, const zoact_pert& p, const zoact_adam& h,
-                       uint32_t* status, hipStream_t s) {
+                       uint32_t* status, const zoact_pert_pair* next, uint16_t* out, hipStream_t s) {
   if (A.k == 0) return hipSuccess;
   const AdamConst c{h.beta1, h.beta2, h.eps, h.weight_decay, h.step_size, h.inv_sqrt_bc2, h.one_minus_beta1,
                     h.one_minus_beta2};
   const dim3 grid((unsigned)grid_for((A.k + 3) >> 2));
-  if (A.c_dtype == ZOACT_BF16)
-    adam_kernel<true><<<grid, dim3(256), 0, s>>>(A.c, A.m, A.v, A.k, loss_pm, p.seed, p.step, p.query, p.eps, c,
-                                                 status);
-  else
-    adam_kernel<false><<<grid, dim3(256), 0, s>>>(A.c, A.m, A.v, A.k, loss_pm, p.seed, p.step, p.query, p.eps, c,
-                                                  status);
+  const zoact_pert_pair nx = next ? *next : zoact_pert_pair{};
+#define ZO_ADAM(BF, NX)                                                                                             \
+  adam_kernel<BF, NX><<<grid, dim3(256), 0, s>>>(A.c, A.m, A.v, A.k, loss_pm, p.seed, p.step, p.query, p.eps, c, \
+                                                 status, nx, out)
+  const bool bf = A.c_dtype == ZOACT_BF16;
+  if (next) {
+    if (bf) ZO_ADAM(true, true); else ZO_ADAM(false, true);
+  } else {
+    if (bf) ZO_ADAM(true, false); else ZO_ADAM(false, false);
+  }
+#undef ZO_ADAM
   return hipGetLastError();
 }
 

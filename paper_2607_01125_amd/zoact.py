@@ -96,6 +96,8 @@ SIGNATURES = {
     "zoact_mse_pm": ([_P, _I32, _P, _I64, _I64, _P, _P, _SZ, _P], _I32),
     "zoact_xent_pm": ([_P, _P, _I64, _I64, _I64, _P, _P, _SZ, _P], _I32),
     "zoact_step": ([ctypes.POINTER(ArenaDesc), _P, ctypes.POINTER(Pert), ctypes.POINTER(AdamDesc), _P, _P], _I32),
+    "zoact_step_perturb": ([ctypes.POINTER(ArenaDesc), _P, ctypes.POINTER(Pert), ctypes.POINTER(AdamDesc), _P,
+                            ctypes.POINTER(Pert), _P, _P], _I32),
     "zoact_step_sgd": ([ctypes.POINTER(ArenaDesc), _P, ctypes.POINTER(Pert), _F, _P, _P], _I32),
     "zoact_basis_workspace_bytes": ([_I64, _I32, ctypes.POINTER(EigOpts)], _SZ),
     "zoact_basis_init_workspace_bytes": ([_I64, _I32, ctypes.POINTER(EigOpts)], _SZ),
@@ -295,6 +297,14 @@ def step(arena: Arena, loss_pm: torch.Tensor, pert: Pert, adam: AdamDesc, status
     a = arena.desc()
     _check(lib().zoact_step(ctypes.byref(a), _ptr(loss_pm), ctypes.byref(pert), ctypes.byref(adam), _ptr(status),
                             _stream(stream)))
+
+
+def step_perturb(arena: Arena, loss_pm: torch.Tensor, pert: Pert, adam: AdamDesc, next_pert: Pert,
+                 ch_next: torch.Tensor, status: torch.Tensor | None = None, stream=None):
+    """step(), then perturb_coeffs(arena, 0, k, next_pert, ch_next), in one pass."""
+    a = arena.desc()
+    _check(lib().zoact_step_perturb(ctypes.byref(a), _ptr(loss_pm), ctypes.byref(pert), ctypes.byref(adam),
+                                    _ptr(status), ctypes.byref(next_pert), _ptr(ch_next), _stream(stream)))
 
 
 def step_sgd(arena: Arena, loss_pm: torch.Tensor, pert: Pert, lr: float, status: torch.Tensor | None = None,

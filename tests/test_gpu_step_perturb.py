@@ -1,0 +1,76 @@
+"""The fused update + next perturbation (zoact_step_perturb) against its two parts
+(zoact_step, then zoact_perturb_coeffs over the whole arena), bit for bit.  The parts
+are pinned against the oracle elsewhere; this checks that the one-pass form changes
+nothing: the update, the moments, the next step's C +/- eps Z from the stored C, and
+the non-finite loss case (arena untouched, status set, perturbation still written)."""
+import math
+
+import pytest
+import torch
+
+from paper_2607_01125_amd import zoact as Z
+
+from gpu_helpers import announce, dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _arena(k, bf16c, seed):
+    g = torch.Generator().manual_seed(seed)
+    c = (torch.randn(k, generator=g) * 0.05).to(dev())
+    m = (torch.randn(k, generator=g) * 1e-3).to(dev())
+    v = (torch.rand(k, generator=g) * 1e-5).to(dev())
+    if bf16c:
+        c = c.to(torch.bfloat16)
+    return Z.Arena(c, m, v)
+
+
+def _clone(a):
+    return Z.Arena(a.c.clone(), a.m.clone(), a.v.clone())
+
+
+def _bits(t):
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
+
+
+@pytest.mark.parametrize("bf16c", [False, True])
+@pytest.mark.parametrize("k,losses", [(131072, (0.731, 0.729)), (4099, (1.25, 1.5)), (3, (2.0, 1.0)),
+                                      (1030, (math.inf, 1.0))])
+def test_step_perturb_equals_step_then_perturb(bf16c, k, losses):
+    announce("step_perturb", bf16c, k, losses)
+    a1 = _arena(k, bf16c, k)
+    a2 = _clone(a1)
+    loss = torch.tensor(losses, dtype=torch.float32, device=dev())
+    pert = Z.Pert(7, 11, 0, 1e-3)
+    nxt = Z.Pert(7, 12, 0, 1e-3)
+    adam = Z.adam_desc(1e-4, 11)
+    st1 = torch.zeros(1, dtype=torch.int32, device=dev())
+    st2 = torch.zeros(1, dtype=torch.int32, device=dev())
+    ch1 = torch.empty(2 * k, dtype=torch.bfloat16, device=dev())
+    ch2 = torch.full((2 * k,), float("nan"), dtype=torch.bfloat16, device=dev())
+    c0 = a1.c.clone()
+
+    Z.step(a1, loss, pert, adam, st1)
+    Z.perturb_coeffs(a1, 0, k, nxt, ch1)
+    Z.step_perturb(a2, loss, pert, adam, nxt, ch2, st2)
+    torch.cuda.synchronize()
+
+    for name in ("c", "m", "v"):
+        assert torch.equal(_bits(getattr(a1, name)), _bits(getattr(a2, name))), name
+    assert torch.equal(ch1.view(torch.int16), ch2.view(torch.int16))
+    assert int(st1.item()) == int(st2.item())
+    if not math.isfinite(losses[0] - losses[1]):
+        assert int(st2.item()) & 1
+        assert torch.equal(_bits(a2.c), _bits(c0))
+    else:
+        assert int(st2.item()) == 0
+        assert not torch.equal(_bits(a2.c), _bits(c0))
+
+
+def test_step_perturb_rejects_bad_arguments():
+    a = _arena(64, False, 1)
+    loss = torch.zeros(2, dtype=torch.float32, device=dev())
+    ch = torch.empty(128, dtype=torch.bfloat16, device=dev())
+    p = Z.Pert(1, 1, 0, 1e-3)
+    with pytest.raises(Z.ZoactError):
+        Z.step_perturb(a, loss, p, Z.adam_desc(1e-4, 1), p, ch[1:])   # misaligned ch_next
