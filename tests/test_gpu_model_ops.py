@@ -147,11 +147,12 @@ def test_attention_bf16(B, S, H, Hkv, hd):
     assert np.mean(np.abs(got - want)) <= 0.05 * np.mean(tol)
 
 
-def test_attention_llama_shape_sampled():
-    """32 sequences of 256 tokens, 32 query and 8 key/value heads of 128: the attention of
-    the Llama-3-8B step (both perturbation halves).  The oracle runs on three of the
+@pytest.mark.parametrize("B,S,H,Hkv,hd", [(32, 256, 32, 8, 128), (64, 256, 16, 4, 64)])
+def test_attention_full_length_sampled(B, S, H, Hkv, hd):
+    """Full 256-token sequences on grids that fill the chip (whole-sequence-resident kernel):
+    32 sequences with 32 query and 8 key/value heads of 128 (the attention of the Llama-3-8B
+    step, both perturbation halves), and head size 64.  The oracle runs on three of the
     sequences; same bound as test_attention_bf16."""
-    B, S, H, Hkv, hd = 32, 256, 32, 8, 128
     announce("attention bf16 sampled", B, S, H, Hkv, hd)
     ld = (H + 2 * Hkv) * hd
     qkv = _vals((B * S, ld), 1.0, 5, 4242, bf16=True)
@@ -161,7 +162,7 @@ def test_attention_llama_shape_sampled():
                 float(np.float32(1.0 / math.sqrt(hd))))
     got = host(out).reshape(B, S, H * hd)
     x = qkv.reshape(B, S, ld)
-    for b in (0, 17, 31):
+    for b in (0, B // 2 + 1, B - 1):
         q = x[b:b + 1, :, :H * hd].reshape(1, S, H, hd)
         k = x[b:b + 1, :, H * hd:(H + Hkv) * hd].reshape(1, S, Hkv, hd)
         v = x[b:b + 1, :, (H + Hkv) * hd:].reshape(1, S, Hkv, hd)
