@@ -62,6 +62,18 @@ zoact_status zoact_attention(const void* q, int64_t ldq, const void* k, int64_t 
                              int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
                              float scale, int32_t dtype, void* out, zoact_stream stream);
 
+/* zoact_rope on q (n_heads) and k (n_kv_heads) with the fp32 tables cos/sin
+ * [seq][head_dim/2] (16-byte aligned), then zoact_attention: the same output bits as the
+ * two calls.  Where the whole sequence is held in LDS (bf16, seq <= 256, four or more
+ * query heads per key/value head, a grid of at least one workgroup per compute unit) the
+ * rotation happens as q and k are read and the q and k buffers keep their values; else
+ * they are rotated in place first.  So after the call q and k hold either the rotated or
+ * the original values: callers treat them as consumed. */
+zoact_status zoact_attention_rope(void* q, int64_t ldq, void* k, int64_t ldk, const void* v, int64_t ldv,
+                                  int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                                  float scale, int32_t dtype, const float* cos_t, const float* sin_t, void* out,
+                                  zoact_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -196,6 +196,17 @@ __global__ void __launch_bounds__(256) layernorm_bf16_vec_kernel(const uint16_t*
   }
 }
 
+// One rotary pair: (lo, hi) -> (lo c - hi s, hi c + lo s), products rounded before the
+// sum (no contraction), so that every kernel that rotates gives the same bits.
+__device__ __forceinline__ float rot_lo(float lo, float hi, float c, float s) {
+#pragma clang fp contract(off)
+  return lo * c - hi * s;
+}
+__device__ __forceinline__ float rot_hi(float lo, float hi, float c, float s) {
+#pragma clang fp contract(off)
+  return hi * c + lo * s;
+}
+
 // bf16 rotary embedding with 16-byte accesses: one thread rotates 8 pairs (j .. j + 7 with
 // their partners j + half .. j + half + 7) of one head of one row.
 __global__ void rope_bf16_vec_kernel(uint16_t* __restrict__ x, int64_t rows, int64_t ld, int64_t col0, int heads,
@@ -226,8 +237,8 @@ __global__ void rope_bf16_vec_kernel(uint16_t* __restrict__ x, int64_t rows, int
         const float lo = bf2f((uint16_t)(q ? lw[e] >> 16 : lw[e] & 0xFFFF));
         const float hi = bf2f((uint16_t)(q ? hw[e] >> 16 : hw[e] & 0xFFFF));
         const float c = cv[2 * e + q], sn = sv[2 * e + q];
-        lo_r[q] = f2bf(lo * c - hi * sn);
-        hi_r[q] = f2bf(hi * c + lo * sn);
+        lo_r[q] = f2bf(rot_lo(lo, hi, c, sn));
+        hi_r[q] = f2bf(rot_hi(lo, hi, c, sn));
       }
       lo_o[e] = (uint32_t)lo_r[0] | ((uint32_t)lo_r[1] << 16);
       hi_o[e] = (uint32_t)hi_r[0] | ((uint32_t)hi_r[1] << 16);
@@ -250,8 +261,8 @@ __global__ void rope_kernel(T* __restrict__ x, int64_t rows, int64_t ld, int64_t
     T* p = x + r * ld + col0 + (int64_t)h * hd;
     const float c = ct[pos * half + j], s = st[pos * half + j];
     const float lo = ld_act(p, j), hi = ld_act(p, j + half);
-    st_act(p, j, lo * c - hi * s);
-    st_act(p, j + half, hi * c + lo * s);
+    st_act(p, j, rot_lo(lo, hi, c, s));
+    st_act(p, j + half, rot_hi(lo, hi, c, s));
   }
 }
 
@@ -705,7 +716,8 @@ __global__ void __launch_bounds__(1024 / QB, 1) attention_res_kernel(const uint1
                                                                    const uint16_t* __restrict__ k, int64_t ldk,
                                                                    const uint16_t* __restrict__ v, int64_t ldv,
                                                                    int64_t seq, int heads, int kv_heads, float scale,
-                                                                   uint16_t* __restrict__ out) {
+                                                                   uint16_t* __restrict__ out, const float* __restrict__ rc,
+                                                                   const float* __restrict__ rs) {
   constexpr int KC = HD / 8;    // 16-byte chunks per row
   constexpr int KS = HD / 32;   // 32-deep steps over the head dimension
   constexpr int ND = HD / 16;   // 16-row blocks of the head dimension
@@ -733,7 +745,55 @@ __global__ void __launch_bounds__(1024 / QB, 1) attention_res_kernel(const uint1
   // masked probabilities (exactly zero) never meet non-finite values.  Loads go out in
   // batches (eight K chunks, then four V key pairs, per thread) before their LDS writes.
   const int nkc = nk * KC, nvi = (nk / 2) * KC;
-  for (int c0 = threadIdx.x; c0 < nkc; c0 += 8 * nthr) {
+  // with rotary tables (rc, rs: [seq][HD / 2] fp32) q and k are rotated as they are read,
+  // rounded to bf16 as a separate rotary pass would store them: a thread takes chunk ch of a
+  // key row with its partner ch + KC / 2
+  constexpr int KH = KC / 2;
+  if (rc != nullptr) {
+    const int nkp = nk * KH;
+    for (int c0 = threadIdx.x; c0 < nkp; c0 += 4 * nthr) {
+      uint4 ka[4], kb[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = c0 + u * nthr < nkp ? c0 + u * nthr : nkp - 1;
+        const int key = c / KH, ch = c % KH;
+        const int64_t row = key < seq ? key : seq - 1;
+        const uint16_t* kr = k + (r0 + row) * ldk + (int64_t)hk * HD;
+        ka[u] = *reinterpret_cast<const uint4*>(kr + ch * 8);
+        kb[u] = *reinterpret_cast<const uint4*>(kr + (ch + KH) * 8);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = c0 + u * nthr;
+        if (c < nkp) {
+          const int key = c / KH, ch = c % KH;
+          const int64_t pos = key < seq ? key : seq - 1;
+          const float* cp = rc + pos * (HD / 2) + ch * 8;
+          const float* sp = rs + pos * (HD / 2) + ch * 8;
+          const uint32_t aw[4] = {ka[u].x, ka[u].y, ka[u].z, ka[u].w}, bw[4] = {kb[u].x, kb[u].y, kb[u].z, kb[u].w};
+          uint32_t ao[4], bo[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            uint16_t lo_r[2], hi_r[2];
+#pragma unroll
+            for (int q2 = 0; q2 < 2; ++q2) {
+              const float lo = bf2f((uint16_t)(q2 ? aw[e] >> 16 : aw[e] & 0xFFFF));
+              const float hi = bf2f((uint16_t)(q2 ? bw[e] >> 16 : bw[e] & 0xFFFF));
+              const float cv = cp[2 * e + q2], sv = sp[2 * e + q2];
+              lo_r[q2] = f2bf(rot_lo(lo, hi, cv, sv));
+              hi_r[q2] = f2bf(rot_hi(lo, hi, cv, sv));
+            }
+            ao[e] = (uint32_t)lo_r[0] | ((uint32_t)lo_r[1] << 16);
+            bo[e] = (uint32_t)hi_r[0] | ((uint32_t)hi_r[1] << 16);
+          }
+          *reinterpret_cast<uint4*>(ks + key * HD + ((ch ^ (key & KSW)) * 8)) = make_uint4(ao[0], ao[1], ao[2], ao[3]);
+          *reinterpret_cast<uint4*>(ks + key * HD + (((ch + KH) ^ (key & KSW)) * 8)) =
+              make_uint4(bo[0], bo[1], bo[2], bo[3]);
+        }
+      }
+    }
+  }
+  for (int c0 = threadIdx.x; c0 < (rc != nullptr ? 0 : nkc); c0 += 8 * nthr) {
     uint4 kr[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -795,6 +855,23 @@ __global__ void __launch_bounds__(1024 / QB, 1) attention_res_kernel(const uint1
       const uint16_t* qp = q + (r0 + qr) * ldq + (int64_t)h * HD;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) qf[b][kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + lk * 8);
+      if (rc != nullptr) {
+        // depth kk*32 + lk*8 + e (kk < KS / 2) pairs with the same lane's kk + KS / 2
+#pragma unroll
+        for (int kk = 0; kk < KS / 2; ++kk) {
+          const float* cp = rc + qr * (HD / 2) + kk * 32 + lk * 8;
+          const float* sp = rs + qr * (HD / 2) + kk * 32 + lk * 8;
+          bf16x8 lo8 = qf[b][kk], hi8 = qf[b][kk + KS / 2];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float lo = (float)lo8[e], hi = (float)hi8[e];
+            lo8[e] = (__bf16)rot_lo(lo, hi, cp[e], sp[e]);
+            hi8[e] = (__bf16)rot_hi(lo, hi, cp[e], sp[e]);
+          }
+          qf[b][kk] = lo8;
+          qf[b][kk + KS / 2] = hi8;
+        }
+      }
     }
     const int64_t ulast = q0 + 16 * QB - 1 < seq - 1 ? q0 + 16 * QB - 1 : seq - 1;
     const int nkb = (int)(ulast / 64) + 1;
@@ -1039,9 +1116,23 @@ extern "C" zoact_status zoact_rope(void* x, int32_t dtype, int64_t rows, int64_t
   return launched("rope");
 }
 
-extern "C" zoact_status zoact_attention(const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v,
-                                        int64_t ldv, int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads,
-                                        int32_t head_dim, float scale, int32_t dtype, void* out, zoact_stream stream) {
+// Whole sequence resident in LDS: bf16, groups of four or more query heads per key/value
+// head (sixteen waves per workgroup), seq <= 256, and a grid of one workgroup per
+// (sequence, key/value head, four query heads) that covers every compute unit; smaller
+// grids run the staged kernel, which splits the queries over more workgroups.
+static bool attention_resident(int32_t dtype, int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads,
+                               int32_t head_dim) {
+  if (dtype != ZOACT_BF16 || (head_dim != 64 && head_dim != 128) || n_kv_heads < 1 || n_heads % n_kv_heads) return false;
+  const int G = n_heads / n_kv_heads;
+  const int ncu = cu_count();
+  return ncu > 0 && G % 4 == 0 && seq <= 256 && (int64_t)n_kv_heads * (G / 4) <= 65535 &&
+         n_seq * n_kv_heads * (G / 4) >= ncu;
+}
+
+// Argument checks of the attention entry points (before anything is enqueued).
+static zoact_status attention_check(const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v, int64_t ldv,
+                                    int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                                    int32_t dtype, const void* out) {
   ZO_CHECK(q && k && v && out, "attention: NULL pointer");
   ZO_CHECK(n_seq >= 1 && seq >= 1 && n_heads >= 1 && n_kv_heads >= 1 && n_heads % n_kv_heads == 0,
            "attention: bad shape or head grouping");
@@ -1049,30 +1140,40 @@ extern "C" zoact_status zoact_attention(const void* q, int64_t ldq, const void* 
                ldv >= (int64_t)n_kv_heads * head_dim,
            "attention: row strides smaller than the heads");
   ZO_CHECK(n_seq <= 65535 && n_heads <= 65535, "attention: grid too large");
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (dtype == ZOACT_BF16) {
     ZO_CHECK(head_dim == 64 || head_dim == 128, "attention: bf16 head_dim must be 64 or 128");
     ZO_CHECK(ldq % 8 == 0 && ldk % 8 == 0 && ldv % 8 == 0, "attention: bf16 strides must be multiples of 8");
+  } else if (dtype == ZOACT_F32) {
+    ZO_CHECK(head_dim <= 128 && seq * head_dim <= 4096, "attention: fp32 path needs head_dim <= 128, seq*hd <= 4096");
+  } else {
+    return zoact::set_error(ZOACT_E_INVALID, "attention: dtype must be F32 or BF16");
+  }
+  return ZOACT_OK;
+}
+
+static zoact_status attention_impl(const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v, int64_t ldv,
+                                   int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                                   float scale, int32_t dtype, void* out, const float* rc, const float* rs,
+                                   zoact_stream stream) {
+  const zoact_status chk = attention_check(q, ldq, k, ldk, v, ldv, n_seq, seq, n_heads, n_kv_heads, head_dim, dtype,
+                                           out);
+  if (chk != ZOACT_OK) return chk;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (dtype == ZOACT_BF16) {
     const int G = n_heads / n_kv_heads;
-    // Whole sequence resident in LDS: for groups of four or more query heads per key/value
-    // head (sixteen waves per workgroup), when the grid of one workgroup per (sequence,
-    // key/value head, four query heads) covers every compute unit; smaller grids run the
-    // staged kernel below, which splits the queries over more workgroups
-    const int ncu = cu_count();
-    if (ncu <= 0) return zoact::set_error(ZOACT_E_HIP, "attention: device query failed");
-    if (G % 4 == 0 && seq <= 256 && (int64_t)n_kv_heads * (G / 4) <= 65535 &&
-        n_seq * n_kv_heads * (G / 4) >= ncu) {
+    if (attention_resident(dtype, n_seq, seq, n_heads, n_kv_heads, head_dim)) {
       const dim3 g1((unsigned)n_seq, (unsigned)(n_kv_heads * (G / 4)));
       if (head_dim == 128)
         attention_res_kernel<128, 1><<<g1, 1024, 0, s>>>((const uint16_t*)q, ldq, (const uint16_t*)k, ldk,
                                                          (const uint16_t*)v, ldv, seq, n_heads, n_kv_heads, scale,
-                                                         (uint16_t*)out);
+                                                         (uint16_t*)out, rc, rs);
       else
         attention_res_kernel<64, 1><<<g1, 1024, 0, s>>>((const uint16_t*)q, ldq, (const uint16_t*)k, ldk,
                                                         (const uint16_t*)v, ldv, seq, n_heads, n_kv_heads, scale,
-                                                        (uint16_t*)out);
+                                                        (uint16_t*)out, rc, rs);
       return launched("attention");
     }
+    ZO_CHECK(rc == nullptr, "attention: rotary tables reach only the resident kernel");
     if ((G == 1 || G == 2 || G % 4 == 0) && (int64_t)n_kv_heads * (G < 4 ? 1 : G / 4) <= 65535) {
       constexpr int QB = 2;                     // 16-query blocks per wave
       const int HG = G < 4 ? G : 4;
@@ -1107,4 +1208,32 @@ extern "C" zoact_status zoact_attention(const void* q, int64_t ldq, const void* 
     return zoact::set_error(ZOACT_E_INVALID, "attention: dtype must be F32 or BF16");
   }
   return launched("attention");
+}
+
+extern "C" zoact_status zoact_attention(const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v,
+                                        int64_t ldv, int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads,
+                                        int32_t head_dim, float scale, int32_t dtype, void* out, zoact_stream stream) {
+  return attention_impl(q, ldq, k, ldk, v, ldv, n_seq, seq, n_heads, n_kv_heads, head_dim, scale, dtype, out, nullptr,
+                        nullptr, stream);
+}
+
+extern "C" zoact_status zoact_attention_rope(void* q, int64_t ldq, void* k, int64_t ldk, const void* v, int64_t ldv,
+                                             int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads,
+                                             int32_t head_dim, float scale, int32_t dtype, const float* cos_t,
+                                             const float* sin_t, void* out, zoact_stream stream) {
+  const zoact_status chk = attention_check(q, ldq, k, ldk, v, ldv, n_seq, seq, n_heads, n_kv_heads, head_dim, dtype,
+                                           out);
+  if (chk != ZOACT_OK) return chk;
+  ZO_CHECK(cos_t && sin_t, "attention_rope: NULL rotary table");
+  ZO_CHECK(((uintptr_t)cos_t % 16) == 0 && ((uintptr_t)sin_t % 16) == 0, "attention_rope: tables must be 16-byte aligned");
+  if (attention_resident(dtype, n_seq, seq, n_heads, n_kv_heads, head_dim))
+    return attention_impl(q, ldq, k, ldk, v, ldv, n_seq, seq, n_heads, n_kv_heads, head_dim, scale, dtype, out, cos_t,
+                          sin_t, stream);
+  // other shapes: the rotary pass in place, then attention
+  zoact_status st = zoact_rope(q, dtype, n_seq * seq, ldq, 0, n_heads, head_dim, seq, cos_t, sin_t, stream);
+  if (st != ZOACT_OK) return st;
+  st = zoact_rope(k, dtype, n_seq * seq, ldk, 0, n_kv_heads, head_dim, seq, cos_t, sin_t, stream);
+  if (st != ZOACT_OK) return st;
+  return attention_impl(q, ldq, k, ldk, v, ldv, n_seq, seq, n_heads, n_kv_heads, head_dim, scale, dtype, out, nullptr,
+                        nullptr, stream);
 }

@@ -303,12 +303,10 @@ class Decoder:
                 self._apply(P["k"], B["a"], T, B["k"], pert, None, adapt=False)
                 q, k, v = qkv[:, :d], B["k"], qkv[:, d:]
             if cos_sin is not None:
-                if "qkv" in P:      # q and k heads are adjacent columns of the fused row
-                    Z.rope(qkv, 0, H + Hkv, hd, seq, *cos_sin)
-                else:
-                    Z.rope(qkv, 0, H, hd, seq, *cos_sin)
-                    Z.rope(B["k"], 0, Hkv, hd, seq, *cos_sin)
-            Z.attention(q, k, v, B["att"], 2 * n_seq, seq, H, Hkv, hd, scale)
+                # rotary on q and k, inside the attention where it holds the sequence in LDS
+                Z.attention_rope(q, k, v, B["att"], 2 * n_seq, seq, H, Hkv, hd, scale, *cos_sin)
+            else:
+                Z.attention(q, k, v, B["att"], 2 * n_seq, seq, H, Hkv, hd, scale)
             ut = self._site(l, "o", B["att"], adapt, calibrate)
             self._apply(P["o"], B["att"], T, h_alt, pert, ut, residual=h, adapt=adapt)
             h, h_alt = h_alt, h

@@ -110,6 +110,8 @@ SIGNATURES = {
     "zoact_layernorm": ([_P, _P, _P, _I64, _I64, _F, _I32, _P, _P], _I32),
     "zoact_rope": ([_P, _I32, _I64, _I64, _I64, _I32, _I32, _I64, _P, _P, _P], _I32),
     "zoact_attention": ([_P, _I64, _P, _I64, _P, _I64, _I64, _I64, _I32, _I32, _I32, _F, _I32, _P, _P], _I32),
+    "zoact_attention_rope": ([_P, _I64, _P, _I64, _P, _I64, _I64, _I64, _I32, _I32, _I32, _F, _I32, _P, _P, _P, _P],
+                             _I32),
 }
 
 _lib = None
@@ -396,6 +398,15 @@ def rope(x: torch.Tensor, col0: int, n_heads: int, head_dim: int, seq: int, cos_
     ld = x.shape[-1]
     _check(lib().zoact_rope(_ptr(x), dtype_code(x), x.numel() // ld, ld, col0, n_heads, head_dim, seq, _ptr(cos_t),
                             _ptr(sin_t), _stream(stream)))
+
+
+def attention_rope(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: torch.Tensor, n_seq: int, seq: int,
+                   n_heads: int, n_kv_heads: int, head_dim: int, scale: float, cos_t: torch.Tensor,
+                   sin_t: torch.Tensor, stream=None):
+    """Rotary on q and k, then attention; q and k are consumed (left rotated or not)."""
+    _check(lib().zoact_attention_rope(_ptr(q), q.stride(0), _ptr(k), k.stride(0), _ptr(v), v.stride(0), n_seq, seq,
+                                      n_heads, n_kv_heads, head_dim, scale, dtype_code(out), _ptr(cos_t), _ptr(sin_t),
+                                      _ptr(out), _stream(stream)))
 
 
 def attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: torch.Tensor, n_seq: int, seq: int, n_heads: int,

@@ -174,6 +174,30 @@ def test_attention_full_length_sampled(B, S, H, Hkv, hd):
         assert np.mean(np.abs(got[b] - want)) <= 0.05 * np.mean(tol)
 
 
+@pytest.mark.parametrize("B,S,H,Hkv,hd", [(32, 256, 32, 8, 128), (128, 33, 8, 2, 64), (64, 130, 16, 4, 128),
+                                          (2, 100, 8, 2, 128), (3, 70, 4, 4, 64)])
+def test_attention_rope_equals_rope_then_attention(B, S, H, Hkv, hd):
+    """zoact_attention_rope against zoact_rope on q and k followed by zoact_attention, bit
+    for bit: on chip-filling grids the rotation happens inside the whole-sequence-resident
+    kernel as q and k are read; the last two shapes take the rotary pass first."""
+    announce("attention_rope", B, S, H, Hkv, hd)
+    ld = (H + 2 * Hkv) * hd
+    qkv = t_bf16(_vals((B * S, ld), 1.0, 6, S, bf16=True))
+    cos, sin = om.rope_tables(S, hd, 5e5)
+    ct, st = t_f32(cos), t_f32(sin)
+    scale = float(np.float32(1.0 / math.sqrt(hd)))
+    ref_in = qkv.clone()
+    Z.rope(ref_in, 0, H + Hkv, hd, S, ct, st)
+    ref = torch.empty(B * S, H * hd, dtype=torch.bfloat16, device=dev())
+    Z.attention(ref_in[:, :H * hd], ref_in[:, H * hd:(H + Hkv) * hd], ref_in[:, (H + Hkv) * hd:], ref, B, S, H, Hkv,
+                hd, scale)
+    out = torch.empty_like(ref)
+    Z.attention_rope(qkv[:, :H * hd], qkv[:, H * hd:(H + Hkv) * hd], qkv[:, (H + Hkv) * hd:], out, B, S, H, Hkv, hd,
+                     scale, ct, st)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+
+
 @pytest.mark.parametrize("B,S,H,Hkv,hd", [(4, 64, 4, 4, 32), (2, 17, 4, 2, 16), (1, 1, 1, 1, 8)])
 def test_attention_f32(B, S, H, Hkv, hd):
     announce("attention f32", B, S, H, Hkv, hd)
