@@ -751,25 +751,30 @@ __global__ void __launch_bounds__(1024 / QB, 1) attention_res_kernel(const uint1
   constexpr int KH = KC / 2;
   if (rc != nullptr) {
     const int nkp = nk * KH;
-    for (int c0 = threadIdx.x; c0 < nkp; c0 += 4 * nthr) {
-      uint4 ka[4], kb[4];
+    for (int c0 = threadIdx.x; c0 < nkp; c0 += 2 * nthr) {
+      uint4 ka[2], kb[2];
+      float4 cva[2][2], sva[2][2];   // the 8 cos / sin values of the chunk's pairs
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 2; ++u) {
         const int c = c0 + u * nthr < nkp ? c0 + u * nthr : nkp - 1;
         const int key = c / KH, ch = c % KH;
         const int64_t row = key < seq ? key : seq - 1;
         const uint16_t* kr = k + (r0 + row) * ldk + (int64_t)hk * HD;
         ka[u] = *reinterpret_cast<const uint4*>(kr + ch * 8);
         kb[u] = *reinterpret_cast<const uint4*>(kr + (ch + KH) * 8);
+        const float4* cp = reinterpret_cast<const float4*>(rc + row * (HD / 2) + ch * 8);
+        const float4* sp = reinterpret_cast<const float4*>(rs + row * (HD / 2) + ch * 8);
+        cva[u][0] = cp[0], cva[u][1] = cp[1], sva[u][0] = sp[0], sva[u][1] = sp[1];
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 2; ++u) {
         const int c = c0 + u * nthr;
         if (c < nkp) {
           const int key = c / KH, ch = c % KH;
-          const int64_t pos = key < seq ? key : seq - 1;
-          const float* cp = rc + pos * (HD / 2) + ch * 8;
-          const float* sp = rs + pos * (HD / 2) + ch * 8;
+          const float cv[8] = {cva[u][0].x, cva[u][0].y, cva[u][0].z, cva[u][0].w,
+                               cva[u][1].x, cva[u][1].y, cva[u][1].z, cva[u][1].w};
+          const float sv[8] = {sva[u][0].x, sva[u][0].y, sva[u][0].z, sva[u][0].w,
+                               sva[u][1].x, sva[u][1].y, sva[u][1].z, sva[u][1].w};
           const uint32_t aw[4] = {ka[u].x, ka[u].y, ka[u].z, ka[u].w}, bw[4] = {kb[u].x, kb[u].y, kb[u].z, kb[u].w};
           uint32_t ao[4], bo[4];
 #pragma unroll
@@ -779,9 +784,8 @@ __global__ void __launch_bounds__(1024 / QB, 1) attention_res_kernel(const uint1
             for (int q2 = 0; q2 < 2; ++q2) {
               const float lo = bf2f((uint16_t)(q2 ? aw[e] >> 16 : aw[e] & 0xFFFF));
               const float hi = bf2f((uint16_t)(q2 ? bw[e] >> 16 : bw[e] & 0xFFFF));
-              const float cv = cp[2 * e + q2], sv = sp[2 * e + q2];
-              lo_r[q2] = f2bf(rot_lo(lo, hi, cv, sv));
-              hi_r[q2] = f2bf(rot_hi(lo, hi, cv, sv));
+              lo_r[q2] = f2bf(rot_lo(lo, hi, cv[2 * e + q2], sv[2 * e + q2]));
+              hi_r[q2] = f2bf(rot_hi(lo, hi, cv[2 * e + q2], sv[2 * e + q2]));
             }
             ao[e] = (uint32_t)lo_r[0] | ((uint32_t)lo_r[1] << 16);
             bo[e] = (uint32_t)hi_r[0] | ((uint32_t)hi_r[1] << 16);
@@ -856,17 +860,21 @@ __global__ void __launch_bounds__(1024 / QB, 1) attention_res_kernel(const uint1
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) qf[b][kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + lk * 8);
       if (rc != nullptr) {
-        // depth kk*32 + lk*8 + e (kk < KS / 2) pairs with the same lane's kk + KS / 2
+        // depth kk*32 + lk*8 + e (kk < KS / 2) pairs with the same lane's kk + KS / 2; the
+        // tables are read as aligned 16-byte vectors (rows of HD / 2 floats)
 #pragma unroll
         for (int kk = 0; kk < KS / 2; ++kk) {
-          const float* cp = rc + qr * (HD / 2) + kk * 32 + lk * 8;
-          const float* sp = rs + qr * (HD / 2) + kk * 32 + lk * 8;
+          const float4* cp = reinterpret_cast<const float4*>(rc + qr * (HD / 2) + kk * 32 + lk * 8);
+          const float4* sp = reinterpret_cast<const float4*>(rs + qr * (HD / 2) + kk * 32 + lk * 8);
+          const float4 c0 = cp[0], c1 = cp[1], s0 = sp[0], s1 = sp[1];
+          const float cv[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+          const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
           bf16x8 lo8 = qf[b][kk], hi8 = qf[b][kk + KS / 2];
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const float lo = (float)lo8[e], hi = (float)hi8[e];
-            lo8[e] = (__bf16)rot_lo(lo, hi, cp[e], sp[e]);
-            hi8[e] = (__bf16)rot_hi(lo, hi, cp[e], sp[e]);
+            lo8[e] = (__bf16)rot_lo(lo, hi, cv[e], sv[e]);
+            hi8[e] = (__bf16)rot_hi(lo, hi, cv[e], sv[e]);
           }
           qf[b][kk] = lo8;
           qf[b][kk + KS / 2] = hi8;
