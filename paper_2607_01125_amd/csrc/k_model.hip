@@ -710,7 +710,10 @@ __global__ void __launch_bounds__(256, 2) attention_gqa_kernel(const uint16_t* _
 // barrier is needed after the load.  A wave takes units of QB 16-query blocks (each K and
 // V^T fragment read from LDS feeds QB MFMAs).  Units are dealt so that every wave of a head
 // gets the same causal work: with QB = 2 the two waves take the units u with u mod 4 in
-// {w, 3 - w}; with QB = 1 wave w takes the units with u mod 4 = w.
+// {w, 3 - w}; with QB = 1 wave w takes the units with u mod 4 = w.  The launcher runs
+// QB = 1 (sixteen waves), which measured faster than two blocks per wave.
+// rc, rs (nullable): rotary tables [seq][HD / 2] fp32; when given, q and k are rotated as
+// they are read (rotate-half, the arithmetic and bf16 rounding of the rotary pass).
 template <int HD, int QB>
 __global__ void __launch_bounds__(1024 / QB, 1) attention_res_kernel(const uint16_t* __restrict__ q, int64_t ldq,
                                                                    const uint16_t* __restrict__ k, int64_t ldk,
