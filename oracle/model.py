@@ -29,10 +29,14 @@ attention rounds the probabilities to bf16 before multiplying by V (the normalis
 summed unrounded); logits are fp32; the loss is summed in float64.  fp32 mode computes
 in float64 throughout.
 
-Parity: pinned by tests/test_oracle_model.py (an independent torch float64 autograd
-implementation of the same model agrees to 1e-10; zero-output LM head gives ln V; with
-C = 0 both halves equal the base model; the two-sided difference matches the analytic
-directional derivative as eps -> 0).  Loss values of the random-initialised 8B/13B
+Parity: pinned by tests/test_oracle_model.py -- independent torch float64
+implementations of both families (Llama: complex rotary, SDPA, materialised W_eff; OPT:
+F.layer_norm, learned positions at s + 2, SDPA, ReLU MLP with biases, tied head) agree to
+1e-10 with nonzero norm weights, norm biases and projection biases; a torch rewrite of
+the bf16 rounding points (torch's bfloat16 cast at each stored tensor) gives the same
+logits bit for bit for both families; a zero-output LM head gives ln V; with C = 0 both
+halves equal the base model; the two-sided difference matches the autograd directional
+derivative as eps -> 0.  Loss values of the random-initialised 8B/13B
 shapes themselves are parity unpinned by the paper, which prints none.
 """
 from __future__ import annotations
