@@ -1,29 +1,31 @@
 """Benchmark of the forward-only ZO step on one MI355X.
 
-Headline workload (`single_linear_4096`): one adapted linear layer in bf16,
-d_in = d_out = 4096, rank r = 32, 8192 tokens per perturbation half, activations
-with a planted low-rank structure (64 directions carrying 90% of the variance),
-W ~ N(0, 0.02^2).  One step is the whole hot path of a +/- ZO step:
-    C +/- eps Z (one pass over C)  ->  P = x U (both halves)  ->  fused +/- adapted GEMM
-    whose epilogue sums the squared errors of both halves against a fixed in-subspace
-    teacher (y is never stored)  ->  ZO-Adam on C.
-The activation basis U comes from the one-shot basis initialisation (timed
-separately, outside the step).  Inputs are resident in HBM before timing starts.
+Headline workload (`llama3_8b_bf16_step`): one two-sided ZO step of a random-initialised
+Llama-3-8B-shaped decoder in bf16 -- 32 layers, d = 4096, 32 query / 8 key-value heads of
+128, SwiGLU FFN 14336, vocabulary 128256, rank r = 32 on all seven projections, 16 x 256
+uniform random tokens per perturbation half, eps = 1e-3, Adam lr = 5e-5.  One step is the
+whole hot path: both halves' forward with every adapted linear as one fused +/- GEMM (the
+perturbed coefficients C +/- eps Z read from the previous update pass), the LM head with
+the next-token cross entropy in its epilogue, then ZO-Adam on the 44,040,192 coefficients
+(whose pass also forms the next step's C +/- eps Z).  The basis (Algorithm 1 on 16 x 256
+calibration tokens) is computed before timing and reported separately.  Inputs and
+weights are resident in HBM before the timed region starts.
 
-Besides the headline line the run measures (unless --quick):
-  * the fused +/- adapted linear (coefficient pass + projection + fused GEMM) at the
-    Llama-3-8B layer shapes, M = 8192 stacked rows, bf16 and INT4 weights: TFLOP/s per
-    shape and the FLOP-weighted mean; the o-projection shape across ranks 1..256;
-  * full ZO steps of random-initialised decoders: Llama-3-8B shape in bf16 and with
-    INT4 weights (16 x 256 tokens, r = 32 on all seven projections) and OPT-13B
-    shape in bf16 (8 x 512 tokens, r = 64 on q, v, out, fc1, fc2, basis
-    initialisation from 32 x 512 calibration tokens timed): steps/s, model TFLOP/s;
-  * ZO-Adam over the Llama-3-8B arena (44,040,192 coefficients): GB/s against HBM;
-  * the one-sided q = 8 form of the Llama step (five stacked forwards) and its update.
+`roofline` is the fused +/- adapted GEMM (`gemm_4w64_kernel`) over every adapted-linear
+launch of the timed steps: algorithmic FLOPs per launch (2 M N K + 2 M r N, M = 2 x 4096
+stacked rows; the shared first projection 2 T N K + 2 M r N) over the mean launch duration,
+both from HIP events recorded around each launch on its stream, against the 2.5 PFLOP/s
+dense bf16 MFMA peak.
 
-Prints one JSON line.  `roofline` is the fused GEMM of the headline workload:
-algorithmic FLOPs per launch over its mean duration (HIP events on its stream),
-against the 2.5 PFLOP/s dense bf16 MFMA peak.
+Besides the headline the run measures (unless --quick): the single adapted linear
+(4096 x 4096, r = 32, 8192 tokens per half) in its stacked and shared-input forms; the
+fused +/- adapted linear at the Llama-3-8B layer shapes (bf16, INT4 in-register, INT4 via
+the dequantisation pass) and across ranks; the INT4 Llama step; the OPT-13B-shape step with
+its basis initialisation; ZO-Adam's HBM rate over the Llama arena; the one-sided q = 8 form;
+the tiny fp32 model's 20 steps.  `cpu_baseline` is the oracle timed on the host cores on a
+bounded sample of the headline step, extrapolated to a whole step.
+
+Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -44,6 +46,7 @@ METRIC = "ZO steps/sec (±ε forwards + Adam) and adapted-linear TFLOP/s at 8B s
 DOMINANT_KERNEL = "gemm_4w64_kernel"
 DOMINANT_SOURCES = [os.path.join("paper_2607_01125_amd", "csrc", f)
                     for f in ("k_gemm_4w64.hip", "gemm_4w_epi.hpp", "gemm_common.hpp")]
+HEADLINE = "llama3_8b_bf16_step"
 
 
 class TimingEvent:
@@ -134,9 +137,101 @@ def traffic_record(kernel: str, workload: str, sources):
 
 
 # ------------------------------------------------------------------ CPU baseline (the oracle)
-def cpu_baseline(T, K, N, r, budget_s=12.0):
-    """The oracle (NumPy, float64 products, bf16 rounding emulated) on the same workload:
-    whole steps until about `budget_s` seconds of host time have been spent."""
+def _host_cores():
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count()
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    threads = cores
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
+        if blas:
+            threads = max(blas)
+    except Exception:
+        pass
+    return cores, threads, model
+
+
+def cpu_baseline_llama():
+    """The oracle (NumPy, float64 products, bf16 rounding points emulated) on a bounded
+    sample of the headline step, extrapolated to one whole step.
+
+    A step is L+ and L- (each: embedding, 32 layers, final norm, LM head, cross entropy over
+    16 x 256 tokens) and ZO-Adam over k = 44,040,192 coefficients.  Timed: one half's loss of
+    a one-layer model at full width on 4 of the 16 sequences, once with the full vocabulary
+    and once with an 8-token head; and the Adam update (Gaussians regenerated) over 4,194,304
+    coefficients.  Every step of the oracle is per sequence, per layer or per coefficient, so
+    the step time is  2 halves x 4 x (32 x t_layer + t_head) + (k / 4,194,304) x t_adam  with
+    t_layer the 8-token-head time (it also holds the embedding and the final norm) and t_head
+    the difference of the two."""
+    import dataclasses as dc
+
+    import numpy as np
+
+    import synth
+    from oracle import adam as oadam
+    from oracle import model as om
+    from oracle import rng as orng
+
+    full = synth.LLAMA3_8B
+    shape = synth.shrink(full, n_layers=1)
+    B, S, n_seq = 16, 256, 4
+    t_gen = time.perf_counter()
+    W = synth.model_weights(shape, 0, "bf16")
+    small = dc.replace(shape, vocab=8)
+    Ws = dict(W)
+    Ws["emb"], Ws["head"] = W["emb"][:8].copy(), W["head"][:8].copy()
+    gen_s = time.perf_counter() - t_gen
+    tok = synth.uniform_tokens(B, S, full.vocab, 0, 2)[:n_seq]
+    m_full = om.Model(shape, 0, "bf16", weights=W)
+    m_small = om.Model(small, 0, "bf16", weights=Ws)
+    for m in (m_full, m_small):
+        for key, d_in in {(0, "attn"): 4096, (0, "o"): 4096, (0, "mlp"): 4096, (0, "down"): 14336}.items():
+            q, _ = np.linalg.qr(synth.gen(0, 881, d_in).standard_normal((d_in, full.rank)))
+            m.U[key] = q.astype(np.float32).astype(np.float64)
+    c = np.zeros(m_full.k, np.float32)
+    t0 = time.perf_counter()
+    m_small.loss(tok % 8, c, +1, 1e-3, (1, 1, 0))
+    t_layer = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    m_full.loss(tok, c, +1, 1e-3, (1, 1, 0))
+    t_full = time.perf_counter() - t0
+    t_head = max(t_full - t_layer, 0.0)
+    n_adam = 4_194_304
+    ca = np.zeros(n_adam, np.float32)
+    t0 = time.perf_counter()
+    z = orng.gauss_range(1, 1, 0, 0, n_adam)
+    oadam.zo_adam(ca, ca, ca, 0.25, z, oadam.adam_scalars(5e-5, 1))
+    t_adam = time.perf_counter() - t0
+    k = om.arena_size(full)
+    scale = B // n_seq
+    step_s = 2 * scale * (full.n_layers * t_layer + t_head) + (k / n_adam) * t_adam
+    cores, threads, model = _host_cores()
+    return {"value": round(1.0 / step_s, 7), "unit": "ZO steps/s", "cores": threads, "kind": "oracle",
+            "extrapolated": True, "cpu_model": model, "cores_available": cores,
+            "seconds_per_step": round(step_s, 1),
+            "sample": (f"one half's loss of a one-layer full-width Llama-3-8B-shape model on {n_seq} of {B} "
+                       f"sequences of {S} tokens, with the 128256-token head ({t_full:.2f} s) and with an 8-token "
+                       f"head ({t_layer:.2f} s), plus ZO-Adam with regenerated Gaussians over {n_adam} "
+                       f"coefficients ({t_adam:.2f} s); extrapolated as 2 halves x {scale} x (32 layers x "
+                       f"{t_layer:.2f} s + head {t_head:.2f} s) + {k / n_adam:.1f} x {t_adam:.2f} s = "
+                       f"{step_s:.0f} s per step; NumPy float64 products with the bf16 rounding points "
+                       f"emulated (weights generated untimed in {gen_s:.0f} s)")}
+
+
+def cpu_baseline_single(T, K, N, r, budget_s=8.0):
+    """The oracle on the single-layer workload (stacked form): whole steps until about
+    `budget_s` seconds of host time have been spent."""
     import numpy as np
 
     import synth
@@ -148,7 +243,7 @@ def cpu_baseline(T, K, N, r, budget_s=12.0):
     x, q = synth.planted_lowrank(T, K, seed=0)
     x = synth.bf16_round(x)
     w = synth.bf16_round(synth.normal((N, K), 0.02, 0, 2))
-    ut = synth.bf16_round(q[:, :r].T.copy())          # same shape as the initialised basis
+    ut = synth.bf16_round(q[:, :r].T.copy())
     tgt = synth.bf16_round(synth.normal((T, N), 1.0, 0, 5))
     c = np.zeros(N * r, np.float32)
     m = np.zeros_like(c)
@@ -156,20 +251,15 @@ def cpu_baseline(T, K, N, r, budget_s=12.0):
     xs = np.stack([x, x])
     t0 = time.perf_counter()
     steps = 0
-    while steps < 2 or time.perf_counter() - t0 < budget_s:
+    while steps < 1 or time.perf_counter() - t0 < budget_s:
         t = steps + 1
         y = olin.adapted_linear_pm(xs, w, None, ut, c.reshape(N, r), 1e-3, 1, t, 0, 0, "bf16")
         g = oadam.projected_grad(oloss.mse(y[0], tgt), oloss.mse(y[1], tgt), 1e-3)
         c, m, v, _ = oadam.zo_adam(c, m, v, g, orng.gauss_range(1, t, 0, 0, N * r), oadam.adam_scalars(1e-4, t))
         steps += 1
     dt = time.perf_counter() - t0
-    try:
-        cores = len(os.sched_getaffinity(0))
-    except AttributeError:
-        cores = os.cpu_count()
-    return {"value": round(steps / dt, 4), "unit": "ZO steps/s", "cores": cores, "kind": "oracle",
-            "sample": f"{steps} full steps of the headline workload ({T} tokens per half, d={K}, r={r}), "
-                      f"NumPy float64 products with bf16 rounding emulated, {dt:.1f} s"}
+    return {"value": round(steps / dt, 4), "unit": "ZO steps/s", "kind": "oracle",
+            "sample": f"{steps} full steps ({T} tokens per half, d={K}, r={r}), {dt:.1f} s"}
 
 
 # ------------------------------------------------------------------ headline: single adapted linear
@@ -263,28 +353,28 @@ def bench_single_linear(args, dev):
     # the stacked form (x given twice, base formed per half), same steps continued
     t_next = args.warmup + 1 + args.steps
     zo_step(t_next, shared=False)
-    st_steps = max(args.steps // 2, 5)
+    st_steps = max(args.steps, 5)
     st_ms, st_gemm_ms = timed(t_next + 1, st_steps, False)
-    flops = 2 * T * N * K + 2 * T * K * r + 2 * (2 * T) * r * N      # base once + projection once + two corrections
     gemm_flops = 2 * T * N * K + 2 * (2 * T) * r * N
     st_gemm_flops = 2 * (2 * T) * N * K + 2 * (2 * T) * r * N
-    achieved = gemm_flops / (gemm_ms * 1e-3) / 1e12
     assert int(status.item()) == 0, "non-finite projected gradient"
     return {
-        "ms_per_step": ms_per_step, "init_ms": init_ms, "flops": flops,
-        "roofline": {"kernel": f"{DOMINANT_KERNEL} (fused ± adapted GEMM, shared input, MSE epilogue: "
-                               f"M=8192 base rows, N=K=4096, r=32 per half; timed with the tile-sum kernel "
-                               f"that follows it)",
-                     "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic_record(DOMINANT_KERNEL, "single_linear_4096", DOMINANT_SOURCES),
-                     "flops_per_launch": gemm_flops, "mean_launch_us": round(gemm_ms * 1e3, 1)},
-        "stacked_form": {"steps_per_s": round(1e3 / st_ms, 3), "ms_per_step": round(st_ms, 4),
-                         "gemm_us": round(st_gemm_ms * 1e3, 1),
-                         "gemm_tflops": round(st_gemm_flops / (st_gemm_ms * 1e-3) / 1e12, 1),
-                         "note": "x given for both halves (M=16384 stacked rows)"},
+        "workload": "single adapted linear, bf16, d_in=d_out=4096, r=32, 8192 tokens per half, planted low-rank x "
+                    "(projection + fused ± forward with the MSE in its epilogue + ZO-Adam whose pass also forms the "
+                    "next step's C±εZ)",
+        "stacked": {"steps_per_s": round(1e3 / st_ms, 3), "ms_per_step": round(st_ms, 4),
+                    "gemm_us": round(st_gemm_ms * 1e3, 1),
+                    "gemm_tflops": round(st_gemm_flops / (st_gemm_ms * 1e-3) / 1e12, 1),
+                    "gemm_frac": round(st_gemm_flops / (st_gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                    "note": "x given for both halves (M=16384 stacked rows): the form the survey's cfg2 counts "
+                            "(2MNK + 2MrN = 554.0 GFLOP per launch)"},
+        "shared_x": {"steps_per_s": round(1e3 / ms_per_step, 3), "ms_per_step": round(ms_per_step, 4),
+                     "gemm_us": round(gemm_ms * 1e3, 1),
+                     "gemm_tflops": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
+                     "note": "both halves read one x: x W^T and x U formed once (279.2 GFLOP per launch); "
+                             "reported beside the stacked form, never as it"},
+        "basis_init_ms": round(init_ms, 1),
         "losses": losses,
-        "config": {"tokens_per_half": T, "d_in": K, "d_out": N, "rank": r, "eps": eps, "shared_x": True},
     }
 
 
@@ -429,7 +519,57 @@ def model_step_flops(shape, B, S):
     return lin + head + attn + proj + corr
 
 
-def bench_model(dev, which, warmup=2, steps=5):
+class LaunchTimer:
+    """Decoder.linear_hook that brackets every linear launch with fence-free HIP events on
+    the current stream, recording the launch's shape; the events are preallocated so the
+    timed loop creates none."""
+
+    def __init__(self, n_max):
+        self.pool = [(TimingEvent(), TimingEvent()) for _ in range(n_max)]
+        self.used = []
+        self.on = False
+
+    def __call__(self, stage, lin, T, flags):
+        if not self.on:
+            return
+        import torch
+
+        stream = torch.cuda.current_stream()
+        if stage == "pre":
+            if len(self.used) >= len(self.pool):
+                raise RuntimeError("LaunchTimer: event pool exhausted")
+            ev = self.pool[len(self.used)]
+            ev[0].record(stream)
+            self.used.append((ev, lin.d_in, lin.d_out, lin.r, T, flags))
+        else:
+            self.used[-1][0][1].record(stream)
+
+    def summary(self):
+        """Adapted-linear launches (r > 0): algorithmic FLOPs and durations, per shape and in total."""
+        import paper_2607_01125_amd.zoact as Z
+
+        shapes, n, tot_f, tot_s = {}, 0, 0.0, 0.0
+        for (e0, e1), K, N, r, T, flags in self.used:
+            if r == 0:
+                continue
+            shared = bool(flags & Z.SHARED_X)
+            n_out = N // 2 if flags & Z.EPI_SWIGLU else N
+            f = (2 * T * N * K if shared else 2 * (2 * T) * N * K) + 2 * (2 * T) * r * N
+            sec = e0.elapsed_time(e1) * 1e-3
+            key = f"{2 * T}x{N}x{K}" + (" shared" if shared else "") + (" swiglu" if flags & Z.EPI_SWIGLU else "")
+            d = shapes.setdefault(key, {"launches": 0, "flop": f, "s": 0.0, "out_features": n_out})
+            d["launches"] += 1
+            d["s"] += sec
+            n += 1
+            tot_f += f
+            tot_s += sec
+        per = {k: {"launches": v["launches"], "mean_us": round(v["s"] / v["launches"] * 1e6, 1),
+                   "gflop_per_launch": round(v["flop"] / 1e9, 2),
+                   "tflops": round(v["flop"] * v["launches"] / v["s"] / 1e12, 1)} for k, v in shapes.items()}
+        return n, tot_f, tot_s, per
+
+
+def bench_model(dev, which, warmup=2, steps=5, extras=True, roofline=False):
     import torch
 
     import synth
@@ -460,15 +600,24 @@ def bench_model(dev, which, warmup=2, steps=5):
     g.basis_init(calib)
     torch.cuda.synchronize()
     init_s = time.perf_counter() - t0
+    timer = None
+    if roofline:
+        timer = LaunchTimer(steps * (4 * shape.n_layers + 8))
+        g.linear_hook = timer
     for _ in range(warmup):
         g.step(tok, 1, 1e-3, lr)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if timer is not None:
+        timer.on = True
     e0.record()
     for _ in range(steps):
         g.step(tok, 1, 1e-3, lr)
     e1.record()
     torch.cuda.synchronize()
+    if timer is not None:
+        timer.on = False
+        g.linear_hook = None
     ms = e0.elapsed_time(e1) / steps
     flops = model_step_flops(shape, B, S)
     rec = {"steps_per_s": round(1e3 / ms, 3), "ms_per_step": round(ms, 2),
@@ -476,7 +625,20 @@ def bench_model(dev, which, warmup=2, steps=5):
            "basis_init_s": round(init_s, 3), "calibration_tokens": CB * CS, "tokens_per_half": B * S,
            "rank": shape.rank, "k": g.k, "losses": [float(v) for v in g.loss_pm.cpu().numpy()],
            "status": int(g.status.item()), "setup_s": round(setup_s, 1)}
-    if which in ("llama_bf16", "llama_int4"):
+    if timer is not None:
+        n, tot_f, tot_s, per = timer.summary()
+        achieved = tot_f / tot_s / 1e12
+        rec["roofline"] = {
+            "kernel": f"{DOMINANT_KERNEL} (fused ± adapted GEMM) over the {n} adapted-linear launches of the "
+                      f"{steps} timed steps ({n // steps} per step: q|k|v, o, gate|up with SwiGLU, down per layer; "
+                      f"M = {2 * B * S} stacked rows, r = {shape.rank})",
+            "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic_record(DOMINANT_KERNEL, HEADLINE, DOMINANT_SOURCES),
+            "flops_per_launch": round(tot_f / n), "mean_launch_us": round(tot_s / n * 1e6, 1),
+            "launches": n, "per_shape": per,
+            "gemm_share_of_step": round(tot_s / (ms * 1e-3 * steps), 4)}
+    if extras and which in ("llama_bf16", "llama_int4"):
         # ZO-Adam over the model's arena (HBM-bound): 24 B per coefficient (fp32 C), 20 (bf16 C)
         pert = Z.Pert(1, 99, 0, 1e-3)
         adam = Z.adam_desc(lr, 99)
@@ -494,6 +656,35 @@ def bench_model(dev, which, warmup=2, steps=5):
         rec["adam"] = {"coefficients": g.k, "bytes_per_coefficient": per, "us": round(us, 1),
                        "achieved_GBps": round(gbs, 1), "peak_GBps": PEAK_HBM_GBS,
                        "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        # the update pass that also writes the next step's C +/- eps Z (the step's own form):
+        # 24 (20) bytes of the update plus 4 bytes of perturbed coefficients per coefficient
+        ch = torch.empty(2 * g.k, dtype=torch.bfloat16, device=dev)
+        nxt = Z.Pert(1, 100, 0, 1e-3)
+        Z.step_perturb(g.arena, g.loss_pm, pert, adam, nxt, ch, g.status)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            Z.step_perturb(g.arena, g.loss_pm, pert, adam, nxt, ch, g.status)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        gbs = g.k * (per + 4) / (us * 1e-6) / 1e9
+        rec["adam_perturb"] = {"bytes_per_coefficient": per + 4, "us": round(us, 1), "achieved_GBps": round(gbs, 1),
+                               "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        # the coefficient pass alone (C +/- eps Z over the arena): 4 (2) + 4 bytes per coefficient
+        Z.perturb_coeffs(g.arena, 0, g.k, nxt, ch)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            Z.perturb_coeffs(g.arena, 0, g.k, nxt, ch)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        pb = (2 if g.c_bf16 else 4) + 4
+        gbs = g.k * pb / (us * 1e-6) / 1e9
+        rec["perturb"] = {"bytes_per_coefficient": pb, "us": round(us, 1), "achieved_GBps": round(gbs, 1),
+                          "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        del ch
         # Algorithm 2's one-sided form with q = 8 queries: L and L_1..L_8 in five stacked
         # forwards, then the update that regenerates eight Gaussians per coefficient
         q = 8
@@ -520,19 +711,44 @@ def bench_model(dev, which, warmup=2, steps=5):
     del g
     torch.cuda.empty_cache()
     log(f"{which}: {rec['steps_per_s']} steps/s, {rec['model_tflops']} TFLOP/s, init {rec['basis_init_s']} s"
+        + (f", GEMM {rec['roofline']['achieved']} TFLOP/s" if "roofline" in rec else "")
         + (f", one-sided q=8 {rec['one_sided_q8']['ms_per_step']} ms/step" if "one_sided_q8" in rec else ""))
     return rec
+
+
+def bench_tiny(dev, steps=20):
+    """The tiny fp32 model (2 layers, d = 128, r = 8 on q and v, 4 x 64 tokens): its 20 ZO
+    steps after the basis from 4 x 64 calibration tokens (launch-bound; steps/s only)."""
+    import torch
+
+    import synth
+    from paper_2607_01125_amd import model as gm
+
+    shape = synth.TINY
+    g = gm.Decoder(shape, synth.model_weights(shape, 0, "fp32"), "fp32", device=dev)
+    g.basis_init(torch.from_numpy(synth.uniform_tokens(4, 64, shape.vocab, 0, 1)).to(dev))
+    tok = torch.from_numpy(synth.uniform_tokens(4, 64, shape.vocab, 0, 2)).to(dev)
+    g.step(tok, 0, 1e-3, 1e-4)
+    g.t = 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.step(tok, 0, 1e-3, 1e-4)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    return {"steps": steps, "steps_per_s": round(steps / dt, 1), "ms_per_step": round(dt / steps * 1e3, 3),
+            "losses_last": [float(v) for v in g.loss_pm.cpu().numpy()]}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="single_linear_4096", choices=["single_linear_4096"])
+    ap.add_argument("--workload", default=HEADLINE, choices=[HEADLINE])
     ap.add_argument("--quick", action="store_true", help="headline workload only")
-    ap.add_argument("--models", default="llama_bf16,llama_int4,opt_bf16",
-                    help="comma-separated model runs (llama_bf16, llama_int4, opt_bf16; empty for none)")
+    ap.add_argument("--models", default="llama_int4,opt_bf16",
+                    help="comma-separated further model runs (llama_int4, opt_bf16; empty for none)")
     ap.add_argument("--no-shapes", action="store_true", help="skip the 8B layer-shape sweep")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -546,44 +762,52 @@ def main():
     import torch
 
     dev = torch.device("cuda:0")
-    log("headline: single adapted linear 4096, r=32, 8192 tokens per half")
-    head = bench_single_linear(args, dev)
+    log("headline: Llama-3-8B-shape bf16 ZO step, 16 x 256 tokens per half, r = 32")
+    head = bench_model(dev, "llama_bf16", warmup=args.warmup, steps=args.steps, extras=not args.quick,
+                       roofline=True)
     ms = head["ms_per_step"]
     out = {
         "metric": METRIC,
-        "value": round(1e3 / ms, 3),
+        "value": head["steps_per_s"],
         "unit": "ZO steps/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms, 4),
+        "ms_per_step": ms,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic (planted low-rank activations, random-init W, seeded)",
-        "config": {"workload": "single adapted linear, bf16, d_in=d_out=4096, r=32, 8192 tokens per ± half "
-                               "(projection + fused ± forward with the MSE in its epilogue + ZO-Adam, whose pass "
-                               "also forms the next step's C±εZ; "
-                               "both halves read the same x, so x W^T and x U are formed once)",
-                   **head["config"], "parallelism": "single GPU"},
-        "adapted_linear_tflops": round(head["flops"] / (ms * 1e-3) / 1e12, 1),
-        "basis_init_ms": round(head["init_ms"], 1),
+        "data": "synthetic (random-init weights N(0, 0.02^2), uniform random tokens, seeded)",
+        "config": {"workload": "Llama-3-8B-shape decoder, bf16, random init: 32 layers, d=4096, GQA 32q/8kv x 128, "
+                               "SwiGLU FFN 14336, vocab 128256; r=32 on q,k,v,o,gate,up,down; 16x256 tokens per ± "
+                               "half; one two-sided ZO step (± forward with the fused LM head + cross entropy, "
+                               "ZO-Adam over 44,040,192 coefficients)",
+                   "tokens_per_half": 4096, "rank": 32, "eps": 1e-3, "lr": 5e-5, "parallelism": "single GPU"},
+        "model_tflops": head["model_tflops"],
+        "step_tflop": head["step_tflop"],
+        "basis_init_s": head["basis_init_s"],
         "roofline": head["roofline"],
-        "stacked_form": head["stacked_form"],
         "losses": head["losses"],
+        "llama3_8b_bf16": {k: v for k, v in head.items() if k not in ("roofline", "losses")},
     }
     log(f"headline: {out['value']} steps/s, fused GEMM {head['roofline']['achieved']} TFLOP/s "
-        f"(stacked form {head['stacked_form']['steps_per_s']} steps/s)")
+        f"({head['roofline']['frac']:.3f} of peak)")
     if not args.quick:
+        out["single_linear_4096"] = bench_single_linear(args, dev)
+        log(f"single linear: stacked {out['single_linear_4096']['stacked']['steps_per_s']} steps/s "
+            f"({out['single_linear_4096']['stacked']['gemm_tflops']} TFLOP/s), shared x "
+            f"{out['single_linear_4096']['shared_x']['steps_per_s']} steps/s")
         if not args.no_shapes:
             out["adapted_linear_8b_shapes"] = bench_linear_shapes(dev)
         runs = [w for w in args.models.split(",") if w]
         for w in runs:
-            if w not in ("llama_bf16", "llama_int4", "opt_bf16"):
+            if w not in ("llama_int4", "opt_bf16"):
                 raise SystemExit(f"unknown model run {w!r}")
         if runs:
             out["models"] = {w: bench_model(dev, w) for w in runs}
+        out["tiny_fp32_20_steps"] = bench_tiny(dev)
+        log(f"tiny fp32: {out['tiny_fp32_20_steps']['steps_per_s']} steps/s")
     if args.calibrate_copy_mib:
         n = args.calibrate_copy_mib << 20
         src = torch.ones(n, dtype=torch.uint8, device=dev)
@@ -594,8 +818,11 @@ def main():
         out["copy_calibration_bytes"] = n
         del src, dst
     if not args.no_cpu_baseline:
-        log("cpu baseline (oracle)")
-        out["cpu_baseline"] = cpu_baseline(8192, 4096, 4096, 32)
+        log("cpu baseline (oracle, sampled headline step)")
+        out["cpu_baseline"] = cpu_baseline_llama()
+        log(f"cpu baseline: {out['cpu_baseline']['seconds_per_step']} s per step (extrapolated)")
+        if not args.quick:
+            out["cpu_baseline_single_linear"] = cpu_baseline_single(8192, 4096, 4096, 32)
     print(json.dumps(out), flush=True)
 
 

@@ -536,22 +536,6 @@ hipError_t launch_bf16(const GemmArgs& a, dim3 grid, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Schedule of the bf16 fused GEMM: 0 = four-wave pipelined (default, fastest measured: the
-// 64-deep stages where they apply, else the 32-deep ones), 1 = eight-wave ping-pong,
-// 2 = generic, 3 = the 32-deep four-wave schedule only.  ZOACT_GEMM_SCHEDULE selects one for A/B
-// measurements; the generic kernel is the fallback for shapes outside the others' coverage.
-int schedule_choice() {
-  static const int v = [] {
-    const char* e = getenv("ZOACT_GEMM_SCHEDULE");
-    if (e == nullptr) return 0;
-    if (e[0] == '1') return 1;
-    if (e[0] == '2') return 2;
-    if (e[0] == '3') return 3;   // the 32-deep four-wave schedule only
-    return 0;
-  }();
-  return v;
-}
-
 // INT4 weights to bf16 in one streaming pass: thread = 16 packed bytes (32 weights of one
 // row, inside one group of 128) -> 64 bytes out.
 __global__ void __launch_bounds__(256) dequant_int4_kernel(const uint4* __restrict__ w, const uint16_t* __restrict__ sc,
@@ -572,7 +556,6 @@ __global__ void __launch_bounds__(256) dequant_int4_kernel(const uint4* __restri
 
 }  // namespace
 
-hipError_t launch_linear_pm_pp(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
 hipError_t launch_linear_pm_4w(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, hipStream_t s);
 hipError_t launch_linear_pm_4w64(const gemm::GemmArgs& a, int w_dtype, int epi, bool out_f32, bool shared,
                                  hipStream_t s);
@@ -643,17 +626,13 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
   const bool of = y_dtype == ZOACT_F32;
   // one half's x and p read by both halves: the 64-deep schedule's shared-input form only
   if (flags & ZOACT_SHARED_X) return launch_linear_pm_4w64(a, L.w_dtype, epi, of, true, s);
-  const int sched = schedule_choice();
-  if (sched == 0 || sched == 3) {
-    hipError_t e = sched == 0 ? launch_linear_pm_4w64(a, L.w_dtype, epi, of, false, s) : hipErrorNotSupported;
-    if (e != hipErrorNotSupported) return e;
-    e = launch_linear_pm_4w(a, L.w_dtype, epi, of, s);
-    if (e != hipErrorNotSupported) return e;
-  }
-  if (sched <= 1 || sched == 3) {
-    const hipError_t e = launch_linear_pm_pp(a, L.w_dtype, epi, of, s);
-    if (e != hipErrorNotSupported) return e;
-  }
+  // the 64-deep persistent schedule where it applies (bf16 weights, C_h precomputed or
+  // r = 0), else the 32-deep one (C_h formed in its prologue; INT4 in registers), else the
+  // generic kernel (shapes outside both)
+  hipError_t e = launch_linear_pm_4w64(a, L.w_dtype, epi, of, false, s);
+  if (e != hipErrorNotSupported) return e;
+  e = launch_linear_pm_4w(a, L.w_dtype, epi, of, s);
+  if (e != hipErrorNotSupported) return e;
 #define ZO_DISPATCH(I4, EP, OF) \
   if (i4 == I4 && epi == EP && of == OF) return launch_bf16<I4, EP, OF>(a, grid, s);
   ZO_DISPATCH(false, 0, false)
@@ -675,8 +654,7 @@ hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const 
   a.tgt = static_cast<const uint16_t*>(target);
   a.part = part;
   const bool shared = (flags & ZOACT_SHARED_X) != 0;
-  hipError_t e = (schedule_choice() == 0 || shared) ? launch_linear_pm_4w64(a, L.w_dtype, EPI_MSE, false, shared, s)
-                                                   : hipErrorNotSupported;
+  hipError_t e = launch_linear_pm_4w64(a, L.w_dtype, EPI_MSE, false, shared, s);
   if (e == hipErrorNotSupported && !shared) e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
   if (e != hipSuccess) return e;
   return launch_sum_mean(part, (int64_t)a.tiles_m_half * a.tiles_n * 4, (double)T * (double)L.d_out, loss_pm, s);
@@ -703,8 +681,7 @@ hipError_t launch_linear_xent(const zoact_linear& L, const zoact_arena* A, const
   a.tok = tokens;
   a.seq = S;
   a.xnblk = (int32_t)nblk;
-  const hipError_t e = schedule_choice() == 0 ? launch_linear_pm_4w64(a, L.w_dtype, EPI_XENT, false, false, s)
-                                              : hipErrorNotSupported;
+  const hipError_t e = launch_linear_pm_4w64(a, L.w_dtype, EPI_XENT, false, false, s);
   if (e != hipSuccess) return e;
   return launch_xent_combine(a.xpart, a.xtgt, T, S, (int)nblk, T / S, part, loss_pm, s);
 }

@@ -58,6 +58,18 @@ typedef uint32_t vu2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ vf4 ld_nt(const float* p) { return __builtin_nontemporal_load(reinterpret_cast<const vf4*>(p)); }
 __device__ __forceinline__ void st_nt(float* p, vf4 v) { __builtin_nontemporal_store(v, reinterpret_cast<vf4*>(p)); }
 
+// Four bf16 values (fp32 rounded to nearest even) in one 8-byte streaming store; p 8-byte aligned.
+__device__ __forceinline__ void st4_bf16_nt(uint16_t* p, float a, float b, float c, float d) {
+  const vu2 v = {(uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16), (uint32_t)f2bf(c) | ((uint32_t)f2bf(d) << 16)};
+  __builtin_nontemporal_store(v, reinterpret_cast<vu2*>(p));
+}
+
+// C + s eps Z of one value for s in {-1, 0, +1} (fp32, no contraction).
+__device__ __forceinline__ float pert_one(float c, float ez, int32_t s) {
+#pragma clang fp contract(off)
+  return s > 0 ? c + ez : (s < 0 ? c - ez : c);
+}
+
 // With NEXT, the same pass also writes the next step's perturbed coefficients from the C it
 // leaves behind, exactly as perturb_kernel would over the whole arena (out bf16 [2][k]):
 // out[h][e] = bf16(C'[e] + s_h (eps' Z(e; q'_h))), C' the stored value (bf16 C: the rounded
@@ -75,10 +87,20 @@ __global__ void __launch_bounds__(256) adam_kernel(void* __restrict__ cptr, floa
     if (status != nullptr && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, 1u);
     if (!NEXT) return;
   }
-  // next perturbation of arena indices 4b .. 4b + nl - 1 from their stored values cs
+  // next perturbation of arena indices 4b .. 4b + nl - 1 from their stored values cs: a whole
+  // block in two 8-byte stores when both halves' rows stay 8-byte aligned (k % 4 == 0)
+  const bool vec_out = (k & 3) == 0;
   auto next_pert = [&](int64_t b, const float* cs, int nl) {
     const float4 za = rng::gauss_block(nx.seed, nx.step, nx.query[0], (uint64_t)b);
     const float4 zb = nx.query[0] == nx.query[1] ? za : rng::gauss_block(nx.seed, nx.step, nx.query[1], (uint64_t)b);
+    if (nl == 4 && vec_out) {
+      const int64_t e = 4 * b;
+      st4_bf16_nt(out + e, pert_one(cs[0], nx.eps * za.x, nx.sign[0]), pert_one(cs[1], nx.eps * za.y, nx.sign[0]),
+                  pert_one(cs[2], nx.eps * za.z, nx.sign[0]), pert_one(cs[3], nx.eps * za.w, nx.sign[0]));
+      st4_bf16_nt(out + k + e, pert_one(cs[0], nx.eps * zb.x, nx.sign[1]), pert_one(cs[1], nx.eps * zb.y, nx.sign[1]),
+                  pert_one(cs[2], nx.eps * zb.z, nx.sign[1]), pert_one(cs[3], nx.eps * zb.w, nx.sign[1]));
+      return;
+    }
     for (int l = 0; l < nl; ++l) {
       const int64_t e = 4 * b + l;
       const float c = cs[l];
@@ -171,8 +193,40 @@ __global__ void __launch_bounds__(256) sgd_kernel(void* __restrict__ cptr, int64
   }
 }
 
-// out[h][e - e0] = bf16(C[e] + s_h eps Z(e; q_h)) (s_h = 0: bf16(C[e])); one Philox block
-// (4 arena indices) per thread and half.
+// out[h][e - e0] = bf16(C[e] + s_h eps Z(e; q_h)) (s_h = 0: bf16(C[e])) for a range of whole
+// Philox blocks (e0 % 4 == 0, n % 4 == 0): per block one 16-byte (8-byte with bf16 C)
+// streaming load of C and one 8-byte streaming store per half.  HBM-bound: 8 (6) bytes per
+// coefficient.
+template <bool BF16C>
+__global__ void __launch_bounds__(256) perturb_vec_kernel(const void* __restrict__ cptr, int64_t e0, int64_t n,
+                                                          uint64_t seed, uint32_t step, uint32_t q0, uint32_t q1,
+                                                          int32_t s0, int32_t s1, float eps,
+                                                          uint16_t* __restrict__ out) {
+#pragma clang fp contract(off)
+  const int64_t nb = n >> 2, b0 = e0 >> 2;
+  const bool same = q0 == q1;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nb; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t b = b0 + i;
+    float c0, c1, c2, c3;
+    if (BF16C) {
+      const vu2 cb = __builtin_nontemporal_load(reinterpret_cast<const vu2*>(reinterpret_cast<const uint16_t*>(cptr) + 4 * b));
+      c0 = bf2f((uint16_t)(cb.x & 0xFFFFu)); c1 = bf2f((uint16_t)(cb.x >> 16));
+      c2 = bf2f((uint16_t)(cb.y & 0xFFFFu)); c3 = bf2f((uint16_t)(cb.y >> 16));
+    } else {
+      const vf4 cf = ld_nt(reinterpret_cast<const float*>(cptr) + 4 * b);
+      c0 = cf.x; c1 = cf.y; c2 = cf.z; c3 = cf.w;
+    }
+    const float4 za = rng::gauss_block(seed, step, q0, (uint64_t)b);
+    const float4 zb = same ? za : rng::gauss_block(seed, step, q1, (uint64_t)b);
+    st4_bf16_nt(out + 4 * i, pert_one(c0, eps * za.x, s0), pert_one(c1, eps * za.y, s0), pert_one(c2, eps * za.z, s0),
+                pert_one(c3, eps * za.w, s0));
+    st4_bf16_nt(out + n + 4 * i, pert_one(c0, eps * zb.x, s1), pert_one(c1, eps * zb.y, s1),
+                pert_one(c2, eps * zb.z, s1), pert_one(c3, eps * zb.w, s1));
+  }
+}
+
+// The same for any range: one Philox block (4 arena indices) per thread and half, element
+// by element.
 template <bool BF16C>
 __global__ void __launch_bounds__(256) perturb_kernel(const void* __restrict__ cptr, int64_t e0, int64_t n,
                                                       uint64_t seed, uint32_t step, uint32_t q0, uint32_t q1,
@@ -299,6 +353,15 @@ hipError_t launch_perturb(const zoact_arena& A, int64_t e0, int64_t n, const zoa
                           hipStream_t s) {
   const int64_t nb = ((e0 + n - 1) >> 2) - (e0 >> 2) + 1;
   const dim3 grid((unsigned)grid_for(nb));
+  if ((e0 & 3) == 0 && (n & 3) == 0 && (reinterpret_cast<uintptr_t>(A.c) & 15u) == 0) {
+    if (A.c_dtype == ZOACT_BF16)
+      perturb_vec_kernel<true><<<grid, dim3(256), 0, s>>>(A.c, e0, n, p.seed, p.step, p.query[0], p.query[1],
+                                                          p.sign[0], p.sign[1], p.eps, out);
+    else
+      perturb_vec_kernel<false><<<grid, dim3(256), 0, s>>>(A.c, e0, n, p.seed, p.step, p.query[0], p.query[1],
+                                                           p.sign[0], p.sign[1], p.eps, out);
+    return hipGetLastError();
+  }
   if (A.c_dtype == ZOACT_BF16)
     perturb_kernel<true><<<grid, dim3(256), 0, s>>>(A.c, e0, n, p.seed, p.step, p.query[0], p.query[1], p.sign[0],
                                                     p.sign[1], p.eps, out);

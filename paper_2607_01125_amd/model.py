@@ -86,6 +86,12 @@ def arena_layout(shape) -> list:
     return out
 
 
+def _pair_key(pert) -> tuple:
+    """(seed, step, queries, signs, eps) of a Pert or PertPair."""
+    pp = Z.as_pair(pert)
+    return (pp.seed, pp.step, tuple(pp.query), tuple(pp.sign), float(pp.eps))
+
+
 def interleave_gate_up(wg: torch.Tensor, wu: torch.Tensor) -> torch.Tensor:
     """Rows 32j..32j+15 = gate rows 16j..16j+15, rows 32j+16..32j+31 = the matching up rows."""
     ff = wg.shape[0]
@@ -132,6 +138,16 @@ class Decoder:
         self._bufs = {}
         self._rope = {}
         self._ch = self._ch_all = None   # per-step C +/- eps Z of the whole arena (bf16 modes)
+        # the perturbation the last update pass wrote into _ch_all for the next step:
+        # (pair key, arena.c._version after the pass); any torch-side write to C bumps the
+        # version and the forward forms the perturbation again
+        self._ch_next = None
+        # optional callable(stage, lin, T, flags) around every linear launch ("pre"/"post"),
+        # for per-launch timing
+        self.linear_hook = None
+        # layer 0 reads the same embedding in both halves: its first projection forms x W^T
+        # and x U once (ZOACT_SHARED_X) when the layer qualifies
+        self.shared_first = True
         # INT4 layers: dequantised once per forward into one bf16 buffer (the largest layer's
         # size) and run on the bf16 schedule; False keeps the in-register INT4 GEMM
         self._wdq = None
@@ -251,16 +267,32 @@ class Decoder:
             wdq = self._wdq[:lin.d_out * lin.d_in].view(lin.d_out, lin.d_in)
             Z.dequant_int4(lin.w, lin.w_scales, wdq)
             lin = dataclasses.replace(lin, w=wdq, w_scales=None)
+        hook = self.linear_hook
         if adapt and blk is not None and site_ut is not None:
             lin.r, lin.ut = self.r, site_ut
             if self._ch is not None:
                 lin.ch, lin.ch_stride = self._ch[blk.offset:], self.k
             else:
                 lin.ch, lin.ch_stride = None, 0
+            if hook:
+                hook("pre", lin, T, flags)
             Z.linear_fwd_pm(lin, self.arena, x, T, B["p"], y, pert, residual, flags)
         else:
             lin.r, lin.ut, lin.ch, lin.ch_stride = 0, None, None, 0
+            if hook:
+                hook("pre", lin, T, flags)
             Z.linear_fwd_pm(lin, None, x, T, None, y, pert, residual, flags)
+        if hook:
+            hook("post", lin, T, flags)
+
+    def _shared_ok(self, lin_blk, site_ut) -> bool:
+        """Whether the shared-input form covers this projection: bf16 weights (or INT4 run on
+        its dequantised copy), the perturbed coefficients precomputed, 8 <= r <= 32 with
+        r % 8 == 0, depth a multiple of 64, no SwiGLU."""
+        lin, blk = lin_blk
+        return (self.shared_first and self.act == torch.bfloat16 and blk is not None and site_ut is not None
+                and self._ch is not None and (lin.w.dtype == torch.bfloat16 or self._wdq is not None)
+                and 8 <= self.r <= 32 and self.r % 8 == 0 and lin.d_in % 64 == 0 and lin.d_in >= 128)
 
     def forward(self, tokens: torch.Tensor, pert: Z.Pert | Z.PertPair, *, calibrate=None, distinct_halves=False,
                 head: bool = True):
@@ -283,22 +315,37 @@ class Decoder:
         if adapt and self.act == torch.bfloat16 and self.k > 0:
             if self._ch_all is None:
                 self._ch_all = torch.empty(2 * self.k, dtype=torch.bfloat16, device=self.dev)
-            Z.perturb_coeffs(self.arena, 0, self.k, pert, self._ch_all)
+            # the previous update pass may have written this step's perturbation already
+            if self._ch_next != (_pair_key(pert), self.arena.c._version):
+                Z.perturb_coeffs(self.arena, 0, self.k, pert, self._ch_all)
             self._ch = self._ch_all
+        self._ch_next = None
         Z.embed(tokens, self.emb, B["h0"], seq, self.pos, pos_offset=2, distinct_halves=distinct_halves)
         h, h_alt = B["h0"], B["h1"]
         cos_sin = self._rope_tables(seq) if s.family == "llama" else None
         d, dkv, H, Hkv, hd = self.d, self.dkv, self.H, self.Hkv, self.hd
         scale = float(np.float32(1.0 / math.sqrt(hd)))
         for l, P in enumerate(self.layers):
-            # attention block
-            self._norm(h, P["n1"], P.get("n1b"), B["a"])
-            ut = self._site(l, "attn", B["a"], adapt, calibrate)
+            # attention block.  Layer 0 of a forward whose halves read the same tokens: both
+            # halves' inputs are the same embedding rows, so the norm and the projection run
+            # on one half and the fused q|k|v forms x W^T once (the same bits as stacked)
             qkv = B["qkv"]
-            if "qkv" in P:
+            shared = (l == 0 and adapt and not distinct_halves and "qkv" in P
+                      and self._shared_ok(P["qkv"], self.ut.get((0, "attn"))))
+            if shared:
+                a1 = B["a"][:T]
+                self._norm(h[:T], P["n1"], P.get("n1b"), a1)
+                ut = self._site(l, "attn", a1, adapt, calibrate)
+                self._apply(P["qkv"], a1, T, qkv, pert, ut, flags=Z.SHARED_X, adapt=adapt)
+                q, k, v = qkv[:, :d], qkv[:, d:d + dkv], qkv[:, d + dkv:]
+            elif "qkv" in P:
+                self._norm(h, P["n1"], P.get("n1b"), B["a"])
+                ut = self._site(l, "attn", B["a"], adapt, calibrate)
                 self._apply(P["qkv"], B["a"], T, qkv, pert, ut, adapt=adapt)
                 q, k, v = qkv[:, :d], qkv[:, d:d + dkv], qkv[:, d + dkv:]
             else:
+                self._norm(h, P["n1"], P.get("n1b"), B["a"])
+                ut = self._site(l, "attn", B["a"], adapt, calibrate)
                 self._apply(P["qv"], B["a"], T, qkv, pert, ut, adapt=adapt)
                 self._apply(P["k"], B["a"], T, B["k"], pert, None, adapt=False)
                 q, k, v = qkv[:, :d], B["k"], qkv[:, d:]
@@ -336,7 +383,7 @@ class Decoder:
             if (l, site) in self._adapted_sites:
                 raise RuntimeError(f"no basis for site {(l, site)}: run basis_init or set_basis first")
             return None
-        Z.project(x, ut, self._cur["p"])
+        Z.project(x, ut, self._cur["p"][:x.shape[0]])
         return ut
 
     def site_dims(self):
@@ -401,11 +448,17 @@ class Decoder:
         return self._loss_pair(tokens, Z.Pert(seed, t, 0, eps), self.loss_pm)
 
     def step(self, tokens: torch.Tensor, seed: int, eps: float, lr: float, optimizer: str = "adam"):
-        """One two-sided ZO step: L+ and L-, g = (L+ - L-) / (2 eps), update C with Z regenerated."""
+        """One two-sided ZO step: L+ and L-, g = (L+ - L-) / (2 eps), update C with Z regenerated.
+        In bf16 modes the Adam pass also writes the next step's C +/- eps Z (one pass over the
+        arena instead of two), which the next step's forward then reads."""
         self.t += 1
         pert = Z.Pert(seed, self.t, 0, eps)
         self.losses(tokens, seed, self.t, eps)
-        if optimizer == "adam":
+        if optimizer == "adam" and self._ch_all is not None:
+            nxt = Z.Pert(seed, self.t + 1, 0, eps)
+            Z.step_perturb(self.arena, self.loss_pm, pert, Z.adam_desc(lr, self.t), nxt, self._ch_all, self.status)
+            self._ch_next = (_pair_key(nxt), self.arena.c._version)
+        elif optimizer == "adam":
             Z.step(self.arena, self.loss_pm, pert, Z.adam_desc(lr, self.t), self.status)
         elif optimizer == "sgd":
             Z.step_sgd(self.arena, self.loss_pm, pert, lr, self.status)

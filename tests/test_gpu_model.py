@@ -236,3 +236,49 @@ def test_fused_head_xent_matches_stored_logits(shape, B, S):
     g._loss_pair(tok, pert, fused)
     np.testing.assert_allclose(host(fused), host(stored), rtol=2e-6)
     assert host(fused)[0] != host(fused)[1]
+
+
+# ------------------------------------------------------------------ the step's own fusions
+def test_steps_with_the_update_pass_forming_the_next_perturbation():
+    """Decoder.step in bf16: the update pass writes the next step's C +/- eps Z and the next
+    forward reads it instead of forming it again.  Three steps give the same losses and
+    arena, bit for bit, as three steps that form it afresh each time; a torch-side write to C
+    between steps is seen (the perturbation is formed again)."""
+    announce("step chain with the fused update pass")
+    om_m, g1 = _models(LLAMA_S, "bf16", seed=8)
+    _, g2 = _models(LLAMA_S, "bf16", seed=8)
+    tok = t_i32(synth.uniform_tokens(2, 64, LLAMA_S.vocab, 8, 5))
+    for t in range(3):
+        l1 = host(g1.step(tok, 5, 1e-3, 5e-5))
+        g2._ch_next = None                  # forget what the update pass wrote
+        l2 = host(g2.step(tok, 5, 1e-3, 5e-5))
+        np.testing.assert_array_equal(l1, l2)
+    for a, b in ((g1.arena.c, g2.arena.c), (g1.arena.m, g2.arena.m), (g1.arena.v, g2.arena.v)):
+        assert torch.equal(a, b)
+    assert g1._ch_next is not None
+    # an outside write to C invalidates the cached perturbation
+    g1.arena.c.add_(1e-3)
+    g2.arena.c.add_(1e-3)
+    l1 = host(g1.step(tok, 5, 1e-3, 5e-5))
+    g2._ch_next = None
+    l2 = host(g2.step(tok, 5, 1e-3, 5e-5))
+    np.testing.assert_array_equal(l1, l2)
+
+
+@pytest.mark.parametrize("mode", ["bf16", "int4"])
+def test_shared_first_projection_bitwise(mode):
+    """Layer 0's q|k|v in its shared-input form (both halves read the same embedding rows):
+    logits bit for bit those of the stacked form."""
+    announce("shared first projection", mode)
+    om_m, g = _models(LLAMA_S, mode, seed=9)
+    g.arena.c.copy_(torch.from_numpy(synth.normal((om_m.k,), 0.05, 9, 9)).to(g.arena.c.dtype))
+    tok = t_i32(synth.uniform_tokens(2, 64, LLAMA_S.vocab, 9, 4))
+    pert = Z.Pert(4, 2, 0, 1e-2)
+    calls = []
+    g.linear_hook = lambda stage, lin, T, flags: calls.append(flags) if stage == "pre" else None
+    a = host(g.forward(tok, pert))
+    g.linear_hook = None
+    assert calls[0] & Z.SHARED_X and not any(f & Z.SHARED_X for f in calls[1:])
+    g.shared_first = False
+    b = host(g.forward(tok, pert))
+    np.testing.assert_array_equal(a, b)

@@ -190,7 +190,7 @@ def test_linear_pm_bf16(T, K, N, r, off):
 
 
 @pytest.mark.parametrize("c_bf16", [False, True])
-@pytest.mark.parametrize("e0,n", [(0, 4096), (3, 1001), (44_040_192 - 777, 777)])
+@pytest.mark.parametrize("e0,n", [(0, 4096), (3, 1001), (44_040_192 - 777, 777), (8, 1000), (44_040_192 - 4096, 4096)])
 def test_perturb_coeffs_bitwise(c_bf16, e0, n):
     """bf16(C + eps Z) and bf16(C - eps Z) over an unaligned arena range, bit for bit."""
     announce("perturb_coeffs", c_bf16, e0, n)
