@@ -166,6 +166,64 @@ __global__ void __launch_bounds__(256) adam_kernel(void* __restrict__ cptr, floa
   }
 }
 
+// adam_kernel<BF16C, true> for its common case: the next perturbation is the +/- pair of
+// one query (signs +1, -1) and the arena holds whole Philox blocks (k % 4 == 0).  Per block
+// the loads of C, m, v are issued first and both Gaussians (this step's, for the update, and
+// the next step's) are formed while they are in flight; then the update, its stores, and
+// the two 8-byte stores of the next step's C +/- eps Z.  Bit for bit adam_kernel<BF16C, true>.
+template <bool BF16C>
+__global__ void __launch_bounds__(256) adam_next_pm_kernel(void* __restrict__ cptr, float* __restrict__ mptr,
+                                                           float* __restrict__ vptr, int64_t k, const float* loss_pm,
+                                                           uint64_t seed, uint32_t step, uint32_t query, float eps,
+                                                           AdamConst h, uint32_t* status, uint64_t nseed,
+                                                           uint32_t nstep, uint32_t nquery, float neps,
+                                                           uint16_t* __restrict__ out) {
+#pragma clang fp contract(off)
+  const float g = projected_grad(loss_pm, eps);
+  const bool upd = __builtin_isfinite(g);
+  if (!upd && status != nullptr && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(status, 1u);
+  const int64_t nb = k >> 2;
+  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb; b += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t e = 4 * b;
+    float c[4];
+    if (BF16C) {
+      const vu2 cb = __builtin_nontemporal_load(reinterpret_cast<const vu2*>(reinterpret_cast<const uint16_t*>(cptr) + e));
+      c[0] = bf2f((uint16_t)(cb.x & 0xFFFFu)); c[1] = bf2f((uint16_t)(cb.x >> 16));
+      c[2] = bf2f((uint16_t)(cb.y & 0xFFFFu)); c[3] = bf2f((uint16_t)(cb.y >> 16));
+    } else {
+      const vf4 cf = ld_nt(reinterpret_cast<const float*>(cptr) + e);
+      c[0] = cf.x; c[1] = cf.y; c[2] = cf.z; c[3] = cf.w;
+    }
+    vf4 m4 = {}, v4 = {};
+    if (upd) {
+      m4 = ld_nt(mptr + e);
+      v4 = ld_nt(vptr + e);
+    }
+    const float4 zn = rng::gauss_block(nseed, nstep, nquery, (uint64_t)b);
+    if (upd) {
+      const float4 z = rng::gauss_block(seed, step, query, (uint64_t)b);
+      float m[4] = {m4.x, m4.y, m4.z, m4.w}, v[4] = {v4.x, v4.y, v4.z, v4.w};
+      const float zz[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+      for (int l = 0; l < 4; ++l) c[l] = adam_one(c[l], m[l], v[l], g * zz[l], h);
+      st_nt(mptr + e, vf4{m[0], m[1], m[2], m[3]});
+      st_nt(vptr + e, vf4{v[0], v[1], v[2], v[3]});
+      if (BF16C) {
+#pragma unroll
+        for (int l = 0; l < 4; ++l) c[l] = bf2f(f2bf(c[l]));   // the stored value
+        const vu2 cb = {(uint32_t)f2bf(c[0]) | ((uint32_t)f2bf(c[1]) << 16),
+                        (uint32_t)f2bf(c[2]) | ((uint32_t)f2bf(c[3]) << 16)};
+        __builtin_nontemporal_store(cb, reinterpret_cast<vu2*>(reinterpret_cast<uint16_t*>(cptr) + e));
+      } else {
+        st_nt(reinterpret_cast<float*>(cptr) + e, vf4{c[0], c[1], c[2], c[3]});
+      }
+    }
+    const float ez[4] = {neps * zn.x, neps * zn.y, neps * zn.z, neps * zn.w};
+    st4_bf16_nt(out + e, c[0] + ez[0], c[1] + ez[1], c[2] + ez[2], c[3] + ez[3]);
+    st4_bf16_nt(out + k + e, c[0] - ez[0], c[1] - ez[1], c[2] - ez[2], c[3] - ez[3]);
+  }
+}
+
 template <bool BF16C>
 __global__ void __launch_bounds__(256) sgd_kernel(void* __restrict__ cptr, int64_t k, const float* loss_pm,
                                                   uint64_t seed, uint32_t step, uint32_t query, float eps, float lr,
@@ -400,6 +458,17 @@ hipError_t launch_adam(const zoact_arena& A, const float* loss_pm, const zoact_p
   adam_kernel<BF, NX><<<grid, dim3(256), 0, s>>>(A.c, A.m, A.v, A.k, loss_pm, p.seed, p.step, p.query, p.eps, c, \
                                                  status, nx, out)
   const bool bf = A.c_dtype == ZOACT_BF16;
+  if (next && (A.k & 3) == 0 && next->query[0] == next->query[1] && next->sign[0] == 1 && next->sign[1] == -1) {
+    if (bf)
+      adam_next_pm_kernel<true><<<grid, dim3(256), 0, s>>>(A.c, A.m, A.v, A.k, loss_pm, p.seed, p.step, p.query, p.eps,
+                                                            c, status, next->seed, next->step, next->query[0],
+                                                            next->eps, out);
+    else
+      adam_next_pm_kernel<false><<<grid, dim3(256), 0, s>>>(A.c, A.m, A.v, A.k, loss_pm, p.seed, p.step, p.query,
+                                                             p.eps, c, status, next->seed, next->step, next->query[0],
+                                                             next->eps, out);
+    return hipGetLastError();
+  }
   if (next) {
     if (bf) ZO_ADAM(true, true); else ZO_ADAM(false, true);
   } else {

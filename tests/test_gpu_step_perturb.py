@@ -35,7 +35,7 @@ def _bits(t):
 
 @pytest.mark.parametrize("bf16c", [False, True])
 @pytest.mark.parametrize("k,losses", [(131072, (0.731, 0.729)), (4099, (1.25, 1.5)), (3, (2.0, 1.0)),
-                                      (1030, (math.inf, 1.0))])
+                                      (1030, (math.inf, 1.0)), (1032, (math.nan, 1.0)), (44_040_192, (3.5, 3.25))])
 def test_step_perturb_equals_step_then_perturb(bf16c, k, losses):
     announce("step_perturb", bf16c, k, losses)
     a1 = _arena(k, bf16c, k)
