@@ -37,7 +37,8 @@
  *    coef_offset + n * r + i.  Z at arena index e for (seed, step, query) is a
  *    pure function of those four values and is never stored.
  *  - No C++ exception crosses this boundary.  The library is thread-safe; its
- *    only global state is the per-thread error text.
+ *    only global state is the per-thread error text, and per GPU the static scratch
+ *    array of zoact_linear_mse_pair_noalloc (and its cached device address).
  */
 #ifndef ZOACT_H
 #define ZOACT_H
@@ -264,6 +265,21 @@ size_t zoact_linear_mse_workspace_bytes(int64_t T, int64_t d_out);
 zoact_status zoact_linear_mse_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t T,
                                    uint32_t flags, const void* p, const zoact_pert_pair* pp, const void* target,
                                    float* loss_pm, void* ws, size_t ws_bytes, zoact_stream stream);
+/* zoact_linear_mse_pair without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation).  The per-tile partial sums go to a static device array of the library,
+ * ZOACT_MSE_SCRATCH_BYTES per GPU, held by each GPU the library runs on until the process
+ * ends; the call itself allocates and frees nothing.  Same arguments, kernels and results
+ * (bit for bit) as zoact_linear_mse_pair.  Every call on one GPU shares that GPU's array:
+ * calls whose work overlaps on one GPU (different streams, or other threads) race on it
+ * and must be ordered by the caller.  Errors: a shape needing more than the scratch,
+ * zoact_linear_mse_workspace_bytes(T, d_out) > ZOACT_MSE_SCRATCH_BYTES (T = 8192 tokens
+ * per half allow d_out up to 1,048,576) -> ZOACT_E_INVALID; the others as
+ * zoact_linear_mse_pair. */
+#define ZOACT_MSE_SCRATCH_BYTES (1u << 20)
+zoact_status zoact_linear_mse_pair_noalloc(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t T,
+                                           uint32_t flags, const void* p, const zoact_pert_pair* pp,
+                                           const void* target, float* loss_pm, zoact_stream stream);
 zoact_status zoact_mse_pm(const void* y, int32_t dtype, const void* target, int64_t T, int64_t N,
                           float* loss_pm, void* ws, size_t ws_bytes, zoact_stream stream);
 zoact_status zoact_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V,

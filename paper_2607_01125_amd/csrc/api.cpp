@@ -249,6 +249,24 @@ zoact_status zoact_linear_mse_pair(const zoact_linear* L, const zoact_arena* A, 
                     "linear_mse");
 }
 
+zoact_status zoact_linear_mse_pair_noalloc(const zoact_linear* L, const zoact_arena* A, const void* x, int64_t T,
+                                           uint32_t flags, const void* p, const zoact_pert_pair* pp,
+                                           const void* target, float* loss_pm, zoact_stream stream) {
+  CHECK(target != nullptr && loss_pm != nullptr, "linear_mse_noalloc: NULL target or loss");
+  CHECK(L != nullptr && aligned16(target), "linear_mse_noalloc: NULL layer or misaligned target");
+  CHECK((flags & ~(uint32_t)ZOACT_SHARED_X) == 0, "linear_mse_noalloc: flags 0x%x (only ZOACT_SHARED_X applies)",
+        flags);
+  const zoact_status v = validate_linear(L, A, x, ZOACT_BF16, T, p, nullptr, flags, pp, target, ZOACT_BF16);
+  if (v != ZOACT_OK) return v;
+  const size_t need = zoact_linear_mse_workspace_bytes(T, L->d_out);
+  CHECK(need <= (size_t)ZOACT_MSE_SCRATCH_BYTES,
+        "linear_mse_noalloc: T=%lld, d_out=%lld need %zu bytes of partial sums, more than the static scratch "
+        "of %zu bytes (use zoact_linear_mse_pair with a workspace)",
+        (long long)T, (long long)L->d_out, need, (size_t)ZOACT_MSE_SCRATCH_BYTES);
+  return hip_status(zoact::launch_linear_mse_noalloc(*L, A, x, T, flags, p, *pp, target, loss_pm, st(stream)),
+                    "linear_mse_noalloc");
+}
+
 zoact_status zoact_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V, float* loss_pm,
                            void* ws, size_t ws_bytes, zoact_stream stream) {
   CHECK(logits && tokens && loss_pm, "xent_pm: NULL pointer");

@@ -41,6 +41,10 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
 hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, uint32_t flags, const void* p,
                              const zoact_pert_pair& pert, const void* target, double* part, float* loss_pm,
                              hipStream_t s);
+// The same with the partial sums in the library's static device scratch (no workspace).
+hipError_t launch_linear_mse_noalloc(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T,
+                                     uint32_t flags, const void* p, const zoact_pert_pair& pert, const void* target,
+                                     float* loss_pm, hipStream_t s);
 hipError_t launch_sum_mean(const double* part, int64_t n, double count, float* loss_pm, hipStream_t s);
 // LM head of both halves with the next-token cross entropy fused into its epilogue (logits
 // not stored); ws holds the per-row block partials, target logits and loss partials.

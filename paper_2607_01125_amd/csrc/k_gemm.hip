@@ -34,6 +34,8 @@
 //    keep both operands L2-resident.
 #include <stdlib.h>
 
+#include <mutex>
+
 #include "gemm_common.hpp"
 
 namespace zoact {
@@ -658,6 +660,48 @@ hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const 
   if (e == hipErrorNotSupported && !shared) e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
   if (e != hipSuccess) return e;
   return launch_sum_mean(part, (int64_t)a.tiles_m_half * a.tiles_n * 4, (double)T * (double)L.d_out, loss_pm, s);
+}
+
+// Partial sums of the no-allocation regression-loss call: one array per GPU the library
+// runs on, kept until the process ends.  Host code never passes `scratch` itself to a
+// kernel (on the host it is only a stand-in for the symbol); it uses the device address
+// that hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) double scratch[ZOACT_MSE_SCRATCH_BYTES / sizeof(double)];
+
+// Device address of `scratch` on the current device, looked up once per device with that
+// device current and kept; nullptr (and *err set) if the lookup fails.
+static void* mse_scratch_ptr(hipError_t* err) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= 64) {
+    *err = e != hipSuccess ? e : hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || ptr == nullptr) {
+      *err = e != hipSuccess ? e : hipErrorInvalidSymbol;
+      return nullptr;
+    }
+    addr[dev] = ptr;
+  }
+  *err = hipSuccess;
+  return addr[dev];
+}
+
+hipError_t launch_linear_mse_noalloc(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T,
+                                     uint32_t flags, const void* p, const zoact_pert_pair& pert, const void* target,
+                                     float* loss_pm, hipStream_t s) {
+  hipError_t e = hipSuccess;
+  void* part = mse_scratch_ptr(&e);
+  if (part == nullptr) return e;
+  // every partial slot is written by the GEMM's epilogue before the sum reads it, so the
+  // previous call's contents need no clearing
+  return launch_linear_mse(L, A, x, T, flags, p, pert, target, static_cast<double*>(part), loss_pm, s);
 }
 
 size_t linear_xent_ws_bytes(int64_t T, int64_t d_out) {

@@ -93,6 +93,8 @@ SIGNATURES = {
     "zoact_linear_mse_workspace_bytes": ([_I64, _I64], _SZ),
     "zoact_linear_mse_pair": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I64, _U32, _P,
                                ctypes.POINTER(PertPair), _P, _P, _P, _SZ, _P], _I32),
+    "zoact_linear_mse_pair_noalloc": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I64, _U32, _P,
+                                       ctypes.POINTER(PertPair), _P, _P, _P], _I32),
     "zoact_mse_pm": ([_P, _I32, _P, _I64, _I64, _P, _P, _SZ, _P], _I32),
     "zoact_xent_pm": ([_P, _P, _I64, _I64, _I64, _P, _P, _SZ, _P], _I32),
     "zoact_step": ([ctypes.POINTER(ArenaDesc), _P, ctypes.POINTER(Pert), ctypes.POINTER(AdamDesc), _P, _P], _I32),
@@ -275,6 +277,21 @@ def linear_mse(layer: Linear, arena: Arena | None, x: torch.Tensor, T: int, p: t
     _check(lib().zoact_linear_mse_pair(ctypes.byref(d), ctypes.byref(a) if a is not None else None, _ptr(x), T,
                                        flags, _ptr(p), ctypes.byref(pp), _ptr(target), _ptr(loss_pm), _ptr(ws),
                                        ws.numel() * ws.element_size(), _stream(stream)))
+
+
+MSE_SCRATCH_BYTES = 1 << 20   # ZOACT_MSE_SCRATCH_BYTES
+
+
+def linear_mse_noalloc(layer: Linear, arena: Arena | None, x: torch.Tensor, T: int, p: torch.Tensor | None,
+                       pert: Pert | PertPair, target: torch.Tensor, loss_pm: torch.Tensor, stream=None,
+                       flags: int = 0):
+    """linear_mse() with the partial sums in the library's static device scratch (no workspace)."""
+    d = layer.desc()
+    a = arena.desc() if arena is not None else None
+    pp = as_pair(pert)
+    _check(lib().zoact_linear_mse_pair_noalloc(ctypes.byref(d), ctypes.byref(a) if a is not None else None, _ptr(x),
+                                               T, flags, _ptr(p), ctypes.byref(pp), _ptr(target), _ptr(loss_pm),
+                                               _stream(stream)))
 
 
 def loss_workspace_bytes() -> int:
