@@ -468,17 +468,38 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
       for (int f = 0; f < 8; ++f) v[f] = val(2 * q + (f >> 2), j, f & 3);
     }
   };
+  // the values of token block j's four pairs: without the in-epilogue correction all 32
+  // accumulator elements are read first (in block order), so that the arithmetic of the
+  // block's outputs is independent work the scheduler can interleave; with it, pair by pair
+  float vj[4][8];
+  auto block_vals = [&](int j) {
+    if constexpr (!CORR) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int f = 0; f < 8; ++f) vj[q][f] = val(2 * q + (f >> 2), j, f & 3);
+    }
+  };
+  auto pair_of = [&](int q, int j, float (&v)[8]) {
+    if constexpr (CORR) {
+      pair_vals(q, j, v);
+    } else {
+#pragma unroll
+      for (int f = 0; f < 8; ++f) v[f] = vj[q][f];
+    }
+  };
   if constexpr (EPI == EPI_MSE) {
     float sq = 0.f;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       float sj = 0.f;
+      block_vals(j);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         // squared error of the bf16-rounded outputs (features lk*8 .. +7) against the target;
         // a pair past N is computed too and its terms dropped
         float v[8];
-        pair_vals(q, j, v);
+        pair_of(q, j, v);
         const uint32_t t[4] = {tq[j][q].x, tq[j][q].y, tq[j][q].z, tq[j][q].w};
         float sp = 0.f;
 #pragma unroll
@@ -559,11 +580,12 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
     const int vy = (int)((lr * a.N + lk * 8) * ESZ);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
+      block_vals(j);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         // (a pair past N is computed too; its store goes through an offset past the range)
         float o[8];
-        pair_vals(q, j, o);
+        pair_of(q, j, o);
         if (res) {
           const uint32_t t[4] = {tr[j][q].x, tr[j][q].y, tr[j][q].z, tr[j][q].w};
 #pragma unroll
@@ -604,7 +626,7 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
     const int vy = (int)((lr * nout + lk * 4) * ESZ);
     // output block b of token block j: the residual added, one store per lane (none for a
     // block past N)
-    auto emit = [&](int j, int b, float (&o)[4]) {
+    auto emit = [&](int j, int b, float (&o)[4], int voff) {
       if (res) {
         o[0] += bf_lo(tv[j][b].x);
         o[1] += bf_hi(tv[j][b].x);
@@ -619,23 +641,37 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
       if (OUT_F32)
         __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{__float_as_uint(o[0]), __float_as_uint(o[1]),
                                                        __float_as_uint(o[2]), __float_as_uint(o[3])},
-                                               ys, vy, so, 0);
+                                               ys, voff, so, 0);
       else
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])}, ys, vy,
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])}, ys, voff,
                                               so, 0);
     };
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       if constexpr (SW) {
         // blocks 2q (gate) and 2q + 1 (up) of the 16-interleaved fused projection give
-        // output block q
+        // output block q.  The token block's 32 values are read first, so the 16 outputs'
+        // exp / reciprocal chains are independent work the scheduler can interleave (one at
+        // a time, each waits out the latency of its transcendental steps).
+        float gv[4][4], uv[4][4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            gv[q][e] = val(2 * q, j, e);
+            uv[q][e] = val(2 * q + 1, j, e);
+          }
+        float ov[4][4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) ov[q][e] = silu(gv[q][e]) * uv[q][e];
+        // an output block past N: its store goes through an offset past the range (in the
+        // wave's last row the block's own offset would still lie inside it)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          if (nw + q * 32 >= a.N) continue;   // uniform
-          float o[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) o[e] = silu(val(2 * q, j, e)) * val(2 * q + 1, j, e);
-          emit(j, q, o);
+          float o[4] = {ov[q][0], ov[q][1], ov[q][2], ov[q][3]};
+          emit(j, q, o, nw + q * 32 < a.N ? vy : OFF_NONE);
         }
       } else {
 #pragma unroll
@@ -644,7 +680,7 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
           float o[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) o[e] = val(i, j, e);
-          emit(j, i, o);
+          emit(j, i, o, vy);
         }
       }
       __builtin_amdgcn_sched_barrier(0);
