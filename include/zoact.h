@@ -176,7 +176,21 @@ zoact_status zoact_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e
 zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut,
                            int32_t r, void* p, zoact_stream stream);
 
-/* ------------------------------------------------------ fused +/- adapted linear
+/* The projection of a site whose input is a norm's output (the attention and MLP inputs
+ * of a decoder layer), fused with that norm: y = RMSNorm(x) * w, or LayerNorm(x) * w + b,
+ * over rows of d features (fp32 statistics, one rounding of y to bf16; eps as in the
+ * norm), and p = y U (the X V_r factor of Section 3's perturbed forward) from the rounded
+ * y, fp32 accumulation, one rounding.  x, y [rows][d], w, b [d], U^T [r][d], p [rows][r],
+ * all bf16; the rows are read once.  The same values as the norm followed by zoact_project
+ * up to the order of the fp32 sums.  Requirements: 16-byte aligned x, w, b, U^T, y;
+ * d = 128, or d % 256 == 0 with d / 256 in {1, 2, 4, 8, 16, 20} (up to 5120); 1 <= r <= 128;
+ * other shapes -> ZOACT_E_UNSUPPORTED (run the norm and zoact_project instead). */
+zoact_status zoact_rmsnorm_project(const void* x, const void* w, int64_t rows, int64_t d, float eps, const void* ut,
+                                   int32_t r, void* y, void* p, zoact_stream stream);
+zoact_status zoact_layernorm_project(const void* x, const void* w, const void* b, int64_t rows, int64_t d, float eps,
+                                     const void* ut, int32_t r, void* y, void* p, zoact_stream stream);
+
+/* ------------------------------------------------------ fused +/- adapted linear/* ------------------------------------------------------ fused +/- adapted linear
  * Section 3's perturbed forward evaluated for both signs in one pass over W:
  *   y[h] = epilogue(residual[h] + x[h] W^T + b + p[h] (C + s_h eps Z)^T),  s = (+1, -1)
  * x [2][T][d_in] and p [2][T][r] (from zoact_project on x; one copy of each,

@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libzoact.so")
 BUILD = os.path.join(ROOT, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["api.cpp", "k_step.hip", "k_gemm.hip", "k_gemm_4w.hip", "k_gemm_4w64.hip", "k_loss.hip", "k_basis.hip", "k_model.hip"]
+SOURCES = ["api.cpp", "k_step.hip", "k_gemm.hip", "k_gemm_4w.hip", "k_gemm_4w64.hip", "k_loss.hip", "k_basis.hip", "k_model.hip", "k_norm_proj.hip"]
 FLAGS = ["-O3", "-fPIC", "-std=c++17", "--offload-arch=gfx950", "-I", os.path.join(ROOT, "include"),
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wno-unused-result"]
 

@@ -145,6 +145,28 @@ static zoact_status validate_linear(const zoact_linear* L, const zoact_arena* A,
   return ZOACT_OK;
 }
 
+static zoact_status norm_project(bool layernorm, const void* x, const void* w, const void* b, int64_t rows, int64_t d,
+                                 float eps, const void* ut, int32_t r, void* y, void* p, zoact_stream stream) {
+  const char* who = layernorm ? "layernorm_project" : "rmsnorm_project";
+  CHECK(x && w && ut && y && p && (!layernorm || b), "%s: NULL pointer", who);
+  CHECK(rows >= 1 && d >= 1 && rows <= 0x7FFFFFFF, "%s: bad shape (rows=%lld, d=%lld)", who, (long long)rows,
+        (long long)d);
+  CHECK(r >= 1 && r <= 256, "%s: r=%d outside [1, 256]", who, r);
+  CHECK(aligned16(x) && aligned16(w) && aligned16(ut) && aligned16(y) && (!layernorm || aligned16(b)),
+        "%s: x, w, b, ut and y must be 16-byte aligned", who);
+  return hip_status(zoact::launch_norm_project(layernorm, x, w, b, rows, d, eps, ut, r, y, p, st(stream)), who);
+}
+
+zoact_status zoact_rmsnorm_project(const void* x, const void* w, int64_t rows, int64_t d, float eps, const void* ut,
+                                   int32_t r, void* y, void* p, zoact_stream stream) {
+  return norm_project(false, x, w, nullptr, rows, d, eps, ut, r, y, p, stream);
+}
+
+zoact_status zoact_layernorm_project(const void* x, const void* w, const void* b, int64_t rows, int64_t d, float eps,
+                                     const void* ut, int32_t r, void* y, void* p, zoact_stream stream) {
+  return norm_project(true, x, w, b, rows, d, eps, ut, r, y, p, stream);
+}
+
 zoact_status zoact_linear_fwd_pair(const zoact_linear* L, const zoact_arena* A, const void* x, int32_t x_dtype,
                                    int64_t T, const void* p, const void* residual, uint32_t flags,
                                    const zoact_pert_pair* pert, void* y, int32_t y_dtype, zoact_stream stream) {

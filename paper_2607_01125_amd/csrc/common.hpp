@@ -33,6 +33,10 @@ hipError_t launch_dequant_int4(const void* w, const void* scales, int64_t d_out,
                                hipStream_t s);
 hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut, int32_t r,
                           void* p, hipStream_t s);
+// Norm (RMSNorm, or LayerNorm with bias b) of n_tok rows and the projection of its output,
+// P = y U (bf16); hipErrorNotSupported outside the fused kernel's shapes.
+hipError_t launch_norm_project(bool layernorm, const void* x, const void* w, const void* b, int64_t n_tok, int64_t d,
+                               float eps, const void* ut, int r, void* y, void* p, hipStream_t s);
 hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const void* x, int32_t x_dtype, int64_t T,
                             const void* p, const void* residual, uint32_t flags, const zoact_pert_pair& pert,
                             void* y, int32_t y_dtype, hipStream_t s);

@@ -42,6 +42,10 @@ import torch
 from . import zoact as Z
 
 SITES = ("attn", "o", "mlp", "down")
+# widths covered by zoact_rmsnorm_project / zoact_layernorm_project, and the largest row
+# count at which the decoder uses them
+NORM_PROJECT_WIDTHS = (128, 256, 512, 1024, 2048, 4096, 5120)
+NORM_PROJECT_MAX_ROWS = 4096
 
 
 @dataclass
@@ -148,6 +152,14 @@ class Decoder:
         # layer 0 reads the same embedding in both halves: its first projection forms x W^T
         # and x U once (ZOACT_SHARED_X) when the layer qualifies
         self.shared_first = True
+        # norms that feed an adapted site (attention and MLP inputs) also form the site's
+        # projection P = x U in the same pass where the library covers the width and it is
+        # the faster form: up to NORM_PROJECT_MAX_ROWS rows (measured on MI355X at d = 4096,
+        # r = 32: 4096 rows 25.3 us fused against 29.4 us for the norm and the projection
+        # apart; 8192 rows 42.0 against 39.6 us -- the fused pass re-reads its 16-token
+        # rows from L2 or memory between the statistics and the projection, and the
+        # separate norm already runs near the memory rate)
+        self.fuse_norm_project = mode != "fp32" and self.r <= 128 and self.d in NORM_PROJECT_WIDTHS
         # INT4 layers: dequantised once per forward into one bf16 buffer (the largest layer's
         # size) and run on the bf16 schedule; False keeps the in-register INT4 GEMM
         self._wdq = None
@@ -254,6 +266,23 @@ class Decoder:
         return self._rope[seq]
 
     # ---------------------------------------------------------------- forward of both halves
+    def _norm_site(self, l, site, x, w, b, y, adapt, calibrate):
+        """The norm of x into y, then the site's projection of y into P (U^T of the site, or
+        None where it is not adapted); one fused pass where the library covers it."""
+        if (adapt and self.fuse_norm_project and x.shape[0] <= NORM_PROJECT_MAX_ROWS
+                and (l, site) in self._adapted_sites):
+            ut = self.ut.get((l, site))
+            if ut is None:
+                raise RuntimeError(f"no basis for site {(l, site)}: run basis_init or set_basis first")
+            p = self._cur["p"][:x.shape[0]]
+            if self.s.family == "llama":
+                Z.rmsnorm_project(x, w, y, self.s.norm_eps, ut, p)
+            else:
+                Z.layernorm_project(x, w, b, y, self.s.norm_eps, ut, p)
+            return ut
+        self._norm(x, w, b, y)
+        return self._site(l, site, y, adapt, calibrate)
+
     def _norm(self, x, w, b, y):
         if self.s.family == "llama":
             Z.rmsnorm(x, w, y, self.s.norm_eps)
@@ -334,18 +363,15 @@ class Decoder:
                       and self._shared_ok(P["qkv"], self.ut.get((0, "attn"))))
             if shared:
                 a1 = B["a"][:T]
-                self._norm(h[:T], P["n1"], P.get("n1b"), a1)
-                ut = self._site(l, "attn", a1, adapt, calibrate)
+                ut = self._norm_site(l, "attn", h[:T], P["n1"], P.get("n1b"), a1, adapt, calibrate)
                 self._apply(P["qkv"], a1, T, qkv, pert, ut, flags=Z.SHARED_X, adapt=adapt)
                 q, k, v = qkv[:, :d], qkv[:, d:d + dkv], qkv[:, d + dkv:]
             elif "qkv" in P:
-                self._norm(h, P["n1"], P.get("n1b"), B["a"])
-                ut = self._site(l, "attn", B["a"], adapt, calibrate)
+                ut = self._norm_site(l, "attn", h, P["n1"], P.get("n1b"), B["a"], adapt, calibrate)
                 self._apply(P["qkv"], B["a"], T, qkv, pert, ut, adapt=adapt)
                 q, k, v = qkv[:, :d], qkv[:, d:d + dkv], qkv[:, d + dkv:]
             else:
-                self._norm(h, P["n1"], P.get("n1b"), B["a"])
-                ut = self._site(l, "attn", B["a"], adapt, calibrate)
+                ut = self._norm_site(l, "attn", h, P["n1"], P.get("n1b"), B["a"], adapt, calibrate)
                 self._apply(P["qv"], B["a"], T, qkv, pert, ut, adapt=adapt)
                 self._apply(P["k"], B["a"], T, B["k"], pert, None, adapt=False)
                 q, k, v = qkv[:, :d], B["k"], qkv[:, d:]
@@ -358,8 +384,7 @@ class Decoder:
             self._apply(P["o"], B["att"], T, h_alt, pert, ut, residual=h, adapt=adapt)
             h, h_alt = h_alt, h
             # MLP block
-            self._norm(h, P["n2"], P.get("n2b"), B["a"])
-            ut = self._site(l, "mlp", B["a"], adapt, calibrate)
+            ut = self._norm_site(l, "mlp", h, P["n2"], P.get("n2b"), B["a"], adapt, calibrate)
             flags = Z.EPI_SWIGLU if s.family == "llama" else Z.EPI_RELU
             self._apply(P["gu"], B["a"], T, B["ff"], pert, ut, flags=flags, adapt=adapt)
             ut = self._site(l, "down", B["ff"], adapt, calibrate)

@@ -77,6 +77,8 @@ SIGNATURES = {
     "zoact_last_error": ([], ctypes.c_char_p),
     "zoact_gen_z": ([_U64, _U32, _U32, _I64, _I64, _P, _P], _I32),
     "zoact_project": ([_P, _I32, _I64, _I64, _P, _I32, _P, _P], _I32),
+    "zoact_rmsnorm_project": ([_P, _P, _I64, _I64, _F, _P, _I32, _P, _P, _P], _I32),
+    "zoact_layernorm_project": ([_P, _P, _P, _I64, _I64, _F, _P, _I32, _P, _P, _P], _I32),
     "zoact_linear_fwd_pm": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I32, _I64, _P, _P, _U32,
                              ctypes.POINTER(Pert), _P, _I32, _P], _I32),
     "zoact_perturb_coeffs": ([ctypes.POINTER(ArenaDesc), _I64, _I64, ctypes.POINTER(Pert), _P, _P], _I32),
@@ -209,6 +211,23 @@ def project(x: torch.Tensor, ut: torch.Tensor, p: torch.Tensor, stream=None):
     d_in = x.shape[-1]
     n_tok = x.numel() // d_in
     _check(lib().zoact_project(_ptr(x), dtype_code(x), n_tok, d_in, _ptr(ut), ut.shape[0], _ptr(p), _stream(stream)))
+
+
+def rmsnorm_project(x: torch.Tensor, w: torch.Tensor, y: torch.Tensor, eps: float, ut: torch.Tensor, p: torch.Tensor,
+                    stream=None):
+    """y = RMSNorm(x) * w and p = y U in one pass (bf16); raises ZoactError(E_UNSUPPORTED)
+    outside the fused kernel's shapes."""
+    d = x.shape[-1]
+    _check(lib().zoact_rmsnorm_project(_ptr(x), _ptr(w), x.numel() // d, d, eps, _ptr(ut), ut.shape[0], _ptr(y),
+                                       _ptr(p), _stream(stream)))
+
+
+def layernorm_project(x: torch.Tensor, w: torch.Tensor, b: torch.Tensor, y: torch.Tensor, eps: float,
+                      ut: torch.Tensor, p: torch.Tensor, stream=None):
+    """y = LayerNorm(x) * w + b and p = y U in one pass (bf16)."""
+    d = x.shape[-1]
+    _check(lib().zoact_layernorm_project(_ptr(x), _ptr(w), _ptr(b), x.numel() // d, d, eps, _ptr(ut), ut.shape[0],
+                                         _ptr(y), _ptr(p), _stream(stream)))
 
 
 def linear_fwd_pm(layer: Linear, arena: Arena | None, x: torch.Tensor, T: int, p: torch.Tensor | None,

@@ -79,9 +79,16 @@ def _models(shape, mode, seed=0, perturb=False):
 
 
 def _logits_close(got, want, rel, what):
+    """The bar: norm-relative error <= rel.  Element-wise, no logit beyond rel |want| +
+    3 rel rms(want): a logit is a dot product of bf16 activations that differ from the
+    oracle's by rounding decisions, so its error is a sum of many small terms with a
+    normal tail, which thousands of logits sample out to several standard deviations."""
+    rms = np.sqrt(np.mean(want ** 2))
     err = np.linalg.norm(got - want) / np.linalg.norm(want)
+    print(f"[parity] {what}: norm-relative {err:.3e}, max |d|/rms {np.max(np.abs(got - want)) / rms:.3e}",
+          flush=True)
     assert err <= rel, f"{what}: norm-relative error {err:.3e} > {rel}"
-    bound = rel * np.abs(want) + rel * np.sqrt(np.mean(want ** 2))
+    bound = rel * np.abs(want) + 3 * rel * rms
     bad = np.abs(got - want) > bound
     assert not bad.any(), f"{what}: {bad.sum()} elements outside {rel} (first {np.argwhere(bad)[0]})"
 
