@@ -494,6 +494,36 @@ def bench_ranks(dev, reps, ranks=(1, 8, 32, 64, 128, 256)):
 
 
 # ------------------------------------------------------------------ full models
+# Algorithm 1 over a model: adaptive subspace iteration to a residual of 1e-4 of
+# theta_1, estimated every 8 iterations, at most 64 (sites that miss it are reported)
+BASIS_TOL = 1e-4
+
+
+def basis_opts():
+    from paper_2607_01125_amd import zoact as Z
+    return Z.EigOpts(0, 64, 0x5EED, BASIS_TOL, 1, 8)
+
+
+def summarise_basis_report(rep: dict) -> dict:
+    """Per-model convergence summary of Decoder.basis_report: worst residual, smallest gap
+    theta_r / theta_{r+1}, iterations, sites that missed the bound; and the same per site kind."""
+    import numpy as np
+
+    def summ(vals):
+        res = [v["resid"] for v in vals]
+        gap = [v["gap"] for v in vals]
+        its = [v["iters"] for v in vals]
+        return {"sites": len(vals), "not_converged": sum(not v["converged"] for v in vals),
+                "resid_max": float(f"{max(res):.3g}"), "resid_median": float(f"{float(np.median(res)):.3g}"),
+                "gap_min": round(min(gap), 5), "gap_median": round(float(np.median(gap)), 5),
+                "iters_min": min(its), "iters_median": int(np.median(its)), "iters_max": max(its)}
+    kinds = sorted({site for (_, site) in rep})
+    out = summ(list(rep.values()))
+    out["tol"] = BASIS_TOL
+    out["by_site"] = {k: summ([v for (l, site), v in rep.items() if site == k]) for k in kinds}
+    return out
+
+
 def model_step_flops(shape, B, S):
     """Algorithmic FLOPs of one +/- step: both halves' linears, LM head, causal attention,
     projection (once per adapted site) and correction."""
@@ -597,9 +627,12 @@ def bench_model(dev, which, warmup=2, steps=5, extras=True, roofline=False):
     tok = torch.from_numpy(synth.uniform_tokens(B, S, shape.vocab, 0, 2)).to(dev)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    g.basis_init(calib)
+    g.basis_init(calib, basis_opts(), report=True)
     torch.cuda.synchronize()
     init_s = time.perf_counter() - t0
+    basis = summarise_basis_report(g.basis_report)
+    log(f"{which}: basis {basis['sites']} sites, {basis['not_converged']} above tol, resid max "
+        f"{basis['resid_max']}, gap min {basis['gap_min']}, iterations {basis['iters_min']}-{basis['iters_max']}")
     timer = None
     if roofline:
         timer = LaunchTimer(steps * (4 * shape.n_layers + 8))
@@ -622,7 +655,7 @@ def bench_model(dev, which, warmup=2, steps=5, extras=True, roofline=False):
     flops = model_step_flops(shape, B, S)
     rec = {"steps_per_s": round(1e3 / ms, 3), "ms_per_step": round(ms, 2),
            "model_tflops": round(flops / (ms * 1e-3) / 1e12, 1), "step_tflop": round(flops / 1e12, 2),
-           "basis_init_s": round(init_s, 3), "calibration_tokens": CB * CS, "tokens_per_half": B * S,
+           "basis_init_s": round(init_s, 3), "basis": basis, "calibration_tokens": CB * CS, "tokens_per_half": B * S,
            "rank": shape.rank, "k": g.k, "losses": [float(v) for v in g.loss_pm.cpu().numpy()],
            "status": int(g.status.item()), "setup_s": round(setup_s, 1)}
     if timer is not None:

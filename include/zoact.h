@@ -143,12 +143,38 @@ typedef struct {
   float step_size, inv_sqrt_bc2, one_minus_beta1, one_minus_beta2;
 } zoact_adam;
 
-/* Options of the eigensolver behind zoact_basis_from_gram (NULL = defaults). */
+/* Options of the eigensolver behind zoact_basis_from_gram (NULL = defaults; a field
+   at 0 takes its default).  Fixed mode (adaptive == 0) runs max_iter subspace
+   iterations and synchronises nothing unless tol > 0, in which case the call waits for
+   the stream, reads the final residual and returns ZOACT_E_NOCONVERGE when it is above
+   tol (the outputs are written all the same).  Adaptive mode (adaptive != 0, needs
+   tol > 0) estimates the residual from the iteration's own products (one readback per
+   check) after check_every and 2 check_every iterations, then at the iteration where the
+   estimates' geometric rate predicts tol (at least check_every later; no further checks
+   once that lies past max_iter or the estimate stops falling); it stops as soon as an
+   estimate is at or below tol, then checks the exact residual and goes on iterating
+   while that is above tol and iterations remain. */
 typedef struct {
-  int32_t oversample; /* extra block columns p (default r)                  */
-  int32_t iters;      /* subspace iterations (default 64)                   */
-  uint64_t seed;      /* seed of the random start block                     */
+  int32_t oversample;  /* extra block columns p (default r)                     */
+  int32_t max_iter;    /* subspace iterations, the most in adaptive mode (64)   */
+  uint64_t seed;       /* seed of the random start block                        */
+  float tol;           /* residual bound (0: none)                              */
+  int32_t adaptive;    /* stop early once the residual is below tol             */
+  int32_t check_every; /* iterations between adaptive checks (default 8)        */
 } zoact_eig_opts;
+
+/* Convergence report of one basis solve, written to device memory at the end of the
+   call (in stream order).  resid = max_i ||G u_i - theta_i u_i|| / theta_1 of the
+   returned basis (fp64 products); gap = theta_r / theta_{r+1}, the last kept over
+   the first discarded Ritz value (1 means no gap: the top-r subspace is then not
+   determined by G); iters = subspace iterations run; converged = resid <= tol, or 1
+   when tol == 0. */
+typedef struct {
+  float resid;
+  float gap;
+  int32_t iters;
+  int32_t converged;
+} zoact_eig_report;
 
 /* ------------------------------------------------------------------ info */
 const char* zoact_version(void);
@@ -341,29 +367,33 @@ zoact_status zoact_step_q_sgd(const zoact_arena* A, const float* losses, int32_t
  * Top-r right singular vectors of the calibration activations X_l, i.e. the top-r
  * eigenvectors of the uncentred Gram X^T X, largest first, each column signed so
  * that its largest-magnitude entry is positive.
- * zoact_gram: g [d][d] fp32 (+)= X^T X for x [n_tok][d] (F32 or BF16); `accumulate`
- *   != 0 adds to g (chunked calibration batches).
+ * zoact_gram: g [d][d] fp32 (+)= X^T X for x [n_tok] rows of d values (F32 or BF16)
+ *   with row stride ld_x >= d elements; `accumulate` != 0 adds to g (chunked
+ *   calibration batches).  BF16 needs d % 64 == 0, ld_x % 8 == 0 and x 16-byte aligned.
  * zoact_basis_from_gram: top-r eigenpairs of g by randomised block subspace
  *   iteration (block r + oversample), Rayleigh-Ritz and a Jacobi eigensolver of
  *   the projected block; writes ut [r][d] in ut_dtype (F32/BF16), optional
- *   ut_master fp32 [r][d], eigvals fp32 [r] (descending) and resid fp32 [1]
- *   (max_i ||G u_i - lambda_i u_i|| / lambda_1).  Workspace: ws of at least
- *   zoact_basis_workspace_bytes(d, r, opts) bytes.
+ *   ut_master fp32 [r][d], eigvals fp32 [r] (descending) and the convergence report
+ *   (device, nullable; see zoact_eig_report).  Iteration control and synchronisation:
+ *   see zoact_eig_opts.  Workspace: ws of at least zoact_basis_workspace_bytes(d, r,
+ *   opts) bytes.
  * zoact_basis_init: zoact_gram followed by zoact_basis_from_gram, with g at the
  *   start of ws; ws needs zoact_basis_init_workspace_bytes(d, r, opts) bytes (the
  *   Gram d*d fp32, padded to 256 bytes, then the solver's workspace).
- * Errors: r < 1, r > 256, r + p > d, n_tok < r -> ZOACT_E_INVALID; a workspace that
- * is NULL or too small -> ZOACT_E_WORKSPACE. */
+ * Errors: r < 1, r > 256, r + p > d, n_tok < r, ld_x < d, negative tol or
+ * check_every, adaptive with tol == 0 -> ZOACT_E_INVALID; a workspace that is NULL or
+ * too small -> ZOACT_E_WORKSPACE; residual above tol -> ZOACT_E_NOCONVERGE (outputs
+ * written, report->converged = 0). */
 size_t zoact_basis_workspace_bytes(int64_t d, int32_t r, const zoact_eig_opts* opts);
 size_t zoact_basis_init_workspace_bytes(int64_t d, int32_t r, const zoact_eig_opts* opts);
-zoact_status zoact_gram(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, float* g,
+zoact_status zoact_gram(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, int64_t ld_x, float* g,
                         int32_t accumulate, zoact_stream stream);
 zoact_status zoact_basis_from_gram(const float* g, int64_t d, int32_t r, const zoact_eig_opts* opts,
                                    void* ut, int32_t ut_dtype, float* ut_master, float* eigvals,
-                                   float* resid, void* ws, size_t ws_bytes, zoact_stream stream);
-zoact_status zoact_basis_init(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, int32_t r,
+                                   zoact_eig_report* report, void* ws, size_t ws_bytes, zoact_stream stream);
+zoact_status zoact_basis_init(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, int64_t ld_x, int32_t r,
                               const zoact_eig_opts* opts, void* ut, int32_t ut_dtype, float* ut_master,
-                              float* eigvals, float* resid, void* ws, size_t ws_bytes,
+                              float* eigvals, zoact_eig_report* report, void* ws, size_t ws_bytes,
                               zoact_stream stream);
 
 #ifdef __cplusplus

@@ -364,18 +364,21 @@ zoact_status zoact_step_q_sgd(const zoact_arena* A, const float* losses, int32_t
                     "step_q_sgd");
 }
 
-static void eig_defaults(int32_t r, const zoact_eig_opts* o, int32_t& p, int32_t& iters, uint64_t& seed) {
-  p = (o && o->oversample > 0) ? o->oversample : r;
-  iters = (o && o->iters > 0) ? o->iters : 64;
-  seed = o ? o->seed : 0x5eedULL;
+// Options with every default resolved (r is the basis rank).
+static zoact_eig_opts eig_resolve(int32_t r, const zoact_eig_opts* o) {
+  zoact_eig_opts e{};
+  e.oversample = (o && o->oversample > 0) ? o->oversample : r;
+  e.max_iter = (o && o->max_iter > 0) ? o->max_iter : 64;
+  e.seed = o ? o->seed : 0x5eedULL;
+  e.tol = o ? o->tol : 0.f;
+  e.adaptive = o ? o->adaptive : 0;
+  e.check_every = (o && o->check_every > 0) ? o->check_every : 8;
+  return e;
 }
 
 size_t zoact_basis_workspace_bytes(int64_t d, int32_t r, const zoact_eig_opts* opts) {
-  int32_t p, it;
-  uint64_t sd;
-  eig_defaults(r, opts, p, it, sd);
   if (d < 1 || r < 1) return 0;
-  return zoact::basis_ws_bytes(d, r, p);
+  return zoact::basis_ws_bytes(d, r, eig_resolve(r, opts).oversample);
 }
 
 // Gram block at the start of the workspace, padded to 256 bytes so the solver's
@@ -387,48 +390,59 @@ size_t zoact_basis_init_workspace_bytes(int64_t d, int32_t r, const zoact_eig_op
   return solver ? gram_ws_bytes(d) + solver : 0;
 }
 
-zoact_status zoact_gram(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, float* g, int32_t accumulate,
-                        zoact_stream stream) {
+zoact_status zoact_gram(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, int64_t ld_x, float* g,
+                        int32_t accumulate, zoact_stream stream) {
   CHECK(x && g, "gram: NULL pointer");
   CHECK(float_type(x_dtype), "gram: dtype must be F32 or BF16");
   CHECK(n_tok >= 1 && d >= 1, "gram: empty shape");
-  if (x_dtype == ZOACT_BF16) CHECK(d % 64 == 0, "gram: bf16 needs d %% 64 == 0");
-  return hip_status(zoact::launch_gram(x, x_dtype, n_tok, d, g, accumulate, st(stream)), "gram");
+  CHECK(ld_x >= d, "gram: row stride %lld < d = %lld", (long long)ld_x, (long long)d);
+  if (x_dtype == ZOACT_BF16) {
+    CHECK(d % 64 == 0, "gram: bf16 needs d %% 64 == 0");
+    CHECK(ld_x % 8 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0,
+          "gram: bf16 needs a row stride that is a multiple of 8 and x 16-byte aligned");
+  }
+  return hip_status(zoact::launch_gram(x, x_dtype, n_tok, d, ld_x, g, accumulate, st(stream)), "gram");
 }
 
 zoact_status zoact_basis_from_gram(const float* g, int64_t d, int32_t r, const zoact_eig_opts* opts, void* ut,
-                                   int32_t ut_dtype, float* ut_master, float* eigvals, float* resid, void* ws,
-                                   size_t ws_bytes, zoact_stream stream) {
-  int32_t p, iters;
-  uint64_t seed;
-  eig_defaults(r, opts, p, iters, seed);
+                                   int32_t ut_dtype, float* ut_master, float* eigvals, zoact_eig_report* report,
+                                   void* ws, size_t ws_bytes, zoact_stream stream) {
+  const zoact_eig_opts o = eig_resolve(r, opts);
+  const int32_t p = o.oversample;
   CHECK(g && ut, "basis_from_gram: NULL g or ut");
   CHECK(float_type(ut_dtype), "basis_from_gram: ut dtype must be F32 or BF16");
   CHECK(r >= 1 && r <= 256, "basis_from_gram: r=%d outside [1, 256]", r);
   CHECK(d >= 2 && r + p <= d, "basis_from_gram: r + oversample = %d exceeds d = %lld", r + p, (long long)d);
   CHECK(r + p <= 512, "basis_from_gram: block r + oversample = %d exceeds 512", r + p);
+  CHECK(o.tol >= 0.f, "basis_from_gram: negative tol");
+  CHECK(!o.adaptive || o.tol > 0.f, "basis_from_gram: adaptive mode needs tol > 0");
+  CHECK(!opts || (opts->max_iter >= 0 && opts->check_every >= 0 && opts->oversample >= 0),
+        "basis_from_gram: negative option");
   const size_t need = zoact::basis_ws_bytes(d, r, p);
   if (ws == nullptr || ws_bytes < need) return fail(ZOACT_E_WORKSPACE, "basis_from_gram: workspace needs %zu bytes", need);
-  return hip_status(
-      zoact::launch_basis_from_gram(g, d, r, p, iters, seed, ut, ut_dtype, ut_master, eigvals, resid, ws, st(stream)),
-      "basis_from_gram");
+  bool met = true;
+  const zoact_status s = hip_status(zoact::launch_basis_from_gram(g, d, r, p, o, ut, ut_dtype, ut_master, eigvals,
+                                                                  report, ws, st(stream), met),
+                                    "basis_from_gram");
+  if (s != ZOACT_OK) return s;
+  if (!met) return fail(ZOACT_E_NOCONVERGE, "basis_from_gram: residual above tol %g after %d iterations", o.tol,
+                        o.max_iter);
+  return ZOACT_OK;
 }
 
-zoact_status zoact_basis_init(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, int32_t r,
+zoact_status zoact_basis_init(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d, int64_t ld_x, int32_t r,
                               const zoact_eig_opts* opts, void* ut, int32_t ut_dtype, float* ut_master, float* eigvals,
-                              float* resid, void* ws, size_t ws_bytes, zoact_stream stream) {
+                              zoact_eig_report* report, void* ws, size_t ws_bytes, zoact_stream stream) {
   CHECK(n_tok >= r, "basis_init: n_tok=%lld < r=%d", (long long)n_tok, r);
-  int32_t p, iters;
-  uint64_t seed;
-  eig_defaults(r, opts, p, iters, seed);
+  const int32_t p = eig_resolve(r, opts).oversample;
   CHECK(r >= 1 && r <= 256 && d >= 2 && r + p <= d, "basis_init: bad r=%d for d=%lld", r, (long long)d);
   const size_t gbytes = gram_ws_bytes(d);
   const size_t need = gbytes + zoact::basis_ws_bytes(d, r, p);
   if (ws == nullptr || ws_bytes < need) return fail(ZOACT_E_WORKSPACE, "basis_init: workspace needs %zu bytes", need);
   float* g = static_cast<float*>(ws);
-  zoact_status s = zoact_gram(x, x_dtype, n_tok, d, g, 0, stream);
+  zoact_status s = zoact_gram(x, x_dtype, n_tok, d, ld_x, g, 0, stream);
   if (s != ZOACT_OK) return s;
-  return zoact_basis_from_gram(g, d, r, opts, ut, ut_dtype, ut_master, eigvals, resid,
+  return zoact_basis_from_gram(g, d, r, opts, ut, ut_dtype, ut_master, eigvals, report,
                                static_cast<char*>(ws) + gbytes, ws_bytes - gbytes, stream);
 }
 

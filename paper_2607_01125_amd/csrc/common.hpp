@@ -62,11 +62,12 @@ hipError_t launch_mse_pm(const void* y, int32_t dtype, const void* target, int64
                          void* ws, hipStream_t s);
 hipError_t launch_xent_pm(const float* logits, const int32_t* tokens, int64_t B, int64_t S, int64_t V,
                           float* loss_pm, void* ws, hipStream_t s);
-hipError_t launch_gram(const void* x, int32_t dtype, int64_t n_tok, int64_t d, float* g, int accumulate,
+hipError_t launch_gram(const void* x, int32_t dtype, int64_t n_tok, int64_t d, int64_t ld, float* g, int accumulate,
                        hipStream_t s);
-hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t p, int32_t iters, uint64_t seed,
-                                  void* ut, int32_t ut_dtype, float* ut_master, float* eigvals, float* resid,
-                                  void* ws, hipStream_t s);
+// `o` with every default resolved; `met` = false when tol > 0 and the final residual is above it.
+hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t p, const zoact_eig_opts& o, void* ut,
+                                  int32_t ut_dtype, float* ut_master, float* eigvals, zoact_eig_report* report, void* ws,
+                                  hipStream_t s, bool& met);
 size_t basis_ws_bytes(int64_t d, int32_t r, int32_t p);
 
 // Record the detail text of a failed call for zoact_last_error() and return `st`.

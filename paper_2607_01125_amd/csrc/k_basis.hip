@@ -20,6 +20,11 @@
 #include "common.hpp"
 #include "rng.hpp"
 
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <utility>
+
 namespace zoact {
 
 namespace {
@@ -27,8 +32,35 @@ namespace {
 constexpr int GT = 128;  // Gram output tile
 
 // --------------------------------------------------------------- Gram, bf16 MFMA
+// One workgroup per 128 x 128 tile of the upper triangle; four waves of 64 x 64
+// (4 x 4 v_mfma_f32_16x16x32_bf16 tiles).  Tokens advance 64 at a time.  The MFMA wants
+// each lane's 8 contraction values (tokens) consecutive, X has features consecutive, so
+// each thread loads an 8 token x 8 feature block (eight 16-byte row loads, coalesced
+// across the 16 lanes that cover 128 features), transposes it in registers with byte
+// permutes and writes eight 16-byte feature rows into the LDS tile [feature][token].  The
+// LDS tiles are double-buffered and the next block's loads are issued before the current
+// block's MFMAs, one barrier per 64 tokens.  A diagonal tile loads its operand once.
+constexpr int GK = 64;        // tokens per step
+constexpr int GLD = GK + 8;   // LDS row pitch (elements): 144 bytes
+
+// 8 x 8 transpose of 16-bit values: in[e] holds row e (8 values), out[j] column j.
+__device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;   // high or low halves
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t* a = reinterpret_cast<const uint32_t*>(&in[2 * q]);
+      const uint32_t* b = reinterpret_cast<const uint32_t*>(&in[2 * q + 1]);
+      w[q] = __builtin_amdgcn_perm(b[j >> 1], a[j >> 1], sel);
+    }
+    out[j] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
 __global__ void __launch_bounds__(256) gram_bf16_kernel(const uint16_t* __restrict__ x, int64_t n_tok, int64_t d,
-                                                        float* __restrict__ g, int accumulate, int ntile) {
+                                                        int64_t ld, float* __restrict__ g, int accumulate, int ntile) {
   // upper-triangular tile index -> (ti, tj), ti <= tj
   int t = blockIdx.x, ti = 0;
   while (t >= ntile - ti) {
@@ -36,48 +68,60 @@ __global__ void __launch_bounds__(256) gram_bf16_kernel(const uint16_t* __restri
     ++ti;
   }
   const int tj = ti + t;
-  __shared__ __align__(16) uint16_t sa[GT][40];  // [feature][token], padded
-  __shared__ __align__(16) uint16_t sb[GT][40];
+  const bool diag = ti == tj;
+  __shared__ __align__(16) uint16_t sm[2][2][GT * GLD];   // [buffer][operand][feature][token]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lk = lane >> 4;
   const int wi = (wave >> 1) * 64, wj = (wave & 1) * 64;
+  const int64_t fi0 = (int64_t)ti * GT, fj0 = (int64_t)tj * GT;
+  // this thread's load block: operand, token group (8 tokens), feature group (8 features)
+  const int opnd = threadIdx.x >> 7, tg = (threadIdx.x >> 4) & 7, fg = threadIdx.x & 15;
+  const bool loader = !(diag && opnd == 1);
+  const int64_t feat = (opnd ? fj0 : fi0) + fg * 8;
+  const bool fvalid = feat < d;
+  uint4 rows[8];
+  auto load = [&](int64_t k0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int64_t tk = k0 + tg * 8 + e;
+      rows[e] = (loader && fvalid && tk < n_tok) ? *reinterpret_cast<const uint4*>(x + tk * ld + feat)
+                                                 : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
   floatx4 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int64_t fi0 = (int64_t)ti * GT, fj0 = (int64_t)tj * GT;
-  for (int64_t k0 = 0; k0 < n_tok; k0 += 32) {
-    // 32 tokens x 128 features per operand: 512 chunks of 8 features, 2 per thread
+  const int nsteps = (int)((n_tok + GK - 1) / GK);
+  load(0);
+  for (int step = 0; step < nsteps; ++step) {
+    const int buf = step & 1;
+    if (loader) {
+      uint4 cols[8];
+      transpose8x8(rows, cols);
+      uint16_t* dst = &sm[buf][opnd][(fg * 8) * GLD + tg * 8];
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int idx = threadIdx.x + 256 * c;
-      const int tok = idx >> 4, fc = idx & 15;
-      const int64_t tk = k0 + tok;
-      uint4 va = make_uint4(0, 0, 0, 0), vb = make_uint4(0, 0, 0, 0);
-      if (tk < n_tok) {
-        if (fi0 + fc * 8 < d) va = *reinterpret_cast<const uint4*>(x + tk * d + fi0 + fc * 8);
-        if (fj0 + fc * 8 < d) vb = *reinterpret_cast<const uint4*>(x + tk * d + fj0 + fc * 8);
-      }
-      const uint16_t* pa = reinterpret_cast<const uint16_t*>(&va);
-      const uint16_t* pb = reinterpret_cast<const uint16_t*>(&vb);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        sa[fc * 8 + e][tok] = pa[e];
-        sb[fc * 8 + e][tok] = pb[e];
-      }
+      for (int j = 0; j < 8; ++j) *reinterpret_cast<uint4*>(dst + j * GLD) = cols[j];
     }
     __syncthreads();
-    bf16x8 af[4], bfr[4];
+    if (step + 1 < nsteps) load((int64_t)(step + 1) * GK);
+    const uint16_t* sa = sm[buf][0];
+    const uint16_t* sb = sm[buf][diag ? 0 : 1];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(&sa[wi + i * 16 + lr][lk * 8]);
+    for (int kh = 0; kh < GK / 32; ++kh) {
+      bf16x8 af[4], bfr[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(&sb[wj + j * 16 + lr][lk * 8]);
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(sa + (wi + i * 16 + lr) * GLD + kh * 32 + lk * 8);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < 4; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8*>(sb + (wj + j * 16 + lr) * GLD + kh * 32 + lk * 8);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    __syncthreads();
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -91,17 +135,17 @@ __global__ void __launch_bounds__(256) gram_bf16_kernel(const uint16_t* __restri
           float v = acc[i][j][q];
           if (accumulate) v += g[r * d + c];
           g[r * d + c] = v;
-          if (ti != tj) g[c * d + r] = v;
+          if (!diag) g[c * d + r] = v;
         }
       }
 }
 
-__global__ void gram_f32_kernel(const float* __restrict__ x, int64_t n_tok, int64_t d, float* __restrict__ g,
-                                int accumulate) {
+__global__ void gram_f32_kernel(const float* __restrict__ x, int64_t n_tok, int64_t d, int64_t ld,
+                                float* __restrict__ g, int accumulate) {
   for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < d * d; o += (int64_t)gridDim.x * blockDim.x) {
     const int64_t i = o / d, j = o % d;
     double s = 0.0;
-    for (int64_t t = 0; t < n_tok; ++t) s += (double)x[t * d + i] * (double)x[t * d + j];
+    for (int64_t t = 0; t < n_tok; ++t) s += (double)x[t * ld + i] * (double)x[t * ld + j];
     g[o] = accumulate ? g[o] + (float)s : (float)s;
   }
 }
@@ -143,6 +187,9 @@ struct EigWs {
   double* theta;  // [b]
   int* order;     // [b]
   double* u;      // [d][r]
+  double* h;      // [b][b] projected block Q^T Y of a convergence check
+  double* info;   // [4]: estimated residual, final residual
+  float* info32;  // [4]: the same in fp32, for the host to read
 };
 
 EigWs carve(void* ws, int64_t d, int b, int r, int ks) {
@@ -161,6 +208,9 @@ EigWs carve(void* ws, int64_t d, int b, int r, int ks) {
   w.theta = reinterpret_cast<double*>(p); p += align256((size_t)b * 8);
   w.order = reinterpret_cast<int*>(p); p += align256((size_t)b * 4);
   w.u = reinterpret_cast<double*>(p); p += align256((size_t)d * r * 8);
+  w.h = reinterpret_cast<double*>(p); p += align256((size_t)b * b * 8);
+  w.info = reinterpret_cast<double*>(p); p += 256;
+  w.info32 = reinterpret_cast<float*>(p); p += 256;
   return w;
 }
 
@@ -168,7 +218,7 @@ size_t carve_bytes(int64_t d, int b, int r, int ks) {
   return align256((size_t)d * b * 8) * 2 + align256((size_t)d * b * 4) + align256((size_t)ks * d * b * 8) +
          align256((size_t)NPART * b * b * 8) + align256((size_t)b * b * 8) * 3 + align256((size_t)b * (b + 1) * 8) * 2 +
          align256((size_t)b * 8) +
-         align256((size_t)b * 4) + align256((size_t)d * r * 8);
+         align256((size_t)b * 4) + align256((size_t)d * r * 8) + align256((size_t)b * b * 8) + 512;
 }
 
 __global__ void omega_kernel(double* q, float* q32, int64_t d, int b, uint64_t seed) {
@@ -513,6 +563,123 @@ __global__ void __launch_bounds__(256) chol_inv_kernel(const double* __restrict_
       linvt[k * b + jj] = jj > k ? A[k * ld + jj] : (jj == k ? xd[k] : 0.0);
 }
 
+// The same factorisation and inverse for b <= 16 BS (BS = 4, 8) with the matrix in
+// registers: 256 threads as a 16 x 16 grid, thread (ti, tk) holding the BS x BS block of
+// rows ti BS .., columns tk BS .. (order padded with identity).  Elimination is
+// right-looking in the unscaled (LDL^T) form: at step j the threads holding column j
+// publish it through LDS and every element of the trailing part takes
+// a_ik -= (a_ij / a_jj) a_kj, one barrier per step (the column buffer alternates between
+// two slots; the upper triangle is updated too and ignored).  L_ik = a_ik / sqrt(a_kk)
+// then goes to LDS, and L X = I is solved the same way, row k of X published at step k
+// and subtracted from the rows below it.  Pivots at or below 1e-300 are replaced by
+// 1e-300 (a rank-deficient block stays finite), as in chol_inv_kernel.
+template <int BS>
+__global__ void __launch_bounds__(256) chol_inv_blk_kernel(const double* __restrict__ m, double* __restrict__ linvt,
+                                                           int b) {
+  constexpr int BP = 16 * BS, LD = BP + 1;
+  __shared__ double A[BP * LD];
+  __shared__ double col[2][BP];
+  __shared__ double piv[BP];
+  __shared__ double xd[BP];   // 1 / L_kk
+  const int ti = threadIdx.x >> 4, tk = threadIdx.x & 15;
+  const int i0 = ti * BS, k0 = tk * BS;
+  double a[BS][BS];
+#pragma unroll
+  for (int ii = 0; ii < BS; ++ii)
+#pragma unroll
+    for (int kk = 0; kk < BS; ++kk) {
+      const int i = i0 + ii, k = k0 + kk;
+      a[ii][kk] = (i < b && k < b) ? m[(int64_t)i * b + k] : (i == k ? 1.0 : 0.0);
+    }
+  for (int j = 0; j < b; ++j) {
+    double* cj = col[j & 1];
+    if (tk == j / BS) {
+      const int jc = j % BS;
+#pragma unroll
+      for (int ii = 0; ii < BS; ++ii) {
+        double v = a[ii][0];   // column jc of the block, by selects (registers stay static)
+#pragma unroll
+        for (int q = 1; q < BS; ++q) v = jc == q ? a[ii][q] : v;
+        cj[i0 + ii] = v;
+      }
+    }
+    __syncthreads();
+    const double pv = cj[j] > 1e-300 ? cj[j] : 1e-300;
+    const double ipv = 1.0 / pv;
+    if (k0 + BS - 1 > j && i0 + BS - 1 > j) {   // block reaches past row and column j
+      double ck[BS];
+#pragma unroll
+      for (int kk = 0; kk < BS; ++kk) ck[kk] = cj[k0 + kk];
+#pragma unroll
+      for (int ii = 0; ii < BS; ++ii) {
+        const double f = cj[i0 + ii] * ipv;
+#pragma unroll
+        for (int kk = 0; kk < BS; ++kk)
+          if (k0 + kk > j) a[ii][kk] = fma(-f, ck[kk], a[ii][kk]);
+      }
+    }
+    if (threadIdx.x == 0) piv[j] = pv;
+  }
+  __syncthreads();
+  for (int k = threadIdx.x; k < BP; k += 256) {
+    const double l = k < b ? sqrt(piv[k]) : 1.0;
+    piv[k] = l;
+    xd[k] = 1.0 / l;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int ii = 0; ii < BS; ++ii)
+#pragma unroll
+    for (int kk = 0; kk < BS; ++kk) {
+      const int i = i0 + ii, k = k0 + kk;
+      if (k < i) A[i * LD + k] = i < b ? a[ii][kk] * xd[k] : 0.0;
+      else if (k == i) A[i * LD + k] = piv[k];
+    }
+  // X = L^{-1}: the block starts as I and row k is final at step k
+#pragma unroll
+  for (int ii = 0; ii < BS; ++ii)
+#pragma unroll
+    for (int kk = 0; kk < BS; ++kk) a[ii][kk] = (i0 + ii == k0 + kk) ? 1.0 : 0.0;
+  __syncthreads();
+  for (int k = 0; k < b; ++k) {
+    double* xr = col[k & 1];
+    if (ti == k / BS) {
+      const int r = k % BS;
+#pragma unroll
+      for (int ii = 0; ii < BS; ++ii)
+        if (ii == r) {
+#pragma unroll
+          for (int kk = 0; kk < BS; ++kk) {
+            a[ii][kk] *= xd[k];
+            xr[k0 + kk] = a[ii][kk];
+          }
+        }
+    }
+    __syncthreads();
+    if (i0 + BS - 1 > k && k0 <= k) {   // rows below k; X is zero right of column k
+      double xk[BS];
+#pragma unroll
+      for (int kk = 0; kk < BS; ++kk) xk[kk] = xr[k0 + kk];
+#pragma unroll
+      for (int ii = 0; ii < BS; ++ii) {
+        const double l = A[(i0 + ii) * LD + k];
+        if (i0 + ii > k) {
+#pragma unroll
+          for (int kk = 0; kk < BS; ++kk) a[ii][kk] = fma(-l, xk[kk], a[ii][kk]);
+        }
+      }
+    }
+  }
+  // linvt[c][i] = X[i][c]
+#pragma unroll
+  for (int ii = 0; ii < BS; ++ii)
+#pragma unroll
+    for (int kk = 0; kk < BS; ++kk) {
+      const int i = i0 + ii, c = k0 + kk;
+      if (i < b && c < b) linvt[(int64_t)c * b + i] = i >= c ? a[ii][kk] : 0.0;
+    }
+}
+
 // q[i][j] = sum over k <= j of y[i][k] linvt[k][j]  (Q = Y L^{-T}); also the fp32 copy.
 // Rows are processed 256 / b at a time (b <= 256: one thread per output), staged in LDS.
 __global__ void __launch_bounds__(256) apply_linv_kernel(const double* __restrict__ y, const double* __restrict__ linvt,
@@ -705,6 +872,112 @@ __global__ void __launch_bounds__(256) jacobi_kernel(const double* __restrict__ 
   }
 }
 
+// One-sided (Hestenes) Jacobi for b <= BP (BP = 64 or 128) on a symmetric positive
+// semidefinite H: the columns a_p of A (A = H at the start) are rotated in disjoint pairs,
+// round-robin as above, until every pair is orthogonal.  Then A = H V with V orthogonal
+// and A^T A diagonal, so V diagonalises H^2 and hence H: a_p = theta_p v_p, the
+// eigenvalue is the column norm and the eigenvector the normalised column (accurate for
+// the large eigenvalues the basis keeps; no V is accumulated).  A sits in LDS column by
+// column (stride BP + 1); each pair is worked on by G = 512 / BP lanes, RPL = BP / G rows
+// each, held in registers between the pair's dot products and its update; one barrier
+// per round.  A pair rotates when |a_p . a_q| > 1e-15 ||a_p|| ||a_q||; the sweeps stop
+// once the largest such ratio of a sweep is at most 1e-13.  Outputs as jacobi_kernel.
+template <int BP>
+__global__ void __launch_bounds__(256) jacobi1s_kernel(const double* __restrict__ hg, double* __restrict__ s_out,
+                                                       double* __restrict__ theta, int* __restrict__ order, int b,
+                                                       int sweeps) {
+  constexpr int LD = BP + 1, G = 512 / BP, RPL = BP / G;
+  __shared__ double A[BP * LD];
+  __shared__ double nrm[BP];
+  __shared__ double wmax[4];
+  const int t = threadIdx.x, grp = t / G, gl = t % G;
+  const int n = (b + 1) & ~1;
+  for (int e = t; e < BP * BP; e += 256) {
+    const int c = e / BP, i = e % BP;
+    A[c * LD + i] = (i < b && c < b) ? hg[c * b + i] : 0.0;   // column c of H (= row c)
+  }
+  __syncthreads();
+  for (int sw = 0; sw < sweeps; ++sw) {
+    double worst = 0.0;
+    for (int round = 0; round < n - 1; ++round) {
+      if (grp < n / 2) {
+        int p, q;
+        if (grp == 0) {
+          p = 0;
+          q = 1 + (round % (n - 1));
+        } else {
+          p = 1 + ((round + grp) % (n - 1));
+          q = 1 + ((round + n - 1 - grp) % (n - 1));
+        }
+        if (p > q) { const int tt = p; p = q; q = tt; }
+        if (q < b) {
+          double ap[RPL], aq[RPL];
+          double al = 0.0, be = 0.0, ga = 0.0;
+#pragma unroll
+          for (int k = 0; k < RPL; ++k) {
+            ap[k] = A[p * LD + k * G + gl];
+            aq[k] = A[q * LD + k * G + gl];
+            al = fma(ap[k], ap[k], al);
+            be = fma(aq[k], aq[k], be);
+            ga = fma(ap[k], aq[k], ga);
+          }
+#pragma unroll
+          for (int o = 1; o < G; o <<= 1) {
+            al += __shfl_xor(al, o, 64);
+            be += __shfl_xor(be, o, 64);
+            ga += __shfl_xor(ga, o, 64);
+          }
+          const double nn = sqrt(al * be);
+          if (fabs(ga) > 1e-15 * nn && fabs(ga) > 1e-300) {
+            worst = fmax(worst, fabs(ga) / nn);
+            const double zeta = (be - al) / (2.0 * ga);
+            const double tq = (zeta >= 0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+            const double cc = 1.0 / sqrt(1.0 + tq * tq), ss = tq * cc;
+#pragma unroll
+            for (int k = 0; k < RPL; ++k) {
+              A[p * LD + k * G + gl] = cc * ap[k] - ss * aq[k];
+              A[q * LD + k * G + gl] = ss * ap[k] + cc * aq[k];
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) worst = fmax(worst, __shfl_xor(worst, o, 64));
+    if ((t & 63) == 0) wmax[t >> 6] = worst;
+    __syncthreads();
+    const double w = fmax(fmax(wmax[0], wmax[1]), fmax(wmax[2], wmax[3]));
+    __syncthreads();
+    if (w <= 1e-13) break;
+  }
+  if (t < b) {
+    double s2 = 0.0;
+    for (int i = 0; i < b; ++i) s2 = fma(A[t * LD + i], A[t * LD + i], s2);
+    nrm[t] = sqrt(s2);
+  }
+  __syncthreads();
+  if (t < b) {   // rank by value, descending, lower index first on ties
+    const double v = nrm[t];
+    int rank = 0;
+    for (int j = 0; j < b; ++j) rank += (nrm[j] > v || (nrm[j] == v && j < t)) ? 1 : 0;
+    order[rank] = t;
+    theta[rank] = v;
+  }
+  for (int e = t; e < b * b; e += 256) {
+    const int k = e / b, c = e % b;
+    s_out[e] = A[c * LD + k] / fmax(nrm[c], 1e-300);
+  }
+}
+
+// Symmetric eigenproblem of the b x b block: one-sided Jacobi up to b = 128, else the
+// two-sided kernel with its matrices in global memory.
+void eig_small(const double* h, EigWs& w, int b, hipStream_t s) {
+  if (b <= 64) jacobi1s_kernel<64><<<1, 256, 0, s>>>(h, w.s, w.theta, w.order, b, 40);
+  else if (b <= 128) jacobi1s_kernel<128><<<1, 256, 0, s>>>(h, w.s, w.theta, w.order, b, 40);
+  else jacobi_kernel<false, 12><<<1, 256, 0, s>>>(h, w.chol, w.jac, w.s, w.theta, w.order, b, 40);
+}
+
 // u[d][r] = Q[d][b] S[:, order[:r]]
 __global__ void ritz_vectors_kernel(const double* __restrict__ q, const double* __restrict__ s, const int* __restrict__ order,
                                     double* __restrict__ u, int64_t d, int b, int r) {
@@ -758,9 +1031,11 @@ __global__ void __launch_bounds__(256) finish_basis_kernel(const double* __restr
   if (threadIdx.x == 0 && eigvals) eigvals[c] = (float)theta[c];
 }
 
-// resid = max_c ||G u_c - theta_c u_c|| / theta_0, with y = G u already formed.
+// resid = max_c ||G u_c - theta_c u_c|| / theta_0, with y = G u already formed; written
+// to info[1] (fp64) and info32[1] (fp32).
 __global__ void __launch_bounds__(256) resid_kernel(const double* __restrict__ y, const double* __restrict__ u,
-                                                    const double* __restrict__ theta, int64_t d, int r, float* resid) {
+                                                    const double* __restrict__ theta, int64_t d, int r, double* info,
+                                                    float* info32) {
   __shared__ double sh[256];
   double worst = 0.0;
   for (int c = 0; c < r; ++c) {
@@ -778,7 +1053,96 @@ __global__ void __launch_bounds__(256) resid_kernel(const double* __restrict__ y
     if (threadIdx.x == 0) worst = fmax(worst, sqrt(sh[0]));
     __syncthreads();
   }
-  if (threadIdx.x == 0) *resid = (float)(worst / fmax(fabs(theta[0]), 1e-300));
+  if (threadIdx.x == 0) {
+    const double v = worst / fmax(fabs(theta[0]), 1e-300);
+    info[1] = v;
+    info32[1] = (float)v;
+  }
+}
+
+// h <- (h + h^T) / 2 in place (b x b).  The check's projected block comes from the fp32
+// products and is symmetric only to their rounding; the Jacobi solver needs it exact.
+__global__ void sym_kernel(double* h, int b) {
+  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < b * b; e += gridDim.x * blockDim.x) {
+    const int i = e / b, j = e % b;
+    if (i < j) {
+      const double v = 0.5 * (h[i * b + j] + h[j * b + i]);
+      h[i * b + j] = v;
+      h[j * b + i] = v;
+    }
+  }
+}
+
+// Convergence estimate of the current block without another product: with Q orthonormal,
+// Y = G Q (the iteration's fp32 product), H = sym(Q^T Y) and M = Y^T Y, the Ritz pair
+// (theta_c, Q s_c) of a unit eigenvector s_c of H has residual
+//   ||Y s_c - theta_c Q s_c||^2 = s_c^T M s_c - theta_c^2,  theta_c = s_c^T H s_c.
+// Workgroup c (one of the top r) forms both quadratic forms (thread k: (M s)_k and
+// (H s)_k, coalesced over k since M and H are symmetric) into part[c], part[r + c].
+__global__ void __launch_bounds__(256) est_cols_kernel(const double* __restrict__ m, const double* __restrict__ h,
+                                                       const double* __restrict__ sv, const int* __restrict__ order,
+                                                       int b, int r, double* __restrict__ part) {
+  __shared__ double sc[512];
+  __shared__ double rm[256], rh[256];
+  const int c = blockIdx.x, t = threadIdx.x, col = order[c];
+  for (int k = t; k < b; k += 256) sc[k] = sv[k * b + col];
+  __syncthreads();
+  double qm = 0.0, qh = 0.0;
+  for (int k = t; k < b; k += 256) {
+    double um = 0.0, uh = 0.0;
+    for (int i = 0; i < b; ++i) {
+      um = fma(m[i * b + k], sc[i], um);
+      uh = fma(h[i * b + k], sc[i], uh);
+    }
+    qm = fma(sc[k], um, qm);
+    qh = fma(sc[k], uh, qh);
+  }
+  rm[t] = qm;
+  rh[t] = qh;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o) {
+      rm[t] += rm[t + o];
+      rh[t] += rh[t + o];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    part[c] = rm[0];
+    part[r + c] = rh[0];
+  }
+}
+
+// max_c sqrt(max(s_c^T M s_c - theta_c^2, 0)) / theta_0 into info[0] and info32[0].
+__global__ void est_final_kernel(const double* __restrict__ part, int r, double* info, float* info32) {
+  if (threadIdx.x != 0) return;
+  double worst = 0.0;
+  for (int c = 0; c < r; ++c) {
+    const double th = part[r + c];
+    worst = fmax(worst, sqrt(fmax(part[c] - th * th, 0.0)));
+  }
+  const double v = worst / fmax(fabs(part[r]), 1e-300);
+  info[0] = v;
+  info32[0] = (float)v;
+}
+
+// The caller's convergence report: residual (info[1]), gap theta_{r-1} / theta_r of the
+// final Ritz values (0-based: last kept over first discarded), iterations, and whether
+// the residual meets tol (always 1 when tol == 0).
+__global__ void report_kernel(zoact_eig_report* rep, const double* info, const double* theta, int r, int iters,
+                              float tol) {
+  const float res = (float)info[1];
+  rep->resid = res;
+  rep->gap = (float)(theta[r - 1] / fmax(fabs(theta[r]), 1e-300));
+  rep->iters = iters;
+  rep->converged = (tol <= 0.f || res <= tol) ? 1 : 0;
+}
+
+// (L^{-1})^T of the Cholesky factor of w.m into w.linvt.
+void chol_inv(EigWs& w, int b, hipStream_t s) {
+  if (b <= 64) chol_inv_blk_kernel<4><<<1, 256, 0, s>>>(w.m, w.linvt, b);
+  else if (b <= 128) chol_inv_blk_kernel<8><<<1, 256, 0, s>>>(w.m, w.linvt, b);
+  else chol_inv_kernel<false, 1><<<1, 256, 0, s>>>(w.m, w.chol, w.linvt, b);
 }
 
 // Q = orth(Y) by Cholesky-QR (applied `passes` times).  Reads y, leaves the
@@ -791,9 +1155,7 @@ hipError_t orth(EigWs& w, int64_t d, int b, int passes, hipStream_t s) {
   double* dst = w.q;
   for (int pass = 0; pass < passes; ++pass) {
     cross(src, src, d, b, w.mp, w.m, s);
-    if (b <= 64) chol_inv_kernel<true, 4><<<1, 256, 0, s>>>(w.m, w.chol, w.linvt, b);
-    else if (b <= 128) chol_inv_kernel<true, 2><<<1, 256, 0, s>>>(w.m, w.chol, w.linvt, b);
-    else chol_inv_kernel<false, 1><<<1, 256, 0, s>>>(w.m, w.chol, w.linvt, b);
+    chol_inv(w, b, s);
     apply_linv_kernel<<<gapp, 256, 0, s>>>(src, w.linvt, d, b, dst, pass == passes - 1 ? w.q32 : nullptr);
     double* t = src;
     src = dst;
@@ -828,43 +1190,28 @@ size_t basis_ws_bytes(int64_t d, int32_t r, int32_t p) {
   return carve_bytes(d, r + p, r, ks);
 }
 
-hipError_t launch_gram(const void* x, int32_t dtype, int64_t n_tok, int64_t d, float* g, int accumulate, hipStream_t s) {
+hipError_t launch_gram(const void* x, int32_t dtype, int64_t n_tok, int64_t d, int64_t ld, float* g, int accumulate,
+                       hipStream_t s) {
   if (dtype == ZOACT_BF16) {
     const int nt = (int)((d + GT - 1) / GT);
-    gram_bf16_kernel<<<dim3((unsigned)(nt * (nt + 1) / 2)), 256, 0, s>>>(static_cast<const uint16_t*>(x), n_tok, d, g,
-                                                                          accumulate, nt);
+    gram_bf16_kernel<<<dim3((unsigned)(nt * (nt + 1) / 2)), 256, 0, s>>>(static_cast<const uint16_t*>(x), n_tok, d, ld,
+                                                                          g, accumulate, nt);
   } else {
     int64_t gb = (d * d + 255) / 256;
     if (gb > 65535) gb = 65535;
-    gram_f32_kernel<<<dim3((unsigned)gb), 256, 0, s>>>(static_cast<const float*>(x), n_tok, d, g, accumulate);
+    gram_f32_kernel<<<dim3((unsigned)gb), 256, 0, s>>>(static_cast<const float*>(x), n_tok, d, ld, g, accumulate);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t p, int32_t iters, uint64_t seed,
-                                  void* ut, int32_t ut_dtype, float* ut_master, float* eigvals, float* resid, void* ws,
-                                  hipStream_t s) {
-  const int b = r + p;
-  int ks;
-  int64_t kchunk;
-  ksplit_for(d, ks, kchunk);
-  EigWs w = carve(ws, d, b, r, ks);
-  const int64_t n = d * b;
-  const unsigned g1 = (unsigned)((n + 255) / 256 > 4096 ? 4096 : (n + 255) / 256);
-  omega_kernel<<<g1, 256, 0, s>>>(w.q, w.q32, d, b, seed);
-  const dim3 gq_grid((unsigned)((d + GQ_ROWS - 1) / GQ_ROWS), (unsigned)ks, (unsigned)((b + 63) / 64));
-  for (int it = 0; it <= iters; ++it) {
-    gq32_kernel<<<gq_grid, 256, 0, s>>>(g, w.q32, reinterpret_cast<float*>(w.part), d, b, kchunk);
-    sum_parts_kernel<float><<<g1, 256, 0, s>>>(reinterpret_cast<const float*>(w.part), ks, n, w.y);
-    hipError_t e = orth(w, d, b, it == iters ? 2 : 1, s);
-    if (e != hipSuccess) return e;
-  }
-  // Rayleigh-Ritz with fp64 accumulation: H = Q^T (G Q)
-  hipError_t e = gx64(g, w.q, d, b, w, w.y, s);
+// Rayleigh-Ritz of the orthonormal block w.q with fp64 accumulation, the basis outputs,
+// and (when `resid` is set) the residual of the result into info[1] / info32[1].
+static hipError_t finish(const float* g, int64_t d, int b, int r, EigWs& w, void* ut, int32_t ut_dtype,
+                         float* ut_master, float* eigvals, bool resid, hipStream_t s) {
+  hipError_t e = gx64(g, w.q, d, b, w, w.y, s);   // H = Q^T (G Q)
   if (e != hipSuccess) return e;
   cross(w.q, w.y, d, b, w.mp, w.m, s);
-  if (b <= 96) jacobi_kernel<true, 12><<<1, 256, 0, s>>>(w.m, w.chol, w.jac, w.s, w.theta, w.order, b, 40);
-  else jacobi_kernel<false, 12><<<1, 256, 0, s>>>(w.m, w.chol, w.jac, w.s, w.theta, w.order, b, 40);
+  eig_small(w.m, w, b, s);
   int64_t gb = (d * r + 255) / 256;
   if (gb > 65535) gb = 65535;
   ritz_vectors_kernel<<<dim3((unsigned)gb), 256, 0, s>>>(w.q, w.s, w.order, w.u, d, b, r);
@@ -873,8 +1220,100 @@ hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t 
   if (resid) {
     e = gx64(g, w.u, d, r, w, w.y, s);   // y = G u
     if (e != hipSuccess) return e;
-    resid_kernel<<<1, 256, 0, s>>>(w.y, w.u, w.theta, d, r, resid);
+    resid_kernel<<<1, 256, 0, s>>>(w.y, w.u, w.theta, d, r, w.info, w.info32);
   }
+  return hipGetLastError();
+}
+
+static hipError_t read_info(const EigWs& w, int k, float& v, hipStream_t s) {
+  hipError_t e = hipMemcpyAsync(&v, w.info32 + k, sizeof(float), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  return e;
+}
+
+// Subspace iteration: product k (k = 0 .. max_iter) forms Y = G Q_{k-1} (Q_{-1} = Omega)
+// and Q_k = orth(Y).  Fixed mode runs all max_iter + 1 products, the last with a second
+// Cholesky-QR pass, with no host synchronisation unless tol > 0 (then the final residual
+// is read back).  Adaptive mode estimates the residual of the top-r Ritz pairs at
+// checks (est_cols_kernel, from the products already formed), reads it back, and when
+// it is at or below tol finishes with Rayleigh-Ritz and the exact residual; if that is
+// still above tol and products remain, the iteration continues from Q.
+hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t p, const zoact_eig_opts& o, void* ut,
+                                  int32_t ut_dtype, float* ut_master, float* eigvals, zoact_eig_report* report, void* ws,
+                                  hipStream_t s, bool& met) {
+  const int b = r + p;
+  int ks;
+  int64_t kchunk;
+  ksplit_for(d, ks, kchunk);
+  EigWs w = carve(ws, d, b, r, ks);
+  const int64_t n = d * b;
+  const unsigned g1 = (unsigned)((n + 255) / 256 > 4096 ? 4096 : (n + 255) / 256);
+  const dim3 gq_grid((unsigned)((d + GQ_ROWS - 1) / GQ_ROWS), (unsigned)ks, (unsigned)((b + 63) / 64));
+  const bool adaptive = o.adaptive != 0;
+  const bool want_resid = report != nullptr || o.tol > 0.f;
+  met = true;
+  omega_kernel<<<g1, 256, 0, s>>>(w.q, w.q32, d, b, o.seed);
+  int k = 0;
+  hipError_t e;
+  // Checks: the first two check_every iterations apart; from then on at the iteration
+  // where the estimates' geometric rate predicts tol, at least check_every later, and
+  // none once the prediction lies past max_iter or the estimate stops falling (the run
+  // then ends like the fixed mode, with the exact residual deciding).
+  int next_check = adaptive ? o.check_every : INT32_MAX;
+  int prev_k = -1;
+  float prev_est = 0.f;
+  for (;;) {
+    bool final_product = k == o.max_iter;
+    const bool check = !final_product && k == next_check;
+    gq32_kernel<<<gq_grid, 256, 0, s>>>(g, w.q32, reinterpret_cast<float*>(w.part), d, b, kchunk);
+    sum_parts_kernel<float><<<g1, 256, 0, s>>>(reinterpret_cast<const float*>(w.part), ks, n, w.y);
+    if (check) {
+      cross(w.q, w.y, d, b, w.mp, w.h, s);   // H = Q^T Y before Q is replaced
+      sym_kernel<<<(unsigned)((b * b + 255) / 256), 256, 0, s>>>(w.h, b);
+    }
+    e = orth(w, d, b, final_product ? 2 : 1, s);   // leaves M = Y^T Y of the first pass in w.m
+    if (e != hipSuccess) return e;
+    if (check) {
+      eig_small(w.h, w, b, s);
+      est_cols_kernel<<<(unsigned)r, 256, 0, s>>>(w.m, w.h, w.s, w.order, b, r, w.mp);
+      est_final_kernel<<<1, 64, 0, s>>>(w.mp, r, w.info, w.info32);
+      float est = 0.f;
+      if ((e = read_info(w, 0, est, s)) != hipSuccess) return e;
+      next_check = k + o.check_every;
+      if (prev_k >= 0 && est > o.tol) {
+        if (!(est < prev_est) || !(est > 0.f)) {
+          next_check = INT32_MAX;
+        } else {
+          const double rate = std::log((double)est / prev_est) / (k - prev_k);   // < 0
+          const double need = std::log((double)o.tol / est) / rate;
+          next_check = k + need > (double)o.max_iter ? INT32_MAX : k + std::max(o.check_every, (int)std::ceil(need));
+        }
+      }
+      prev_k = k;
+      prev_est = est;
+      if (est <= o.tol) {
+        // second Cholesky-QR pass of Q, as the last product of the fixed mode gets
+        std::swap(w.y, w.q);
+        if ((e = orth(w, d, b, 1, s)) != hipSuccess) return e;
+        final_product = true;
+      }
+    }
+    if (final_product) {
+      if ((e = finish(g, d, b, r, w, ut, ut_dtype, ut_master, eigvals, want_resid, s)) != hipSuccess) return e;
+      if (o.tol > 0.f) {
+        float res = 0.f;
+        if ((e = read_info(w, 1, res, s)) != hipSuccess) return e;
+        met = res <= o.tol;
+        if (!met && adaptive && k < o.max_iter) {
+          ++k;
+          continue;   // Q (and its fp32 copy) are intact: keep iterating
+        }
+      }
+      break;
+    }
+    ++k;
+  }
+  if (report) report_kernel<<<1, 1, 0, s>>>(report, w.info, w.theta, r, k, o.tol);
   return hipGetLastError();
 }
 

@@ -417,12 +417,16 @@ class Decoder:
         return {(b.layer, b.site): d_in[b.site] for b in self.blocks}
 
     # ---------------------------------------------------------------- Algorithm 1
-    def basis_init(self, calib_tokens: torch.Tensor, opts: Z.EigOpts | None = None, keep_eigvals=False):
+    def basis_init(self, calib_tokens: torch.Tensor, opts: Z.EigOpts | None = None, keep_eigvals=False,
+                   report=False):
         """Unperturbed calibration forward, then the top-r basis of each adapted site's inputs.
 
         calib_tokens int32 [n_seq][seq] with n_seq even: the two halves of the stacked
         forward carry the first and second n_seq/2 sequences, so every site sees all
-        n_seq * seq calibration tokens once.
+        n_seq * seq calibration tokens once.  With `report` each site's convergence report
+        (residual, gap theta_r / theta_{r+1}, iterations, converged) lands in
+        self.basis_report after the call; a site whose residual stays above opts.tol keeps
+        its best-effort basis and is reported with converged = False.
         """
         n_seq, seq = calib_tokens.shape
         if n_seq % 2:
@@ -431,19 +435,25 @@ class Decoder:
         ws = torch.empty(max(Z.basis_init_workspace_bytes(dd, self.r, opts) for dd in set(dims.values())),
                          dtype=torch.uint8, device=self.dev)
         self.eigvals = {}
+        reps = {}
 
         def hook(l, site, x):
             if (l, site) not in dims:
                 return
             ut = torch.empty(self.r, dims[(l, site)], dtype=self.act, device=self.dev)
             ev = torch.empty(self.r, dtype=torch.float32, device=self.dev) if keep_eigvals else None
-            Z.basis_init(x, self.r, ut, ws, opts, eigvals=ev)
+            rep = Z.eig_report_tensor(self.dev) if report else None
+            Z.basis_init(x, self.r, ut, ws, opts, eigvals=ev, report=rep)
             self.ut[(l, site)] = ut
             if keep_eigvals:
                 self.eigvals[(l, site)] = ev
+            if report:
+                reps[(l, site)] = rep
 
         tok = calib_tokens.reshape(2, n_seq // 2, seq).contiguous()
         self.forward(tok, Z.Pert(0, 0, 0, 0.0), calibrate=hook, distinct_halves=True)
+        if report:
+            self.basis_report = {k: Z.read_eig_report(v) for k, v in reps.items()}
         return self.ut
 
     def set_basis(self, ut: dict):

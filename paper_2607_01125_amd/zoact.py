@@ -64,7 +64,19 @@ class AdamDesc(ctypes.Structure):
 
 
 class EigOpts(ctypes.Structure):
-    _fields_ = [("oversample", ctypes.c_int32), ("iters", ctypes.c_int32), ("seed", ctypes.c_uint64)]
+    _fields_ = [("oversample", ctypes.c_int32), ("max_iter", ctypes.c_int32), ("seed", ctypes.c_uint64),
+                ("tol", ctypes.c_float), ("adaptive", ctypes.c_int32), ("check_every", ctypes.c_int32)]
+
+
+def eig_report_tensor(device) -> torch.Tensor:
+    """Device buffer for one zoact_eig_report (resid f32, gap f32, iters i32, converged i32)."""
+    return torch.zeros(4, dtype=torch.int32, device=device)
+
+
+def read_eig_report(t: torch.Tensor) -> dict:
+    h = t.cpu()
+    f = h.view(torch.float32)
+    return {"resid": float(f[0]), "gap": float(f[1]), "iters": int(h[2]), "converged": bool(h[3])}
 
 
 _P = ctypes.c_void_p
@@ -105,9 +117,10 @@ SIGNATURES = {
     "zoact_step_sgd": ([ctypes.POINTER(ArenaDesc), _P, ctypes.POINTER(Pert), _F, _P, _P], _I32),
     "zoact_basis_workspace_bytes": ([_I64, _I32, ctypes.POINTER(EigOpts)], _SZ),
     "zoact_basis_init_workspace_bytes": ([_I64, _I32, ctypes.POINTER(EigOpts)], _SZ),
-    "zoact_gram": ([_P, _I32, _I64, _I64, _P, _I32, _P], _I32),
+    "zoact_gram": ([_P, _I32, _I64, _I64, _I64, _P, _I32, _P], _I32),
     "zoact_basis_from_gram": ([_P, _I64, _I32, ctypes.POINTER(EigOpts), _P, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
-    "zoact_basis_init": ([_P, _I32, _I64, _I64, _I32, ctypes.POINTER(EigOpts), _P, _I32, _P, _P, _P, _P, _SZ, _P],
+    "zoact_basis_init": ([_P, _I32, _I64, _I64, _I64, _I32, ctypes.POINTER(EigOpts), _P, _I32, _P, _P, _P, _P, _SZ,
+                          _P],
                          _I32),
     "zoact_embed": ([_P, _I64, _I32, _I64, _P, _P, _I64, _I32, _I64, _I64, _I32, _P, _P], _I32),
     "zoact_rmsnorm": ([_P, _P, _I64, _I64, _F, _I32, _P, _P], _I32),
@@ -377,25 +390,43 @@ def basis_init_workspace_bytes(d: int, r: int, opts: EigOpts | None = None) -> i
     return int(lib().zoact_basis_init_workspace_bytes(d, r, ctypes.byref(opts) if opts is not None else None))
 
 
+def _rows(x: torch.Tensor):
+    """(n_tok, d, row stride) of a 2-D activation matrix with unit column stride."""
+    if x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be 2-D with contiguous rows")
+    return x.shape[0], x.shape[1], x.stride(0)
+
+
+def _check_basis(st: int) -> bool:
+    """True on success, False when the residual bound was not met (outputs written)."""
+    if st == E_NOCONVERGE:
+        return False
+    _check(st)
+    return True
+
+
 def gram(x: torch.Tensor, g: torch.Tensor, accumulate: bool = False, stream=None):
-    n_tok, d = x.shape
-    _check(lib().zoact_gram(_ptr(x), dtype_code(x), n_tok, d, _ptr(g), int(accumulate), _stream(stream)))
+    n_tok, d, ld = _rows(x)
+    _check(lib().zoact_gram(_ptr(x), dtype_code(x), n_tok, d, ld, _ptr(g), int(accumulate), _stream(stream)))
 
 
 def basis_from_gram(g: torch.Tensor, r: int, ut: torch.Tensor, ws: torch.Tensor, opts: EigOpts | None = None,
-                    ut_master=None, eigvals=None, resid=None, stream=None):
+                    ut_master=None, eigvals=None, report=None, stream=None) -> bool:
+    """Returns False when opts.tol was not met (ZOACT_E_NOCONVERGE; the basis is still written)."""
     d = g.shape[0]
-    _check(lib().zoact_basis_from_gram(_ptr(g), d, r, ctypes.byref(opts) if opts is not None else None, _ptr(ut),
-                                       dtype_code(ut), _ptr(ut_master), _ptr(eigvals), _ptr(resid), _ptr(ws),
-                                       ws.numel() * ws.element_size(), _stream(stream)))
+    return _check_basis(lib().zoact_basis_from_gram(
+        _ptr(g), d, r, ctypes.byref(opts) if opts is not None else None, _ptr(ut), dtype_code(ut), _ptr(ut_master),
+        _ptr(eigvals), _ptr(report), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def basis_init(x: torch.Tensor, r: int, ut: torch.Tensor, ws: torch.Tensor, opts: EigOpts | None = None,
-               ut_master=None, eigvals=None, resid=None, stream=None):
-    n_tok, d = x.shape
-    _check(lib().zoact_basis_init(_ptr(x), dtype_code(x), n_tok, d, r, ctypes.byref(opts) if opts is not None
-                                  else None, _ptr(ut), dtype_code(ut), _ptr(ut_master), _ptr(eigvals), _ptr(resid),
-                                  _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+               ut_master=None, eigvals=None, report=None, stream=None) -> bool:
+    """Returns False when opts.tol was not met (ZOACT_E_NOCONVERGE; the basis is still written)."""
+    n_tok, d, ld = _rows(x)
+    return _check_basis(lib().zoact_basis_init(
+        _ptr(x), dtype_code(x), n_tok, d, ld, r, ctypes.byref(opts) if opts is not None else None, _ptr(ut),
+        dtype_code(ut), _ptr(ut_master), _ptr(eigvals), _ptr(report), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
 
 
 def adam_desc(lr: float, t: int, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,

@@ -76,10 +76,17 @@ def test_validation_rejects_before_launch():
     assert L.zoact_mse_pm(ctypes.c_void_p(16), Z.BF16, ctypes.c_void_p(16), 4, 4, ctypes.c_void_p(16),
                           ctypes.c_void_p(16), 8, None) == Z.E_WORKSPACE
     # basis: fewer tokens than r, oversampled block larger than d
-    assert L.zoact_basis_init(ctypes.c_void_p(16), Z.BF16, 4, 64, 8, None, ctypes.c_void_p(16), Z.BF16, None, None,
-                              None, ctypes.c_void_p(16), 1 << 30, None) == Z.E_INVALID
+    assert L.zoact_basis_init(ctypes.c_void_p(16), Z.BF16, 4, 64, 64, 8, None, ctypes.c_void_p(16), Z.BF16, None,
+                              None, None, ctypes.c_void_p(16), 1 << 30, None) == Z.E_INVALID
     assert L.zoact_basis_from_gram(ctypes.c_void_p(16), 64, 40, None, ctypes.c_void_p(16), Z.F32, None, None, None,
                                    ctypes.c_void_p(16), 1 << 30, None) == Z.E_INVALID
+    # basis: adaptive mode without a tolerance, negative tolerance
+    for opts in (Z.EigOpts(0, 0, 1, 0.0, 1, 0), Z.EigOpts(0, 0, 1, -1.0, 0, 0)):
+        assert L.zoact_basis_from_gram(ctypes.c_void_p(16), 64, 8, ctypes.byref(opts), ctypes.c_void_p(16), Z.F32,
+                                       None, None, None, ctypes.c_void_p(16), 1 << 30, None) == Z.E_INVALID
+    # Gram: row stride below d, bf16 row stride not a multiple of 8
+    assert L.zoact_gram(ctypes.c_void_p(16), Z.F32, 8, 64, 63, ctypes.c_void_p(16), 0, None) == Z.E_INVALID
+    assert L.zoact_gram(ctypes.c_void_p(16), Z.BF16, 8, 64, 68, ctypes.c_void_p(16), 0, None) == Z.E_INVALID
 
 
 def test_basis_workspace_grows_with_block():

@@ -419,17 +419,98 @@ def test_basis_init_matches_oracle(d, r, bf16):
     ut = torch.empty(r, d, dtype=torch.bfloat16 if bf16 else torch.float32, device=dev())
     master = torch.empty(r, d, dtype=torch.float32, device=dev())
     ev = torch.empty(r, dtype=torch.float32, device=dev())
-    res = torch.empty(1, dtype=torch.float32, device=dev())
+    rep = Z.eig_report_tensor(dev())
     ws = torch.empty(Z.basis_init_workspace_bytes(d, r), dtype=torch.uint8, device=dev())
-    Z.basis_init(t_bf16(x) if bf16 else t_f32(x), r, ut, ws, ut_master=master, eigvals=ev, resid=res)
+    assert Z.basis_init(t_bf16(x) if bf16 else t_f32(x), r, ut, ws, ut_master=master, eigvals=ev, report=rep)
     um = host(master).T
     assert np.max(np.abs(um.T @ um - np.eye(r))) <= 1e-5
     assert obasis.overlap(um, u_ref) >= 1 - 1e-6
     assert_rel_close(host(ev), lam_ref, 1e-4, "eigenvalues")
     assert np.max(np.abs(um - u_ref)) <= 1e-4          # same canonical sign
-    assert float(host(res)[0]) <= 1e-5
+    info = Z.read_eig_report(rep)
+    print(f"[parity] basis d={d} r={r}: {info}", flush=True)
+    assert info["resid"] <= 1e-5 and info["iters"] == 64 and info["converged"]
+    _check_gap(info["gap"], _spectrum(x), r)
     if bf16:
         np.testing.assert_array_equal(host(ut), rne_bf16(host(master)))
+
+
+def _spectrum(x):
+    """Eigenvalues of X^T X, descending (fp64)."""
+    return np.linalg.eigvalsh(x.astype(np.float64).T @ x.astype(np.float64))[::-1]
+
+
+def _check_gap(gap, lam, r):
+    """The reported gap is theta_r / theta_{r+1} of the block's Ritz values.  theta_r has
+    converged with the basis; theta_{r+1} is a lower bound of lambda_{r+1} (Ritz values
+    interlace) that converges only at the rate lambda_{r+p+1} / lambda_{r+1}, so the
+    report bounds the true gap from above, and closely on these spectra."""
+    true_gap = lam[r - 1] / lam[r]
+    assert true_gap * (1 - 1e-4) <= gap <= 1.1 * true_gap, (gap, true_gap)
+
+
+@pytest.mark.parametrize("d,r", [(512, 32), (640, 64), (384, 100)])
+def test_basis_adaptive_stops_early(d, r):
+    """Adaptive mode on a spectrum with a gap stops at a check well before max_iter, meets
+    the tolerance, and reports a gap consistent with the spectrum's lambda_r / lambda_{r+1}."""
+    announce("basis adaptive", d, r)
+    x = _gapped_x(2 * d, d, r, seed=3 * d + r)
+    u_ref, _ = obasis.basis_init(x, r)
+    lam = _spectrum(x)
+    ut = torch.empty(r, d, dtype=torch.float32, device=dev())
+    rep = Z.eig_report_tensor(dev())
+    opts = Z.EigOpts(0, 64, 7, 1e-4, 1, 4)
+    ws = torch.empty(Z.basis_init_workspace_bytes(d, r, opts), dtype=torch.uint8, device=dev())
+    assert Z.basis_init(t_f32(x), r, ut, ws, opts, report=rep)
+    info = Z.read_eig_report(rep)
+    print(f"[parity] adaptive d={d} r={r}: {info}", flush=True)
+    assert info["converged"] and info["resid"] <= 1e-4
+    assert info["iters"] % 4 == 0 and 4 <= info["iters"] < 64
+    assert obasis.overlap(host(ut).T, u_ref) >= 1 - 1e-6
+    _check_gap(info["gap"], lam, r)
+
+
+def test_basis_noconverge_keeps_best_effort():
+    """One iteration on a flat spectrum cannot meet tol = 1e-7: ZOACT_E_NOCONVERGE, the
+    report says so, and the basis written is still orthonormal; a second call on the
+    same workspace with a reachable bound converges."""
+    announce("basis noconverge")
+    d, r = 256, 16
+    x = synth.normal((4 * d, d), 1.0, 4, 4)
+    ut = torch.empty(r, d, dtype=torch.float32, device=dev())
+    rep = Z.eig_report_tensor(dev())
+    opts = Z.EigOpts(0, 1, 3, 1e-7, 0, 0)
+    ws = torch.empty(Z.basis_init_workspace_bytes(d, r, opts), dtype=torch.uint8, device=dev())
+    assert not Z.basis_init(t_f32(x), r, ut, ws, opts, report=rep)
+    info = Z.read_eig_report(rep)
+    print(f"[parity] noconverge: {info}", flush=True)
+    assert not info["converged"] and info["resid"] > 1e-7 and info["iters"] == 1
+    u = host(ut).T
+    assert np.isfinite(u).all() and np.max(np.abs(u.T @ u - np.eye(r))) <= 1e-5
+    # the same flat spectrum, iterated to a bound the fp32 Gram can support
+    opts2 = Z.EigOpts(0, 512, 3, 1e-3, 1, 8)
+    ok = Z.basis_init(t_f32(x), r, ut, ws, opts2, report=rep)
+    info2 = Z.read_eig_report(rep)
+    print(f"[parity] flat spectrum adaptive: {info2}", flush=True)
+    assert ok and info2["converged"] and info2["resid"] <= 1e-3 and info2["iters"] <= 512
+
+
+def test_basis_init_row_stride():
+    """x given as a column slice of a wider matrix (row stride > d) yields the same bits
+    as the contiguous copy."""
+    announce("basis row stride")
+    d, r = 256, 16
+    wide = synth.bf16_round(synth.normal((600, d + 64), 1.0, 5, 5))
+    x_wide = t_bf16(wide)
+    view = x_wide[:, 32:32 + d]
+    assert view.stride(0) == d + 64
+    outs = []
+    for xx in (view, view.contiguous()):
+        ut = torch.empty(r, d, dtype=torch.float32, device=dev())
+        ws = torch.empty(Z.basis_init_workspace_bytes(d, r), dtype=torch.uint8, device=dev())
+        Z.basis_init(xx, r, ut, ws)
+        outs.append(host(ut))
+    np.testing.assert_array_equal(outs[0], outs[1])
 
 
 # ------------------------------------------------------------------ full single-layer workload, sampled
