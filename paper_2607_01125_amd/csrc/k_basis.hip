@@ -4,17 +4,19 @@
 //
 //  * Gram: for bf16 X a v_mfma_f32_16x16x32_bf16 kernel over 128 x 128 output
 //    tiles of the upper triangle (mirrored on store), contraction over tokens in
-//    steps of 32; the X tile is transposed through LDS so that each lane's
-//    fragment holds 8 consecutive tokens of one feature.  Every output tile is
-//    owned by one workgroup and summed in token order (deterministic).  fp32 X
-//    uses a plain SIMT kernel (small models).
+//    steps of 64; 8 x 8 blocks of X are transposed in registers so that each lane's
+//    fragment holds 8 consecutive tokens of one feature.  Every output tile is owned
+//    by one workgroup and summed in token order (deterministic).  fp32 X uses a plain
+//    SIMT kernel (small models).
 //  * Eigenvectors: randomised block subspace iteration (Halko, Martinsson, Tropp
-//    2011) with block b = r + p: Q = orth(G Omega), then `iters` times
-//    Q = orth(G Q); orth is Cholesky-QR applied twice; Rayleigh-Ritz H = Q^T G Q;
-//    the b x b eigenproblem is solved by a parallel cyclic Jacobi method in one
-//    workgroup (round-robin pairing, all disjoint rotations of a round at once);
-//    U = Q S[:, top r].  The iteration's products G Q run on fp32 MFMA; the
-//    orthonormalisation, the Rayleigh-Ritz product and all small matrices are fp64.
+//    2011) with block b = r + p: Q = orth(G Omega), then up to max_iter times
+//    Q = orth(G Q); orth is Cholesky-QR (twice on the last block); Rayleigh-Ritz
+//    H = Q^T G Q; the b x b eigenproblem is solved in one workgroup by a one-sided
+//    Jacobi method (b <= 128) or a two-sided one (larger b), all disjoint rotations of
+//    a round at once; U = Q S[:, top r].  The iteration's products G Q run on fp32
+//    MFMA; the orthonormalisation, the Rayleigh-Ritz product and all small matrices
+//    are fp64.  An adaptive mode stops once an estimate of the top-r residuals, formed
+//    from the iteration's own products, meets the caller's bound.
 //  * Sign: each column is flipped so its largest-magnitude entry is positive,
 //    lowest index on ties.
 #include "common.hpp"
@@ -477,30 +479,17 @@ void cross(const double* a, const double* bm, int64_t d, int b, double* mp, doub
   reduce_parts_kernel<<<(unsigned)(((int64_t)b * b + 63) / 64), 256, 0, s>>>(mp, np, (int64_t)b * b, m);
 }
 
-// Sum over the G consecutive lanes of a group (G = 1, 2 or 4), fixed order.
-template <int G>
-__device__ __forceinline__ double group_sum(double v) {
-  if (G >= 2) v += __shfl_xor(v, 1, 64);
-  if (G >= 4) v += __shfl_xor(v, 2, 64);
-  return v;
-}
-
 // M = L L^T (left-looking Cholesky), then X = L^{-1} by forward substitution, written
-// out transposed: linvt[k][j] = X[j][k].  One workgroup; G lanes share each row (or
-// column) and split its dot products.  The matrix sits in LDS with row stride b + 1
-// (conflict-free column access) when it fits (b <= 128), else in `scratch` with the
-// same layout.  L occupies the lower triangle; column c of X is kept transposed in row
-// c's upper part (A[c][i] = X[i][c], i > c) and its diagonal in `xd`.
-template <bool IN_LDS, int G>
-__global__ void __launch_bounds__(256) chol_inv_kernel(const double* __restrict__ m, double* __restrict__ scratch,
+// out transposed: linvt[k][j] = X[j][k].  For blocks past the register-blocked kernel
+// below (b > 128): one workgroup, one lane per row (or column), the matrix in `scratch`
+// with row stride b + 1.  L occupies the lower triangle; column c of X is kept transposed
+// in row c's upper part (A[c][i] = X[i][c], i > c) and its diagonal in `xd`.
+__global__ void __launch_bounds__(256) chol_inv_kernel(const double* __restrict__ m, double* __restrict__ A,
                                                        double* __restrict__ linvt, int b) {
-  __shared__ double lds[IN_LDS ? 128 * 129 : 1];
   __shared__ double xd[512];
   __shared__ double sq[512];   // running sum of squares of each row of L
-  constexpr int R = 256 / G;   // rows in flight
   const int ld = b + 1;
-  double* A = IN_LDS ? lds : scratch;
-  const int t = threadIdx.x, gl = t % G;
+  const int t = threadIdx.x;
   for (int i = t / 64; i < b; i += 4)
     for (int k = t % 64; k < b; k += 64) A[i * ld + k] = m[i * b + k];
   for (int i = t; i < b; i += 256) sq[i] = 0.0;
@@ -515,25 +504,22 @@ __global__ void __launch_bounds__(256) chol_inv_kernel(const double* __restrict_
   for (int j = 0; j < b - 1; ++j) {
     const double* lj = A + j * ld;
     const double inv = 1.0 / lj[j];
-    for (int i = j + 1 + t / G; i < b; i += R) {
+    for (int i = j + 1 + t; i < b; i += 256) {
       double* li = A + i * ld;
       double s0 = 0.0, s1 = 0.0;
-      int k = gl;
-      for (; k + G < j; k += 2 * G) {
+      int k = 0;
+      for (; k + 1 < j; k += 2) {
         s0 = fma(li[k], lj[k], s0);
-        s1 = fma(li[k + G], lj[k + G], s1);
+        s1 = fma(li[k + 1], lj[k + 1], s1);
       }
       if (k < j) s0 = fma(li[k], lj[k], s0);
-      const double dotv = group_sum<G>(s0 + s1);
-      if (gl == 0) {
-        const double v = (li[j] - dotv) * inv;
-        li[j] = v;
-        const double ss = sq[i] + v * v;
-        sq[i] = ss;
-        if (i == j + 1) {
-          const double dd = li[i] - ss;
-          li[i] = dd > 1e-300 ? sqrt(dd) : 1e-150;
-        }
+      const double v = (li[j] - (s0 + s1)) * inv;
+      li[j] = v;
+      const double ss = sq[i] + v * v;
+      sq[i] = ss;
+      if (i == j + 1) {
+        const double dd = li[i] - ss;
+        li[i] = dd > 1e-300 ? sqrt(dd) : 1e-150;
       }
     }
     __syncthreads();
@@ -542,19 +528,18 @@ __global__ void __launch_bounds__(256) chol_inv_kernel(const double* __restrict_
   // x_i = -(sum_{k=c}^{i-1} L_ik x_k) / L_ii, x_k (k > c) stored at A[c][k]
   for (int c = t; c < b; c += 256) xd[c] = 1.0 / A[c * ld + c];
   __syncthreads();
-  for (int c = t / G; c < b; c += R) {
+  for (int c = t; c < b; c += 256) {
     double* xr = A + c * ld;
     for (int i = c + 1; i < b; ++i) {
       const double* li = A + i * ld;
-      double s0 = gl == 0 ? li[c] * xd[c] : 0.0, s1 = 0.0;
-      int k = c + 1 + gl;
-      for (; k + G < i; k += 2 * G) {
+      double s0 = li[c] * xd[c], s1 = 0.0;
+      int k = c + 1;
+      for (; k + 1 < i; k += 2) {
         s0 = fma(li[k], xr[k], s0);
-        s1 = fma(li[k + G], xr[k + G], s1);
+        s1 = fma(li[k + 1], xr[k + 1], s1);
       }
       if (k < i) s0 = fma(li[k], xr[k], s0);
-      const double xi = -group_sum<G>(s0 + s1) * xd[i];
-      if (gl == 0) xr[i] = xi;
+      xr[i] = -(s0 + s1) * xd[i];
     }
   }
   __syncthreads();
@@ -563,9 +548,10 @@ __global__ void __launch_bounds__(256) chol_inv_kernel(const double* __restrict_
       linvt[k * b + jj] = jj > k ? A[k * ld + jj] : (jj == k ? xd[k] : 0.0);
 }
 
-// The same factorisation and inverse for b <= 16 BS (BS = 4, 8) with the matrix in
-// registers: 256 threads as a 16 x 16 grid, thread (ti, tk) holding the BS x BS block of
-// rows ti BS .., columns tk BS .. (order padded with identity).  Elimination is
+// The same factorisation and inverse for b <= 32 BS (BS = 2, 4) with the matrix in
+// registers: 1024 threads as a 32 x 32 grid, thread (ti, tk) holding the BS x BS block of
+// rows ti BS .., columns tk BS .. (order padded with identity; four waves per SIMD hide
+// each other's latency).  Elimination is
 // right-looking in the unscaled (LDL^T) form: at step j the threads holding column j
 // publish it through LDS and every element of the trailing part takes
 // a_ik -= (a_ij / a_jj) a_kj, one barrier per step (the column buffer alternates between
@@ -574,14 +560,14 @@ __global__ void __launch_bounds__(256) chol_inv_kernel(const double* __restrict_
 // and subtracted from the rows below it.  Pivots at or below 1e-300 are replaced by
 // 1e-300 (a rank-deficient block stays finite), as in chol_inv_kernel.
 template <int BS>
-__global__ void __launch_bounds__(256) chol_inv_blk_kernel(const double* __restrict__ m, double* __restrict__ linvt,
-                                                           int b) {
-  constexpr int BP = 16 * BS, LD = BP + 1;
+__global__ void __launch_bounds__(1024) chol_inv_blk_kernel(const double* __restrict__ m, double* __restrict__ linvt,
+                                                            int b) {
+  constexpr int TG = 32, NT = TG * TG, BP = TG * BS, LD = BP + 1;
   __shared__ double A[BP * LD];
   __shared__ double col[2][BP];
   __shared__ double piv[BP];
   __shared__ double xd[BP];   // 1 / L_kk
-  const int ti = threadIdx.x >> 4, tk = threadIdx.x & 15;
+  const int ti = threadIdx.x / TG, tk = threadIdx.x % TG;
   const int i0 = ti * BS, k0 = tk * BS;
   double a[BS][BS];
 #pragma unroll
@@ -621,7 +607,7 @@ __global__ void __launch_bounds__(256) chol_inv_blk_kernel(const double* __restr
     if (threadIdx.x == 0) piv[j] = pv;
   }
   __syncthreads();
-  for (int k = threadIdx.x; k < BP; k += 256) {
+  for (int k = threadIdx.x; k < BP; k += NT) {
     const double l = k < b ? sqrt(piv[k]) : 1.0;
     piv[k] = l;
     xd[k] = 1.0 / l;
@@ -731,20 +717,18 @@ __global__ void __launch_bounds__(256) apply_linv_kernel(const double* __restric
 // Parallel cyclic Jacobi on the symmetric b x b matrix hg, eigenvectors in s (global,
 // [b][b]), eigenvalues sorted descending into theta/order.  Round-robin pairing: in
 // each of the n-1 rounds of a sweep, index 0 is fixed and the others rotate, giving
-// n/2 disjoint pairs (n = b rounded up to even).  H and the rotations S are worked on
-// with row stride b + 1 (conflict-free column access), both in LDS when b <= 96, else
-// in `work` and `swork` ([b][b + 1] each); S is written to s ([b][b]) at the end.
-template <bool IN_LDS, int PMAX>
+// n/2 disjoint pairs (n = b rounded up to even).  For blocks past the one-sided kernel
+// below (b > 128): H and the rotations S are worked on in `work` and `swork` ([b][b + 1]
+// each, row stride b + 1); S is written to s ([b][b]) at the end.
+template <int PMAX>
 __global__ void __launch_bounds__(256) jacobi_kernel(const double* __restrict__ hg, double* __restrict__ work,
                                                      double* __restrict__ swork, double* __restrict__ s_out,
                                                      double* theta, int* order, int b, int sweeps) {
-  __shared__ double hl[IN_LDS ? 96 * 97 : 1];
-  __shared__ double sl[IN_LDS ? 96 * 97 : 1];
   __shared__ double cs[256], sn[256];
   __shared__ int pp[256], qq[256];
   __shared__ double off_sh[256], tot_sh[256];
-  double* h = IN_LDS ? hl : work;
-  double* s = IN_LDS ? sl : swork;
+  double* h = work;
+  double* s = swork;
   const int ld = b + 1;
   const int n = (b + 1) & ~1;
   const int t = threadIdx.x;
@@ -878,21 +862,22 @@ __global__ void __launch_bounds__(256) jacobi_kernel(const double* __restrict__ 
 // and A^T A diagonal, so V diagonalises H^2 and hence H: a_p = theta_p v_p, the
 // eigenvalue is the column norm and the eigenvector the normalised column (accurate for
 // the large eigenvalues the basis keeps; no V is accumulated).  A sits in LDS column by
-// column (stride BP + 1); each pair is worked on by G = 512 / BP lanes, RPL = BP / G rows
-// each, held in registers between the pair's dot products and its update; one barrier
-// per round.  A pair rotates when |a_p . a_q| > 1e-15 ||a_p|| ||a_q||; the sweeps stop
-// once the largest such ratio of a sweep is at most 1e-13.  Outputs as jacobi_kernel.
+// column (stride BP + 1); each pair is worked on by 16 lanes, BP / 16 rows each, held in
+// registers between the pair's dot products and its update (8 BP threads: several waves
+// per SIMD hide each other's latency); one barrier per round.  A pair rotates when
+// |a_p . a_q| > 1e-15 ||a_p|| ||a_q||; the sweeps stop once the largest such ratio of a
+// sweep is at most 1e-13.  Outputs as jacobi_kernel.
 template <int BP>
-__global__ void __launch_bounds__(256) jacobi1s_kernel(const double* __restrict__ hg, double* __restrict__ s_out,
-                                                       double* __restrict__ theta, int* __restrict__ order, int b,
-                                                       int sweeps) {
-  constexpr int LD = BP + 1, G = 512 / BP, RPL = BP / G;
+__global__ void __launch_bounds__(8 * BP) jacobi1s_kernel(const double* __restrict__ hg, double* __restrict__ s_out,
+                                                          double* __restrict__ theta, int* __restrict__ order, int b,
+                                                          int sweeps) {
+  constexpr int LD = BP + 1, G = 16, RPL = BP / G, NT = 8 * BP, NW = NT / 64;
   __shared__ double A[BP * LD];
   __shared__ double nrm[BP];
-  __shared__ double wmax[4];
+  __shared__ double wmax[NW];
   const int t = threadIdx.x, grp = t / G, gl = t % G;
   const int n = (b + 1) & ~1;
-  for (int e = t; e < BP * BP; e += 256) {
+  for (int e = t; e < BP * BP; e += NT) {
     const int c = e / BP, i = e % BP;
     A[c * LD + i] = (i < b && c < b) ? hg[c * b + i] : 0.0;   // column c of H (= row c)
   }
@@ -904,23 +889,33 @@ __global__ void __launch_bounds__(256) jacobi1s_kernel(const double* __restrict_
         int p, q;
         if (grp == 0) {
           p = 0;
-          q = 1 + (round % (n - 1));
+          q = 1 + round;
         } else {
-          p = 1 + ((round + grp) % (n - 1));
-          q = 1 + ((round + n - 1 - grp) % (n - 1));
+          int a1 = round + grp, a2 = round - grp;   // round +- grp modulo n - 1
+          if (a1 >= n - 1) a1 -= n - 1;
+          if (a2 < 0) a2 += n - 1;
+          p = 1 + a1;
+          q = 1 + a2;
         }
         if (p > q) { const int tt = p; p = q; q = tt; }
         if (q < b) {
           double ap[RPL], aq[RPL];
-          double al = 0.0, be = 0.0, ga = 0.0;
+          double al0 = 0.0, al1 = 0.0, be0 = 0.0, be1 = 0.0, ga0 = 0.0, ga1 = 0.0;
 #pragma unroll
           for (int k = 0; k < RPL; ++k) {
             ap[k] = A[p * LD + k * G + gl];
             aq[k] = A[q * LD + k * G + gl];
-            al = fma(ap[k], ap[k], al);
-            be = fma(aq[k], aq[k], be);
-            ga = fma(ap[k], aq[k], ga);
           }
+#pragma unroll
+          for (int k = 0; k < RPL; k += 2) {
+            al0 = fma(ap[k], ap[k], al0);
+            be0 = fma(aq[k], aq[k], be0);
+            ga0 = fma(ap[k], aq[k], ga0);
+            al1 = fma(ap[k + 1], ap[k + 1], al1);
+            be1 = fma(aq[k + 1], aq[k + 1], be1);
+            ga1 = fma(ap[k + 1], aq[k + 1], ga1);
+          }
+          double al = al0 + al1, be = be0 + be1, ga = ga0 + ga1;
 #pragma unroll
           for (int o = 1; o < G; o <<= 1) {
             al += __shfl_xor(al, o, 64);
@@ -947,7 +942,9 @@ __global__ void __launch_bounds__(256) jacobi1s_kernel(const double* __restrict_
     for (int o = 1; o < 64; o <<= 1) worst = fmax(worst, __shfl_xor(worst, o, 64));
     if ((t & 63) == 0) wmax[t >> 6] = worst;
     __syncthreads();
-    const double w = fmax(fmax(wmax[0], wmax[1]), fmax(wmax[2], wmax[3]));
+    double w = 0.0;
+#pragma unroll
+    for (int q = 0; q < NW; ++q) w = fmax(w, wmax[q]);
     __syncthreads();
     if (w <= 1e-13) break;
   }
@@ -964,7 +961,7 @@ __global__ void __launch_bounds__(256) jacobi1s_kernel(const double* __restrict_
     order[rank] = t;
     theta[rank] = v;
   }
-  for (int e = t; e < b * b; e += 256) {
+  for (int e = t; e < b * b; e += NT) {
     const int k = e / b, c = e % b;
     s_out[e] = A[c * LD + k] / fmax(nrm[c], 1e-300);
   }
@@ -973,9 +970,9 @@ __global__ void __launch_bounds__(256) jacobi1s_kernel(const double* __restrict_
 // Symmetric eigenproblem of the b x b block: one-sided Jacobi up to b = 128, else the
 // two-sided kernel with its matrices in global memory.
 void eig_small(const double* h, EigWs& w, int b, hipStream_t s) {
-  if (b <= 64) jacobi1s_kernel<64><<<1, 256, 0, s>>>(h, w.s, w.theta, w.order, b, 40);
-  else if (b <= 128) jacobi1s_kernel<128><<<1, 256, 0, s>>>(h, w.s, w.theta, w.order, b, 40);
-  else jacobi_kernel<false, 12><<<1, 256, 0, s>>>(h, w.chol, w.jac, w.s, w.theta, w.order, b, 40);
+  if (b <= 64) jacobi1s_kernel<64><<<1, 512, 0, s>>>(h, w.s, w.theta, w.order, b, 40);
+  else if (b <= 128) jacobi1s_kernel<128><<<1, 1024, 0, s>>>(h, w.s, w.theta, w.order, b, 40);
+  else jacobi_kernel<12><<<1, 256, 0, s>>>(h, w.chol, w.jac, w.s, w.theta, w.order, b, 40);
 }
 
 // u[d][r] = Q[d][b] S[:, order[:r]]
@@ -1140,9 +1137,9 @@ __global__ void report_kernel(zoact_eig_report* rep, const double* info, const d
 
 // (L^{-1})^T of the Cholesky factor of w.m into w.linvt.
 void chol_inv(EigWs& w, int b, hipStream_t s) {
-  if (b <= 64) chol_inv_blk_kernel<4><<<1, 256, 0, s>>>(w.m, w.linvt, b);
-  else if (b <= 128) chol_inv_blk_kernel<8><<<1, 256, 0, s>>>(w.m, w.linvt, b);
-  else chol_inv_kernel<false, 1><<<1, 256, 0, s>>>(w.m, w.chol, w.linvt, b);
+  if (b <= 64) chol_inv_blk_kernel<2><<<1, 1024, 0, s>>>(w.m, w.linvt, b);
+  else if (b <= 128) chol_inv_blk_kernel<4><<<1, 1024, 0, s>>>(w.m, w.linvt, b);
+  else chol_inv_kernel<<<1, 256, 0, s>>>(w.m, w.chol, w.linvt, b);
 }
 
 // Q = orth(Y) by Cholesky-QR (applied `passes` times).  Reads y, leaves the
