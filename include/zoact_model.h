@@ -74,6 +74,13 @@ zoact_status zoact_attention_rope(void* q, int64_t ldq, void* k, int64_t ldk, co
                                   float scale, int32_t dtype, const float* cos_t, const float* sin_t, void* out,
                                   zoact_stream stream);
 
+/* Post-state of zoact_attention_rope for a configuration on the current device: 1 when
+ * the call rotates q and k in place, 0 when it leaves them as they were.  Host only (no
+ * GPU work); an invalid configuration (dtype other than F32/BF16, a count below 1, head
+ * grouping that does not divide) gives -1. */
+int32_t zoact_attention_rope_in_place(int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads,
+                                      int32_t head_dim, int32_t dtype);
+
 #ifdef __cplusplus
 }
 #endif

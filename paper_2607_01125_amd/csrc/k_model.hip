@@ -1228,6 +1228,14 @@ extern "C" zoact_status zoact_attention(const void* q, int64_t ldq, const void* 
                         nullptr, stream);
 }
 
+extern "C" int32_t zoact_attention_rope_in_place(int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads,
+                                                 int32_t head_dim, int32_t dtype) {
+  if ((dtype != ZOACT_F32 && dtype != ZOACT_BF16) || n_seq < 1 || seq < 1 || n_heads < 1 || n_kv_heads < 1 ||
+      head_dim < 1 || n_heads % n_kv_heads != 0)
+    return -1;
+  return attention_resident(dtype, n_seq, seq, n_heads, n_kv_heads, head_dim) ? 0 : 1;
+}
+
 extern "C" zoact_status zoact_attention_rope(void* q, int64_t ldq, void* k, int64_t ldk, const void* v, int64_t ldv,
                                              int64_t n_seq, int64_t seq, int32_t n_heads, int32_t n_kv_heads,
                                              int32_t head_dim, float scale, int32_t dtype, const float* cos_t,

@@ -127,6 +127,7 @@ SIGNATURES = {
     "zoact_layernorm": ([_P, _P, _P, _I64, _I64, _F, _I32, _P, _P], _I32),
     "zoact_rope": ([_P, _I32, _I64, _I64, _I64, _I32, _I32, _I64, _P, _P, _P], _I32),
     "zoact_attention": ([_P, _I64, _P, _I64, _P, _I64, _I64, _I64, _I32, _I32, _I32, _F, _I32, _P, _P], _I32),
+    "zoact_attention_rope_in_place": ([_I64, _I64, _I32, _I32, _I32, _I32], _I32),
     "zoact_attention_rope": ([_P, _I64, _P, _I64, _P, _I64, _I64, _I64, _I32, _I32, _I32, _F, _I32, _P, _P, _P, _P],
                              _I32),
 }
@@ -465,6 +466,11 @@ def rope(x: torch.Tensor, col0: int, n_heads: int, head_dim: int, seq: int, cos_
     ld = x.shape[-1]
     _check(lib().zoact_rope(_ptr(x), dtype_code(x), x.numel() // ld, ld, col0, n_heads, head_dim, seq, _ptr(cos_t),
                             _ptr(sin_t), _stream(stream)))
+
+
+def attention_rope_in_place(n_seq: int, seq: int, n_heads: int, n_kv_heads: int, head_dim: int, dtype: int) -> int:
+    """1 if attention_rope rotates q and k in place for this configuration, 0 if it leaves them."""
+    return int(lib().zoact_attention_rope_in_place(n_seq, seq, n_heads, n_kv_heads, head_dim, dtype))
 
 
 def attention_rope(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out: torch.Tensor, n_seq: int, seq: int,

@@ -89,6 +89,13 @@ def test_validation_rejects_before_launch():
     assert L.zoact_gram(ctypes.c_void_p(16), Z.BF16, 8, 64, 68, ctypes.c_void_p(16), 0, None) == Z.E_INVALID
 
 
+def test_attention_rope_post_state_query_rejects_bad_configs():
+    L = Z.lib()
+    assert L.zoact_attention_rope_in_place(1, 8, 3, 2, 64, Z.BF16) == -1   # 3 query heads over 2 kv heads
+    assert L.zoact_attention_rope_in_place(1, 8, 4, 2, 64, 7) == -1        # unknown dtype
+    assert L.zoact_attention_rope_in_place(0, 8, 4, 2, 64, Z.BF16) == -1
+
+
 def test_basis_workspace_grows_with_block():
     a = Z.basis_workspace_bytes(4096, 32)
     b = Z.basis_workspace_bytes(4096, 64)

@@ -192,10 +192,16 @@ def test_attention_rope_equals_rope_then_attention(B, S, H, Hkv, hd):
     Z.attention(ref_in[:, :H * hd], ref_in[:, H * hd:(H + Hkv) * hd], ref_in[:, (H + Hkv) * hd:], ref, B, S, H, Hkv,
                 hd, scale)
     out = torch.empty_like(ref)
+    before = qkv.clone()
     Z.attention_rope(qkv[:, :H * hd], qkv[:, H * hd:(H + Hkv) * hd], qkv[:, (H + Hkv) * hd:], out, B, S, H, Hkv, hd,
                      scale, ct, st)
     torch.cuda.synchronize()
     assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+    # the documented post-state of q and k: rotated in place, or untouched
+    in_place = Z.attention_rope_in_place(B, S, H, Hkv, hd, Z.BF16)
+    assert in_place == (0 if (B, S) in ((32, 256), (128, 33), (64, 130)) else 1)
+    want = ref_in if in_place else before
+    assert torch.equal(qkv.view(torch.int16), want.view(torch.int16))
 
 
 @pytest.mark.parametrize("B,S,H,Hkv,hd", [(4, 64, 4, 4, 32), (2, 17, 4, 2, 16), (1, 1, 1, 1, 8)])
