@@ -47,6 +47,21 @@ DOMINANT_KERNEL = "gemm_4w64_kernel"
 DOMINANT_SOURCES = [os.path.join("paper_2607_01125_amd", "csrc", f)
                     for f in ("k_gemm_4w64.hip", "gemm_4w_epi.hpp", "gemm_common.hpp")]
 HEADLINE = "llama3_8b_bf16_step"
+_LLAMA_TXT = ("32 layers, d=4096, GQA 32q/8kv x 128, SwiGLU FFN 14336, vocab 128256; r=32 on q,k,v,o,gate,up,down; "
+              "16x256 tokens per ± half")
+# workloads bench.py can time as its line (the headline by default; the others for profiling)
+WORKLOADS = {
+    HEADLINE: ("llama_bf16", "Llama-3-8B-shape decoder, bf16, random init: " + _LLAMA_TXT + "; one two-sided ZO step "
+               "(± forward with the fused LM head + cross entropy, ZO-Adam over 44,040,192 coefficients)",
+               {"tokens_per_half": 4096, "rank": 32, "eps": 1e-3, "lr": 5e-5}),
+    "llama3_8b_int4_step": ("llama_int4", "Llama-3-8B-shape decoder, INT4 weights (groups of 128 along the input, "
+                            "bf16 scales), bf16 activations, random init: " + _LLAMA_TXT + "; one two-sided ZO step",
+                            {"tokens_per_half": 4096, "rank": 32, "eps": 1e-3, "lr": 5e-5}),
+    "opt13b_bf16_step": ("opt_bf16", "OPT-13B-shape decoder, bf16, random init: 40 layers, d=5120, 40 heads x 128, "
+                         "ReLU FFN 20480, vocab 50272, learned positions; r=64 on q,v,o,fc1,fc2; 8x512 tokens per ± "
+                         "half; one two-sided ZO step", {"tokens_per_half": 4096, "rank": 64, "eps": 1e-3,
+                                                         "lr": 2.5e-5}),
+}
 
 
 class TimingEvent:
@@ -599,7 +614,7 @@ class LaunchTimer:
         return n, tot_f, tot_s, per
 
 
-def bench_model(dev, which, warmup=2, steps=5, extras=True, roofline=False):
+def bench_model(dev, which, warmup=2, steps=5, extras=True, roofline=False, workload=HEADLINE):
     import torch
 
     import synth
@@ -635,7 +650,7 @@ def bench_model(dev, which, warmup=2, steps=5, extras=True, roofline=False):
         f"{basis['resid_max']}, gap min {basis['gap_min']}, iterations {basis['iters_min']}-{basis['iters_max']}")
     timer = None
     if roofline:
-        timer = LaunchTimer(steps * (4 * shape.n_layers + 8))
+        timer = LaunchTimer(steps * (6 * shape.n_layers + 8))   # at most 5 linears per layer (OPT: q|v, k, o, fc1, fc2)
         g.linear_hook = timer
     for _ in range(warmup):
         g.step(tok, 1, 1e-3, lr)
@@ -661,13 +676,14 @@ def bench_model(dev, which, warmup=2, steps=5, extras=True, roofline=False):
     if timer is not None:
         n, tot_f, tot_s, per = timer.summary()
         achieved = tot_f / tot_s / 1e12
+        sites = "q|k|v, o, gate|up with SwiGLU, down" if which != "opt_bf16" else "q|v, o, fc1 with ReLU, fc2"
         rec["roofline"] = {
             "kernel": f"{DOMINANT_KERNEL} (fused ± adapted GEMM) over the {n} adapted-linear launches of the "
-                      f"{steps} timed steps ({n // steps} per step: q|k|v, o, gate|up with SwiGLU, down per layer; "
+                      f"{steps} timed steps ({n // steps} per step: {sites} per layer; "
                       f"M = {2 * B * S} stacked rows, r = {shape.rank})",
             "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": traffic_record(DOMINANT_KERNEL, HEADLINE, DOMINANT_SOURCES),
+            "traffic": traffic_record(DOMINANT_KERNEL, workload, DOMINANT_SOURCES),
             "flops_per_launch": round(tot_f / n), "mean_launch_us": round(tot_s / n * 1e6, 1),
             "launches": n, "per_shape": per,
             "gemm_share_of_step": round(tot_s / (ms * 1e-3 * steps), 4)}
@@ -778,8 +794,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default=HEADLINE, choices=[HEADLINE])
-    ap.add_argument("--quick", action="store_true", help="headline workload only")
+    ap.add_argument("--workload", default=HEADLINE, choices=list(WORKLOADS),
+                    help="the workload of the JSON line (default: the headline)")
+    ap.add_argument("--quick", action="store_true", help="that workload only")
     ap.add_argument("--models", default="llama_int4,opt_bf16",
                     help="comma-separated further model runs (llama_int4, opt_bf16; empty for none)")
     ap.add_argument("--no-shapes", action="store_true", help="skip the 8B layer-shape sweep")
@@ -795,9 +812,10 @@ def main():
     import torch
 
     dev = torch.device("cuda:0")
-    log("headline: Llama-3-8B-shape bf16 ZO step, 16 x 256 tokens per half, r = 32")
-    head = bench_model(dev, "llama_bf16", warmup=args.warmup, steps=args.steps, extras=not args.quick,
-                       roofline=True)
+    which, wtext, wconf = WORKLOADS[args.workload]
+    log(f"headline: {args.workload}")
+    head = bench_model(dev, which, warmup=args.warmup, steps=args.steps, extras=not args.quick, roofline=True,
+                       workload=args.workload)
     ms = head["ms_per_step"]
     out = {
         "metric": METRIC,
@@ -812,17 +830,13 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (random-init weights N(0, 0.02^2), uniform random tokens, seeded)",
-        "config": {"workload": "Llama-3-8B-shape decoder, bf16, random init: 32 layers, d=4096, GQA 32q/8kv x 128, "
-                               "SwiGLU FFN 14336, vocab 128256; r=32 on q,k,v,o,gate,up,down; 16x256 tokens per ± "
-                               "half; one two-sided ZO step (± forward with the fused LM head + cross entropy, "
-                               "ZO-Adam over 44,040,192 coefficients)",
-                   "tokens_per_half": 4096, "rank": 32, "eps": 1e-3, "lr": 5e-5, "parallelism": "single GPU"},
+        "config": {"workload": wtext, **wconf, "parallelism": "single GPU"},
         "model_tflops": head["model_tflops"],
         "step_tflop": head["step_tflop"],
         "basis_init_s": head["basis_init_s"],
         "roofline": head["roofline"],
         "losses": head["losses"],
-        "llama3_8b_bf16": {k: v for k, v in head.items() if k not in ("roofline", "losses")},
+        args.workload.replace("_step", ""): {k: v for k, v in head.items() if k not in ("roofline", "losses")},
     }
     log(f"headline: {out['value']} steps/s, fused GEMM {head['roofline']['achieved']} TFLOP/s "
         f"({head['roofline']['frac']:.3f} of peak)")
@@ -850,7 +864,7 @@ def main():
         torch.cuda.synchronize()
         out["copy_calibration_bytes"] = n
         del src, dst
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.workload == HEADLINE:
         log("cpu baseline (oracle, sampled headline step)")
         out["cpu_baseline"] = cpu_baseline_llama()
         log(f"cpu baseline: {out['cpu_baseline']['seconds_per_step']} s per step (extrapolated)")
