@@ -585,7 +585,8 @@ class LaunchTimer:
                 raise RuntimeError("LaunchTimer: event pool exhausted")
             ev = self.pool[len(self.used)]
             ev[0].record(stream)
-            self.used.append((ev, lin.d_in, lin.d_out, lin.r, T, flags))
+            plain = lin.plain[1] - lin.plain[0] if lin.r else 0
+            self.used.append((ev, lin.d_in, lin.d_out, lin.r, T, flags, plain))
         else:
             self.used[-1][0][1].record(stream)
 
@@ -594,14 +595,16 @@ class LaunchTimer:
         import paper_2607_01125_amd.zoact as Z
 
         shapes, n, tot_f, tot_s = {}, 0, 0.0, 0.0
-        for (e0, e1), K, N, r, T, flags in self.used:
+        for (e0, e1), K, N, r, T, flags, plain in self.used:
             if r == 0:
                 continue
             shared = bool(flags & Z.SHARED_X)
             n_out = N // 2 if flags & Z.EPI_SWIGLU else N
-            f = (2 * T * N * K if shared else 2 * (2 * T) * N * K) + 2 * (2 * T) * r * N
+            # the correction covers the adapted features only (a plain range has none)
+            f = (2 * T * N * K if shared else 2 * (2 * T) * N * K) + 2 * (2 * T) * r * (N - plain)
             sec = e0.elapsed_time(e1) * 1e-3
-            key = f"{2 * T}x{N}x{K}" + (" shared" if shared else "") + (" swiglu" if flags & Z.EPI_SWIGLU else "")
+            key = (f"{2 * T}x{N}x{K}" + (" shared" if shared else "") + (" swiglu" if flags & Z.EPI_SWIGLU else "")
+                   + (f" ({plain} features plain)" if plain else ""))
             d = shapes.setdefault(key, {"launches": 0, "flop": f, "s": 0.0, "out_features": n_out})
             d["launches"] += 1
             d["s"] += sec

@@ -124,6 +124,15 @@ typedef struct {
                            r % 8 == 0: 16-byte aligned, stride a multiple of 8;
                            otherwise 2-byte alignment suffices                     */
   int64_t ch_half_stride;
+  int64_t plain_begin;  /* output features [plain_begin, plain_end) are not adapted (a
+                           projection fused with adapted ones, e.g. k inside q|k|v):
+                           they get no correction and have no coefficient rows, so
+                           feature n >= plain_end uses coefficient row
+                           n - (plain_end - plain_begin).  Empty (equal) by default;
+                           ignored when r == 0.  Non-empty needs BF16 activations and
+                           weights, ch given, both bounds multiples of 256 and no
+                           ZOACT_SHARED_X (else ZOACT_E_UNSUPPORTED or INVALID)       */
+  int64_t plain_end;
 } zoact_linear;
 
 /* The coefficient arena and its Adam moments (updated in place by zoact_step). */
@@ -197,10 +206,18 @@ zoact_status zoact_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e
 /* ------------------------------------------------------ projection X U
  * The X V_r factor of the perturbed forward (Section 3, Y+ = XW + (X V_r)(B + mu Z)).
  * x [n_tok][d_in] and U^T [r][d_in] in dtype (F32 or BF16); p [n_tok][r] same
- * dtype, fp32 accumulation, one rounding on store.  1 <= r <= 256; d_in % 8 == 0
- * for BF16. */
+ * dtype, fp32 accumulation, one rounding on store.  1 <= r <= 256; d_in % 32 == 0
+ * for BF16, x and ut 16-byte aligned.
+ * ws (nullable, device): with BF16 and r <= 64, a workspace of at least
+ * zoact_project_workspace_bytes(n_tok, d_in, r) bytes lets the depth be split over
+ * workgroups as well (fewer U^T bytes per byte of x; fp32 partials, summed in a fixed
+ * order by a second pass, so the same values on every run); calls that overlap on one
+ * workspace race.  The split form is taken where it is the faster one (d_in > 4096 or
+ * n_tok <= 4096); otherwise, with ws NULL or too small, the single-pass kernel (values
+ * may differ from the split form in the last bit). */
+size_t zoact_project_workspace_bytes(int64_t n_tok, int64_t d_in, int32_t r);
 zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut,
-                           int32_t r, void* p, zoact_stream stream);
+                           int32_t r, void* p, void* ws, size_t ws_bytes, zoact_stream stream);
 
 /* The projection of a site whose input is a norm's output (the attention and MLP inputs
  * of a decoder layer), fused with that norm: y = RMSNorm(x) * w, or LayerNorm(x) * w + b,

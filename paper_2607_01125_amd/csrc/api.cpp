@@ -74,8 +74,13 @@ zoact_status zoact_gen_z(uint64_t seed, uint32_t step, uint32_t query, int64_t e
   return hip_status(zoact::launch_gen_z(seed, step, query, e0, n, out, st(stream)), "gen_z");
 }
 
+size_t zoact_project_workspace_bytes(int64_t n_tok, int64_t d_in, int32_t r) {
+  if (n_tok < 1 || d_in < 1 || r < 1) return 0;
+  return zoact::project_ws_bytes(n_tok, d_in, r);
+}
+
 zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut, int32_t r, void* p,
-                           zoact_stream stream) {
+                           void* ws, size_t ws_bytes, zoact_stream stream) {
   CHECK(float_type(dtype), "project: dtype must be F32 or BF16");
   CHECK(n_tok >= 1 && d_in >= 1, "project: empty shape (n_tok=%lld, d_in=%lld)", (long long)n_tok, (long long)d_in);
   CHECK(r >= 1 && r <= 256, "project: r=%d outside [1, 256]", r);
@@ -83,6 +88,12 @@ zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t 
   if (dtype == ZOACT_BF16) {
     CHECK(d_in % 32 == 0, "project: bf16 needs d_in %% 32 == 0 (d_in=%lld)", (long long)d_in);
     CHECK(aligned16(x) && aligned16(ut), "project: x and ut must be 16-byte aligned");
+    // the depth-split form where it measured faster: deep inputs, or few tokens (at
+    // 8192 x 4096 the single pass is level with it)
+    if (ws && r <= 64 && ws_bytes >= zoact::project_ws_bytes(n_tok, d_in, r) && (d_in > 4096 || n_tok <= 4096)) {
+      CHECK(aligned16(ws), "project: ws must be 16-byte aligned");
+      return hip_status(zoact::launch_project_split(x, n_tok, d_in, ut, r, p, ws, st(stream)), "project");
+    }
   }
   return hip_status(zoact::launch_project(x, dtype, n_tok, d_in, ut, r, p, st(stream)), "project");
 }
@@ -110,19 +121,30 @@ static zoact_status validate_linear(const zoact_linear* L, const zoact_arena* A,
   CHECK(!(flags & ZOACT_SHARED_X) || x_dtype == ZOACT_BF16, "linear_fwd_pm: SHARED_X needs BF16 activations");
   CHECK(!((flags & ZOACT_EPI_SWIGLU) && (flags & ZOACT_EPI_RELU)), "linear_fwd_pm: SWIGLU and RELU are exclusive");
   CHECK(float_type(x_dtype) && float_type(y_dtype), "linear_fwd_pm: activation types must be F32 or BF16");
+  int64_t rows = L->d_out;   // coefficient rows of the layer
   if (L->r > 0) {
     CHECK(A != nullptr && A->c != nullptr, "linear_fwd_pm: r > 0 needs an arena");
     CHECK(L->ut != nullptr && p != nullptr, "linear_fwd_pm: r > 0 needs ut and p");
-    CHECK(L->coef_offset >= 0 && L->coef_offset + L->d_out * (int64_t)L->r <= A->k,
+    CHECK(L->plain_begin >= 0 && L->plain_begin <= L->plain_end && L->plain_end <= L->d_out,
+          "linear_fwd_pm: plain range [%lld, %lld) outside [0, d_out]", (long long)L->plain_begin,
+          (long long)L->plain_end);
+    if (L->plain_end > L->plain_begin) {
+      CHECK(L->plain_begin % 256 == 0 && L->plain_end % 256 == 0,
+            "linear_fwd_pm: plain range bounds must be multiples of 256");
+      CHECK(L->ch != nullptr && x_dtype == ZOACT_BF16 && L->w_dtype == ZOACT_BF16 && !(flags & ZOACT_SHARED_X),
+            "linear_fwd_pm: a plain range needs BF16 weights and activations, ch, and no SHARED_X");
+      rows -= L->plain_end - L->plain_begin;
+    }
+    CHECK(L->coef_offset >= 0 && L->coef_offset + rows * (int64_t)L->r <= A->k,
           "linear_fwd_pm: coefficient block [%lld, %lld) outside the arena (k=%lld)", (long long)L->coef_offset,
-          (long long)(L->coef_offset + L->d_out * (int64_t)L->r), (long long)A->k);
+          (long long)(L->coef_offset + rows * (int64_t)L->r), (long long)A->k);
     CHECK(float_type(A->c_dtype), "linear_fwd_pm: arena dtype must be F32 or BF16");
   }
   if (flags & ZOACT_EPI_SWIGLU) CHECK(L->d_out % 32 == 0, "linear_fwd_pm: SWIGLU needs d_out %% 32 == 0");
   if (L->ch != nullptr) {
     CHECK(x_dtype == ZOACT_BF16 && L->r > 0, "linear_fwd_pm: precomputed coefficients need BF16 activations and r > 0");
-    CHECK(L->ch_half_stride >= L->d_out * (int64_t)L->r && (reinterpret_cast<uintptr_t>(L->ch) & 1) == 0,
-          "linear_fwd_pm: ch must be 2-byte aligned with a half stride >= d_out * r");
+    CHECK(L->ch_half_stride >= rows * (int64_t)L->r && (reinterpret_cast<uintptr_t>(L->ch) & 1) == 0,
+          "linear_fwd_pm: ch must be 2-byte aligned with a half stride >= (coefficient rows) * r");
     if (L->r % 8 == 0)
       CHECK(aligned16(L->ch) && L->ch_half_stride % 8 == 0,
             "linear_fwd_pm: with r %% 8 == 0, ch must be 16-byte aligned with a half stride that is a multiple of 8");

@@ -31,6 +31,9 @@ hipError_t launch_step_q(const zoact_arena& A, const float* losses, int32_t q, u
                          const zoact_adam* h, float lr, uint32_t* status, hipStream_t s);
 hipError_t launch_dequant_int4(const void* w, const void* scales, int64_t d_out, int64_t d_in, void* out,
                                hipStream_t s);
+size_t project_ws_bytes(int64_t n_tok, int64_t d_in, int32_t r);
+hipError_t launch_project_split(const void* x, int64_t n_tok, int64_t d_in, const void* ut, int32_t r, void* p,
+                                void* ws, hipStream_t s);
 hipError_t launch_project(const void* x, int32_t dtype, int64_t n_tok, int64_t d_in, const void* ut, int32_t r,
                           void* p, hipStream_t s);
 // Norm (RMSNorm, or LayerNorm with bias b) of n_tok rows and the projection of its output,

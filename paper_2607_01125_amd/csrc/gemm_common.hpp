@@ -36,6 +36,8 @@ struct GemmArgs {
   float2* xpart;         // EPI_XENT: (max, sum of exp) per row and 128-column block [2 T][xnblk]
   float* xtgt;           // EPI_XENT: the logit of each row's next token [2 T]
   int32_t xnblk;         // EPI_XENT: ceil(N / 128)
+  int64_t plain_begin;   // output features [plain_begin, plain_end): no correction, no coefficient rows
+  int64_t plain_end;
 };
 
 // Internal epilogue selector (not a public flag): the tile's squared errors against tgt

@@ -514,6 +514,112 @@ __global__ void __launch_bounds__(256) project_bf16_kernel(const uint16_t* __res
   }
 }
 
+// The same product with the depth also split over workgroups (workspace form): workgroup
+// (b, s) owns 16 TB tokens and depth chunk s of S, its 4 waves splitting the chunk further
+// (64-deep steps, the next step's x and U^T fragments in flight).  More tokens per
+// workgroup than above means fewer U^T bytes per x byte (r / (16 TB) instead of r / 32).
+// Each workgroup writes its fp32 partial [16 TB][r] (waves summed in a fixed order) to
+// part[s]; a second pass adds the S partials in the order s = 0 .. S - 1 and rounds once
+// to bf16.  (Letting the last workgroup of a token block do the sum needs a device-scope
+// release per workgroup, which on this GPU writes back the XCD's L2: it measured four
+// times slower than the second launch.)
+template <int RB, int TB>
+__global__ void __launch_bounds__(256) project_split_kernel(const uint16_t* __restrict__ x,
+                                                            const uint16_t* __restrict__ ut, uint16_t* __restrict__ p,
+                                                            int64_t n_tok, int64_t d, int r, int64_t chunk,
+                                                            float* __restrict__ part) {
+  constexpr int TOK = 16 * TB, NC = RB * 16;
+  __shared__ float red[4][TOK][NC + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lk = lane >> 4;
+  const int64_t t0 = (int64_t)blockIdx.x * TOK;
+  const int sp = blockIdx.y;
+  floatx4 acc[TB][RB];
+#pragma unroll
+  for (int i = 0; i < TB; ++i)
+#pragma unroll
+    for (int j = 0; j < RB; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const uint16_t* xr[TB];
+#pragma unroll
+  for (int i = 0; i < TB; ++i) {
+    int64_t t = t0 + i * 16 + lr;
+    t = t < n_tok ? t : n_tok - 1;
+    xr[i] = x + t * d + lk * 8;
+  }
+  const bf16x8 zero8 = {};
+  // this wave's depth range: a quarter of the chunk, a multiple of 32
+  const int64_t c0 = (int64_t)sp * chunk, c1 = c0 + chunk < d ? c0 + chunk : d;
+  int64_t wq = (chunk + 3) / 4;
+  wq = (wq + 31) / 32 * 32;
+  const int64_t k_begin = c0 + wave * wq, k_end = k_begin + wq < c1 ? k_begin + wq : c1;
+  bf16x8 a[2][TB], an[2][TB], bq[2][RB], bn[2][RB];
+  auto load = [&](int64_t k) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const bool in = k + u * 32 < k_end;
+#pragma unroll
+      for (int i = 0; i < TB; ++i) an[u][i] = in ? *reinterpret_cast<const bf16x8*>(xr[i] + k + u * 32) : zero8;
+#pragma unroll
+      for (int j = 0; j < RB; ++j) {
+        const int rc = j * 16 + lr;
+        bn[u][j] = (in && rc < r) ? *reinterpret_cast<const bf16x8*>(ut + (int64_t)rc * d + k + u * 32 + lk * 8) : zero8;
+      }
+    }
+  };
+  if (k_begin < k_end) load(k_begin);
+  for (int64_t k = k_begin; k < k_end; k += 64) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+#pragma unroll
+      for (int i = 0; i < TB; ++i) a[u][i] = an[u][i];
+#pragma unroll
+      for (int j = 0; j < RB; ++j) bq[u][j] = bn[u][j];
+    }
+    if (k + 64 < k_end) load(k + 64);
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int i = 0; i < TB; ++i)
+#pragma unroll
+        for (int j = 0; j < RB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][i], bq[u][j], acc[i][j], 0, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < TB; ++i)
+#pragma unroll
+    for (int j = 0; j < RB; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) red[wave][i * 16 + lk * 4 + q][j * 16 + lr] = acc[i][j][q];
+  __syncthreads();
+  // this workgroup's partial: waves summed in order
+  float* mine = part + ((int64_t)sp * n_tok + t0) * r;
+  for (int e = threadIdx.x; e < TOK * NC; e += 256) {
+    const int tl = e / NC, col = e % NC;
+    if (t0 + tl < n_tok && col < r)
+      mine[(int64_t)tl * r + col] = ((red[0][tl][col] + red[1][tl][col]) + red[2][tl][col]) + red[3][tl][col];
+  }
+}
+
+// p = bf16(part[0] + part[1] + ... + part[S - 1]), in that order, 4 outputs per thread.
+__global__ void __launch_bounds__(256) project_sum_kernel(const float* __restrict__ part, int nsplit, int64_t n,
+                                                          uint16_t* __restrict__ p, int vec) {
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i >= n) return;
+  if (vec) {   // n % 4 == 0, p 8-byte aligned
+    float4 v = *reinterpret_cast<const float4*>(part + i);
+    for (int q = 1; q < nsplit; ++q) {
+      const float4 w = *reinterpret_cast<const float4*>(part + (int64_t)q * n + i);
+      v.x += w.x, v.y += w.y, v.z += w.z, v.w += w.w;
+    }
+    *reinterpret_cast<uint2*>(p + i) = make_uint2(pack2(f2bf(v.x), f2bf(v.y)), pack2(f2bf(v.z), f2bf(v.w)));
+  } else {
+    for (int64_t e = i; e < i + 4 && e < n; ++e) {
+      float v = part[e];
+      for (int q = 1; q < nsplit; ++q) v += part[(int64_t)q * n + e];
+      p[e] = f2bf(v);
+    }
+  }
+}
+
 __global__ void project_f32_kernel(const float* x, const float* ut, float* p, int64_t n_tok, int64_t d, int r) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_tok * r; i += (int64_t)gridDim.x * blockDim.x) {
     const int64_t t = i / r;
@@ -589,6 +695,10 @@ static GemmArgs bf16_args(const zoact_linear& L, const zoact_arena* A, const voi
   a.n_tail = (L.r + 63) / 64;
   a.ch = static_cast<const uint16_t*>(L.ch);
   a.ch_stride = L.ch_half_stride;
+  if (L.r > 0) {
+    a.plain_begin = L.plain_begin;
+    a.plain_end = L.plain_end;
+  }
   return a;
 }
 
@@ -597,6 +707,7 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
                             int32_t y_dtype, hipStream_t s) {
   const int epi = (flags & ZOACT_EPI_SWIGLU) ? ZOACT_EPI_SWIGLU : (flags & ZOACT_EPI_RELU) ? ZOACT_EPI_RELU : 0;
   if (x_dtype == ZOACT_F32) {
+    if (L.r > 0 && L.plain_end > L.plain_begin) return hipErrorNotSupported;
     GemmArgsF32 a{};
     a.x = static_cast<const float*>(x);
     a.w = static_cast<const float*>(L.w);
@@ -628,6 +739,8 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
   const bool of = y_dtype == ZOACT_F32;
   // one half's x and p read by both halves: the 64-deep schedule's shared-input form only
   if (flags & ZOACT_SHARED_X) return launch_linear_pm_4w64(a, L.w_dtype, epi, of, true, s);
+  // a plain feature range: the 64-deep schedule only
+  if (a.plain_end > a.plain_begin) return launch_linear_pm_4w64(a, L.w_dtype, epi, of, false, s);
   // the 64-deep persistent schedule where it applies (bf16 weights, C_h precomputed or
   // r = 0), else the 32-deep one (C_h formed in its prologue; INT4 in registers), else the
   // generic kernel (shapes outside both)
@@ -657,7 +770,8 @@ hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const 
   a.part = part;
   const bool shared = (flags & ZOACT_SHARED_X) != 0;
   hipError_t e = launch_linear_pm_4w64(a, L.w_dtype, EPI_MSE, false, shared, s);
-  if (e == hipErrorNotSupported && !shared) e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
+  if (e == hipErrorNotSupported && !shared && a.plain_end == a.plain_begin)
+    e = launch_linear_pm_4w(a, L.w_dtype, EPI_MSE, false, s);
   if (e != hipSuccess) return e;
   return launch_sum_mean(part, (int64_t)a.tiles_m_half * a.tiles_n * 4, (double)T * (double)L.d_out, loss_pm, s);
 }
@@ -738,6 +852,42 @@ hipError_t launch_dequant_int4(const void* w, const void* scales, int64_t d_out,
   dequant_int4_kernel<<<dim3((unsigned)g), dim3(256), 0, s>>>(static_cast<const uint4*>(w),
                                                                static_cast<const uint16_t*>(scales), units, d_in / 32,
                                                                d_in / 128, static_cast<uint4*>(out));
+  return hipGetLastError();
+}
+
+// Depth split of the workspace form: about four chunks of a multiple of 256, and at most
+// as many as leave each wave 64 deep.
+static int project_nsplit(int64_t d_in) {
+  int ns = (int)(d_in / 1024);
+  return ns < 1 ? 1 : (ns > 4 ? 4 : ns);
+}
+constexpr int PROJ_SPLIT_TB = 4;   // 64 tokens per workgroup
+
+size_t project_ws_bytes(int64_t n_tok, int64_t d_in, int32_t r) {
+  return (size_t)project_nsplit(d_in) * (size_t)n_tok * (size_t)r * 4;
+}
+
+hipError_t launch_project_split(const void* x, int64_t n_tok, int64_t d_in, const void* ut, int32_t r, void* p,
+                                void* ws, hipStream_t s) {
+  const int ns = project_nsplit(d_in);
+  int64_t chunk = (d_in + ns - 1) / ns;
+  chunk = (chunk + 255) / 256 * 256;
+  const int64_t nb = (n_tok + 16 * PROJ_SPLIT_TB - 1) / (16 * PROJ_SPLIT_TB);
+  float* part = static_cast<float*>(ws);
+  const dim3 grid((unsigned)nb, (unsigned)ns);
+  const auto* xx = static_cast<const uint16_t*>(x);
+  const auto* uu = static_cast<const uint16_t*>(ut);
+  auto* pp = static_cast<uint16_t*>(p);
+  const int rb = (r + 15) / 16;
+#define ZO_PS(RB) project_split_kernel<RB, PROJ_SPLIT_TB><<<grid, dim3(256), 0, s>>>(xx, uu, pp, n_tok, d_in, r, chunk, part)
+  if (rb <= 1) ZO_PS(1);
+  else if (rb <= 2) ZO_PS(2);
+  else if (rb <= 4) ZO_PS(4);
+  else return hipErrorNotSupported;
+#undef ZO_PS
+  const int64_t n = n_tok * r;
+  const int vec = (n % 4 == 0) && (reinterpret_cast<uintptr_t>(p) % 8 == 0);
+  project_sum_kernel<<<dim3((unsigned)((n + 1023) / 1024)), dim3(256), 0, s>>>(part, ns, n, pp, vec);
   return hipGetLastError();
 }
 

@@ -253,15 +253,20 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
     // global memory (C_h precomputed) through buffer loads: rows past T or N read zeros
     // (their outputs are not stored), columns past r are zeroed, element-wise when r is
     // not a multiple of 8.  With the shared input: the shared p and C_1, for half 1.
-    if (a.r > 0) {
+    // (a tile inside the plain feature range has none; past it, C_h rows are shifted back
+    // by the range's width)
+    const int64_t plen = a.plain_end - a.plain_begin;
+    if (a.r > 0 && !(g.n0 >= a.plain_begin && g.n0 < a.plain_end)) {
       const int kts = (a.r + 31) >> 5;
+      const int64_t cn0 = g.n0 >= a.plain_end ? g.n0 - plen : g.n0;
       const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(a.p + (int64_t)p_half * a.T * a.r, (uint32_t)(a.T * a.r * 2));
-      const __amdgpu_buffer_rsrc_t crs = buffer_rsrc(a.ch + (int64_t)c_half * a.ch_stride, (uint32_t)(a.N * a.r * 2));
+      const __amdgpu_buffer_rsrc_t crs =
+          buffer_rsrc(a.ch + (int64_t)c_half * a.ch_stride, (uint32_t)((a.N - plen) * a.r * 2));
       const bool vec = (a.r & 7) == 0;
       const int pvo = ((wm0 + lr) * a.r + lk * 8) * 2, cvo = ((wn0 + (PERM ? prow : lr)) * a.r + lk * 8) * 2;
       // C_h rows of W block i (the permuted order with PERM): first row's byte offset
       auto crow = [&](int i) -> int {
-        return (int)((g.n0 + (PERM ? (i >> 1) * 32 + (i & 1) * 4 : i * 16)) * a.r * 2);
+        return (int)((cn0 + (PERM ? (i >> 1) * 32 + (i & 1) * 4 : i * 16)) * a.r * 2);
       };
       for (int t = 0; t < kts; ++t) {
         const int col = t * 32 + lk * 8;
@@ -360,6 +365,8 @@ hipError_t launch_linear_pm_4w64(const GemmArgs& a, int w_dtype, int epi, bool o
   if (a.T * a.r * 2 >= (int64_t(1) << 31) || a.N * a.r * 2 >= (int64_t(1) << 31)) return hipErrorNotSupported;
   if (epi == EPI_XENT && 2 * a.T * (int64_t)a.xnblk * 8 >= (int64_t(1) << 31)) return hipErrorNotSupported;
   if (shared && (a.r < 8 || a.r > 32 || (a.r & 7) != 0)) return hipErrorNotSupported;
+  if (a.plain_end > a.plain_begin && (shared || (a.plain_begin & 255) != 0 || (a.plain_end & 255) != 0))
+    return hipErrorNotSupported;
 #define ZO_4W64(EP, OF, SH) \
   if (epi == EP && out_f32 == OF && shared == SH) return launch_4w64<EP, OF, SH>(a, s);
   ZO_4W64(0, false, false)

@@ -16,9 +16,11 @@ Models (the random-initialised shapes of the paper's Section 5 experiments):
 Adapted projections (Section 3, y = x W^T + (x U) C^T) read one of four input sites
 per layer -- "attn" (q, k, v), "o", "mlp" (gate/up or fc1) and "down" (down or fc2) --
 and projections reading the same site share its basis U.  Projections that read one
-site are fused into one linear call: q|k|v (or q|v, with k a separate plain linear when
-k is not adapted) and gate|up, whose rows interleave blocks of 16 gate and 16 up
-features so the SwiGLU epilogue pairs them inside a tile.
+site are fused into one linear call: q|k|v (when k is not adapted, as in OPT, k is the
+call's plain feature range -- no correction, no coefficient rows -- or, where the fast
+schedule does not cover that, a separate plain linear beside q|v) and gate|up, whose
+rows interleave blocks of 16 gate and 16 up features so the SwiGLU epilogue pairs them
+inside a tile.
 
 Coefficient arena: per layer, in order, [q|k|v] (or [q|v]), o, gate|up, down (Llama)
 or [q|v], out, fc1, fc2 (OPT); each block holds rows x r coefficients row-major, where
@@ -129,7 +131,7 @@ class Decoder:
         self.k = sum(b.rows * b.r for b in self.blocks)
         self._adapted_sites = {(b.layer, b.site) for b in self.blocks}
         self.r = s.rank
-        self._pack(W)
+        self._pack(W, int4_dequant)
         self.ut = {}                      # (layer, site) -> U^T [r][d_in] (activation dtype)
         self.arena = Z.Arena(torch.zeros(self.k, dtype=torch.bfloat16 if self.c_bf16 else torch.float32,
                                          device=self.dev),
@@ -139,6 +141,7 @@ class Decoder:
         self.loss_pm = torch.zeros(2, dtype=torch.float32, device=self.dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=self.dev)
         self.loss_ws = torch.empty(Z.loss_workspace_bytes(), dtype=torch.uint8, device=self.dev)
+        self._proj_ws = None     # the depth-split projection's partial sums (grown on demand)
         self._bufs = {}
         self._rope = {}
         self._ch = self._ch_all = None   # per-step C +/- eps Z of the whole arena (bf16 modes)
@@ -187,9 +190,14 @@ class Decoder:
             return interleave_gate_up(*ws), None
         return torch.cat(ws).contiguous(), None
 
-    def _pack(self, W):
+    def _pack(self, W, int4_dequant=True):
         s, d, dkv, ff = self.s, self.d, self.dkv, self.s.d_ff
         ad = set(s.adapted)
+        # q and v adapted, k not (OPT): one q|k|v launch with k as its plain feature range
+        # where the 64-deep schedule covers it (bf16 schedule, precomputed C +/- eps Z, range
+        # bounds on 256-feature tiles); else q|v and k as two launches
+        plain_k = ({"q", "v"} <= ad and "k" not in ad and self.act == torch.bfloat16
+                   and (self.mode == "bf16" or int4_dequant) and d % 256 == 0 and dkv % 256 == 0)
         self.layers = []
         for l in range(s.n_layers):
             L = W[l]
@@ -200,6 +208,13 @@ class Decoder:
             if fused_qkv:
                 w, sc = self._lin_w(L["wq"], L["wk"], L["wv"])
                 P["qkv"] = self._linear(l, "qkv", w, sc, d, d + 2 * dkv)
+            elif plain_k:
+                w, sc = self._lin_w(L["wq"], L["wk"], L["wv"])
+                bias = (torch.cat([self._t(L["bq"]), self._t(L["bk"]), self._t(L["bv"])])
+                        if s.family == "opt" else None)
+                lin, blk = self._linear(l, "qv", w, sc, d, d + 2 * dkv, bias)
+                lin.plain = (d, d + dkv)
+                P["qkv"] = (lin, blk)
             else:
                 w, sc = self._lin_w(L["wq"], L["wv"])
                 bias = torch.cat([self._t(L["bq"]), self._t(L["bv"])]) if s.family == "opt" else None
@@ -321,7 +336,8 @@ class Decoder:
         lin, blk = lin_blk
         return (self.shared_first and self.act == torch.bfloat16 and blk is not None and site_ut is not None
                 and self._ch is not None and (lin.w.dtype == torch.bfloat16 or self._wdq is not None)
-                and 8 <= self.r <= 32 and self.r % 8 == 0 and lin.d_in % 64 == 0 and lin.d_in >= 128)
+                and 8 <= self.r <= 32 and self.r % 8 == 0 and lin.d_in % 64 == 0 and lin.d_in >= 128
+                and lin.plain[0] == lin.plain[1])
 
     def forward(self, tokens: torch.Tensor, pert: Z.Pert | Z.PertPair, *, calibrate=None, distinct_halves=False,
                 head: bool = True):
@@ -408,7 +424,11 @@ class Decoder:
             if (l, site) in self._adapted_sites:
                 raise RuntimeError(f"no basis for site {(l, site)}: run basis_init or set_basis first")
             return None
-        Z.project(x, ut, self._cur["p"][:x.shape[0]])
+        n_tok = x.shape[0]
+        need = Z.project_workspace_bytes(n_tok, x.shape[1], self.r) if self.act == torch.bfloat16 else 0
+        if need and (self._proj_ws is None or self._proj_ws.numel() < need):
+            self._proj_ws = torch.empty(need, dtype=torch.uint8, device=self.dev)
+        Z.project(x, ut, self._cur["p"][:n_tok], self._proj_ws if need else None)
         return ut
 
     def site_dims(self):

@@ -48,7 +48,8 @@ class LinearDesc(ctypes.Structure):
     _fields_ = [("w_dtype", ctypes.c_int32), ("w", ctypes.c_void_p), ("w_scales", ctypes.c_void_p),
                 ("bias", ctypes.c_void_p), ("ut", ctypes.c_void_p), ("d_in", ctypes.c_int64),
                 ("d_out", ctypes.c_int64), ("r", ctypes.c_int32), ("coef_offset", ctypes.c_int64),
-                ("ch", ctypes.c_void_p), ("ch_half_stride", ctypes.c_int64)]
+                ("ch", ctypes.c_void_p), ("ch_half_stride", ctypes.c_int64), ("plain_begin", ctypes.c_int64),
+                ("plain_end", ctypes.c_int64)]
 
 
 class ArenaDesc(ctypes.Structure):
@@ -88,7 +89,8 @@ SIGNATURES = {
     "zoact_status_str": ([_I32], ctypes.c_char_p),
     "zoact_last_error": ([], ctypes.c_char_p),
     "zoact_gen_z": ([_U64, _U32, _U32, _I64, _I64, _P, _P], _I32),
-    "zoact_project": ([_P, _I32, _I64, _I64, _P, _I32, _P, _P], _I32),
+    "zoact_project_workspace_bytes": ([_I64, _I64, _I32], _SZ),
+    "zoact_project": ([_P, _I32, _I64, _I64, _P, _I32, _P, _P, _SZ, _P], _I32),
     "zoact_rmsnorm_project": ([_P, _P, _I64, _I64, _F, _P, _I32, _P, _P, _P], _I32),
     "zoact_layernorm_project": ([_P, _P, _P, _I64, _I64, _F, _P, _I32, _P, _P, _P], _I32),
     "zoact_linear_fwd_pm": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I32, _I64, _P, _P, _U32,
@@ -189,13 +191,15 @@ class Linear:
     w_scales: torch.Tensor | None = None
     ch: torch.Tensor | None = None      # precomputed bf16(C +/- eps Z): half 0 at ch, half 1 at ch + ch_stride
     ch_stride: int = 0
+    plain: tuple = (0, 0)               # output features [begin, end) not adapted (no coefficient rows)
 
     def desc(self) -> LinearDesc:
         wd = INT4_G128 if self.w.dtype == torch.uint8 else dtype_code(self.w)
         return LinearDesc(wd, self.w.data_ptr(), self.w_scales.data_ptr() if self.w_scales is not None else None,
                           self.bias.data_ptr() if self.bias is not None else None,
                           self.ut.data_ptr() if self.ut is not None else None, self.d_in, self.d_out, self.r,
-                          self.coef_offset, self.ch.data_ptr() if self.ch is not None else None, self.ch_stride)
+                          self.coef_offset, self.ch.data_ptr() if self.ch is not None else None, self.ch_stride,
+                          self.plain[0], self.plain[1])
 
 
 @dataclass
@@ -221,10 +225,17 @@ def gen_z(seed: int, step: int, query: int, e0: int, n: int, out: torch.Tensor, 
     _check(lib().zoact_gen_z(seed, step, query, e0, n, _ptr(out), _stream(stream)))
 
 
-def project(x: torch.Tensor, ut: torch.Tensor, p: torch.Tensor, stream=None):
+def project_workspace_bytes(n_tok: int, d_in: int, r: int) -> int:
+    return int(lib().zoact_project_workspace_bytes(n_tok, d_in, r))
+
+
+def project(x: torch.Tensor, ut: torch.Tensor, p: torch.Tensor, ws: torch.Tensor | None = None, stream=None):
+    """p = x U; with a workspace `ws` (project_workspace_bytes) the depth-split form."""
     d_in = x.shape[-1]
     n_tok = x.numel() // d_in
-    _check(lib().zoact_project(_ptr(x), dtype_code(x), n_tok, d_in, _ptr(ut), ut.shape[0], _ptr(p), _stream(stream)))
+    nb = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().zoact_project(_ptr(x), dtype_code(x), n_tok, d_in, _ptr(ut), ut.shape[0], _ptr(p), _ptr(ws), nb,
+                               _stream(stream)))
 
 
 def rmsnorm_project(x: torch.Tensor, w: torch.Tensor, y: torch.Tensor, eps: float, ut: torch.Tensor, p: torch.Tensor,

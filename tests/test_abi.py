@@ -49,8 +49,12 @@ def test_validation_rejects_before_launch():
     assert b"negative" in L.zoact_last_error()
     assert L.zoact_gen_z(1, 1, 0, 0, 10, None, None) == Z.E_INVALID
     # r out of range for the projection
-    assert L.zoact_project(ctypes.c_void_p(16), Z.BF16, 8, 64, ctypes.c_void_p(16), 0, ctypes.c_void_p(16), None) == Z.E_INVALID
-    assert L.zoact_project(ctypes.c_void_p(16), Z.BF16, 8, 64, ctypes.c_void_p(16), 300, ctypes.c_void_p(16), None) == Z.E_INVALID
+    assert L.zoact_project(ctypes.c_void_p(16), Z.BF16, 8, 64, ctypes.c_void_p(16), 0, ctypes.c_void_p(16), None, 0,
+                           None) == Z.E_INVALID
+    assert L.zoact_project(ctypes.c_void_p(16), Z.BF16, 8, 64, ctypes.c_void_p(16), 300, ctypes.c_void_p(16), None, 0,
+                           None) == Z.E_INVALID
+    assert L.zoact_project(ctypes.c_void_p(16), Z.BF16, 8, 64, ctypes.c_void_p(16), 8, ctypes.c_void_p(16),
+                           ctypes.c_void_p(24), 1 << 20, None) == Z.E_INVALID        # misaligned workspace
     # INT4 layer with d_in not a multiple of 128
     d = Z.LinearDesc(Z.INT4_G128, 16, 16, None, None, 64, 64, 0, 0)
     st = L.zoact_linear_fwd_pm(ctypes.byref(d), None, ctypes.c_void_p(16), Z.BF16, 4, None, None, 0,

@@ -99,6 +99,24 @@ def test_project_bf16(n_tok, d, r):
     assert_bf16_close(host(p), olin.project(x, ut, "bf16"), what="project")
 
 
+@pytest.mark.parametrize("n_tok,d,r", [(1000, 512, 32), (77, 256, 8), (2048, 1024, 64), (33, 128, 1),
+                                       (4100, 4096, 32), (300, 14336, 32), (129, 5120, 64)])
+def test_project_bf16_depth_split(n_tok, d, r):
+    """The workspace form (depth split over workgroups, partials summed in a fixed order by
+    a second pass) against the oracle, and the same bits on a second call."""
+    announce("project bf16 split", n_tok, d, r)
+    x = synth.bf16_round(synth.normal((n_tok, d), 1.0, 1, n_tok + d))
+    ut = synth.bf16_round(synth.normal((r, d), 1.0 / np.sqrt(d), 2, d + r))
+    ws = torch.empty(Z.project_workspace_bytes(n_tok, d, r), dtype=torch.uint8, device=dev())
+    outs = []
+    for _ in range(2):
+        p = torch.empty(n_tok, r, dtype=torch.bfloat16, device=dev())
+        Z.project(t_bf16(x), t_bf16(ut), p, ws)
+        outs.append(host(p))
+    assert_bf16_close(outs[0], olin.project(x, ut, "bf16"), what="project split")
+    np.testing.assert_array_equal(outs[0], outs[1])
+
+
 def test_project_f32():
     announce("project f32")
     x = synth.normal((300, 128), 1.0, 1, 1)
@@ -749,6 +767,60 @@ def test_linear_pm_shared_x_bitwise(T, K, N, r, flags, out_f32, resid):
     if not out_f32 and not resid and flags == 0:
         ref = _oracle_linear(x, w, b, ut, c.reshape(N, r), 0, r, 1e-2, T + N + r, 2)
         assert_bf16_close(gs.reshape(2, T, N), ref, what="shared x vs oracle")
+
+
+@pytest.mark.parametrize("T,K,dq,dk,dv,r,flags", [
+    (1000, 512, 512, 256, 256, 32, 0),            # ragged tokens, k between q and v
+    (300, 256, 256, 512, 256, 64, Z.EPI_RELU),     # k wider than q and v, ReLU
+    (4100, 128, 768, 256, 512, 8, 0),              # ragged last token tile, 204 tiles
+])
+def test_linear_plain_range_equals_two_calls(T, K, dq, dk, dv, r, flags):
+    """q|k|v in one call with k as the plain feature range (no correction, no coefficient
+    rows) gives the same bits as q|v adapted and k plain in two calls."""
+    announce("linear plain range", T, K, dq, dk, dv, r, flags)
+    N = dq + dk + dv
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=T + N + r, bias=True)
+    rows = dq + dv
+    c = synth.normal((rows * r,), 0.02, N + r, 5)
+    arena = Z.Arena(t_f32(c), torch.zeros(c.size, device=dev()), torch.zeros(c.size, device=dev()))
+    pert = Z.Pert(N + r, 3, 0, 1e-2)
+    ch = torch.empty(2 * rows * r, dtype=torch.bfloat16, device=dev())
+    Z.perturb_coeffs(arena, 0, rows * r, pert, ch)
+    xt = t_bf16(x.reshape(2 * T, K))
+    p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev())
+    Z.project(xt, t_bf16(ut), p)
+    fused = Z.Linear(t_bf16(w), K, N, r, t_bf16(ut), 0, t_bf16(b), ch=ch, ch_stride=rows * r, plain=(dq, dq + dk))
+    yf = torch.full((2 * T, N), float("nan"), dtype=torch.bfloat16, device=dev())
+    Z.linear_fwd_pm(fused, arena, xt, T, p, yf, pert, flags=flags)
+    sel = np.r_[0:dq, dq + dk:N]
+    qv = Z.Linear(t_bf16(np.ascontiguousarray(w[sel])), K, rows, r, t_bf16(ut), 0, t_bf16(np.ascontiguousarray(b[sel])),
+                  ch=ch, ch_stride=rows * r)
+    kk = Z.Linear(t_bf16(np.ascontiguousarray(w[dq:dq + dk])), K, dk, 0, None, 0,
+                  t_bf16(np.ascontiguousarray(b[dq:dq + dk])))
+    yqv = torch.empty(2 * T, rows, dtype=torch.bfloat16, device=dev())
+    yk = torch.empty(2 * T, dk, dtype=torch.bfloat16, device=dev())
+    Z.linear_fwd_pm(qv, arena, xt, T, p, yqv, pert, flags=flags)
+    Z.linear_fwd_pm(kk, None, xt, T, None, yk, pert, flags=flags)
+    want = torch.cat([yqv[:, :dq], yk, yqv[:, dq:]], dim=1)
+    assert torch.equal(yf.view(torch.int16), want.view(torch.int16)), "fused q|k|v differs from the two calls"
+
+
+def test_linear_plain_range_rejected_where_not_covered():
+    """A plain range off the 256-feature tiles, or with fp32 activations: an error, not a
+    silent fallback."""
+    T, K, N, r = 64, 128, 768, 8
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=7, bias=False)
+    c = synth.normal((512 * r,), 0.02, 7, 5)
+    arena = Z.Arena(t_f32(c), torch.zeros(c.size, device=dev()), torch.zeros(c.size, device=dev()))
+    pert = Z.Pert(7, 1, 0, 1e-2)
+    ch = torch.empty(2 * 512 * r, dtype=torch.bfloat16, device=dev())
+    Z.perturb_coeffs(arena, 0, 512 * r, pert, ch)
+    xt = t_bf16(x.reshape(2 * T, K))
+    p = torch.zeros(2 * T, r, dtype=torch.bfloat16, device=dev())
+    y = torch.empty(2 * T, N, dtype=torch.bfloat16, device=dev())
+    bad = Z.Linear(t_bf16(w), K, N, r, t_bf16(ut), 0, None, ch=ch, ch_stride=512 * r, plain=(128, 384))
+    with pytest.raises(Z.ZoactError):
+        Z.linear_fwd_pm(bad, arena, xt, T, p, y, pert)
 
 
 def test_linear_mse_shared_x_equals_stacked():
