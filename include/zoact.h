@@ -133,6 +133,16 @@ typedef struct {
                            weights, ch given, both bounds multiples of 256 and no
                            ZOACT_SHARED_X (else ZOACT_E_UNSUPPORTED or INVALID)       */
   int64_t plain_end;
+  void* ws;             /* optional workspace (16-byte aligned) of ws_bytes >=
+                           zoact_linear_workspace_bytes(): where the tiles leave a last
+                           round of the persistent grid at most half full (for example
+                           640 tiles on 256 compute units), BF16 plain or ReLU outputs
+                           without ZOACT_SHARED_X, the depth of that round's tiles is
+                           split over two workgroups and their halves summed (first +
+                           second) before the epilogue: other summation order, same
+                           bits in both halves of the pair.  NULL: not used.  Calls
+                           that overlap on one workspace race.                        */
+  size_t ws_bytes;
 } zoact_linear;
 
 /* The coefficient arena and its Adam moments (updated in place by zoact_step). */
@@ -261,6 +271,10 @@ zoact_status zoact_linear_fwd_pair(const zoact_linear* L, const zoact_arena* A, 
                                    int32_t x_dtype, int64_t T, const void* p, const void* residual,
                                    uint32_t flags, const zoact_pert_pair* pp, void* y, int32_t y_dtype,
                                    zoact_stream stream);
+
+/* Bytes of the optional zoact_linear workspace on the current device (one 256 KB tile
+ * slot per compute unit). */
+size_t zoact_linear_workspace_bytes(void);
 
 /* INT4 weights to bf16: out[n][k] = bf16(q[n][k] * s[n][k / 128]), the dequantised weight
  * the INT4 GEMM forms in registers (same packing as zoact_linear.w).  At large token counts

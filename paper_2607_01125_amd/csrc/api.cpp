@@ -98,6 +98,11 @@ zoact_status zoact_project(const void* x, int32_t dtype, int64_t n_tok, int64_t 
   return hip_status(zoact::launch_project(x, dtype, n_tok, d_in, ut, r, p, st(stream)), "project");
 }
 
+size_t zoact_linear_workspace_bytes(void) {
+  const int n = zoact::cu_count();
+  return n > 0 ? (size_t)n * 256 * 1024 : 0;
+}
+
 zoact_status zoact_dequant_int4(const void* w, const void* w_scales, int64_t d_out, int64_t d_in, void* out,
                                 zoact_stream stream) {
   CHECK(w && w_scales && out, "dequant_int4: NULL pointer");
@@ -141,6 +146,7 @@ static zoact_status validate_linear(const zoact_linear* L, const zoact_arena* A,
     CHECK(float_type(A->c_dtype), "linear_fwd_pm: arena dtype must be F32 or BF16");
   }
   if (flags & ZOACT_EPI_SWIGLU) CHECK(L->d_out % 32 == 0, "linear_fwd_pm: SWIGLU needs d_out %% 32 == 0");
+  CHECK(L->ws == nullptr || aligned16(L->ws), "linear_fwd_pm: ws must be 16-byte aligned");
   if (L->ch != nullptr) {
     CHECK(x_dtype == ZOACT_BF16 && L->r > 0, "linear_fwd_pm: precomputed coefficients need BF16 activations and r > 0");
     CHECK(L->ch_half_stride >= rows * (int64_t)L->r && (reinterpret_cast<uintptr_t>(L->ch) & 1) == 0,

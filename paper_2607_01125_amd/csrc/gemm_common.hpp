@@ -38,6 +38,10 @@ struct GemmArgs {
   int32_t xnblk;         // EPI_XENT: ceil(N / 128)
   int64_t plain_begin;   // output features [plain_begin, plain_end): no correction, no coefficient rows
   int64_t plain_end;
+  float* tail_ws;        // split tail (64-deep schedule): the half tiles' fp32 accumulators
+  int64_t tail_ws_bytes;
+  int32_t tail_first;    // first virtual tile that is half a tile (= the tile count: none)
+  int32_t tail_cols;     // feature tiles (the last ones, both halves' token tiles) of the split tail
 };
 
 // Internal epilogue selector (not a public flag): the tile's squared errors against tgt

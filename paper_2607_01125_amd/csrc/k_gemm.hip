@@ -699,6 +699,8 @@ static GemmArgs bf16_args(const zoact_linear& L, const zoact_arena* A, const voi
     a.plain_begin = L.plain_begin;
     a.plain_end = L.plain_end;
   }
+  a.tail_ws = static_cast<float*>(L.ws);
+  a.tail_ws_bytes = L.ws ? (int64_t)L.ws_bytes : 0;
   return a;
 }
 

@@ -53,6 +53,28 @@ __device__ __forceinline__ int dma8_lane_off(int64_t ld) {
 
 __device__ __forceinline__ int mod5(int v) { return v >= 5 ? v - 5 : v; }
 
+// Split tail: with R = ntiles mod grid tiles left for a last, partly idle round (R at most
+// half the grid), those R tiles are each computed as two halves of the depth by two
+// workgroups (virtual tiles tail_first .. tail_first + 2R - 1, tail_first = ntiles - R), so
+// the last round takes half the time.  The R tiles are the last tail_cols feature tiles
+// with every token tile of both halves (R must be a multiple of the token tiles), so a
+// tile and its twin in the other half are computed the same way: the two halves of the
+// ± pair keep identical arithmetic.  A half tile stores its fp32 accumulators (in the
+// accumulator layout, lane-major: coalesced) to tail_ws; a second kernel adds the two
+// halves in the order first + second and runs the same epilogue.
+struct VTile {
+  int tile, k0, nst, kh;   // tile index, first 64-deep stage, stages, depth half (-1: whole)
+};
+__device__ __forceinline__ VTile vtile(const GemmArgs& a, int v, int NS) {
+  if (v < a.tail_first) return VTile{v, 0, NS, -1};
+  const int u = v - a.tail_first, h0 = (NS + 1) >> 1;
+  return (u & 1) ? VTile{a.tail_first + (u >> 1), h0, NS - h0, 1} : VTile{a.tail_first + (u >> 1), 0, h0, 0};
+}
+// fp32 accumulators of half tile u (virtual index - tail_first): [u][wave][i * 8 + j][lane] x float4
+__device__ __forceinline__ floatx4* tail_slot(const GemmArgs& a, int u, int wave) {
+  return reinterpret_cast<floatx4*>(a.tail_ws) + ((int64_t)u * 4 + wave) * 64 * 64;
+}
+
 // Token tile, feature tile and half of virtual tile v of ntiles (XCD-contiguous runs,
 // grouped token-major order: a workgroup's tiles v, v + grid, ... stay on its XCD when the
 // grid is a multiple of 8).
@@ -61,10 +83,21 @@ struct TileGeom {
   int64_t m0, n0;
 };
 __device__ __forceinline__ TileGeom tile_geom(const GemmArgs& a, int ntiles, int v, bool shared) {
+  const int tiles_m = shared ? a.tiles_m_half : 2 * a.tiles_m_half;   // (shared input: one half's tokens)
+  if (v >= a.tail_first) {   // split tail: feature tile columns past tiles_n - tail_cols
+    const int t = v - a.tail_first;
+    TileGeom g;
+    g.tm = t % tiles_m;
+    g.tn = a.tiles_n - a.tail_cols + t / tiles_m;
+    g.half = shared ? 0 : g.tm / a.tiles_m_half;
+    g.m0 = (int64_t)(g.tm % a.tiles_m_half) * 256;
+    g.n0 = (int64_t)g.tn * 256;
+    return g;
+  }
+  ntiles = a.tail_first;     // the tiles before the tail: tiles_n - tail_cols feature columns
   int lin = v;
   if ((ntiles & 7) == 0) lin = (v & 7) * (ntiles >> 3) + (v >> 3);
-  const int tiles_m = shared ? a.tiles_m_half : 2 * a.tiles_m_half;   // (shared input: one half's tokens)
-  const int per_group = 4 * a.tiles_n;
+  const int per_group = 4 * (a.tiles_n - a.tail_cols);
   const int first_m = (lin / per_group) * 4;
   const int gsz = min(4, tiles_m - first_m);
   TileGeom g;
@@ -82,7 +115,7 @@ __device__ __forceinline__ TileGeom tile_geom(const GemmArgs& a, int ntiles, int
 // fragments, so the next tile starts without a prologue while this one finishes (rank
 // correction, epilogue straight from the accumulators, no LDS).
 template <int EPI, bool OUT_F32, bool SHARED>
-__global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles) {
+__global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles, int nvirt) {
   constexpr bool PERM = epi_perm(EPI);
   extern __shared__ __align__(16) uint16_t lds[];
   char* const lb = reinterpret_cast<char*>(lds);
@@ -163,19 +196,23 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
   };
 
   int v = blockIdx.x;
-  TileGeom g = tile_geom(a, ntiles, v, SHARED);
+  VTile vt = vtile(a, v, NS);
+  TileGeom g = tile_geom(a, ntiles, vt.tile, SHARED);
   __amdgpu_buffer_rsrc_t xrs = buffer_rsrc(a.x + (int64_t)g.half * a.T * a.K, xbytes);
 
   // ---- prologue of the first tile: stages 0 and 1 in flight (slots 0..3), stage 0
   // landed in every wave's rows (the barrier)
+  {
+    const int64_t kb = (int64_t)vt.k0 * 64;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) dma(wrs, src_base(g.n0, 0), 0, i);
+    for (int i = 0; i < 8; ++i) dma(wrs, src_base(g.n0, kb), 0, i);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) dma(xrs, src_base(g.m0, 0), 1, i);
+    for (int i = 0; i < 8; ++i) dma(xrs, src_base(g.m0, kb), 1, i);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) dma(wrs, src_base(g.n0, 64), 2, i);
+    for (int i = 0; i < 8; ++i) dma(wrs, src_base(g.n0, kb + 64), 2, i);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) dma(xrs, src_base(g.m0, 64), 3, i);
+    for (int i = 0; i < 8; ++i) dma(xrs, src_base(g.m0, kb + 64), 3, i);
+  }
   __builtin_amdgcn_s_waitcnt(WAIT_VM16);
   barrier();
 
@@ -201,8 +238,9 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
     // iterations), so the compiler places no LDS waits inside it
     __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);
     const int vn = v + (int)gridDim.x;
-    const bool has_next = vn < ntiles;
-    const TileGeom gn = tile_geom(a, ntiles, has_next ? vn : v, SHARED);
+    const bool has_next = vn < nvirt;
+    const VTile vtn = vtile(a, has_next ? vn : v, NS);
+    const TileGeom gn = tile_geom(a, ntiles, vtn.tile, SHARED);
     const __amdgpu_buffer_rsrc_t xrs_n = buffer_rsrc(a.x + (int64_t)gn.half * a.T * a.K, xbytes);
 
     // ---- main loop: one stage (two sub-steps) per iteration.  Stages S + 2 past this
@@ -210,11 +248,12 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
     // rows past the end (or zeros) into slots nobody reads again.
     // (The second sub-step sits under a test that always holds: written this way the
     // register allocator keeps every accumulator in place across the loop.)
-    const int nsub = 2 * NS;
+    const int nst = vt.nst;
+    const int nsub = 2 * nst;
     for (int j = 0; j < nsub; j += 2) {
       const int st = j >> 1;
-      const bool nx = has_next && st + 2 >= NS;
-      const int64_t kd = (int64_t)(nx ? st + 2 - NS : st + 2) * 64;
+      const bool nx = has_next && st + 2 >= nst;
+      const int64_t kd = (int64_t)(nx ? vtn.k0 + st + 2 - nst : vt.k0 + st + 2) * 64;
       const int wb = src_base(nx ? gn.n0 : g.n0, kd), xb = src_base(nx ? gn.m0 : g.m0, kd);
       const __amdgpu_buffer_rsrc_t xr = nx ? xrs_n : xrs;
       const int sw1 = mod5(s5 + 2), sx1 = mod5(s5 + 3), sw2 = mod5(s5 + 4);
@@ -256,7 +295,7 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
     // (a tile inside the plain feature range has none; past it, C_h rows are shifted back
     // by the range's width)
     const int64_t plen = a.plain_end - a.plain_begin;
-    if (a.r > 0 && !(g.n0 >= a.plain_begin && g.n0 < a.plain_end)) {
+    if (a.r > 0 && vt.kh <= 0 && !(g.n0 >= a.plain_begin && g.n0 < a.plain_end)) {
       const int kts = (a.r + 31) >> 5;
       const int64_t cn0 = g.n0 >= a.plain_end ? g.n0 - plen : g.n0;
       const __amdgpu_buffer_rsrc_t prs = buffer_rsrc(a.p + (int64_t)p_half * a.T * a.r, (uint32_t)(a.T * a.r * 2));
@@ -308,9 +347,24 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
       }
     }
 
-    epilogue_regs<EPI, OUT_F32>(a, acc, tq, wave, lane, g.m0, g.n0, SHARED ? 1 : g.half, g.tm, g.tn);
+    if (vt.kh >= 0) {
+      // half a tile: its accumulators to the split tail's slot, the epilogue runs later
+      floatx4* slot = tail_slot(a, v - a.tail_first, wave);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          floatx4 t;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) t[e] = acc_read(acc[i][j][e]);
+          slot[(i * 8 + j) * 64 + lane] = t;
+        }
+    } else {
+      epilogue_regs<EPI, OUT_F32>(a, acc, tq, wave, lane, g.m0, g.n0, SHARED ? 1 : g.half, g.tm, g.tn);
+    }
     if (!has_next) break;
     v = vn;
+    vt = vtn;
     g = gn;
     xrs = xrs_n;
   }
@@ -318,8 +372,28 @@ __global__ void __launch_bounds__(NT, 1) gemm_4w64_kernel(GemmArgs a, int ntiles
   __builtin_amdgcn_s_waitcnt(WAIT_VM0);
 }
 
+// The split tail's R tiles: workgroup t adds the two halves of tile tail_first + t (first +
+// second, the same order for every run) and runs the tile's epilogue on the sum.
+template <int EPI, bool OUT_F32>
+__global__ void __launch_bounds__(NT, 1) tail_combine_kernel(GemmArgs a, int ntiles) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x;
+  const TileGeom g = tile_geom(a, ntiles, a.tail_first + t, false);
+  const floatx4* h0 = tail_slot(a, 2 * t, wave);
+  const floatx4* h1 = tail_slot(a, 2 * t + 1, wave);
+  floatx4 acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = h0[(i * 8 + j) * 64 + lane] + h1[(i * 8 + j) * 64 + lane];
+  uint4 tq[8][4];
+  epilogue_regs<EPI, OUT_F32>(a, acc, tq, wave, lane, g.m0, g.n0, g.half, g.tm, g.tn);
+}
+
 template <int EPI, bool OUT_F32, bool SHARED>
-hipError_t launch_4w64(const GemmArgs& a, hipStream_t s) {
+hipError_t launch_4w64(const GemmArgs& a_in, hipStream_t s) {
+  GemmArgs a = a_in;
   static bool attr_set = false;  // benign race: every thread sets the same value
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_4w64_kernel<EPI, OUT_F32, SHARED>),
@@ -331,7 +405,20 @@ hipError_t launch_4w64(const GemmArgs& a, hipStream_t s) {
   const int ncu = cu_count();
   if (ncu <= 0) return hipErrorInvalidDevice;
   const unsigned grid = (unsigned)(ntiles < ncu ? ntiles : ncu);
-  gemm_4w64_kernel<EPI, OUT_F32, SHARED><<<dim3(grid), dim3(NT), LDS_BYTES, s>>>(a, ntiles);
+  // the split tail where it applies: plain or ReLU outputs, a last round at most half
+  // full after at least one full one and made of whole feature-tile columns, at least 4
+  // stages (2 per half), a workspace
+  const int rest = ntiles % (int)grid, tiles_m = 2 * a.tiles_m_half;
+  const bool split = (EPI == 0 || EPI == ZOACT_EPI_RELU) && !SHARED && ntiles > (int)grid && rest > 0 &&
+                     2 * rest <= (int)grid && rest % tiles_m == 0 && (a.K >> 6) >= 4 && a.tail_ws != nullptr &&
+                     a.tail_ws_bytes >= (int64_t)rest * 2 * 4 * 64 * 64 * 16;
+  a.tail_first = split ? ntiles - rest : ntiles;
+  a.tail_cols = split ? rest / tiles_m : 0;
+  const int nvirt = split ? ntiles + rest : ntiles;
+  gemm_4w64_kernel<EPI, OUT_F32, SHARED><<<dim3(grid), dim3(NT), LDS_BYTES, s>>>(a, ntiles, nvirt);
+  if constexpr ((EPI == 0 || EPI == ZOACT_EPI_RELU) && !SHARED) {
+    if (split) tail_combine_kernel<EPI, OUT_F32><<<dim3((unsigned)rest), dim3(NT), 0, s>>>(a, ntiles);
+  }
   return hipGetLastError();
 }
 

@@ -132,6 +132,15 @@ class Decoder:
         self._adapted_sites = {(b.layer, b.site) for b in self.blocks}
         self.r = s.rank
         self._pack(W, int4_dequant)
+        # the fused GEMM's workspace for splitting a partly idle last round of tiles (bf16 modes)
+        if self.act == torch.bfloat16:
+            nb = Z.linear_workspace_bytes()
+            if nb:
+                lin_ws = torch.empty(nb, dtype=torch.uint8, device=self.dev)
+                for P in self.layers:
+                    for v in P.values():
+                        if isinstance(v, tuple):
+                            v[0].ws = lin_ws
         self.ut = {}                      # (layer, site) -> U^T [r][d_in] (activation dtype)
         self.arena = Z.Arena(torch.zeros(self.k, dtype=torch.bfloat16 if self.c_bf16 else torch.float32,
                                          device=self.dev),

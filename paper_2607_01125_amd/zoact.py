@@ -49,7 +49,7 @@ class LinearDesc(ctypes.Structure):
                 ("bias", ctypes.c_void_p), ("ut", ctypes.c_void_p), ("d_in", ctypes.c_int64),
                 ("d_out", ctypes.c_int64), ("r", ctypes.c_int32), ("coef_offset", ctypes.c_int64),
                 ("ch", ctypes.c_void_p), ("ch_half_stride", ctypes.c_int64), ("plain_begin", ctypes.c_int64),
-                ("plain_end", ctypes.c_int64)]
+                ("plain_end", ctypes.c_int64), ("ws", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t)]
 
 
 class ArenaDesc(ctypes.Structure):
@@ -96,6 +96,7 @@ SIGNATURES = {
     "zoact_linear_fwd_pm": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I32, _I64, _P, _P, _U32,
                              ctypes.POINTER(Pert), _P, _I32, _P], _I32),
     "zoact_perturb_coeffs": ([ctypes.POINTER(ArenaDesc), _I64, _I64, ctypes.POINTER(Pert), _P, _P], _I32),
+    "zoact_linear_workspace_bytes": ([], _SZ),
     "zoact_dequant_int4": ([_P, _P, _I64, _I64, _P, _P], _I32),
     "zoact_linear_fwd_pair": ([ctypes.POINTER(LinearDesc), ctypes.POINTER(ArenaDesc), _P, _I32, _I64, _P, _P, _U32,
                                ctypes.POINTER(PertPair), _P, _I32, _P], _I32),
@@ -192,6 +193,7 @@ class Linear:
     ch: torch.Tensor | None = None      # precomputed bf16(C +/- eps Z): half 0 at ch, half 1 at ch + ch_stride
     ch_stride: int = 0
     plain: tuple = (0, 0)               # output features [begin, end) not adapted (no coefficient rows)
+    ws: torch.Tensor | None = None      # optional workspace (linear_workspace_bytes)
 
     def desc(self) -> LinearDesc:
         wd = INT4_G128 if self.w.dtype == torch.uint8 else dtype_code(self.w)
@@ -199,7 +201,8 @@ class Linear:
                           self.bias.data_ptr() if self.bias is not None else None,
                           self.ut.data_ptr() if self.ut is not None else None, self.d_in, self.d_out, self.r,
                           self.coef_offset, self.ch.data_ptr() if self.ch is not None else None, self.ch_stride,
-                          self.plain[0], self.plain[1])
+                          self.plain[0], self.plain[1], self.ws.data_ptr() if self.ws is not None else None,
+                          self.ws.numel() * self.ws.element_size() if self.ws is not None else 0)
 
 
 @dataclass
@@ -223,6 +226,10 @@ def version() -> str:
 
 def gen_z(seed: int, step: int, query: int, e0: int, n: int, out: torch.Tensor, stream=None):
     _check(lib().zoact_gen_z(seed, step, query, e0, n, _ptr(out), _stream(stream)))
+
+
+def linear_workspace_bytes() -> int:
+    return int(lib().zoact_linear_workspace_bytes())
 
 
 def project_workspace_bytes(n_tok: int, d_in: int, r: int) -> int:

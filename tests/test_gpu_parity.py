@@ -805,6 +805,51 @@ def test_linear_plain_range_equals_two_calls(T, K, dq, dk, dv, r, flags):
     assert torch.equal(yf.view(torch.int16), want.view(torch.int16)), "fused q|k|v differs from the two calls"
 
 
+@pytest.mark.parametrize("flags,resid,bias", [(0, True, True), (Z.EPI_RELU, False, False)])
+def test_linear_split_tail(flags, resid, bias):
+    """640 tiles (4096 tokens per half, 5120 features) on a 256-CU grid leave a last round
+    of 128 tiles; with a workspace their depth is split over two workgroups.  Against the
+    same call without the workspace (the same products, other summation order) and the
+    oracle on sampled rows; with equal halves and eps = 0 both halves stay bitwise equal."""
+    T, K, N, r = 4096, 512, 5120, 32
+    announce("linear split tail", T, K, N, r, flags, resid, bias)
+    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=11, bias=bias)
+    x[1] = x[0]
+    c = synth.normal((N * r,), 0.02, 11, 5)
+    arena = Z.Arena(t_f32(c), torch.zeros(c.size, device=dev()), torch.zeros(c.size, device=dev()))
+    pert = Z.Pert(11, 2, 0, 0.0)
+    ch = torch.empty(2 * N * r, dtype=torch.bfloat16, device=dev())
+    Z.perturb_coeffs(arena, 0, N * r, pert, ch)
+    xt = t_bf16(x.reshape(2 * T, K))
+    p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev())
+    Z.project(xt, t_bf16(ut), p)
+    res_np = synth.bf16_round(synth.normal((T, N), 0.5, 11, 7)) if resid else None
+    res = t_bf16(np.concatenate([res_np, res_np])) if resid else None
+    ws = torch.empty(Z.linear_workspace_bytes(), dtype=torch.uint8, device=dev())
+    outs = []
+    for use_ws in (True, False):
+        lay = Z.Linear(t_bf16(w), K, N, r, t_bf16(ut), 0, t_bf16(b) if bias else None, ch=ch, ch_stride=N * r,
+                       ws=ws if use_ws else None)
+        y = torch.full((2 * T, N), float("nan"), dtype=torch.bfloat16, device=dev())
+        Z.linear_fwd_pm(lay, arena, xt, T, p, y, pert, residual=res, flags=flags)
+        outs.append(host(y))
+    ys, yn = outs
+    np.testing.assert_array_equal(ys[:T], ys[T:])   # the pair's halves
+    assert_bf16_close(ys, yn, what="split tail vs whole depth")
+    rows = np.r_[0:8, 2040:2048, T - 8:T]
+    xr = x[0][rows].astype(np.float64)
+    pr = synth.bf16_round((xr @ ut.astype(np.float64).T).astype(np.float32)).astype(np.float64)   # P as stored
+    cm = synth.bf16_round(c.astype(np.float32)).reshape(N, r).astype(np.float64)                # bf16(C + 0 Z)
+    want = xr @ w.astype(np.float64).T + pr @ cm.T
+    if bias:
+        want = want + b.astype(np.float64)
+    if resid:
+        want = want + res_np[rows].astype(np.float64)
+    if flags == Z.EPI_RELU:
+        want = np.maximum(want, 0.0)
+    assert_bf16_close(ys[rows], want, what="split tail vs oracle")
+
+
 def test_linear_plain_range_rejected_where_not_covered():
     """A plain range off the 256-feature tiles, or with fp32 activations: an error, not a
     silent fallback."""
