@@ -38,6 +38,32 @@ def test_gen_z_bit_exact(seed, step, query, e0, n):
     np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
 
 
+# 10^8 indices in chunks of 4M: contiguous runs from 0 (the Llama arena and beyond), runs past
+# 2^34 (the counter's high word), other seeds, steps and queries; the oracle's chunks are
+# computed in worker processes (spawned: they load no GPU runtime)
+_Z_CHUNK = 1 << 22
+_Z_RUNS = ([(7, 11, 0, i * _Z_CHUNK) for i in range(12)]
+           + [(2**64 - 1, 2**32 - 2, 5, (1 << 34) - 3 * _Z_CHUNK // 2 + i * _Z_CHUNK) for i in range(6)]
+           + [(1234567, 1 + i, i % 3, (i + 1) * 123_456_789) for i in range(6)]
+           + [(0, 0, 0, 44_040_192 - _Z_CHUNK + 8_000_000 - 4_000_000)])   # 25 x 4M >= 10^8
+
+
+def test_gen_z_bit_exact_1e8():
+    import multiprocessing as mp
+    from concurrent.futures import ProcessPoolExecutor
+    assert len(_Z_RUNS) * _Z_CHUNK >= 10**8
+    announce("gen_z 1e8", len(_Z_RUNS), _Z_CHUNK)
+    out = torch.empty(_Z_CHUNK, dtype=torch.float32, device=dev())
+    cols = list(zip(*_Z_RUNS))
+    with ProcessPoolExecutor(max_workers=8, mp_context=mp.get_context("spawn")) as ex:
+        wants = ex.map(orng.gauss_range, *cols, [_Z_CHUNK] * len(_Z_RUNS))
+        for (seed, step, query, e0), want in zip(_Z_RUNS, wants):
+            Z.gen_z(seed, step, query, e0, _Z_CHUNK, out)
+            got = out.cpu().numpy()
+            bad = np.flatnonzero(got.view(np.uint32) != want.view(np.uint32))
+            assert bad.size == 0, f"Z differs at {bad.size} indices from {e0 + bad[0]} (seed {seed}, step {step})"
+
+
 # ------------------------------------------------------------------ Adam / SGD
 @pytest.mark.parametrize("c_bf16", [False, True])
 @pytest.mark.parametrize("k", [4, 100_003, 1 << 20])
