@@ -172,13 +172,15 @@ class Decoder:
         # rows from L2 or memory between the statistics and the projection, and the
         # separate norm already runs near the memory rate)
         self.fuse_norm_project = mode != "fp32" and self.r <= 128 and self.d in NORM_PROJECT_WIDTHS
-        # INT4 layers: dequantised once per forward into one bf16 buffer (the largest layer's
-        # size) and run on the bf16 schedule; False keeps the in-register INT4 GEMM
+        # INT4 layers: True dequantises each layer once per forward into one bf16 buffer (the
+        # largest layer's size, allocated on first use) and runs the bf16 schedule; False
+        # keeps the INT4 GEMM that converts the packed weights in LDS.  The first is faster
+        # at every batch size measured on MI355X (Llama-3-8B shape, 256 to 4096 tokens per
+        # half: 24.8 vs 25.6 ms to 97.8 vs 109.3 ms per step): the INT4 GEMM converts each
+        # weight once per 256-token tile, the pass once per forward, and the GEMM then reads
+        # the bf16 copy mostly from the last-level cache.
+        self.int4_dequant = bool(int4_dequant)
         self._wdq = None
-        if mode == "int4" and int4_dequant:
-            n = max(lin.d_out * lin.d_in for P in self.layers for lin, _ in
-                    (v for k, v in P.items() if isinstance(v, tuple)) if lin.w.dtype == torch.uint8)
-            self._wdq = torch.empty(n, dtype=torch.bfloat16, device=self.dev)
 
     # ---------------------------------------------------------------- weights
     def _t(self, a, dtype=None):
@@ -199,14 +201,20 @@ class Decoder:
             return interleave_gate_up(*ws), None
         return torch.cat(ws).contiguous(), None
 
+    def _int4_dq(self, T: int) -> bool:
+        """Whether a forward over T tokens per half runs its INT4 layers dequantised."""
+        return self.mode == "int4" and self.int4_dequant
+
     def _pack(self, W, int4_dequant=True):
         s, d, dkv, ff = self.s, self.d, self.dkv, self.s.d_ff
         ad = set(s.adapted)
         # q and v adapted, k not (OPT): one q|k|v launch with k as its plain feature range
-        # where the 64-deep schedule covers it (bf16 schedule, precomputed C +/- eps Z, range
-        # bounds on 256-feature tiles); else q|v and k as two launches
+        # where the 64-deep schedules cover it (precomputed C +/- eps Z, range bounds on
+        # 256-feature tiles; INT4 weights in whole scale groups); else q|v and k as two
+        # launches
         plain_k = ({"q", "v"} <= ad and "k" not in ad and self.act == torch.bfloat16
-                   and (self.mode == "bf16" or int4_dequant) and d % 256 == 0 and dkv % 256 == 0)
+                   and (self.mode == "bf16" or int4_dequant is True or (d % 128 == 0 and d >= 256))
+                   and d % 256 == 0 and dkv % 256 == 0)
         self.layers = []
         for l in range(s.n_layers):
             L = W[l]
@@ -316,7 +324,12 @@ class Decoder:
     def _apply(self, lin_blk, x, T, y, pert, site_ut, residual=None, flags=0, adapt=True):
         lin, blk = lin_blk
         B = self._cur
-        if self._wdq is not None and lin.w.dtype == torch.uint8:
+        if lin.w.dtype == torch.uint8 and self._int4_dq(T):
+            n = lin.d_out * lin.d_in
+            if self._wdq is None or self._wdq.numel() < n:
+                n = max(n, max(l.d_out * l.d_in for P in self.layers for l, _ in
+                               (v for v in P.values() if isinstance(v, tuple)) if l.w.dtype == torch.uint8))
+                self._wdq = torch.empty(n, dtype=torch.bfloat16, device=self.dev)
             wdq = self._wdq[:lin.d_out * lin.d_in].view(lin.d_out, lin.d_in)
             Z.dequant_int4(lin.w, lin.w_scales, wdq)
             lin = dataclasses.replace(lin, w=wdq, w_scales=None)
@@ -338,13 +351,13 @@ class Decoder:
         if hook:
             hook("post", lin, T, flags)
 
-    def _shared_ok(self, lin_blk, site_ut) -> bool:
-        """Whether the shared-input form covers this projection: bf16 weights (or INT4 run on
-        its dequantised copy), the perturbed coefficients precomputed, 8 <= r <= 32 with
-        r % 8 == 0, depth a multiple of 64, no SwiGLU."""
+    def _shared_ok(self, lin_blk, site_ut, T) -> bool:
+        """Whether the shared-input form covers this projection over T tokens per half: bf16
+        weights (or INT4 run on its dequantised copy), the perturbed coefficients
+        precomputed, 8 <= r <= 32 with r % 8 == 0, depth a multiple of 64, no SwiGLU."""
         lin, blk = lin_blk
         return (self.shared_first and self.act == torch.bfloat16 and blk is not None and site_ut is not None
-                and self._ch is not None and (lin.w.dtype == torch.bfloat16 or self._wdq is not None)
+                and self._ch is not None and (lin.w.dtype == torch.bfloat16 or self._int4_dq(T))
                 and 8 <= self.r <= 32 and self.r % 8 == 0 and lin.d_in % 64 == 0 and lin.d_in >= 128
                 and lin.plain[0] == lin.plain[1])
 
@@ -385,7 +398,7 @@ class Decoder:
             # on one half and the fused q|k|v forms x W^T once (the same bits as stacked)
             qkv = B["qkv"]
             shared = (l == 0 and adapt and not distinct_halves and "qkv" in P
-                      and self._shared_ok(P["qkv"], self.ut.get((0, "attn"))))
+                      and self._shared_ok(P["qkv"], self.ut.get((0, "attn")), T))
             if shared:
                 a1 = B["a"][:T]
                 ut = self._norm_site(l, "attn", h[:T], P["n1"], P.get("n1b"), a1, adapt, calibrate)

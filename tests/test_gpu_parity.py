@@ -345,9 +345,9 @@ def test_linear_pm_int4(c_bf16):
     (64, 4096, 256, 16, 2, True),      # ReLU epilogue, 32 groups per row
 ])
 def test_linear_pm_int4_precomputed(T, K, N, r, flags, c_bf16):
-    """INT4 weights with the precomputed C +/- eps Z (the four-wave INT4 schedule): against
-    the oracle on the dequantised weights, and bitwise against the same layer in bf16
-    holding those dequantised weights."""
+    """INT4 weights with the precomputed C +/- eps Z (the 64-deep schedule converting the
+    packed weights in LDS): against the oracle on the dequantised weights, and bitwise
+    against the same layer in bf16 holding those dequantised weights."""
     announce("linear_pm int4 precomputed", T, K, N, r, flags, c_bf16)
     x, w, b, ut, packed, scales = _layer_inputs(T, K, N, r, seed=K + N, bias=True, int4=True)
     c = synth.normal((N * r,), 0.02, 4, 5)
@@ -360,6 +360,39 @@ def test_linear_pm_int4_precomputed(T, K, N, r, flags, c_bf16):
     np.testing.assert_array_equal(got, same)
     ref = _oracle_linear(x, wq, b, ut, c.reshape(N, r), 0, r, 1e-3, 9, 4, flags=flags)
     assert_bf16_close(got, ref, what="int4 precomputed")
+
+
+@pytest.mark.parametrize("T,K,N,r,flags,out_f32", [
+    (2050, 256, 4112, 32, 0, False),              # 306 tiles, four stages per tile
+    (4100, 384, 4112, 8, Z.EPI_RELU, False),      # 578 tiles, ragged tokens and features, 3 groups
+    (2050, 256, 4128, 16, Z.EPI_SWIGLU, False),   # last feature tile: one gate|up group
+    (2050, 512, 4112, 0, 0, True),                # plain layer, fp32 out
+])
+def test_linear_pm_int4_persistent_tiles(T, K, N, r, flags, out_f32):
+    """INT4 weights on more 256 x 256 tiles than the GPU has CUs: the packed-weight ring,
+    the conversion into LDS and the x ring run from one tile into the next.  Bitwise equal
+    to the bf16 layer holding the dequantised weights, and against the oracle."""
+    announce("linear_pm int4 persistent", T, K, N, r, flags, out_f32)
+    x, w, b, ut, packed, scales = _layer_inputs(T, K, N, max(r, 1), seed=T + K + N + 1, int4=True)
+    if r == 0:
+        ut = None
+    nout = N // 2 if flags & Z.EPI_SWIGLU else N
+    resid = None if out_f32 else synth.bf16_round(synth.normal((2, T, nout), 0.5, 13, T))
+    c = synth.normal((N * max(r, 1),), 0.02, 13, 1)
+    eps, seed, step = 1e-2, 19, 3
+    wq = olin.dequant_int4(packed, scales).astype(np.float32)
+    got = _run_gpu_linear(x, w, b, ut, c, 0, r, eps, seed, step, T, K, N, flags=flags, resid=resid,
+                          out_f32=out_f32, precomputed=r > 0, packed=packed, scales=scales, c_bf16=True)
+    same = _run_gpu_linear(x, wq, b, ut, c, 0, r, eps, seed, step, T, K, N, flags=flags, resid=resid,
+                           out_f32=out_f32, precomputed=r > 0, c_bf16=True)
+    np.testing.assert_array_equal(got, same)
+    if r:
+        ref = _oracle_linear(x, wq, b, ut, rne_bf16(c).reshape(N, r), 0, r, eps, seed, step, flags=flags,
+                             resid=resid)
+        assert_bf16_close(got, ref, atol_rel_rms=2e-3, what="int4 persistent tiles")
+    else:
+        ref = np.stack([x[h].astype(np.float64) @ wq.astype(np.float64).T + b for h in range(2)])
+        assert np.max(np.abs(got - ref)) <= 1e-5 * np.sqrt(np.mean(ref**2)) * 10
 
 
 def test_linear_pm_r0_fp32_logits():
