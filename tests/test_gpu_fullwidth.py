@@ -186,9 +186,22 @@ def test_llama_full_width_shared_first_layer_bitwise(llama_bf16):
 
 
 def test_llama_full_width_int4():
-    """One Llama-3-8B-shape layer with INT4 weights (group 128, bf16 scales) and bf16 C."""
+    """One Llama-3-8B-shape layer with INT4 weights (group 128, bf16 scales) and bf16 C; the
+    INT4 GEMM that converts the packed weights in LDS (int4_dequant=False) gives the same
+    logits bit for bit as the decoder's default dequantise-then-bf16 path."""
     announce("full-width llama int4: weights")
     om_m, g = _build(LLAMA_1L, "int4", 24)
+    c = synth.bf16_round(synth.normal((om_m.k,), 0.05, 24, 10))
+    g.arena.c.copy_(torch.from_numpy(c).to(g.arena.c.dtype))
+    tok = t_i32(synth.uniform_tokens(2, 256, LLAMA_1L.vocab, 24, 5))
+    pert = Z.Pert(5, 3, 0, 1e-2)
+    announce("full-width llama int4: dequantised vs converted in the GEMM")
+    a = g.forward(tok, pert).clone()
+    g.int4_dequant = False
+    b = g.forward(tok, pert)
+    g.int4_dequant = True
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    del a, b
     _forward_and_step(om_m, g, 2, 256, 24, "llama full width int4")
 
 
