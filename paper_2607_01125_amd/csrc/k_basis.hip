@@ -165,14 +165,32 @@ constexpr int NPART = 64;      // workgroups (partial sums) of the column-Gram p
 
 size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 
-// K split of the products: enough workgroups to cover the chip, chunks a multiple of GQ_K.
-void ksplit_for(int64_t d, int& ks, int64_t& kchunk) {
-  const int64_t nrb = (d + GQ_ROWS - 1) / GQ_ROWS;
-  int k = (int)((512 + nrb - 1) / nrb);
-  k = k < 1 ? 1 : (k > 8 ? 8 : k);
-  while (k > 1 && d / k < 256) --k;
-  kchunk = ((d + k - 1) / k + GQ_K - 1) / GQ_K * GQ_K;
-  ks = (int)((d + kchunk - 1) / kchunk);
+// K split of the products for b columns: chunks a multiple of GQ_K and at least 256
+// deep; the grid (row blocks x ks x column blocks of 64) a whole number of workgroups per
+// CU where a split gives one (several workgroups of the products fit on a CU at once, and
+// with a fractional count the CUs that get one more set the time), at least two per CU,
+// else the most even split; at equal balance the fewest chunks (the partials are summed
+// in a second pass).
+void ksplit_for(int64_t d, int b, int& ks, int64_t& kchunk) {
+  const int64_t nrb = (d + GQ_ROWS - 1) / GQ_ROWS, ncb = (b + 63) / 64;
+  const int ncu = cu_count();
+  const int64_t cu = ncu > 0 ? ncu : 256;
+  double best = -1.0;
+  ks = 1;
+  kchunk = (d + GQ_K - 1) / GQ_K * GQ_K;
+  for (int k = 1; k <= 32; ++k) {
+    const int64_t chunk = ((d + k - 1) / k + GQ_K - 1) / GQ_K * GQ_K;
+    if (k > 1 && chunk < 256) break;
+    const int ke = (int)((d + chunk - 1) / chunk);
+    const int64_t wgs = nrb * ke * ncb;
+    double score = (double)wgs / (double)(((wgs + cu - 1) / cu) * cu);
+    if (wgs < 2 * cu) score *= 0.5;
+    if (score > best + 1e-9) {
+      best = score;
+      ks = ke;
+      kchunk = chunk;
+    }
+  }
 }
 
 struct EigWs {
@@ -180,6 +198,8 @@ struct EigWs {
   double* y;      // [d][b] work block
   float* q32;     // [d][b] fp32 copy of q
   double* part;   // [ks][d][b] partial products (fp32 or fp64 elements)
+  int ks;         // the products' K split (ksplit_for) and its chunk
+  int64_t kchunk;
   double* mp;     // [NPART][b][b] partial column Grams
   double* m;      // [b][b]
   double* linvt;  // [b][b] (L^{-1})^T
@@ -1168,9 +1188,8 @@ hipError_t orth(EigWs& w, int64_t d, int b, int passes, hipStream_t s) {
 
 // G X with fp64 accumulation into y [d][nc] (X fp64 [d][nc], nc <= 512).
 hipError_t gx64(const float* g, const double* x, int64_t d, int nc, EigWs& w, double* y, hipStream_t s) {
-  int ks;
-  int64_t kchunk;
-  ksplit_for(d, ks, kchunk);
+  const int ks = w.ks;
+  const int64_t kchunk = w.kchunk;
   gq64_kernel<<<dim3((unsigned)((d + GQ_ROWS - 1) / GQ_ROWS), (unsigned)ks, (unsigned)((nc + 63) / 64)), 256, 0, s>>>(
       g, x, w.part, d, nc, kchunk);
   const int64_t n = d * nc;
@@ -1183,7 +1202,7 @@ hipError_t gx64(const float* g, const double* x, int64_t d, int nc, EigWs& w, do
 size_t basis_ws_bytes(int64_t d, int32_t r, int32_t p) {
   int ks;
   int64_t kchunk;
-  ksplit_for(d, ks, kchunk);
+  ksplit_for(d, r + p, ks, kchunk);
   return carve_bytes(d, r + p, r, ks);
 }
 
@@ -1241,8 +1260,10 @@ hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t 
   const int b = r + p;
   int ks;
   int64_t kchunk;
-  ksplit_for(d, ks, kchunk);
+  ksplit_for(d, b, ks, kchunk);
   EigWs w = carve(ws, d, b, r, ks);
+  w.ks = ks;
+  w.kchunk = kchunk;
   const int64_t n = d * b;
   const unsigned g1 = (unsigned)((n + 255) / 256 > 4096 ? 4096 : (n + 255) / 256);
   const dim3 gq_grid((unsigned)((d + GQ_ROWS - 1) / GQ_ROWS), (unsigned)ks, (unsigned)((b + 63) / 64));
