@@ -243,7 +243,7 @@ zoact_status zoact_rmsnorm_project(const void* x, const void* w, int64_t rows, i
 zoact_status zoact_layernorm_project(const void* x, const void* w, const void* b, int64_t rows, int64_t d, float eps,
                                      const void* ut, int32_t r, void* y, void* p, zoact_stream stream);
 
-/* ------------------------------------------------------ fused +/- adapted linear/* ------------------------------------------------------ fused +/- adapted linear
+/* ------------------------------------------------------ fused +/- adapted linear
  * Section 3's perturbed forward evaluated for both signs in one pass over W:
  *   y[h] = epilogue(residual[h] + x[h] W^T + b + p[h] (C + s_h eps Z)^T),  s = (+1, -1)
  * x [2][T][d_in] and p [2][T][r] (from zoact_project on x; one copy of each,
