@@ -44,6 +44,12 @@ struct GemmArgs {
   int32_t tail_cols;     // feature tiles (the last ones, both halves' token tiles) of the split tail
 };
 
+// Buffer descriptor over [base, base + bytes): loads past the end read 0, stores past it are
+// dropped.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
 // Internal epilogue selector (not a public flag): the tile's squared errors against tgt
 // are summed instead of storing y.
 constexpr int EPI_MSE = 1 << 8;

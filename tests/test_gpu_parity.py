@@ -115,7 +115,8 @@ def test_sgd_bitwise():
 
 
 # ------------------------------------------------------------------ projection
-@pytest.mark.parametrize("n_tok,d,r", [(1000, 512, 32), (77, 256, 8), (2048, 1024, 64), (33, 128, 1)])
+@pytest.mark.parametrize("n_tok,d,r", [(1000, 512, 32), (77, 256, 8), (2048, 1024, 64), (33, 128, 1),
+                                       (1000, 4096, 32), (8200, 4096, 16), (33, 4096, 1)])   # d 4096: the pipelined kernel
 def test_project_bf16(n_tok, d, r):
     announce("project bf16", n_tok, d, r)
     x = synth.bf16_round(synth.normal((n_tok, d), 1.0, 1, n_tok))
