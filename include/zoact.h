@@ -129,8 +129,9 @@ typedef struct {
                            they get no correction and have no coefficient rows, so
                            feature n >= plain_end uses coefficient row
                            n - (plain_end - plain_begin).  Empty (equal) by default;
-                           ignored when r == 0.  Non-empty needs BF16 activations and
-                           weights, ch given, both bounds multiples of 256 and no
+                           ignored when r == 0.  Non-empty needs BF16 activations,
+                           BF16 weights (or INT4 with d_in % 128 == 0, d_in >= 256),
+                           ch given, both bounds multiples of 256 and no
                            ZOACT_SHARED_X (else ZOACT_E_UNSUPPORTED or INVALID)       */
   int64_t plain_end;
   void* ws;             /* optional workspace (16-byte aligned) of ws_bytes >=

@@ -136,8 +136,9 @@ static zoact_status validate_linear(const zoact_linear* L, const zoact_arena* A,
     if (L->plain_end > L->plain_begin) {
       CHECK(L->plain_begin % 256 == 0 && L->plain_end % 256 == 0,
             "linear_fwd_pm: plain range bounds must be multiples of 256");
-      CHECK(L->ch != nullptr && x_dtype == ZOACT_BF16 && L->w_dtype == ZOACT_BF16 && !(flags & ZOACT_SHARED_X),
-            "linear_fwd_pm: a plain range needs BF16 weights and activations, ch, and no SHARED_X");
+      CHECK(L->ch != nullptr && x_dtype == ZOACT_BF16 && (L->w_dtype == ZOACT_BF16 || L->w_dtype == ZOACT_INT4_G128) &&
+                !(flags & ZOACT_SHARED_X),
+            "linear_fwd_pm: a plain range needs BF16 activations, BF16 or INT4 weights, ch, and no SHARED_X");
       rows -= L->plain_end - L->plain_begin;
     }
     CHECK(L->coef_offset >= 0 && L->coef_offset + rows * (int64_t)L->r <= A->k,

@@ -121,6 +121,7 @@ def test_tiny_fp32_twenty_steps():
     ("opt-bf16", OPT_S, "bf16", 2, 40),
     ("llama-int4", LLAMA_S, "int4", 2, 64),
     ("llama-int4-inreg", LLAMA_S, "int4-inreg", 2, 64),
+    ("opt-int4-inreg", OPT_S, "int4-inreg", 2, 40),       # q|k|v with k plain, INT4 converted in the GEMM
     ("llama-bf16-r1", synth.shrink(LLAMA_S, rank=1), "bf16", 2, 64),
     ("llama-bf16-r128", synth.shrink(LLAMA_S, rank=128), "bf16", 2, 48),
     ("llama-int4-r1", synth.shrink(LLAMA_S, rank=1), "int4", 2, 40),

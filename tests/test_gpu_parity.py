@@ -829,17 +829,24 @@ def test_linear_pm_shared_x_bitwise(T, K, N, r, flags, out_f32, resid):
         assert_bf16_close(gs.reshape(2, T, N), ref, what="shared x vs oracle")
 
 
-@pytest.mark.parametrize("T,K,dq,dk,dv,r,flags", [
-    (1000, 512, 512, 256, 256, 32, 0),            # ragged tokens, k between q and v
-    (300, 256, 256, 512, 256, 64, Z.EPI_RELU),     # k wider than q and v, ReLU
-    (4100, 128, 768, 256, 512, 8, 0),              # ragged last token tile, 204 tiles
+@pytest.mark.parametrize("T,K,dq,dk,dv,r,flags,int4", [
+    (1000, 512, 512, 256, 256, 32, 0, False),            # ragged tokens, k between q and v
+    (300, 256, 256, 512, 256, 64, Z.EPI_RELU, False),     # k wider than q and v, ReLU
+    (4100, 128, 768, 256, 512, 8, 0, False),              # ragged last token tile, 204 tiles
+    (1000, 512, 512, 256, 256, 32, 0, True),              # INT4 weights (converted in LDS)
+    (300, 256, 256, 512, 256, 64, Z.EPI_RELU, True),
 ])
-def test_linear_plain_range_equals_two_calls(T, K, dq, dk, dv, r, flags):
+def test_linear_plain_range_equals_two_calls(T, K, dq, dk, dv, r, flags, int4):
     """q|k|v in one call with k as the plain feature range (no correction, no coefficient
     rows) gives the same bits as q|v adapted and k plain in two calls."""
-    announce("linear plain range", T, K, dq, dk, dv, r, flags)
+    announce("linear plain range", T, K, dq, dk, dv, r, flags, int4)
     N = dq + dk + dv
-    x, w, b, ut, _, _ = _layer_inputs(T, K, N, r, seed=T + N + r, bias=True)
+    x, w, b, ut, packed, scales = _layer_inputs(T, K, N, r, seed=T + N + r, bias=True, int4=int4)
+
+    def weights(rows):   # the layer's weights for a row selection, bf16 or packed INT4 with scales
+        if int4:
+            return dict(w=t_u8(np.ascontiguousarray(packed[rows])), w_scales=t_bf16(np.ascontiguousarray(scales[rows])))
+        return dict(w=t_bf16(np.ascontiguousarray(w[rows])))
     rows = dq + dv
     c = synth.normal((rows * r,), 0.02, N + r, 5)
     arena = Z.Arena(t_f32(c), torch.zeros(c.size, device=dev()), torch.zeros(c.size, device=dev()))
@@ -849,14 +856,16 @@ def test_linear_plain_range_equals_two_calls(T, K, dq, dk, dv, r, flags):
     xt = t_bf16(x.reshape(2 * T, K))
     p = torch.empty(2 * T, r, dtype=torch.bfloat16, device=dev())
     Z.project(xt, t_bf16(ut), p)
-    fused = Z.Linear(t_bf16(w), K, N, r, t_bf16(ut), 0, t_bf16(b), ch=ch, ch_stride=rows * r, plain=(dq, dq + dk))
+    fw = weights(np.s_[:])
+    fused = Z.Linear(fw["w"], K, N, r, t_bf16(ut), 0, t_bf16(b), fw.get("w_scales"), ch=ch, ch_stride=rows * r,
+                     plain=(dq, dq + dk))
     yf = torch.full((2 * T, N), float("nan"), dtype=torch.bfloat16, device=dev())
     Z.linear_fwd_pm(fused, arena, xt, T, p, yf, pert, flags=flags)
     sel = np.r_[0:dq, dq + dk:N]
-    qv = Z.Linear(t_bf16(np.ascontiguousarray(w[sel])), K, rows, r, t_bf16(ut), 0, t_bf16(np.ascontiguousarray(b[sel])),
+    qw, kw = weights(sel), weights(np.s_[dq:dq + dk])
+    qv = Z.Linear(qw["w"], K, rows, r, t_bf16(ut), 0, t_bf16(np.ascontiguousarray(b[sel])), qw.get("w_scales"),
                   ch=ch, ch_stride=rows * r)
-    kk = Z.Linear(t_bf16(np.ascontiguousarray(w[dq:dq + dk])), K, dk, 0, None, 0,
-                  t_bf16(np.ascontiguousarray(b[dq:dq + dk])))
+    kk = Z.Linear(kw["w"], K, dk, 0, None, 0, t_bf16(np.ascontiguousarray(b[dq:dq + dk])), kw.get("w_scales"))
     yqv = torch.empty(2 * T, rows, dtype=torch.bfloat16, device=dev())
     yk = torch.empty(2 * T, dk, dtype=torch.bfloat16, device=dev())
     Z.linear_fwd_pm(qv, arena, xt, T, p, yqv, pert, flags=flags)
@@ -926,6 +935,12 @@ def test_linear_plain_range_rejected_where_not_covered():
     bad = Z.Linear(t_bf16(w), K, N, r, t_bf16(ut), 0, None, ch=ch, ch_stride=512 * r, plain=(128, 384))
     with pytest.raises(Z.ZoactError):
         Z.linear_fwd_pm(bad, arena, xt, T, p, y, pert)
+    # INT4 weights with a depth the 64-deep INT4 schedule does not cover (K < 256)
+    packed, scales = synth.quantize_int4_g128(w)
+    bad4 = Z.Linear(t_u8(packed), K, N, r, t_bf16(ut), 0, None, t_bf16(scales), ch=ch, ch_stride=512 * r,
+                    plain=(256, 512))
+    with pytest.raises(Z.ZoactError):
+        Z.linear_fwd_pm(bad4, arena, xt, T, p, y, pert)
 
 
 def test_linear_mse_shared_x_equals_stacked():
