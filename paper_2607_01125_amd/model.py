@@ -33,7 +33,9 @@ everything else, bf16 coefficients by default).
 """
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
+import queue
 
 import math
 from dataclasses import dataclass
@@ -460,7 +462,7 @@ class Decoder:
 
     # ---------------------------------------------------------------- Algorithm 1
     def basis_init(self, calib_tokens: torch.Tensor, opts: Z.EigOpts | None = None, keep_eigvals=False,
-                   report=False):
+                   report=False, concurrency: int = 4):
         """Unperturbed calibration forward, then the top-r basis of each adapted site's inputs.
 
         calib_tokens int32 [n_seq][seq] with n_seq even: the two halves of the stacked
@@ -469,33 +471,79 @@ class Decoder:
         (residual, gap theta_r / theta_{r+1}, iterations, converged) lands in
         self.basis_report after the call; a site whose residual stays above opts.tol keeps
         its best-effort basis and is reported with converged = False.
+
+        `concurrency` sites are solved at once: each site's input is copied as the forward
+        produces it and handed to one of that many host threads, each with its own stream
+        and workspace (the solver's small b x b steps run on one workgroup and its adaptive
+        checks wait on the host, so one site leaves most of the GPU idle).  Every site's
+        result is the same as when solved alone.  1 solves each site inside the forward.
         """
         n_seq, seq = calib_tokens.shape
         if n_seq % 2:
             raise ValueError("the calibration batch needs an even number of sequences")
         dims = self.site_dims()
-        ws = torch.empty(max(Z.basis_init_workspace_bytes(dd, self.r, opts) for dd in set(dims.values())),
-                         dtype=torch.uint8, device=self.dev)
+        nws = max(Z.basis_init_workspace_bytes(dd, self.r, opts) for dd in set(dims.values()))
+        k = max(1, int(concurrency))
+        wss = [torch.empty(nws, dtype=torch.uint8, device=self.dev) for _ in range(k)]
         self.eigvals = {}
         reps = {}
 
-        def hook(l, site, x):
-            if (l, site) not in dims:
-                return
-            ut = torch.empty(self.r, dims[(l, site)], dtype=self.act, device=self.dev)
+        def outputs(key):   # the site's basis, eigenvalues and report (allocated on the current stream)
+            ut = torch.empty(self.r, dims[key], dtype=self.act, device=self.dev)
             ev = torch.empty(self.r, dtype=torch.float32, device=self.dev) if keep_eigvals else None
             rep = Z.eig_report_tensor(self.dev) if report else None
-            Z.basis_init(x, self.r, ut, ws, opts, eigvals=ev, report=rep)
-            self.ut[(l, site)] = ut
+            self.ut[key] = ut
             if keep_eigvals:
-                self.eigvals[(l, site)] = ev
+                self.eigvals[key] = ev
             if report:
-                reps[(l, site)] = rep
+                reps[key] = rep
+            return ut, ev, rep
 
         tok = calib_tokens.reshape(2, n_seq // 2, seq).contiguous()
-        self.forward(tok, Z.Pert(0, 0, 0, 0.0), calibrate=hook, distinct_halves=True)
+        if k == 1:
+            def hook(l, site, x):
+                if (l, site) in dims:
+                    ut, ev, rep = outputs((l, site))
+                    Z.basis_init(x, self.r, ut, wss[0], opts, eigvals=ev, report=rep)
+
+            self.forward(tok, Z.Pert(0, 0, 0, 0.0), calibrate=hook, distinct_halves=True)
+        else:
+            streams = [torch.cuda.Stream(device=self.dev) for _ in range(k)]
+            idle = queue.SimpleQueue()
+            for i in range(k):
+                idle.put(i)
+
+            def work(x, out, ready):
+                i = idle.get()
+                try:
+                    s = streams[i]
+                    s.wait_event(ready)
+                    ut, ev, rep = out
+                    Z.basis_init(x, self.r, ut, wss[i], opts, eigvals=ev, report=rep, stream=s)
+                    for t in (x, *out):
+                        if t is not None:
+                            t.record_stream(s)
+                finally:
+                    idle.put(i)
+
+            futures = []
+            with concurrent.futures.ThreadPoolExecutor(max_workers=k) as pool:
+                def hook(l, site, x):
+                    if (l, site) not in dims:
+                        return
+                    xc = x.clone()
+                    out = outputs((l, site))
+                    ready = torch.cuda.Event()
+                    ready.record()
+                    futures.append(pool.submit(work, xc, out, ready))
+
+                self.forward(tok, Z.Pert(0, 0, 0, 0.0), calibrate=hook, distinct_halves=True)
+                for f in futures:
+                    f.result()
+            for st in streams:
+                st.synchronize()
         if report:
-            self.basis_report = {k: Z.read_eig_report(v) for k, v in reps.items()}
+            self.basis_report = {k2: Z.read_eig_report(v) for k2, v in reps.items()}
         return self.ut
 
     def set_basis(self, ut: dict):

@@ -228,6 +228,29 @@ def test_basis_init_over_model(shape, mode):
 
 
 # ------------------------------------------------------------------ fused LM head + cross entropy
+@pytest.mark.parametrize("shape,mode", [(LLAMA_S, "bf16"), (OPT_S, "bf16")], ids=["llama", "opt"])
+def test_basis_init_concurrent_sites_bitwise(shape, mode):
+    """Decoder.basis_init solving several sites at once (copies of their inputs, one stream
+    and workspace per host thread) gives each site the same basis, eigenvalues and report
+    bits as solving them one at a time inside the forward."""
+    announce("basis init concurrent", shape.name)
+    W = synth.model_weights(shape, 6, "bf16")
+    g = gm.Decoder(shape, W, mode)
+    calib = t_i32(synth.uniform_tokens(4, 64, shape.vocab, 6, 1))
+    opts = Z.EigOpts(oversample=shape.rank, max_iter=24, seed=0x5eed, tol=1e-4, adaptive=1, check_every=4)
+    runs = []
+    for k in (1, 4):
+        g.basis_init(calib, opts, keep_eigvals=True, report=True, concurrency=k)
+        runs.append(({key: host(v.view(torch.int16)) for key, v in g.ut.items()},
+                     {key: host(v) for key, v in g.eigvals.items()}, dict(g.basis_report)))
+    (u1, e1, r1), (u4, e4, r4) = runs
+    assert set(u1) == set(u4) == set(g.site_dims())
+    for key in u1:
+        np.testing.assert_array_equal(u1[key], u4[key])
+        np.testing.assert_array_equal(e1[key].view(np.uint32), e4[key].view(np.uint32))
+        assert r1[key] == r4[key], key
+
+
 @pytest.mark.parametrize("shape,B,S", [(LLAMA_S, 2, 64), (OPT_S, 3, 40)], ids=["llama", "opt"])
 def test_fused_head_xent_matches_stored_logits(shape, B, S):
     """The LM head with the cross entropy in its epilogue (logits never stored) gives the
