@@ -412,8 +412,8 @@ __global__ void __launch_bounds__(NT, 1) tail_combine_kernel(GemmArgs a, int nti
 // into a bf16 W tile, the values zoact_dequant_int4 forms, so the fragments, MFMAs, rank
 // correction and epilogue are those of the bf16 schedule with the dequantised weight (its
 // results are the same bits).  A wave converts the rows it loaded itself, so the packed
-// ring needs no barrier; the conversion of a stage is spread, a quarter chunk per row of
-// MFMAs, over the two sub-steps before the barrier that publishes it.
+// ring needs no barrier; the conversion of a stage is spread, four values (half a 16-byte
+// chunk) per row of MFMAs, over the two sub-steps before the barrier that publishes it.
 //
 // LDS: four 32 KB bf16 slots (stage S: W in slot 2 (S & 1), x in 2 (S & 1) + 1) and a
 // three-stage ring of packed W (8 KB) and scales (1 KB; a 2-byte direct-to-LDS load fills
