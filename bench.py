@@ -34,6 +34,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -131,10 +132,16 @@ def log(*a):
 
 
 def source_hash(rels) -> str:
+    """Hash of the code in the given sources: comments, trailing blanks and empty lines are
+    dropped, so a record taken on a kernel stays valid through comment edits."""
     h = hashlib.sha256()
     for rel in rels:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+        for line in text.splitlines():
+            code = line.split("//", 1)[0].rstrip()
+            if code:
+                h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 
