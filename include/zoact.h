@@ -411,7 +411,15 @@ zoact_status zoact_step_q_sgd(const zoact_arena* A, const float* losses, int32_t
  *   opts) bytes.
  * zoact_basis_init: zoact_gram followed by zoact_basis_from_gram, with g at the
  *   start of ws; ws needs zoact_basis_init_workspace_bytes(d, r, opts) bytes (the
- *   Gram d*d fp32, padded to 256 bytes, then the solver's workspace).
+ *   Gram d*d fp32, padded to 256 bytes, then the solver's workspace).  With fewer
+ *   rows than features (BF16 x, n_tok < d, r + p <= n_tok, d % 64 == 0, ld_x % 8 ==
+ *   0, x 16-byte aligned) and ws also large enough for it, the same singular vectors
+ *   come from the thin SVD's other side (Section 3): the solver runs on the
+ *   n_tok x n_tok token Gram X X^T, whose eigenvectors are X's left singular vectors
+ *   V', and the basis is X^T V' with unit columns (signed as above); the eigenvalues
+ *   are the same, and the report's residual is still that of the returned basis
+ *   against X^T X (formed as X^T (X X^T) V' over the column norms).  A column whose
+ *   singular value is exactly 0 (X of rank below r) is returned as zeros in this form.
  * Errors: r < 1, r > 256, r + p > d, n_tok < r, ld_x < d, negative tol or
  * check_every, adaptive with tol == 0 -> ZOACT_E_INVALID; a workspace that is NULL or
  * too small -> ZOACT_E_WORKSPACE; residual above tol -> ZOACT_E_NOCONVERGE (outputs

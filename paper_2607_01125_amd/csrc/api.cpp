@@ -433,26 +433,36 @@ zoact_status zoact_gram(const void* x, int32_t x_dtype, int64_t n_tok, int64_t d
   return hip_status(zoact::launch_gram(x, x_dtype, n_tok, d, ld_x, g, accumulate, st(stream)), "gram");
 }
 
+// The solver's argument checks, shared by the Gram and the token-side forms (n: rows of
+// the Gram the iteration runs on).
+static zoact_status eig_args(const char* fn, const void* ut, int32_t ut_dtype, int64_t n, int32_t r,
+                             const zoact_eig_opts& o, const zoact_eig_opts* opts) {
+  const int32_t p = o.oversample;
+  CHECK(ut, "%s: NULL ut", fn);
+  CHECK(float_type(ut_dtype), "%s: ut dtype must be F32 or BF16", fn);
+  CHECK(r >= 1 && r <= 256, "%s: r=%d outside [1, 256]", fn, r);
+  CHECK(n >= 2 && r + p <= n, "%s: r + oversample = %d exceeds d = %lld", fn, r + p, (long long)n);
+  CHECK(r + p <= 512, "%s: block r + oversample = %d exceeds 512", fn, r + p);
+  CHECK(o.tol >= 0.f, "%s: negative tol", fn);
+  CHECK(!o.adaptive || o.tol > 0.f, "%s: adaptive mode needs tol > 0", fn);
+  CHECK(!opts || (opts->max_iter >= 0 && opts->check_every >= 0 && opts->oversample >= 0), "%s: negative option", fn);
+  return ZOACT_OK;
+}
+
 zoact_status zoact_basis_from_gram(const float* g, int64_t d, int32_t r, const zoact_eig_opts* opts, void* ut,
                                    int32_t ut_dtype, float* ut_master, float* eigvals, zoact_eig_report* report,
                                    void* ws, size_t ws_bytes, zoact_stream stream) {
   const zoact_eig_opts o = eig_resolve(r, opts);
   const int32_t p = o.oversample;
-  CHECK(g && ut, "basis_from_gram: NULL g or ut");
-  CHECK(float_type(ut_dtype), "basis_from_gram: ut dtype must be F32 or BF16");
-  CHECK(r >= 1 && r <= 256, "basis_from_gram: r=%d outside [1, 256]", r);
-  CHECK(d >= 2 && r + p <= d, "basis_from_gram: r + oversample = %d exceeds d = %lld", r + p, (long long)d);
-  CHECK(r + p <= 512, "basis_from_gram: block r + oversample = %d exceeds 512", r + p);
-  CHECK(o.tol >= 0.f, "basis_from_gram: negative tol");
-  CHECK(!o.adaptive || o.tol > 0.f, "basis_from_gram: adaptive mode needs tol > 0");
-  CHECK(!opts || (opts->max_iter >= 0 && opts->check_every >= 0 && opts->oversample >= 0),
-        "basis_from_gram: negative option");
+  CHECK(g, "basis_from_gram: NULL g");
+  zoact_status s = eig_args("basis_from_gram", ut, ut_dtype, d, r, o, opts);
+  if (s != ZOACT_OK) return s;
   const size_t need = zoact::basis_ws_bytes(d, r, p);
   if (ws == nullptr || ws_bytes < need) return fail(ZOACT_E_WORKSPACE, "basis_from_gram: workspace needs %zu bytes", need);
   bool met = true;
-  const zoact_status s = hip_status(zoact::launch_basis_from_gram(g, d, r, p, o, ut, ut_dtype, ut_master, eigvals,
-                                                                  report, ws, st(stream), met),
-                                    "basis_from_gram");
+  s = hip_status(zoact::launch_basis_from_gram(g, d, r, p, o, ut, ut_dtype, ut_master, eigvals, report, ws, st(stream),
+                                               met),
+                 "basis_from_gram");
   if (s != ZOACT_OK) return s;
   if (!met) return fail(ZOACT_E_NOCONVERGE, "basis_from_gram: residual above tol %g after %d iterations", o.tol,
                         o.max_iter);
@@ -463,11 +473,29 @@ zoact_status zoact_basis_init(const void* x, int32_t x_dtype, int64_t n_tok, int
                               const zoact_eig_opts* opts, void* ut, int32_t ut_dtype, float* ut_master, float* eigvals,
                               zoact_eig_report* report, void* ws, size_t ws_bytes, zoact_stream stream) {
   CHECK(n_tok >= r, "basis_init: n_tok=%lld < r=%d", (long long)n_tok, r);
-  const int32_t p = eig_resolve(r, opts).oversample;
+  const zoact_eig_opts o = eig_resolve(r, opts);
+  const int32_t p = o.oversample;
   CHECK(r >= 1 && r <= 256 && d >= 2 && r + p <= d, "basis_init: bad r=%d for d=%lld", r, (long long)d);
   const size_t gbytes = gram_ws_bytes(d);
   const size_t need = gbytes + zoact::basis_ws_bytes(d, r, p);
   if (ws == nullptr || ws_bytes < need) return fail(ZOACT_E_WORKSPACE, "basis_init: workspace needs %zu bytes", need);
+  // Fewer calibration rows than features: the same singular vectors from the n_tok x n_tok
+  // token-side Gram (smaller to form and to iterate on), when its workspace fits in ws.
+  const bool rows = x && x_dtype == ZOACT_BF16 && n_tok < d && r + p <= n_tok && d % 64 == 0 && ld_x >= d &&
+                    ld_x % 8 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+                    zoact::basis_rows_ws_bytes(n_tok, d, r, p) <= ws_bytes;
+  if (rows) {
+    zoact_status s = eig_args("basis_init", ut, ut_dtype, n_tok, r, o, opts);
+    if (s != ZOACT_OK) return s;
+    bool met = true;
+    s = hip_status(zoact::launch_basis_init_rows(static_cast<const uint16_t*>(x), n_tok, d, ld_x, r, p, o, ut,
+                                                 ut_dtype, ut_master, eigvals, report, ws, st(stream), met),
+                   "basis_init");
+    if (s != ZOACT_OK) return s;
+    if (!met) return fail(ZOACT_E_NOCONVERGE, "basis_init: residual above tol %g after %d iterations", o.tol,
+                          o.max_iter);
+    return ZOACT_OK;
+  }
   float* g = static_cast<float*>(ws);
   zoact_status s = zoact_gram(x, x_dtype, n_tok, d, ld_x, g, 0, stream);
   if (s != ZOACT_OK) return s;

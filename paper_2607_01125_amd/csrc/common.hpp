@@ -45,6 +45,9 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
                             void* y, int32_t y_dtype, hipStream_t s);
 // Adapted linear of both halves with the regression loss fused into the epilogue (y not
 // stored): per-tile sums into part [2][tiles], then loss_pm[h] = sum / (T * d_out).
+// y [2 T][N] fp32 = x [2 T][K] w^T, bf16 operands with dense rows (plain GEMM, no correction).
+hipError_t launch_gemm_nt_f32(const uint16_t* x, int64_t T, const uint16_t* w, int64_t N, int64_t K, float* y,
+                              hipStream_t s);
 hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, uint32_t flags, const void* p,
                              const zoact_pert_pair& pert, const void* target, double* part, float* loss_pm,
                              hipStream_t s);
@@ -72,6 +75,12 @@ hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t 
                                   int32_t ut_dtype, float* ut_master, float* eigvals, zoact_eig_report* report, void* ws,
                                   hipStream_t s, bool& met);
 size_t basis_ws_bytes(int64_t d, int32_t r, int32_t p);
+// Algorithm 1 from the token-side Gram X X^T of bf16 X [n][ld] (D values per row,
+// D % 64 == 0, r + p <= n): same outputs as the Gram form; ws of basis_rows_ws_bytes.
+size_t basis_rows_ws_bytes(int64_t n, int64_t D, int32_t r, int32_t p);
+hipError_t launch_basis_init_rows(const uint16_t* x, int64_t n, int64_t D, int64_t ld, int32_t r, int32_t p,
+                                  const zoact_eig_opts& o, void* ut, int32_t ut_dtype, float* ut_master, float* eigvals,
+                                  zoact_eig_report* report, void* ws, hipStream_t s, bool& met);
 
 // Record the detail text of a failed call for zoact_last_error() and return `st`.
 zoact_status set_error(zoact_status st, const char* msg);

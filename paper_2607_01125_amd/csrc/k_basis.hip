@@ -19,6 +19,12 @@
 //    from the iteration's own products, meets the caller's bound.
 //  * Sign: each column is flipped so its largest-magnitude entry is positive,
 //    lowest index on ties.
+//  * Fewer calibration rows n than features D (the wide inputs of the down
+//    projections): the thin SVD X = U_x S V^T read from its left side.  The same
+//    solver runs on the n x n token Gram X X^T, whose eigenvectors are U_x and whose
+//    eigenvalues are those of X^T X; the basis is V_r = X^T U_x,r S_r^{-1}, formed as
+//    X^T v with each column scaled to unit length in fp64.  Forming X X^T costs
+//    n^2 D instead of D^2 n, and each iteration reads n^2 instead of D^2 values.
 #include "common.hpp"
 #include "rng.hpp"
 
@@ -140,6 +146,225 @@ __global__ void __launch_bounds__(256) gram_bf16_kernel(const uint16_t* __restri
           if (!diag) g[c * d + r] = v;
         }
       }
+}
+
+// --------------------------------------------------------------- token-side Gram
+// G' = X X^T [n][n] for bf16 X [n][ld] (d values per row, d % 64 == 0).  The contraction
+// runs along X's rows, so each lane's MFMA operand (8 depth values of one row) comes
+// straight from global memory with no transpose and no LDS.  One workgroup per 128 x 128
+// tile of the upper triangle, four waves of 64 x 64 (4 x 4 blocks of
+// v_mfma_f32_16x16x32_bf16); depth in 64-deep steps, the next step's operands loaded
+// while the current step's MFMAs run.  A sum over the depth does not depend on which
+// lane holds which depth value as long as both operands agree, so lane group lk takes
+// the 16 consecutive values 16 lk .. 16 lk + 15 of each step (two 16-byte loads: the
+// first half feeds the first MFMA, the second half the second) and a row's 64 values of
+// a step are one 128-byte line.  Entries with row <= column are stored and mirrored, so
+// G' is exactly symmetric; rows past n read zeros and store nothing.
+__global__ void __launch_bounds__(256) gram_rows_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int64_t d,
+                                                             int64_t ld, float* __restrict__ g, int ntile) {
+  int t = blockIdx.x, ti = 0;
+  while (t >= ntile - ti) {
+    t -= ntile - ti;
+    ++ti;
+  }
+  const int tj = ti + t;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lk = lane >> 4;
+  const int64_t i0 = (int64_t)ti * GT + (wave >> 1) * 64, j0 = (int64_t)tj * GT + (wave & 1) * 64;
+  const uint16_t* pa[4];
+  const uint16_t* pb[4];
+  bool va[4], vb[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int64_t ra = i0 + q * 16 + lr, rb = j0 + q * 16 + lr;
+    va[q] = ra < n;
+    vb[q] = rb < n;
+    pa[q] = x + (va[q] ? ra : 0) * ld + lk * 16;   // a row past n reads row 0, then zeros
+    pb[q] = x + (vb[q] ? rb : 0) * ld + lk * 16;
+  }
+  const bf16x8 zero = {};
+  auto load = [&](bf16x8 (&a)[4][2], bf16x8 (&b)[4][2], int64_t k) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const bf16x8 av = *reinterpret_cast<const bf16x8*>(pa[q] + k + h * 8);
+        const bf16x8 bv = *reinterpret_cast<const bf16x8*>(pb[q] + k + h * 8);
+        a[q][h] = va[q] ? av : zero;
+        b[q][h] = vb[q] ? bv : zero;
+      }
+  };
+  floatx4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](const bf16x8 (&a)[4][2], const bf16x8 (&b)[4][2]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i][h], b[j][h], acc[i][j], 0, 0, 0);
+  };
+  bf16x8 a0[4][2], b0[4][2], a1[4][2], b1[4][2];
+  load(a0, b0, 0);
+  int64_t k = 0;
+  for (; k + 128 <= d; k += 128) {
+    load(a1, b1, k + 64);
+    mma(a0, b0);
+    if (k + 128 < d) load(a0, b0, k + 128);
+    mma(a1, b1);
+  }
+  if (k < d) mma(a0, b0);   // d % 128 == 64: the last step, loaded by the loop's last pass
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t r = i0 + i * 16 + lk * 4 + q;
+        const int64_t c = j0 + j * 16 + lr;
+        if (r <= c && c < n) {
+          g[r * n + c] = acc[i][j][q];
+          if (r < c) g[c * n + r] = acc[i][j][q];
+        }
+      }
+}
+
+// Lower triangle of g [n][n] replaced by the upper one (g[i][j] = g[j][i] for i > j),
+// through 32 x 32 LDS tiles so both sides are read and written along rows.
+__global__ void __launch_bounds__(256) mirror_upper_kernel(float* __restrict__ g, int64_t n, int nt) {
+  __shared__ float tl[32][33];
+  int t = blockIdx.x, bi = 0;   // tile (bi, bj), bi < bj: rows bi, columns bj are the source
+  while (t >= nt - 1 - bi) {
+    t -= nt - 1 - bi;
+    ++bi;
+  }
+  const int bj = bi + 1 + t;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int k = ty; k < 32; k += 8) {
+    const int64_t i = (int64_t)bi * 32 + k, j = (int64_t)bj * 32 + tx;
+    tl[k][tx] = (i < n && j < n) ? g[i * n + j] : 0.f;
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    const int64_t i = (int64_t)bj * 32 + k, j = (int64_t)bi * 32 + tx;   // lower-triangle entry (i, j)
+    if (i < n && j < n) g[i * n + j] = tl[tx][k];
+  }
+}
+
+// Diagonal 32 x 32 blocks: entries below the diagonal take their mirror.
+__global__ void __launch_bounds__(256) mirror_diag_kernel(float* __restrict__ g, int64_t n) {
+  __shared__ float tl[32][33];
+  const int64_t b0 = (int64_t)blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int k = ty; k < 32; k += 8)
+    tl[k][tx] = (b0 + k < n && b0 + tx < n) ? g[(b0 + k) * n + b0 + tx] : 0.f;
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8)
+    if (k > tx && b0 + k < n) g[(b0 + k) * n + b0 + tx] = tl[tx][k];
+}
+
+// part[z][D][r] (fp64) = X[rows of chunk z]^T V[rows of chunk z] for bf16 X [n][ld] (D
+// values per row, D % 8 == 0) and V fp64 [n][r]; grid (D / 512 feature blocks, r / 32
+// column blocks, depth chunks of `tchunk` rows).  32 rows of X (512 features) and of V
+// (32 columns) are staged in LDS per step; each thread owns 8 features x 8 columns in
+// fp64 registers and walks the rows in order.
+constexpr int XV_J = 512, XV_C = 32, XV_T = 32;
+__global__ void __launch_bounds__(256) xt_v_kernel(const uint16_t* __restrict__ x, int64_t n, int64_t D, int64_t ld,
+                                                   const double* __restrict__ v, int r, int64_t tchunk,
+                                                   double* __restrict__ part) {
+  __shared__ __align__(16) uint16_t xs[XV_T][XV_J + 8];
+  __shared__ __align__(16) double vs[XV_T][XV_C];
+  const int tc = threadIdx.x & 3, tj = threadIdx.x >> 2;
+  const int64_t j0 = (int64_t)blockIdx.x * XV_J;
+  const int c0 = blockIdx.y * XV_C;
+  const int64_t tb = (int64_t)blockIdx.z * tchunk;
+  const int64_t te = tb + tchunk < n ? tb + tchunk : n;
+  double acc[8][8];
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int b = 0; b < 8; ++b) acc[a][b] = 0.0;
+  for (int64_t t0 = tb; t0 < te; t0 += XV_T) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < XV_T * XV_J / 8; e += 256) {
+      const int tt = e >> 6, jc = (e & 63) * 8;
+      const int64_t t = t0 + tt, j = j0 + jc;
+      uint4 val = make_uint4(0u, 0u, 0u, 0u);
+      if (t < te && j < D) val = *reinterpret_cast<const uint4*>(x + t * ld + j);
+      *reinterpret_cast<uint4*>(&xs[tt][jc]) = val;
+    }
+    for (int e = threadIdx.x; e < XV_T * XV_C; e += 256) {
+      const int tt = e >> 5, c = e & 31;
+      vs[tt][c] = (t0 + tt < te && c0 + c < r) ? v[(t0 + tt) * r + c0 + c] : 0.0;
+    }
+    __syncthreads();
+    for (int tt = 0; tt < XV_T; ++tt) {
+      const uint4 xq = *reinterpret_cast<const uint4*>(&xs[tt][tj * 8]);
+      const uint32_t xw[4] = {xq.x, xq.y, xq.z, xq.w};
+      double xv[8], vv[8];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        xv[2 * a] = (double)__uint_as_float(xw[a] << 16);
+        xv[2 * a + 1] = (double)__uint_as_float(xw[a] & 0xFFFF0000u);
+      }
+#pragma unroll
+      for (int b = 0; b < 8; ++b) vv[b] = vs[tt][tc * 8 + b];
+#pragma unroll
+      for (int a = 0; a < 8; ++a)
+#pragma unroll
+        for (int b = 0; b < 8; ++b) acc[a][b] = fma(xv[a], vv[b], acc[a][b]);
+    }
+  }
+  double* out = part + (int64_t)blockIdx.z * D * r;
+#pragma unroll
+  for (int a = 0; a < 8; ++a) {
+    const int64_t j = j0 + tj * 8 + a;
+    if (j >= D) continue;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const int c = c0 + tc * 8 + b;
+      if (c < r) out[j * r + c] = acc[a][b];
+    }
+  }
+}
+
+// out[e] = sum over z = 0 .. ks-1 of part[z][e], in that order.
+__global__ void __launch_bounds__(256) sum_chunks_kernel(const double* __restrict__ part, int ks, int64_t m,
+                                                         double* __restrict__ out) {
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < m; e += (int64_t)gridDim.x * 256) {
+    double acc = part[e];
+    for (int z = 1; z < ks; ++z) acc += part[(int64_t)z * m + e];
+    out[e] = acc;
+  }
+}
+
+// Columns of a [D][r] scaled to unit length: s[c] = ||a[:, c]|| (fixed-order reduction)
+// and a[:, c] /= s[c]; with compute == 0 the s given is applied instead.  A zero column
+// stays zero.
+__global__ void __launch_bounds__(256) colscale_kernel(double* __restrict__ a, int64_t D, int r, double* __restrict__ s,
+                                                       int compute) {
+  __shared__ double sh[256];
+  const int c = blockIdx.x;
+  double nrm;
+  if (compute) {
+    double acc = 0.0;
+    for (int64_t j = threadIdx.x; j < D; j += 256) acc += a[j * r + c] * a[j * r + c];
+    sh[threadIdx.x] = acc;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+      if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
+      __syncthreads();
+    }
+    nrm = sqrt(sh[0]);
+    if (threadIdx.x == 0) s[c] = nrm;
+  } else {
+    nrm = s[c];
+  }
+  const double inv = nrm > 0.0 ? 1.0 / nrm : 0.0;
+  for (int64_t j = threadIdx.x; j < D; j += 256) a[j * r + c] *= inv;
 }
 
 __global__ void gram_f32_kernel(const float* __restrict__ x, int64_t n_tok, int64_t d, int64_t ld,
@@ -1220,10 +1445,45 @@ hipError_t launch_gram(const void* x, int32_t dtype, int64_t n_tok, int64_t d, i
   return hipGetLastError();
 }
 
+// The token-side form: X (bf16 [n][ld], D values per row) whose Gram X X^T the solver
+// ran on, and the buffers that carry its Ritz vectors back to the D features.
+struct Rows {
+  const uint16_t* x;
+  int64_t D, ld;
+  double* up;    // [D][r] basis
+  double* yp;    // [D][r] X^T X times the basis (residual)
+  double* sc;    // [r] column norms of X^T V
+  double* part;  // [ks][D][r] depth-chunk partials of X^T V
+  int ks;
+  int64_t tchunk;
+};
+
+// Depth split of X^T V over n rows: about two workgroups per CU, chunks a multiple of 32
+// rows (at least 64).
+static void xv_split(int64_t n, int64_t D, int r, int& ks, int64_t& tchunk) {
+  const int64_t blocks = ((D + XV_J - 1) / XV_J) * ((r + XV_C - 1) / XV_C);
+  const int ncu = cu_count();
+  const int64_t want = (2 * (int64_t)(ncu > 0 ? ncu : 256) + blocks - 1) / blocks;
+  tchunk = ((n + want - 1) / want + XV_T - 1) / XV_T * XV_T;
+  if (tchunk < 64) tchunk = 64;
+  ks = (int)((n + tchunk - 1) / tchunk);
+}
+
+// out [D][r] = X^T v for v [n][r] (fp64), summed over the depth chunks in order.
+static void xt_v(const Rows& rw, int64_t n, const double* v, int r, double* out, hipStream_t s) {
+  const dim3 grid((unsigned)((rw.D + XV_J - 1) / XV_J), (unsigned)((r + XV_C - 1) / XV_C), (unsigned)rw.ks);
+  xt_v_kernel<<<grid, 256, 0, s>>>(rw.x, n, rw.D, rw.ld, v, r, rw.tchunk, rw.part);
+  const int64_t m = rw.D * r;
+  sum_chunks_kernel<<<(unsigned)((m + 255) / 256 > 4096 ? 4096 : (m + 255) / 256), 256, 0, s>>>(rw.part, rw.ks, m, out);
+}
+
 // Rayleigh-Ritz of the orthonormal block w.q with fp64 accumulation, the basis outputs,
-// and (when `resid` is set) the residual of the result into info[1] / info32[1].
-static hipError_t finish(const float* g, int64_t d, int b, int r, EigWs& w, void* ut, int32_t ut_dtype,
-                         float* ut_master, float* eigvals, bool resid, hipStream_t s) {
+// and (when `resid` is set) the residual of the result into info[1] / info32[1].  With
+// `rows`, g is X X^T and its Ritz vectors V are eigenvectors of that Gram (X's left
+// singular vectors); the basis is then X^T V with unit columns, X^T X u = X^T (X X^T v) / s
+// gives the residual against X^T X, and the Ritz values are the same eigenvalues.
+static hipError_t finish(const float* g, int64_t d, int b, int r, EigWs& w, const Rows* rows, void* ut,
+                         int32_t ut_dtype, float* ut_master, float* eigvals, bool resid, hipStream_t s) {
   hipError_t e = gx64(g, w.q, d, b, w, w.y, s);   // H = Q^T (G Q)
   if (e != hipSuccess) return e;
   cross(w.q, w.y, d, b, w.mp, w.m, s);
@@ -1231,12 +1491,25 @@ static hipError_t finish(const float* g, int64_t d, int b, int r, EigWs& w, void
   int64_t gb = (d * r + 255) / 256;
   if (gb > 65535) gb = 65535;
   ritz_vectors_kernel<<<dim3((unsigned)gb), 256, 0, s>>>(w.q, w.s, w.order, w.u, d, b, r);
-  finish_basis_kernel<<<dim3((unsigned)r), 256, 0, s>>>(w.u, w.theta, d, r, ut, ut_dtype == ZOACT_BF16 ? 1 : 0,
-                                                        ut_master, eigvals);
+  const int ubf = ut_dtype == ZOACT_BF16 ? 1 : 0;
+  if (!rows) {
+    finish_basis_kernel<<<dim3((unsigned)r), 256, 0, s>>>(w.u, w.theta, d, r, ut, ubf, ut_master, eigvals);
+    if (resid) {
+      e = gx64(g, w.u, d, r, w, w.y, s);   // y = G u
+      if (e != hipSuccess) return e;
+      resid_kernel<<<1, 256, 0, s>>>(w.y, w.u, w.theta, d, r, w.info, w.info32);
+    }
+    return hipGetLastError();
+  }
+  xt_v(*rows, d, w.u, r, rows->up, s);
+  colscale_kernel<<<dim3((unsigned)r), 256, 0, s>>>(rows->up, rows->D, r, rows->sc, 1);
+  finish_basis_kernel<<<dim3((unsigned)r), 256, 0, s>>>(rows->up, w.theta, rows->D, r, ut, ubf, ut_master, eigvals);
   if (resid) {
-    e = gx64(g, w.u, d, r, w, w.y, s);   // y = G u
+    e = gx64(g, w.u, d, r, w, w.y, s);   // X X^T v
     if (e != hipSuccess) return e;
-    resid_kernel<<<1, 256, 0, s>>>(w.y, w.u, w.theta, d, r, w.info, w.info32);
+    xt_v(*rows, d, w.y, r, rows->yp, s);
+    colscale_kernel<<<dim3((unsigned)r), 256, 0, s>>>(rows->yp, rows->D, r, rows->sc, 0);
+    resid_kernel<<<1, 256, 0, s>>>(rows->yp, rows->up, w.theta, rows->D, r, w.info, w.info32);
   }
   return hipGetLastError();
 }
@@ -1254,9 +1527,9 @@ static hipError_t read_info(const EigWs& w, int k, float& v, hipStream_t s) {
 // checks (est_cols_kernel, from the products already formed), reads it back, and when
 // it is at or below tol finishes with Rayleigh-Ritz and the exact residual; if that is
 // still above tol and products remain, the iteration continues from Q.
-hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t p, const zoact_eig_opts& o, void* ut,
-                                  int32_t ut_dtype, float* ut_master, float* eigvals, zoact_eig_report* report, void* ws,
-                                  hipStream_t s, bool& met) {
+static hipError_t solve(const float* g, int64_t d, int32_t r, int32_t p, const zoact_eig_opts& o, const Rows* rows,
+                        void* ut, int32_t ut_dtype, float* ut_master, float* eigvals, zoact_eig_report* report,
+                        void* ws, hipStream_t s, bool& met) {
   const int b = r + p;
   int ks;
   int64_t kchunk;
@@ -1317,7 +1590,8 @@ hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t 
       }
     }
     if (final_product) {
-      if ((e = finish(g, d, b, r, w, ut, ut_dtype, ut_master, eigvals, want_resid, s)) != hipSuccess) return e;
+      if ((e = finish(g, d, b, r, w, rows, ut, ut_dtype, ut_master, eigvals, want_resid, s)) != hipSuccess)
+        return e;
       if (o.tol > 0.f) {
         float res = 0.f;
         if ((e = read_info(w, 1, res, s)) != hipSuccess) return e;
@@ -1333,6 +1607,59 @@ hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t 
   }
   if (report) report_kernel<<<1, 1, 0, s>>>(report, w.info, w.theta, r, k, o.tol);
   return hipGetLastError();
+}
+
+hipError_t launch_basis_from_gram(const float* g, int64_t d, int32_t r, int32_t p, const zoact_eig_opts& o, void* ut,
+                                  int32_t ut_dtype, float* ut_master, float* eigvals, zoact_eig_report* report, void* ws,
+                                  hipStream_t s, bool& met) {
+  return solve(g, d, r, p, o, nullptr, ut, ut_dtype, ut_master, eigvals, report, ws, s, met);
+}
+
+// Token-side workspace: X X^T [n][n] fp32, the solver's workspace for n rows, then the
+// basis and residual blocks [D][r] fp64, the r column norms and the X^T V partials.
+size_t basis_rows_ws_bytes(int64_t n, int64_t D, int32_t r, int32_t p) {
+  int ks;
+  int64_t tchunk;
+  xv_split(n, D, r, ks, tchunk);
+  return align256((size_t)n * n * 4) + basis_ws_bytes(n, r, p) + 2 * align256((size_t)D * r * 8) +
+         align256((size_t)r * 8) + align256((size_t)ks * D * r * 8);
+}
+
+// X X^T: with dense rows and n a multiple of 32 (the GEMM's output rows are whole 16-value
+// blocks) the plain bf16 GEMM (both halves of X against all of X: the full square), then
+// the upper triangle mirrored onto the lower so the matrix is exactly symmetric; otherwise
+// the triangle kernel.
+hipError_t launch_basis_init_rows(const uint16_t* x, int64_t n, int64_t D, int64_t ld, int32_t r, int32_t p,
+                                  const zoact_eig_opts& o, void* ut, int32_t ut_dtype, float* ut_master, float* eigvals,
+                                  zoact_eig_report* report, void* ws, hipStream_t s, bool& met) {
+  char* pw = static_cast<char*>(ws);
+  float* g = reinterpret_cast<float*>(pw);
+  pw += align256((size_t)n * n * 4);
+  void* sws = pw;
+  pw += basis_ws_bytes(n, r, p);
+  Rows rows;
+  rows.x = x;
+  rows.D = D;
+  rows.ld = ld;
+  xv_split(n, D, r, rows.ks, rows.tchunk);
+  rows.up = reinterpret_cast<double*>(pw);
+  pw += align256((size_t)D * r * 8);
+  rows.yp = reinterpret_cast<double*>(pw);
+  pw += align256((size_t)D * r * 8);
+  rows.sc = reinterpret_cast<double*>(pw);
+  pw += align256((size_t)r * 8);
+  rows.part = reinterpret_cast<double*>(pw);
+  if (n % 32 == 0 && ld == D) {
+    hipError_t e = launch_gemm_nt_f32(x, n / 2, x, n, D, g, s);
+    if (e != hipSuccess) return e;
+    const int nt = (int)((n + 31) / 32);
+    if (nt > 1) mirror_upper_kernel<<<dim3((unsigned)((int64_t)nt * (nt - 1) / 2)), 256, 0, s>>>(g, n, nt);
+    mirror_diag_kernel<<<dim3((unsigned)nt), 256, 0, s>>>(g, n);
+  } else {
+    const int nt = (int)((n + GT - 1) / GT);
+    gram_rows_bf16_kernel<<<dim3((unsigned)(nt * (nt + 1) / 2)), 256, 0, s>>>(x, n, D, ld, g, nt);
+  }
+  return solve(g, n, r, p, o, &rows, ut, ut_dtype, ut_master, eigvals, report, sws, s, met);
 }
 
 }  // namespace zoact

@@ -851,6 +851,19 @@ hipError_t launch_linear_pm(const zoact_linear& L, const zoact_arena* A, const v
   return hipErrorNotSupported;
 }
 
+// y [2 T][N] fp32 = x [2 T][K] w^T for bf16 x and w [N][K] (rows dense), through the
+// adapted-linear launch with r = 0 and no perturbation: the library's plain bf16 GEMM.
+hipError_t launch_gemm_nt_f32(const uint16_t* x, int64_t T, const uint16_t* w, int64_t N, int64_t K, float* y,
+                              hipStream_t s) {
+  zoact_linear L{};
+  L.w_dtype = ZOACT_BF16;
+  L.w = w;
+  L.d_in = K;
+  L.d_out = N;
+  zoact_pert_pair pert{};
+  return launch_linear_pm(L, nullptr, x, ZOACT_BF16, T, nullptr, nullptr, 0, pert, y, ZOACT_F32, s);
+}
+
 hipError_t launch_linear_mse(const zoact_linear& L, const zoact_arena* A, const void* x, int64_t T, uint32_t flags,
                              const void* p, const zoact_pert_pair& pert, const void* target, double* part,
                              float* loss_pm, hipStream_t s) {

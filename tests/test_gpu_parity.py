@@ -573,6 +573,114 @@ def test_basis_noconverge_keeps_best_effort():
     assert ok and info2["converged"] and info2["resid"] <= 1e-3 and info2["iters"] <= 512
 
 
+def _gapped_rows_x(t, d, r, seed):
+    """t < d rows: X = A diag(sv) Q^T, A [t][t] and Q [d][t] orthonormal, a gap after r."""
+    rr = np.random.default_rng(seed)
+    q, _ = np.linalg.qr(rr.standard_normal((d, t)))
+    a, _ = np.linalg.qr(rr.standard_normal((t, t)))
+    sv = np.concatenate([np.linspace(30, 12, r), np.linspace(4, 0.5, t - r)])
+    return ((a * sv) @ q.T).astype(np.float32)
+
+
+@pytest.mark.parametrize("t,d,r", [(256, 512, 16), (512, 1024, 32), (1024, 4096, 32), (300, 1024, 32),
+                                    (1000, 2048, 32), (200, 640, 64), (130, 4096, 8), (257, 1024, 16),
+                                    (131, 768, 8)])
+def test_basis_init_token_side_matches_oracle(t, d, r):
+    """bf16 X with fewer rows than features: basis_init solves X X^T (t x t) and maps its
+    Ritz vectors back with X^T.  Same bar as the Gram form against the oracle's top-r
+    eigenvectors of X^T X, and the Gram form on the GPU (zoact_gram +
+    zoact_basis_from_gram) agrees.  X X^T comes from the plain GEMM for t = 256, 512,
+    1024 (multiples of 32) and from the triangle kernel for the ragged and odd t (300,
+    1000, 200, 130, 257, 131); d = 640 is not a multiple of 128."""
+    announce("basis token side", t, d, r)
+    x = synth.bf16_round(_gapped_rows_x(t, d, r, seed=t + d + r))
+    u_ref, lam_ref = obasis.basis_init(x, r)
+    xt = t_bf16(x)
+    outs = []
+    for form in ("rows", "gram"):
+        ut = torch.empty(r, d, dtype=torch.bfloat16, device=dev())
+        master = torch.empty(r, d, dtype=torch.float32, device=dev())
+        ev = torch.empty(r, dtype=torch.float32, device=dev())
+        rep = Z.eig_report_tensor(dev())
+        if form == "rows":
+            ws = torch.empty(Z.basis_init_workspace_bytes(d, r), dtype=torch.uint8, device=dev())
+            assert Z.basis_init(xt, r, ut, ws, ut_master=master, eigvals=ev, report=rep)
+        else:
+            g = torch.empty(d, d, dtype=torch.float32, device=dev())
+            Z.gram(xt, g)
+            ws = torch.empty(Z.basis_workspace_bytes(d, r), dtype=torch.uint8, device=dev())
+            assert Z.basis_from_gram(g, r, ut, ws, ut_master=master, eigvals=ev, report=rep)
+        um = host(master).T
+        info = Z.read_eig_report(rep)
+        print(f"[parity] basis {form} t={t} d={d} r={r}: {info}", flush=True)
+        assert np.max(np.abs(um.T @ um - np.eye(r))) <= 1e-5
+        assert obasis.overlap(um, u_ref) >= 1 - 1e-6
+        assert_rel_close(host(ev), lam_ref, 1e-4, "eigenvalues")
+        assert np.max(np.abs(um - u_ref)) <= 1e-4
+        assert info["resid"] <= 1e-5 and info["iters"] == 64 and info["converged"]
+        _check_gap(info["gap"], _spectrum(x), r)
+        np.testing.assert_array_equal(host(ut), rne_bf16(host(master)))
+        outs.append((um, host(ev)))
+    assert np.max(np.abs(outs[0][0] - outs[1][0])) <= 1e-4
+    assert_rel_close(outs[0][1], outs[1][1], 1e-5, "eigenvalues, token side vs Gram")
+
+
+def test_basis_token_side_adaptive_and_noconverge():
+    """The token-side form under the adaptive mode stops early and meets tol; with one
+    iteration and an unreachable tol it returns ZOACT_E_NOCONVERGE with the residual of
+    the basis it wrote against X^T X, and that basis is still orthonormal."""
+    announce("basis token side adaptive")
+    t, d, r = 512, 2048, 32
+    x = synth.bf16_round(_gapped_rows_x(t, d, r, seed=11))
+    u_ref, _ = obasis.basis_init(x, r)
+    xt = t_bf16(x)
+    ut = torch.empty(r, d, dtype=torch.float32, device=dev())
+    rep = Z.eig_report_tensor(dev())
+    opts = Z.EigOpts(0, 64, 7, 1e-4, 1, 4)
+    ws = torch.empty(Z.basis_init_workspace_bytes(d, r, opts), dtype=torch.uint8, device=dev())
+    assert Z.basis_init(xt, r, ut, ws, opts, report=rep)
+    info = Z.read_eig_report(rep)
+    print(f"[parity] token side adaptive: {info}", flush=True)
+    assert info["converged"] and info["resid"] <= 1e-4 and 4 <= info["iters"] < 64
+    assert obasis.overlap(host(ut).T, u_ref) >= 1 - 1e-6
+    # one iteration from the random start: the residual the report gives is the basis's
+    # own against X^T X, recomputed here in fp64
+    opts1 = Z.EigOpts(0, 1, 3, 1e-9, 0, 0)
+    ev = torch.empty(r, dtype=torch.float32, device=dev())
+    assert not Z.basis_init(xt, r, ut, ws, opts1, eigvals=ev, report=rep)
+    info = Z.read_eig_report(rep)
+    u = host(ut).T.astype(np.float64)
+    assert np.isfinite(u).all() and np.max(np.abs(u.T @ u - np.eye(r))) <= 1e-5
+    x64 = x.astype(np.float64)
+    lam = host(ev).astype(np.float64)
+    res = np.linalg.norm(x64.T @ (x64 @ u) - u * lam, axis=0).max() / lam[0]
+    print(f"[parity] token side one iteration: {info}, fp64 residual {res:.3e}", flush=True)
+    assert not info["converged"] and info["iters"] == 1
+    assert abs(info["resid"] - res) <= 1e-3 * res + 1e-6
+
+
+def test_basis_token_side_row_stride():
+    """Token-side form on a column slice of a wider matrix (row stride > d: the triangle
+    kernel forms X X^T) and on its contiguous copy (the GEMM): both meet the oracle's bar."""
+    announce("basis token side row stride")
+    t, d, r = 224, 512, 16
+    x = synth.bf16_round(_gapped_rows_x(t, d, r, seed=5))
+    wide = np.zeros((t, d + 64), dtype=np.float32)
+    wide[:, 32:32 + d] = x
+    u_ref, lam_ref = obasis.basis_init(x, r)
+    view = t_bf16(wide)[:, 32:32 + d]
+    assert view.stride(0) == d + 64
+    for xx in (view, view.contiguous()):
+        ut = torch.empty(r, d, dtype=torch.float32, device=dev())
+        ev = torch.empty(r, dtype=torch.float32, device=dev())
+        ws = torch.empty(Z.basis_init_workspace_bytes(d, r), dtype=torch.uint8, device=dev())
+        assert Z.basis_init(xx, r, ut, ws, eigvals=ev)
+        um = host(ut).T
+        assert np.max(np.abs(um.T @ um - np.eye(r))) <= 1e-5
+        assert np.max(np.abs(um - u_ref)) <= 1e-4
+        assert_rel_close(host(ev), lam_ref, 1e-4, "eigenvalues")
+
+
 def test_basis_init_row_stride():
     """x given as a column slice of a wider matrix (row stride > d) yields the same bits
     as the contiguous copy."""
