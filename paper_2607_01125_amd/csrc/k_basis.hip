@@ -1273,33 +1273,36 @@ __global__ void __launch_bounds__(256) finish_basis_kernel(const double* __restr
   if (threadIdx.x == 0 && eigvals) eigvals[c] = (float)theta[c];
 }
 
-// resid = max_c ||G u_c - theta_c u_c|| / theta_0, with y = G u already formed; written
-// to info[1] (fp64) and info32[1] (fp32).
-__global__ void __launch_bounds__(256) resid_kernel(const double* __restrict__ y, const double* __restrict__ u,
-                                                    const double* __restrict__ theta, int64_t d, int r, double* info,
-                                                    float* info32) {
+// resid = max_c ||G u_c - theta_c u_c|| / theta_0, with y = G u already formed: one
+// workgroup per column writes its norm to cn[c] (fixed-order reduction), then
+// resid_max_kernel takes the maximum and writes info[1] (fp64) and info32[1] (fp32).
+__global__ void __launch_bounds__(256) resid_cols_kernel(const double* __restrict__ y, const double* __restrict__ u,
+                                                         const double* __restrict__ theta, int64_t d, int r,
+                                                         double* __restrict__ cn) {
   __shared__ double sh[256];
+  const int c = blockIdx.x;
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < d; i += blockDim.x) {
+    const double e = y[i * r + c] - theta[c] * u[i * r + c];
+    s += e * e;
+  }
+  sh[threadIdx.x] = s;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) cn[c] = sqrt(sh[0]);
+}
+
+__global__ void resid_max_kernel(const double* __restrict__ cn, const double* __restrict__ theta, int r, double* info,
+                                 float* info32) {
+  if (threadIdx.x != 0) return;
   double worst = 0.0;
-  for (int c = 0; c < r; ++c) {
-    double s = 0.0;
-    for (int64_t i = threadIdx.x; i < d; i += blockDim.x) {
-      const double e = y[i * r + c] - theta[c] * u[i * r + c];
-      s += e * e;
-    }
-    sh[threadIdx.x] = s;
-    __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) {
-      if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
-      __syncthreads();
-    }
-    if (threadIdx.x == 0) worst = fmax(worst, sqrt(sh[0]));
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) {
-    const double v = worst / fmax(fabs(theta[0]), 1e-300);
-    info[1] = v;
-    info32[1] = (float)v;
-  }
+  for (int c = 0; c < r; ++c) worst = fmax(worst, cn[c]);
+  const double v = worst / fmax(fabs(theta[0]), 1e-300);
+  info[1] = v;
+  info32[1] = (float)v;
 }
 
 // h <- (h + h^T) / 2 in place (b x b).  The check's projected block comes from the fp32
@@ -1477,6 +1480,13 @@ static void xt_v(const Rows& rw, int64_t n, const double* v, int r, double* out,
   sum_chunks_kernel<<<(unsigned)((m + 255) / 256 > 4096 ? 4096 : (m + 255) / 256), 256, 0, s>>>(rw.part, rw.ks, m, out);
 }
 
+// The residual of a finished basis into info[1] / info32[1]; the column norms go to w.mp
+// (free once the Rayleigh-Ritz product is formed).
+static void basis_resid(const double* y, const double* u, const double* theta, int64_t d, int r, EigWs& w, hipStream_t s) {
+  resid_cols_kernel<<<dim3((unsigned)r), 256, 0, s>>>(y, u, theta, d, r, w.mp);
+  resid_max_kernel<<<1, 64, 0, s>>>(w.mp, theta, r, w.info, w.info32);
+}
+
 // Rayleigh-Ritz of the orthonormal block w.q with fp64 accumulation, the basis outputs,
 // and (when `resid` is set) the residual of the result into info[1] / info32[1].  With
 // `rows`, g is X X^T and its Ritz vectors V are eigenvectors of that Gram (X's left
@@ -1497,7 +1507,7 @@ static hipError_t finish(const float* g, int64_t d, int b, int r, EigWs& w, cons
     if (resid) {
       e = gx64(g, w.u, d, r, w, w.y, s);   // y = G u
       if (e != hipSuccess) return e;
-      resid_kernel<<<1, 256, 0, s>>>(w.y, w.u, w.theta, d, r, w.info, w.info32);
+      basis_resid(w.y, w.u, w.theta, d, r, w, s);
     }
     return hipGetLastError();
   }
@@ -1509,7 +1519,7 @@ static hipError_t finish(const float* g, int64_t d, int b, int r, EigWs& w, cons
     if (e != hipSuccess) return e;
     xt_v(*rows, d, w.y, r, rows->yp, s);
     colscale_kernel<<<dim3((unsigned)r), 256, 0, s>>>(rows->yp, rows->D, r, rows->sc, 0);
-    resid_kernel<<<1, 256, 0, s>>>(rows->yp, rows->up, w.theta, rows->D, r, w.info, w.info32);
+    basis_resid(rows->yp, rows->up, w.theta, rows->D, r, w, s);
   }
   return hipGetLastError();
 }
