@@ -531,6 +531,8 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
       const int t = (int)__builtin_amdgcn_raw_buffer_load_b32(trs, (m + 1) * 4, 0, 0);
       nxt[j] = has ? (t < 0 ? 0 : (t >= a.N ? (int)a.N - 1 : t)) : -1;
     }
+    // (a wave wholly inside N, every one but the last column's, skips the per-block tests)
+    const bool full = nw + 128 <= a.N;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       float v[8][4];
@@ -539,34 +541,57 @@ __device__ __forceinline__ void epilogue_regs_impl(const GemmArgs& a, floatx4 (&
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[i][e] = val(i, j, e);
       float mx = -INFINITY;
+      if (full) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (nw + i * 16 < a.N) mx = fmaxf(mx, v[i][e]);
+          for (int e = 0; e < 4; ++e) mx = fmaxf(mx, v[i][e]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (nw + i * 16 < a.N) mx = fmaxf(mx, v[i][e]);
+      }
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      float se = 0.f;
+      const bool mv = j * 16 + lr < rows;
+      const int row = half * (int)a.T + (int)mw + j * 16 + lr;
+      // the row's next-token logit, while the block's values are still the logits
+      const int d = nxt[j] - (int)nw;   // the next token's offset in this wave's block
+      const bool own = mv && d >= 0 && d < 128 && ((d >> 2) & 3) == lk;
+      float tvv = 0.f;
+      if (own) {   // rare (a 128-column block holds a row's next token about once in V / 128)
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (d == i * 16 + lk * 4 + e) tvv = v[i][e];
+      }
+      // exp(logit - max) in place, then four partial sums (element e of every block) added
+      // in a fixed order: the 32 exponentials are independent of each other
+      if (full) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[i][e] = __expf(v[i][e] - mx);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[i][e] = nw + i * 16 < a.N ? __expf(v[i][e] - mx) : 0.f;
+      }
+      float sp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (nw + i * 16 < a.N) se += __expf(v[i][e] - mx);
+        for (int e = 0; e < 4; ++e) sp[e] += v[i][e];
+      float se = (sp[0] + sp[1]) + (sp[2] + sp[3]);
       se += __shfl_xor(se, 16, 64);
       se += __shfl_xor(se, 32, 64);
-      const bool mv = j * 16 + lr < rows;
-      const int row = half * (int)a.T + (int)mw + j * 16 + lr;
       // (a wave wholly past N has no block of its own: index xnblk would be the next row's)
       const int vxp = (mv && lk == 0 && nw < a.N) ? (row * a.xnblk + (int)(nw >> 7)) * 8 : OFF_NONE;
       __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{__float_as_uint(mx), __float_as_uint(se)}, xps, vxp, 0, 0);
-      const int d = nxt[j] - (int)nw;   // the next token's offset in this wave's block
-      float tvv = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (d == i * 16 + lk * 4 + e) tvv = v[i][e];
-      const bool own = mv && d >= 0 && d < 128 && ((d >> 2) & 3) == lk;
       __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(tvv), xts, own ? row * 4 : OFF_NONE, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
