@@ -625,6 +625,30 @@ def test_basis_init_token_side_matches_oracle(t, d, r):
     assert_rel_close(outs[0][1], outs[1][1], 1e-5, "eigenvalues, token side vs Gram")
 
 
+def test_basis_init_fp32_fewer_rows_takes_the_gram_form():
+    """fp32 X with fewer rows than features keeps the Gram form (X^T X of rank t): same bar
+    against the oracle, bitwise equal to zoact_gram + zoact_basis_from_gram on the GPU."""
+    announce("basis fp32 fewer rows")
+    t, d, r = 200, 512, 16
+    x = _gapped_rows_x(t, d, r, seed=21)
+    u_ref, lam_ref = obasis.basis_init(x, r)
+    xt = t_f32(x)
+    ut = torch.empty(r, d, dtype=torch.float32, device=dev())
+    ev = torch.empty(r, dtype=torch.float32, device=dev())
+    ws = torch.empty(Z.basis_init_workspace_bytes(d, r), dtype=torch.uint8, device=dev())
+    assert Z.basis_init(xt, r, ut, ws, eigvals=ev)
+    um = host(ut).T
+    assert np.max(np.abs(um.T @ um - np.eye(r))) <= 1e-5
+    assert np.max(np.abs(um - u_ref)) <= 1e-4
+    assert_rel_close(host(ev), lam_ref, 1e-4, "eigenvalues")
+    g = torch.empty(d, d, dtype=torch.float32, device=dev())
+    Z.gram(xt, g)
+    ut2 = torch.empty_like(ut)
+    ws2 = torch.empty(Z.basis_workspace_bytes(d, r), dtype=torch.uint8, device=dev())
+    assert Z.basis_from_gram(g, r, ut2, ws2)
+    np.testing.assert_array_equal(host(ut), host(ut2))
+
+
 def test_basis_token_side_adaptive_and_noconverge():
     """The token-side form under the adaptive mode stops early and meets tol; with one
     iteration and an unreachable tol it returns ZOACT_E_NOCONVERGE with the residual of
