@@ -23,7 +23,9 @@ fused +/- adapted linear at the Llama-3-8B layer shapes (bf16, INT4 in-register,
 the dequantisation pass) and across ranks; the INT4 Llama step; the OPT-13B-shape step with
 its basis initialisation; ZO-Adam's HBM rate over the Llama arena; the one-sided q = 8 form;
 the tiny fp32 model's 20 steps.  `cpu_baseline` is the oracle timed on the host cores on a
-bounded sample of the headline step, extrapolated to a whole step.
+bounded sample of the headline step, extrapolated to a whole step; without --quick the same
+kind of sample is taken for the INT4 and OPT-13B-shape steps (`models[...].cpu_baseline`) and
+for Algorithm 1 over the Llama and OPT sites (`cpu_baseline_basis_init`).
 
 Prints one JSON line.
 """
@@ -184,6 +186,108 @@ def _host_cores():
     return cores, threads, model
 
 
+_ORACLE_WEIGHTS = {}
+
+
+def _oracle_forward_sample(full, B, S, n_seq, int4=False):
+    """Times the oracle on one half's loss of a one-layer full-width model of `full` over
+    n_seq of B sequences of S tokens, once with the full vocabulary and once with an 8-token
+    head.  Returns (t_layer, t_full, gen_s, dq_s): t_layer (the 8-token-head run) holds the
+    layer plus the embedding and the final norm, t_full - t_layer the LM head; gen_s is the
+    untimed weight generation, dq_s the oracle's INT4 dequantisation of the layer's weights
+    (done once, when the model is built, so not part of a step)."""
+    import dataclasses as dc
+
+    import numpy as np
+
+    import synth
+    from oracle import linear as olin
+    from oracle import model as om
+
+    shape = synth.shrink(full, n_layers=1)
+    t_gen = time.perf_counter()
+    if full.name not in _ORACLE_WEIGHTS:   # the headline and INT4 samples share one draw
+        _ORACLE_WEIGHTS[full.name] = synth.model_weights(shape, 0, "bf16")
+    W = dict(_ORACLE_WEIGHTS[full.name])
+    gen_s = time.perf_counter() - t_gen
+    dq_s = 0.0
+    if int4:
+        L = dict(W[0])
+        for name in ("wq", "wk", "wv", "wo", "wg", "wu", "wd", "w1", "w2"):
+            if name in L:
+                packed, scales = synth.quantize_int4_g128(L[name])
+                t0 = time.perf_counter()
+                L[name] = olin.dequant_int4(packed, scales).astype(np.float32)
+                dq_s += time.perf_counter() - t0
+        W[0] = L
+    small = dc.replace(shape, vocab=8)
+    Ws = dict(W)
+    for key in ("emb", "head"):
+        if key in W:
+            Ws[key] = W[key][:8].copy()
+    tok = synth.uniform_tokens(B, S, full.vocab, 0, 2)[:n_seq]
+    m_full = om.Model(shape, 0, "bf16", weights=W)
+    m_small = om.Model(small, 0, "bf16", weights=Ws)
+    d = full.d_model
+    for m in (m_full, m_small):
+        for key, d_in in {(0, "attn"): d, (0, "o"): d, (0, "mlp"): d, (0, "down"): full.d_ff}.items():
+            q, _ = np.linalg.qr(synth.gen(0, 881, d_in).standard_normal((d_in, full.rank)))
+            m.U[key] = q.astype(np.float32).astype(np.float64)
+    c = np.zeros(m_full.k, np.float32)
+    t0 = time.perf_counter()
+    m_small.loss(tok % 8, c, +1, 1e-3, (1, 1, 0))
+    t_layer = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    m_full.loss(tok, c, +1, 1e-3, (1, 1, 0))
+    t_full = time.perf_counter() - t0
+    return t_layer, t_full, gen_s, dq_s
+
+
+def _oracle_adam_sample(n_adam=4_194_304):
+    """Seconds of the oracle's ZO-Adam (Gaussians regenerated) over n_adam coefficients."""
+    import numpy as np
+
+    from oracle import adam as oadam
+    from oracle import rng as orng
+
+    ca = np.zeros(n_adam, np.float32)
+    t0 = time.perf_counter()
+    z = orng.gauss_range(1, 1, 0, 0, n_adam)
+    oadam.zo_adam(ca, ca, ca, 0.25, z, oadam.adam_scalars(5e-5, 1))
+    return time.perf_counter() - t0
+
+
+def _oracle_step_record(full, B, S, n_seq, what, int4=False):
+    """The oracle's two-sided ZO step on `full`, sampled and extrapolated (see
+    cpu_baseline_llama for the model of the step time)."""
+    from oracle import model as om
+
+    t_layer, t_full, gen_s, dq_s = _oracle_forward_sample(full, B, S, n_seq, int4)
+    t_head = max(t_full - t_layer, 0.0)
+    n_adam = 4_194_304
+    t_adam = _oracle_adam_sample(n_adam)
+    k = om.arena_size(full)
+    scale = B // n_seq
+    L = full.n_layers
+    step_s = 2 * scale * (L * t_layer + t_head) + (k / n_adam) * t_adam
+    cores, threads, model = _host_cores()
+    rec = {"value": round(1.0 / step_s, 7), "unit": "ZO steps/s", "cores": threads, "kind": "oracle",
+           "extrapolated": True, "cpu_model": model, "cores_available": cores,
+           "seconds_per_step": round(step_s, 1),
+           "sample": (f"one half's loss of a one-layer full-width {what} on {n_seq} of {B} "
+                      f"sequences of {S} tokens, with the {full.vocab}-token head ({t_full:.2f} s) and with an "
+                      f"8-token head ({t_layer:.2f} s), plus ZO-Adam with regenerated Gaussians over {n_adam} "
+                      f"coefficients ({t_adam:.2f} s); extrapolated as 2 halves x {scale} x ({L} layers x "
+                      f"{t_layer:.2f} s + head {t_head:.2f} s) + {k / n_adam:.1f} x {t_adam:.2f} s = "
+                      f"{step_s:.0f} s per step; NumPy float64 products with the bf16 rounding points "
+                      f"emulated (weights generated untimed in {gen_s:.0f} s)")}
+    if int4:
+        rec["int4_dequant_s"] = round(L * dq_s, 1)
+        rec["sample"] += (f"; the oracle dequantises the INT4 weights once when the model is built "
+                          f"({dq_s:.2f} s for the layer, {L * dq_s:.0f} s for {L} layers; not in the step)")
+    return rec
+
+
 def cpu_baseline_llama():
     """The oracle (NumPy, float64 products, bf16 rounding points emulated) on a bounded
     sample of the headline step, extrapolated to one whole step.
@@ -196,59 +300,52 @@ def cpu_baseline_llama():
     the step time is  2 halves x 4 x (32 x t_layer + t_head) + (k / 4,194,304) x t_adam  with
     t_layer the 8-token-head time (it also holds the embedding and the final norm) and t_head
     the difference of the two."""
-    import dataclasses as dc
+    import synth
 
+    return _oracle_step_record(synth.LLAMA3_8B, 16, 256, 4, "Llama-3-8B-shape model")
+
+
+def cpu_baseline_model(w):
+    """The oracle's step for the side workloads, sampled as for the headline: the INT4
+    Llama-3-8B shape (weights dequantised by the oracle) on 4 of 16 sequences of 256 tokens,
+    the OPT-13B shape on 1 of 8 sequences of 512 tokens."""
+    import synth
+
+    if w == "llama_int4":
+        return _oracle_step_record(synth.LLAMA3_8B, 16, 256, 4, "INT4 Llama-3-8B-shape model", int4=True)
+    return _oracle_step_record(synth.OPT_13B, 8, 512, 1, "OPT-13B-shape model")
+
+
+def cpu_baseline_basis(full, calib_tokens, t_sample=2048):
+    """The oracle's Algorithm 1 (float64 Gram X^T X, then the top-r eigenvectors) over every
+    adapted site of `full`, sampled on one site of width d_model: the Gram of t_sample
+    calibration rows, and the eigensolve of a d_model x d_model Gram.  Extrapolated per site
+    as  t_gram x (calib_tokens / t_sample) x (d / d_model)^2 + t_eig x (d / d_model)^3  (the
+    Gram's cost is linear in the rows and quadratic in the width; the dense symmetric
+    eigensolver's reduction is cubic in the width)."""
     import numpy as np
 
     import synth
-    from oracle import adam as oadam
-    from oracle import model as om
-    from oracle import rng as orng
+    from oracle import basis as obasis
 
-    full = synth.LLAMA3_8B
-    shape = synth.shrink(full, n_layers=1)
-    B, S, n_seq = 16, 256, 4
-    t_gen = time.perf_counter()
-    W = synth.model_weights(shape, 0, "bf16")
-    small = dc.replace(shape, vocab=8)
-    Ws = dict(W)
-    Ws["emb"], Ws["head"] = W["emb"][:8].copy(), W["head"][:8].copy()
-    gen_s = time.perf_counter() - t_gen
-    tok = synth.uniform_tokens(B, S, full.vocab, 0, 2)[:n_seq]
-    m_full = om.Model(shape, 0, "bf16", weights=W)
-    m_small = om.Model(small, 0, "bf16", weights=Ws)
-    for m in (m_full, m_small):
-        for key, d_in in {(0, "attn"): 4096, (0, "o"): 4096, (0, "mlp"): 4096, (0, "down"): 14336}.items():
-            q, _ = np.linalg.qr(synth.gen(0, 881, d_in).standard_normal((d_in, full.rank)))
-            m.U[key] = q.astype(np.float32).astype(np.float64)
-    c = np.zeros(m_full.k, np.float32)
+    d = full.d_model
+    x = synth.bf16_round(synth.gen(0, 882, d).standard_normal((t_sample, d)).astype(np.float32))
     t0 = time.perf_counter()
-    m_small.loss(tok % 8, c, +1, 1e-3, (1, 1, 0))
-    t_layer = time.perf_counter() - t0
+    g = obasis.gram(x)
+    t_gram = time.perf_counter() - t0
     t0 = time.perf_counter()
-    m_full.loss(tok, c, +1, 1e-3, (1, 1, 0))
-    t_full = time.perf_counter() - t0
-    t_head = max(t_full - t_layer, 0.0)
-    n_adam = 4_194_304
-    ca = np.zeros(n_adam, np.float32)
-    t0 = time.perf_counter()
-    z = orng.gauss_range(1, 1, 0, 0, n_adam)
-    oadam.zo_adam(ca, ca, ca, 0.25, z, oadam.adam_scalars(5e-5, 1))
-    t_adam = time.perf_counter() - t0
-    k = om.arena_size(full)
-    scale = B // n_seq
-    step_s = 2 * scale * (full.n_layers * t_layer + t_head) + (k / n_adam) * t_adam
+    obasis.top_eigvecs(g, full.rank)
+    t_eig = time.perf_counter() - t0
+    widths = [d, d, d, full.d_ff] * full.n_layers
+    total = sum(t_gram * (calib_tokens / t_sample) * (w / d) ** 2 + t_eig * (w / d) ** 3 for w in widths)
     cores, threads, model = _host_cores()
-    return {"value": round(1.0 / step_s, 7), "unit": "ZO steps/s", "cores": threads, "kind": "oracle",
-            "extrapolated": True, "cpu_model": model, "cores_available": cores,
-            "seconds_per_step": round(step_s, 1),
-            "sample": (f"one half's loss of a one-layer full-width Llama-3-8B-shape model on {n_seq} of {B} "
-                       f"sequences of {S} tokens, with the 128256-token head ({t_full:.2f} s) and with an 8-token "
-                       f"head ({t_layer:.2f} s), plus ZO-Adam with regenerated Gaussians over {n_adam} "
-                       f"coefficients ({t_adam:.2f} s); extrapolated as 2 halves x {scale} x (32 layers x "
-                       f"{t_layer:.2f} s + head {t_head:.2f} s) + {k / n_adam:.1f} x {t_adam:.2f} s = "
-                       f"{step_s:.0f} s per step; NumPy float64 products with the bf16 rounding points "
-                       f"emulated (weights generated untimed in {gen_s:.0f} s)")}
+    return {"value": round(total, 1), "unit": "s", "cores": threads, "kind": "oracle", "extrapolated": True,
+            "cpu_model": model,
+            "sample": (f"Algorithm 1 on one width-{d} site: the float64 Gram of {t_sample} rows "
+                       f"({t_gram:.2f} s) and the top-{full.rank} eigenvectors of the {d} x {d} Gram "
+                       f"({t_eig:.2f} s); extrapolated to the {len(widths)} sites (widths {d} and {full.d_ff}) "
+                       f"and {calib_tokens} calibration tokens as t_gram x (tokens / {t_sample}) x (width / {d})^2 "
+                       f"+ t_eig x (width / {d})^3 per site = {total:.0f} s")}
 
 
 def cpu_baseline_single(T, K, N, r, budget_s=8.0):
@@ -880,6 +977,15 @@ def main():
         log(f"cpu baseline: {out['cpu_baseline']['seconds_per_step']} s per step (extrapolated)")
         if not args.quick:
             out["cpu_baseline_single_linear"] = cpu_baseline_single(8192, 4096, 4096, 32)
+            import synth
+            out["cpu_baseline_basis_init"] = cpu_baseline_basis(synth.LLAMA3_8B, 16 * 256)
+            log(f"cpu baseline, basis init: {out['cpu_baseline_basis_init']['value']} s (extrapolated)")
+            for w in out.get("models", {}):
+                out["models"][w]["cpu_baseline"] = cpu_baseline_model(w)
+                if w == "opt_bf16":
+                    out["models"][w]["cpu_baseline_basis_init"] = cpu_baseline_basis(synth.OPT_13B, 32 * 512)
+                log(f"cpu baseline, {w}: {out['models'][w]['cpu_baseline']['seconds_per_step']} s per step "
+                    f"(extrapolated)")
     print(json.dumps(out), flush=True)
 
 
